@@ -1,0 +1,87 @@
+"""Mutation check of the oracle's pins: plausible mistakes planted in copies of the oracle source (on
+the CPU, in a temporary directory) must each make at least one pin fail.
+
+Every mutant below is a one-token slip of the kind the pins are meant to catch: a dropped term, a
+wrong sign, a transposed operand, an off-by-one index, a non-strict comparison, a missing
+renormalisation, a wrong tie order.
+"""
+from __future__ import annotations
+
+import inspect
+import os
+import tempfile
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "albireo_oracle.c")
+
+MUTANTS = [
+    ("presence penalty dropped", "xv = xv - pres;", "xv = xv;"),
+    ("frequency penalty sign", "xv = xv - fc;", "xv = xv + fc;"),
+    ("repetition operand transposed", "if (xv > 0.0f) xv = xv / rep;", "if (xv > 0.0f) xv = xv * rep;"),
+    ("frequency ignores the count", "float fc = freq * (float)cnt[v];", "float fc = freq;"),
+    ("non-strict inverse CDF", "if (C > u) {", "if (C >= u) {"),
+    ("top-p not renormalised over S2", "c = c + gm / Z2;", "c = c + gm / sum;"),
+    ("top-k off by one", "tau_k = ord[k - 1].z;", "tau_k = ord[k].z;"),
+    ("ties ordered by descending id", "return (p->id > q->id) - (p->id < q->id);",
+     "return (p->id < q->id) - (p->id > q->id);"),
+    ("min-p threshold sign", "tau_m = m + lm;", "tau_m = m - lm;"),
+    ("temperature multiplies", "const float r = greedy ? 1.0f : (float)(1.0 / (double)T);",
+     "const float r = greedy ? 1.0f : T;"),
+    ("logprob drops the max", "out->logprobs[i] = id >= 0 ? (double)z[id] - (double)m - L : -INFINITY;",
+     "out->logprobs[i] = id >= 0 ? (double)z[id] - L : -INFINITY;"),
+    ("top-p splits tie groups", "while (g_end < n2 && ord[g_end].z == ord[t].z) {",
+     "while (g_end < n2 && g_end == t) {"),
+    ("draw ignores the kept set", "if (!inS[v]) continue;", "if (0) continue;"),
+    ("greedy takes the highest id", "const int32_t id = ord[0].id;",
+     "int32_t id = ord[0].id; for (int64_t q = 1; q < V && ord[q].z == ord[0].z; ++q) id = ord[q].id;"),
+]
+
+
+def _pin_calls():
+    """(name, callable) for every pin test, with its parametrisations expanded."""
+    calls = []
+    for name, fn in inspect.getmembers(pins, inspect.isfunction):
+        if not name.startswith("test_"):
+            continue
+        params = getattr(fn, "pytestmark", [])
+        sets = [{}]
+        for mark in params:
+            if mark.name != "parametrize":
+                continue
+            argnames, values = mark.args[0], mark.args[1]
+            names = [a.strip() for a in argnames.split(",")] if isinstance(argnames, str) else list(argnames)
+            new = []
+            for s in sets:
+                for v in values:
+                    vv = v if len(names) > 1 else (v,)
+                    d = dict(s)
+                    d.update(zip(names, vv))
+                    new.append(d)
+            sets = new
+        for kw in sets:
+            calls.append((name, fn, kw))
+    return calls
+
+
+@pytest.mark.parametrize("desc,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_killed(desc, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, "mutation anchor not unique: %r" % old
+    with tempfile.TemporaryDirectory() as d:
+        path = os.path.join(d, "mutant.c")
+        with open(path, "w") as f:
+            f.write(src.replace(old, new))
+        lib = oracle.build(force=True, src=path, out=os.path.join(d, "libmutant.so"))
+        variant = oracle.Variant(lib)
+        killed_by = None
+        for name, fn, kw in _pin_calls():
+            try:
+                fn(oracle_mod=variant, **kw)
+            except Exception:  # noqa: BLE001 - any failure of a pin kills the mutant
+                killed_by = name
+                break
+        assert killed_by is not None, "mutant survived every pin: " + desc
