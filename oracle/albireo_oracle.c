@@ -125,7 +125,7 @@ static void sample_row(const oracle_in* in, const oracle_out* out, int64_t i, fl
   float rep = in->rep ? in->rep[i] : 1.0f;
   float freq = in->freq ? in->freq[i] : 0.0f;
   float pres = in->pres ? in->pres[i] : 0.0f;
-  if (isnan(T)) { flags |= OR_BAD_PARAM; T = 1.0f; }
+  if (!isfinite(T)) { flags |= OR_BAD_PARAM; T = 1.0f; }
   if (isnan(p)) { flags |= OR_BAD_PARAM; p = 1.0f; }
   if (isnan(mp)) { flags |= OR_BAD_PARAM; mp = 0.0f; }
   if (!(rep > 0.0f) || isinf(rep)) { flags |= OR_BAD_PARAM; rep = 1.0f; }
