@@ -1,0 +1,160 @@
+"""Benchmark of the per-sequence sampling step on one MI355X.
+
+One step = one albireo_sample call over one batch: B=256 rows at V=152064 (the Qwen-2.5 vocabulary)
+in bf16, with repetition/frequency/presence penalties from 2048-token histories, temperature 0.7,
+top_k 40, top_p 0.95 -- the configuration the headline metric is quoted on.  Inputs are synthetic
+(workloads.generate(3)) and resident in HBM before the timed region; the call rotates over enough
+copies (>= 1 GiB) that every step reads its logits from HBM rather than from the 256 MB MALL.
+
+Prints one JSON line: rows/s (whole job), ms per step, the roofline entry of the sampling kernel
+(algorithmic bytes per launch / its average launch time from HIP events on its stream, against the
+8 TB/s HBM peak) and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sampled rows/sec + achieved HBM GB/s (% of peak), B=256 V=152064 bf16"
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(w) -> int:
+    """Bytes the method itself must move per call: logits once, history ids, CSR offsets, the seven
+    per-row parameter arrays, the uniforms, and the outputs (ids, logprobs, top-n)."""
+    b = w.B * w.V * w.itemsize
+    if w.hist_ids is not None:
+        b += w.hist_ids.size * 4 + (w.B + 1) * 8
+    b += 7 * w.B * 4 + w.B * 4  # parameters + uniforms
+    b += w.B * 4 + w.B * 4      # ids + logprobs
+    b += w.B * w.n_top * 8      # top-n ids + logprobs
+    return int(b)
+
+
+def cpu_baseline(w, seconds_target: float = 15.0) -> dict:
+    """The oracle as it stands, on a bounded sample of rows of the same workload, all host threads."""
+    import numpy as np
+
+    import oracle
+
+    oracle.build(force=False)
+    nthreads = oracle.max_threads()
+    rows_done = 0
+    t0 = time.perf_counter()
+    n = max(nthreads, 8)
+    lo = 0
+    while True:
+        hi = min(lo + n, w.B)
+        oracle.sample(w.row_slice(lo, hi), nthreads=nthreads)
+        rows_done += hi - lo
+        lo = hi % w.B
+        el = time.perf_counter() - t0
+        if el >= seconds_target or rows_done >= 64 * w.B:
+            break
+        n = min(w.B, n * 2)
+    el = time.perf_counter() - t0
+    del np
+    return {"value": rows_done / el, "unit": "rows/s", "cores": nthreads, "kind": "oracle",
+            "sample": "%d rows of the B=256 V=152064 bf16 workload (%.1f s)" % (rows_done, el)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--config", type=int, default=3, help="workload index (3 is the headline one)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the sampling step of one rank's row-share; --gpus %d is not "
+              "supported in this build" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_01927_amd as alb
+    import workloads
+    from workloads.device import to_device
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = workloads.generate(args.config)
+    logits0, u, p = to_device(w, device=dev)
+    nbytes = logits0.numel() * logits0.element_size()
+    ncopy = max(2, -(-(1 << 30) // nbytes))
+    copies = [logits0] + [logits0.clone() for _ in range(ncopy - 1)]
+    ws = alb.Workspace(dev)
+    stream = torch.cuda.current_stream()
+    B, V = w.B, w.V
+    outs = [torch.empty(B, dtype=torch.int32, device=dev), torch.empty(B, dtype=torch.float32, device=dev),
+            torch.empty((B, w.n_top), dtype=torch.int32, device=dev),
+            torch.empty((B, w.n_top), dtype=torch.float32, device=dev),
+            torch.empty(B, dtype=torch.int32, device=dev)]
+
+    call = alb.PreparedSample(logits0, u, p, w.n_top, V, outs, workspace=ws, stream=stream)
+    ptrs = [c.data_ptr() for c in copies]
+
+    def step(i):
+        call(ptrs[i % ncopy])
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # HIP events on the launch stream bracket the timed region: one kernel launch per step, so the
+    # average launch time of the sampling kernel is the elapsed time over the steps
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = e0.elapsed_time(e1)
+    ms_per_step = total_ms / args.steps
+    launch_us = ms_per_step * 1e3
+    alg = algorithmic_bytes(w)
+    achieved = alg / (launch_us * 1e-6) / 1e9
+    rows_per_s = B * args.steps / (total_ms * 1e-3)
+
+    res = {
+        "metric": METRIC,
+        "value": rows_per_s,
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "V": V, "n_top": w.n_top,
+                   "input_copies": ncopy, "input_bytes_rotated": ncopy * nbytes},
+        "hbm_gbs": alg / (ms_per_step * 1e-3) / 1e9,
+        "hbm_frac_of_peak": alg / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "k_sample (one launch per step)", "algorithmic_bytes": alg,
+                     "launch_us_avg": launch_us, "host_wall_us_per_step": wall * 1e6 / args.steps},
+        "wall_s": wall,
+    }
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

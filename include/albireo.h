@@ -1,0 +1,154 @@
+/*
+ * albireo.h -- C ABI of the MI355X (gfx950) per-sequence sampling library.
+ *
+ * The operation is the sampling step Y = Sample(Pr) of the paper's sequence-parallel sampling
+ * (sec. 6.1, Eq. opt_sample): every rank holds a row-share Pr^s of the logits matrix at full
+ * vocabulary width, samples each row independently, and consumes its slice of pre-generated random
+ * numbers (sec. 6.2, "Deterministic random number generation").  The per-row features are the ones
+ * the paper lists as enabled in its workload (sec. 8.1): repetition, frequency and presence
+ * penalties, temperature, top-k, top-p (nucleus) and min-p, plus greedy decoding (sec. 2.1, T4).
+ * The result per row is a token id and its log-probability (App. A, "update sequence" appends the
+ * sampled id with its probability).
+ *
+ * Per row i the library computes, in this order (all fp32 except where noted):
+ *   1. x = logits[i] (bf16 widened exactly).
+ *   2. penalties over the row's history h_i (count c_v of token v in h_i):
+ *        for c_v > 0:  x_v = x_v > 0 ? x_v / rep : x_v * rep;  x_v -= freq * c_v;  x_v -= pres.
+ *   3. temperature T < 1e-5 => greedy: id = lowest index among the maxima of x; logprobs use T = 1.
+ *      otherwise r = (float)(1 / (double)T), z_v = x_v * r (-0 -> +0; -inf stays -inf).
+ *   4. m = max z, LSE = m + log sum_v exp(z_v - m) over the full vocabulary.
+ *   5. min-p:  keep z >= m + (float)log(min(min_p, 1))            (when min_p > 0)
+ *      top-k:  keep z >= the k-th largest z, ties kept            (when 0 < k < V)
+ *      top-p:  over the kept set S2, renormalised, take whole groups of equal z in descending order
+ *              until the cumulative mass reaches p                (when p < 1)
+ *   6. id = first token in ascending id order whose cumulative probability over the kept set S
+ *      exceeds u = uniforms[i]; logprob = z_id - LSE.
+ *
+ * Conventions for every entry point:
+ *   - All array arguments are DEVICE pointers unless marked [host].  The caller owns every buffer.
+ *   - Row-major logits [B, ld]; ld >= V elements; row i starts at logits + i * ld.  Rows need not be
+ *     16-byte aligned; logits must be aligned to its element size.
+ *   - All work is enqueued on `stream`; no entry point synchronises with the host, allocates or frees
+ *     device memory.  Scratch memory comes from the caller's workspace.
+ *   - Host-checkable problems return a non-OK status and enqueue nothing.  Problems that depend on
+ *     device data produce a defined result and a per-row flag bit (ALBIREO_FLAG_*).
+ *   - Results are bit-identical from run to run (no floating-point atomics), and identical for a row
+ *     whether it is sampled alone or inside any batch as long as the row starts at the same address
+ *     modulo 16 bytes (always the case when ld * element size is a multiple of 16 and the buffers are
+ *     16-byte aligned): the reduction order is fixed by V, dtype and that alignment.
+ */
+#ifndef ALBIREO_H
+#define ALBIREO_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { ALBIREO_F32 = 0, ALBIREO_BF16 = 1 } albireo_dtype_t;
+
+typedef enum {
+  ALBIREO_OK = 0,
+  ALBIREO_E_INVALID = 1,     /* bad pointer, size, stride, dtype or n_top                       */
+  ALBIREO_E_UNSUPPORTED = 2, /* shape this build does not handle (e.g. V >= 2^31)                */
+  ALBIREO_E_WORKSPACE = 3,   /* workspace NULL, misaligned or smaller than albireo_workspace_size */
+  ALBIREO_E_LAUNCH = 4       /* the HIP runtime refused the launch                               */
+} albireo_status_t;
+
+/* Per-row flag bits written to out_flags. */
+#define ALBIREO_FLAG_GREEDY 1u    /* temperature < 1e-5: argmax, uniform ignored                   */
+#define ALBIREO_FLAG_EMPTY 2u     /* no finite logit: id = -1, logprob = -inf                      */
+#define ALBIREO_FLAG_BAD_INPUT 4u /* NaN or +inf logit (after penalties/temperature), or a history id
+                                     outside [0, V) (skipped); other outputs of the row unspecified  */
+#define ALBIREO_FLAG_BAD_PARAM 8u /* malformed per-row parameter, replaced by its "off" value:
+                                     temperature NaN or inf -> 1; rep <= 0, NaN or inf -> 1; freq/pres not
+                                     finite -> 0; top_p NaN -> 1; min_p NaN -> 0; history offsets
+                                     decreasing, negative or past hist_len -> no penalties        */
+#define ALBIREO_FLAG_LIMIT 16u    /* a row's history has more distinct ids in one row chunk than
+                                     this build handles on chip (ALBIREO_MAX_UNIQUE_HISTORY); the
+                                     extra ids are ignored                                        */
+
+#define ALBIREO_MAX_TOP_N 32
+#define ALBIREO_MAX_UNIQUE_HISTORY 3072
+
+/*
+ * Per-row sampling metadata (the paper's per-sequence metadata, sec. 3 Challenge 3 and sec. 6.2).
+ * The struct itself lives in host memory and is read during the call only; every member is a device
+ * pointer to a [B] array (or NULL, which turns the feature off for all rows).
+ */
+typedef struct {
+  const float* temperature;        /* [B]  T < 1e-5 (incl. 0 and negatives) => greedy; NULL => 1  */
+  const int32_t* top_k;            /* [B]  k <= 0 or k >= V => off                                 */
+  const float* top_p;              /* [B]  p >= 1 => off; p <= 0 keeps the top group               */
+  const float* min_p;              /* [B]  <= 0 => off; > 1 behaves as 1                           */
+  const float* repetition_penalty; /* [B]  1 => off                                               */
+  const float* frequency_penalty;  /* [B]  0 => off                                               */
+  const float* presence_penalty;   /* [B]  0 => off                                               */
+  const int64_t* hist_offsets;     /* [B+1] CSR row pointers into hist_ids; NULL => no penalties   */
+  const int32_t* hist_ids;         /* [hist_len] token ids; ids outside [0, V) are skipped+flagged */
+  int64_t hist_len;                /* [host value] number of entries in hist_ids                   */
+} albireo_params_t;
+
+/*
+ * Bytes of device workspace needed by any entry point for this shape on the current device.
+ * The workspace must be 256-byte aligned and zero-filled before its first use; every call leaves it
+ * zero-filled again on return (stream order).  One workspace per stream: two calls that run
+ * concurrently must not share one.
+ */
+size_t albireo_workspace_size(int64_t B, int64_t V, albireo_dtype_t dtype, int32_t n_top);
+
+/*
+ * Sample one token per row.
+ *   logits       [B, ld] bf16 bit patterns or fp32 (dtype)
+ *   params       [host] per-row metadata; NULL => every feature off (pure softmax sampling at T = 1)
+ *   uniforms     [B] fp32 in [0, 1): the row's pre-generated random number.  Rank j of a
+ *                sequence-parallel group passes uniforms + its row offset (sec. 6.2).
+ *   out_ids      [B] int32 sampled token id (-1 for an EMPTY row)
+ *   out_logprobs [B] fp32 log-softmax of the processed logits (after penalties and temperature) over
+ *                the full vocabulary, at the sampled id
+ *   n_top        0..ALBIREO_MAX_TOP_N; when > 0, out_top_ids / out_top_logprobs [B, n_top] get the n_top
+ *                largest processed logits (ties -> lower id) with their logprobs; slots beyond the
+ *                number of finite logits get id -1 and -inf
+ *   out_flags    [B] ALBIREO_FLAG_* bits, or NULL
+ * Returns ALBIREO_OK once the work is enqueued.
+ */
+albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
+                                const albireo_params_t* params, const float* uniforms, int32_t* out_ids,
+                                float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
+                                float* out_top_logprobs, uint32_t* out_flags, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Apply steps 1-2 (penalties only) and write the penalised logits as fp32.
+ *   params      [host] uses repetition/frequency/presence penalties and the history; other members ignored
+ *   out_logits  [B, V] fp32, row stride V.  It may alias `logits` only when dtype is F32 and ld == V.
+ */
+albireo_status_t albireo_apply_penalties(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V,
+                                         int64_t ld, const albireo_params_t* params, float* out_logits,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Apply steps 3-5 to already-penalised fp32 logits and report the filtered distribution.
+ *   params         [host] uses temperature, top_k, top_p, min_p; penalty members are ignored
+ *   out_probs      [B, V] fp32 (row stride V) renormalised probabilities over the kept set S, 0 outside
+ *                  S, or NULL.  A greedy row keeps only its argmax (probability 1).
+ *   out_threshold  [B] fp32 min z over S (-inf for an EMPTY row), or NULL
+ *   out_kept       [B] int32 |S|, or NULL
+ *   out_log_norm   [B] fp32 m + log sum_{v in S} exp(z_v - m), or NULL
+ *   out_flags      [B] ALBIREO_FLAG_* bits, or NULL
+ */
+albireo_status_t albireo_topk_topp(const float* logits, int64_t B, int64_t V, int64_t ld,
+                                   const albireo_params_t* params, float* out_probs, float* out_threshold,
+                                   int32_t* out_kept, float* out_log_norm, uint32_t* out_flags,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* albireo_status_string(albireo_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ALBIREO_H */

@@ -1,0 +1,264 @@
+"""Python binding of the gfx950 per-sequence sampling library (``include/albireo.h``).
+
+Argument marshalling only: every step of the sampling path runs in the HIP kernels of
+``libalbireo.so``.  PyTorch supplies device memory and the current HIP stream.  Importing this package
+fails loudly when the built library is missing; there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libalbireo.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        "libalbireo.so is not built (expected at %s); run `python paper_2606_01927_amd/build.py` "
+        "or __graft_entry__.build()" % LIB_PATH)
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+F32, BF16 = 0, 1
+OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_LAUNCH = 0, 1, 2, 3, 4
+FLAG_GREEDY, FLAG_EMPTY, FLAG_BAD_INPUT, FLAG_BAD_PARAM, FLAG_LIMIT = 1, 2, 4, 8, 16
+MAX_TOP_N = 32
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [
+        ("temperature", ctypes.c_void_p), ("top_k", ctypes.c_void_p), ("top_p", ctypes.c_void_p),
+        ("min_p", ctypes.c_void_p), ("repetition_penalty", ctypes.c_void_p),
+        ("frequency_penalty", ctypes.c_void_p), ("presence_penalty", ctypes.c_void_p),
+        ("hist_offsets", ctypes.c_void_p), ("hist_ids", ctypes.c_void_p), ("hist_len", ctypes.c_int64),
+    ]
+
+
+_vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+_lib.albireo_workspace_size.argtypes = [_i64, _i64, ctypes.c_int, _i32]
+_lib.albireo_workspace_size.restype = _sz
+_lib.albireo_sample.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Params), _vp, _vp, _vp,
+                                _i32, _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.albireo_sample.restype = ctypes.c_int
+_lib.albireo_apply_penalties.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Params), _vp,
+                                         _vp, _sz, _vp]
+_lib.albireo_apply_penalties.restype = ctypes.c_int
+_lib.albireo_topk_topp.argtypes = [_vp, _i64, _i64, _i64, ctypes.POINTER(_Params), _vp, _vp, _vp, _vp, _vp,
+                                   _vp, _sz, _vp]
+_lib.albireo_topk_topp.restype = ctypes.c_int
+_lib.albireo_status_string.argtypes = [ctypes.c_int]
+_lib.albireo_status_string.restype = ctypes.c_char_p
+
+EXPORTED = ("albireo_workspace_size", "albireo_sample", "albireo_apply_penalties", "albireo_topk_topp",
+            "albireo_status_string")
+
+
+class AlbireoError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__("%s: %s (status %d)" % (where, status_string(status), status))
+        self.status = status
+
+
+def status_string(status: int) -> str:
+    return _lib.albireo_status_string(int(status)).decode()
+
+
+@dataclasses.dataclass
+class SamplingParams:
+    """Per-row sampling metadata as device tensors ([B] each; None turns a feature off)."""
+    temperature: Optional[torch.Tensor] = None         # float32
+    top_k: Optional[torch.Tensor] = None               # int32
+    top_p: Optional[torch.Tensor] = None               # float32
+    min_p: Optional[torch.Tensor] = None               # float32
+    repetition_penalty: Optional[torch.Tensor] = None  # float32
+    frequency_penalty: Optional[torch.Tensor] = None   # float32
+    presence_penalty: Optional[torch.Tensor] = None    # float32
+    hist_offsets: Optional[torch.Tensor] = None        # int64 [B + 1]
+    hist_ids: Optional[torch.Tensor] = None            # int32
+
+
+_DT = {"temperature": torch.float32, "top_k": torch.int32, "top_p": torch.float32, "min_p": torch.float32,
+       "repetition_penalty": torch.float32, "frequency_penalty": torch.float32,
+       "presence_penalty": torch.float32, "hist_offsets": torch.int64, "hist_ids": torch.int32}
+
+
+def _ptr(t: Optional[torch.Tensor], name: str, device) -> Optional[int]:
+    if t is None:
+        return None
+    if t.device != device or t.dtype != _DT[name] or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous %s tensor on %s" % (name, _DT[name], device))
+    return t.data_ptr()
+
+
+def _params(p: Optional[SamplingParams], device) -> Optional[_Params]:
+    if p is None:
+        return None
+    s = _Params()
+    for f in ("temperature", "top_k", "top_p", "min_p", "repetition_penalty", "frequency_penalty",
+              "presence_penalty", "hist_offsets", "hist_ids"):
+        setattr(s, f, _ptr(getattr(p, f), f, device))
+    s.hist_len = 0 if p.hist_ids is None else int(p.hist_ids.numel())
+    return s
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise ValueError("logits must be bfloat16 or float32")
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def workspace_size(B: int, V: int, dtype: torch.dtype, n_top: int = 0) -> int:
+    return int(_lib.albireo_workspace_size(B, V, BF16 if dtype == torch.bfloat16 else F32, n_top))
+
+
+class Workspace:
+    """A zero-filled device workspace that grows on demand (the library leaves it zeroed)."""
+
+    def __init__(self, device=None):
+        self.device = torch.device("cuda") if device is None else torch.device(device)
+        self.buf = None
+
+    def get(self, nbytes: int):
+        if nbytes == 0:
+            return None, 0
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.zeros(max(nbytes, 256) + 256, dtype=torch.uint8, device=self.device)
+        base = self.buf.data_ptr()
+        off = (-base) % 256
+        return base + off, self.buf.numel() - off
+
+
+_default_ws = {}
+
+
+def _ws_for(device, workspace):
+    if workspace is not None:
+        return workspace
+    key = (device.type, device.index)
+    if key not in _default_ws:
+        _default_ws[key] = Workspace(device)
+    return _default_ws[key]
+
+
+def _rows(logits: torch.Tensor, V: Optional[int]):
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be a 2-D tensor with unit stride along the vocabulary")
+    B = logits.shape[0]
+    V = logits.shape[1] if V is None else V
+    ld = logits.stride(0) if B > 1 else max(V, logits.shape[1])
+    return B, V, ld
+
+
+def sample(logits: torch.Tensor, uniforms: torch.Tensor, params: Optional[SamplingParams] = None,
+           n_top: int = 0, V: Optional[int] = None, workspace: Optional[Workspace] = None, stream=None,
+           out=None):
+    """Sample one token per row.  Returns (ids int32 [B], logprobs float32 [B], top_ids [B, n_top],
+    top_logprobs [B, n_top], flags int32 [B])."""
+    dev = logits.device
+    B, V, ld = _rows(logits, V)
+    if uniforms.dtype != torch.float32 or uniforms.device != dev or uniforms.numel() < B:
+        raise ValueError("uniforms must be a float32 [B] tensor on the logits' device")
+    if out is None:
+        ids = torch.empty(B, dtype=torch.int32, device=dev)
+        lps = torch.empty(B, dtype=torch.float32, device=dev)
+        tids = torch.empty((B, n_top), dtype=torch.int32, device=dev)
+        tlps = torch.empty((B, n_top), dtype=torch.float32, device=dev)
+        flags = torch.empty(B, dtype=torch.int32, device=dev)
+    else:
+        ids, lps, tids, tlps, flags = out
+    dt = _dtype_code(logits)
+    ws = _ws_for(dev, workspace)
+    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)))
+    prm = _params(params, dev)
+    st = _lib.albireo_sample(logits.data_ptr(), dt, B, V, ld, ctypes.byref(prm) if prm else None,
+                             uniforms.data_ptr(), ids.data_ptr(), lps.data_ptr(), n_top,
+                             tids.data_ptr() if n_top else None, tlps.data_ptr() if n_top else None,
+                             flags.data_ptr(), wptr, wbytes, _stream(stream))
+    if st != OK:
+        raise AlbireoError(st, "albireo_sample")
+    return ids, lps, tids, tlps, flags
+
+
+class PreparedSample:
+    """albireo_sample with its arguments marshalled once; calling it enqueues one launch with the
+    given logits pointer (same shape, dtype and stride as at preparation)."""
+
+    def __init__(self, logits: torch.Tensor, uniforms: torch.Tensor, params: Optional[SamplingParams],
+                 n_top: int, V: Optional[int], out, workspace: Optional[Workspace] = None, stream=None):
+        dev = logits.device
+        self.B, self.V, self.ld = _rows(logits, V)
+        self.dt = _dtype_code(logits)
+        ws = _ws_for(dev, workspace)
+        self.wptr, self.wbytes = ws.get(int(_lib.albireo_workspace_size(self.B, self.V, self.dt, n_top)))
+        self.prm = _params(params, dev)
+        self.prm_ref = ctypes.byref(self.prm) if self.prm else None
+        ids, lps, tids, tlps, flags = out
+        self.keep = (uniforms, params, out)
+        self.tail = (self.prm_ref, uniforms.data_ptr(), ids.data_ptr(), lps.data_ptr(), n_top,
+                     tids.data_ptr() if n_top else None, tlps.data_ptr() if n_top else None, flags.data_ptr(),
+                     self.wptr, self.wbytes, _stream(stream))
+        self.fn = _lib.albireo_sample
+
+    def __call__(self, logits_ptr: int) -> None:
+        st = self.fn(logits_ptr, self.dt, self.B, self.V, self.ld, *self.tail)
+        if st != OK:
+            raise AlbireoError(st, "albireo_sample")
+
+
+def apply_penalties(logits: torch.Tensor, params: SamplingParams, V: Optional[int] = None, out=None,
+                    stream=None) -> torch.Tensor:
+    """Penalised logits as fp32 [B, V]."""
+    dev = logits.device
+    B, V, ld = _rows(logits, V)
+    if out is None:
+        out = torch.empty((B, V), dtype=torch.float32, device=dev)
+    prm = _params(params, dev)
+    st = _lib.albireo_apply_penalties(logits.data_ptr(), _dtype_code(logits), B, V, ld,
+                                      ctypes.byref(prm) if prm else None, out.data_ptr(), None, 0,
+                                      _stream(stream))
+    if st != OK:
+        raise AlbireoError(st, "albireo_apply_penalties")
+    return out
+
+
+def topk_topp(logits: torch.Tensor, params: Optional[SamplingParams] = None, V: Optional[int] = None,
+              probs: bool = True, workspace: Optional[Workspace] = None, stream=None):
+    """Filtered distribution of fp32 logits.  Returns (probs [B, V] or None, threshold [B], kept [B],
+    log_norm [B], flags [B])."""
+    if logits.dtype != torch.float32:
+        raise ValueError("topk_topp takes float32 logits")
+    dev = logits.device
+    B, V, ld = _rows(logits, V)
+    pr = torch.empty((B, V), dtype=torch.float32, device=dev) if probs else None
+    thr = torch.empty(B, dtype=torch.float32, device=dev)
+    kept = torch.empty(B, dtype=torch.int32, device=dev)
+    lnorm = torch.empty(B, dtype=torch.float32, device=dev)
+    flags = torch.empty(B, dtype=torch.int32, device=dev)
+    ws = _ws_for(dev, workspace)
+    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, F32, 0)))
+    prm = _params(params, dev)
+    st = _lib.albireo_topk_topp(logits.data_ptr(), B, V, ld, ctypes.byref(prm) if prm else None,
+                                pr.data_ptr() if pr is not None else None, thr.data_ptr(), kept.data_ptr(),
+                                lnorm.data_ptr(), flags.data_ptr(), wptr, wbytes, _stream(stream))
+    if st != OK:
+        raise AlbireoError(st, "albireo_topk_topp")
+    return pr, thr, kept, lnorm, flags
+
+
+def raw_call(name: str):
+    """The C entry point itself (for tests that exercise the boundary's argument checks)."""
+    return getattr(_lib, name)
+
+
+Params = _Params

@@ -1,0 +1,2257 @@
+// albireo.hip -- gfx950 kernels and the C ABI of the per-sequence sampling library.
+//
+// One launch samples B rows.  A row (or, for rows wider than one CU can hold, one of P contiguous
+// chunks of it) is owned by one 1024-thread workgroup that keeps the whole chunk in VGPRs: every
+// logit is read from HBM exactly once with 16-byte loads, all issued up front.  On that resident data
+// the workgroup runs
+//   * the penalty overlay (feature list of sec. 8.1): history counts in an LDS hash; a per-slot LDS
+//     bitmap masks the penalised entries in the registers; their new values live in a small LDS
+//     "extras" list together with the few unaligned head/tail entries of the row;
+//   * an online max / sum-exp pass overlapped with the loads, giving the full-vocabulary log-sum-exp
+//     the logprobs need (sec. 2.1 T4; App. A appends the sampled id with its probability);
+//   * a candidate gather above a provable lower bound of the kept set (the K-th largest per-thread
+//     maximum for top-k / top-n, m + ln(min_p) for min-p, a mass bound for top-p);
+//   * exact resolution of top-k / min-p / top-p and the inverse-CDF draw on that small LDS list, or,
+//     when the kept set is too large for the list, radix histogram selection over the registers and a
+//     draw through an id-ordered scan buffer in the workspace.
+// Rows never interact, which is what lets the paper split sampling across ranks by rows (sec. 6.1,
+// Eq. opt_sample); the P > 1 chunks of one row synchronise through the caller's workspace.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "albireo.h"
+
+namespace {
+
+// ----------------------------------------------------------------------------------------------
+// Geometry and capacities
+// ----------------------------------------------------------------------------------------------
+constexpr int NT = 512;           // threads per workgroup (2 waves per SIMD, 256 VGPRs each)
+constexpr int NW = NT / 64;       // waves per workgroup
+constexpr int JMAX = 38;          // 16-byte register slots per thread (152 VGPRs of row data)
+constexpr int LOG2_HCAP = 12;
+constexpr int HCAP = 1 << LOG2_HCAP;              // LDS hash slots for history counts
+constexpr int UCAP = ALBIREO_MAX_UNIQUE_HISTORY;  // tracked distinct ids (history + head/tail)
+constexpr int LCAP = 2048;        // candidate list capacity
+constexpr int EPT = LCAP / NT;    // list entries per thread in the list scans
+constexpr int MAXP = 8;           // chunks per row supported
+constexpr uint32_t SPIN_LIMIT = 1u << 24;
+constexpr double FIX_SCALE = 4294967296.0;  // fixed-point scale of the general path's masses
+constexpr float MREF0 = -3.0e38f;           // initial sum-exp reference (log2 units)
+constexpr float L2E = 1.44269504088896341f;  // fl32(log2 e): exp(z) is evaluated as 2^(z * L2E)
+
+constexpr uint32_t FLAG_GREEDY = ALBIREO_FLAG_GREEDY;
+constexpr uint32_t FLAG_EMPTY = ALBIREO_FLAG_EMPTY;
+constexpr uint32_t FLAG_BAD_INPUT = ALBIREO_FLAG_BAD_INPUT;
+constexpr uint32_t FLAG_BAD_PARAM = ALBIREO_FLAG_BAD_PARAM;
+constexpr uint32_t FLAG_LIMIT = ALBIREO_FLAG_LIMIT;
+
+struct DevParams {
+  const float* temperature;
+  const int32_t* top_k;
+  const float* top_p;
+  const float* min_p;
+  const float* rep;
+  const float* freq;
+  const float* pres;
+  const int64_t* hist_offsets;
+  const int32_t* hist_ids;
+  int64_t hist_len;
+};
+
+// Per-launch arguments (passed by value).
+struct KArgs {
+  const unsigned char* logits;
+  int64_t B, V, ld;
+  DevParams prm;
+  const float* uniforms;
+  int32_t* out_ids;
+  float* out_logprobs;
+  int32_t n_top;
+  int32_t* out_top_ids;
+  float* out_top_logprobs;
+  uint32_t* out_flags;
+  float* out_probs;
+  float* out_threshold;
+  int32_t* out_kept;
+  float* out_log_norm;
+  int32_t mode;          // 0: sample, 1: topk_topp
+  int32_t P;             // chunks per row
+  int32_t n_groups;      // persistent row groups (grid = n_groups * P)
+  int32_t xcd_map;       // place the P chunks of a group on one XCD
+  int64_t chunk_slots;   // 16-byte body slots per chunk
+  unsigned char* ws;
+  int64_t ws_group_bytes;
+};
+
+// ----------------------------------------------------------------------------------------------
+// Workspace layout of one row group (offsets 256-byte aligned)
+// ----------------------------------------------------------------------------------------------
+struct GroupSync {
+  uint32_t arrive;
+  uint32_t exit;
+  uint32_t error;
+  uint32_t pad[61];
+};
+struct ChunkStats {  // published by every chunk workgroup of a row
+  float xm;          // max x over the chunk
+  float mref;        // reference of s (log2 units)
+  float s;           // sum of 2^(z*L2E - mref)
+  uint32_t flags;
+  float beta_sel;    // K-th largest per-thread maximum z of the chunk
+  int32_t n_list;    // candidates gathered
+  int32_t overflow;
+  float w_total;     // general draw: chunk total
+  int32_t last_pos;  // general draw: last position with positive weight / greedy argmax
+  int32_t n_keep;    // general path: kept count
+  float zmin;        // general path: min z over kept
+  int32_t best;      // general path: lowest position of the maximum
+  uint64_t zs_fix;   // general path: fixed-point mass of the kept set
+  uint32_t pad[2];
+};
+struct GroupRes {    // published by the leader for the dense output
+  float tau;
+  float zs;
+  int32_t id;
+  int32_t pad[13];
+};
+
+__host__ __device__ constexpr int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+struct WsLayout {
+  int64_t sync, stats, res, hist, lists, total;
+  __host__ __device__ WsLayout(int P) {
+    sync = 0;
+    stats = align256(sync + (int64_t)sizeof(GroupSync));
+    res = align256(stats + (int64_t)sizeof(ChunkStats) * P);
+    hist = align256(res + (int64_t)sizeof(GroupRes));
+    lists = align256(hist + (int64_t)P * 256 * 8);
+    total = align256(lists + (int64_t)P * LCAP * 8);
+  }
+};
+
+// ----------------------------------------------------------------------------------------------
+// Scalar helpers
+// ----------------------------------------------------------------------------------------------
+// order-preserving 32-bit key of a float (larger float -> larger key); -inf maps above 0
+__device__ __forceinline__ uint32_t f2key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key2f(uint32_t k) {
+  const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+  return __uint_as_float(u);
+}
+// canonical processed logit: fl32(x * r) with -0 -> +0; -inf stays -inf (also when r == 0)
+__device__ __forceinline__ float canon(float x, float r) {
+  return (x == -INFINITY) ? -INFINITY : __fadd_rn(__fmul_rn(x, r), 0.0f);
+}
+// penalty overlay of one logit seen c > 0 times in the history
+__device__ __forceinline__ float penalise(float x, uint32_t c, float rep, float freq, float pres) {
+  float v = (x > 0.0f) ? __fdiv_rn(x, rep) : __fmul_rn(x, rep);
+  v = __fsub_rn(v, __fmul_rn(freq, (float)c));
+  v = __fsub_rn(v, pres);
+  return v;
+}
+// 2^(a - b) for a <= b; a == b (including both -inf) -> 1
+__device__ __forceinline__ float rel2(float a, float b) { return (a == b) ? 1.0f : __builtin_amdgcn_exp2f(a - b); }
+// candidate sort key: z descending, then position ascending
+__device__ __forceinline__ uint64_t cand_key(float z, int pos) {
+  return ((uint64_t)f2key(z) << 32) | (uint32_t)(~(uint32_t)pos);
+}
+__device__ __forceinline__ float cand_z(uint64_t k) { return key2f((uint32_t)(k >> 32)); }
+__device__ __forceinline__ int cand_pos(uint64_t k) { return (int)(~(uint32_t)k); }
+__device__ __forceinline__ uint64_t fixmass(float w) { return (uint64_t)((double)w * FIX_SCALE); }
+
+template <class T>
+__device__ __forceinline__ T ld_agent(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <class T>
+__device__ __forceinline__ void st_agent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
+__device__ __forceinline__ int wave_id() { return (int)(threadIdx.x >> 6); }
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const int l = lane_id();
+  return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+
+// ----------------------------------------------------------------------------------------------
+// Element types: a 16-byte slot holds 8 bf16 or 4 fp32 logits
+// ----------------------------------------------------------------------------------------------
+struct BF16T {
+  static constexpr int VEC = 8;
+  static constexpr int ES = 2;
+  static constexpr uint32_t NEG = 0xff80ff80u;  // two bf16 -inf
+  __device__ static __forceinline__ float get(const uint4& d, int e) {
+    const uint32_t w = (e >> 1) == 0 ? d.x : (e >> 1) == 1 ? d.y : (e >> 1) == 2 ? d.z : d.w;
+    return (e & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
+  }
+  __device__ static __forceinline__ float load1(const unsigned char* row, int64_t i) {
+    return __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t*>(row)[i]) << 16);
+  }
+  // bit e of b selects element e; dword k holds element 2k (low half) and 2k+1 (high half)
+  __device__ static __forceinline__ uint4 mask_of(uint32_t b) {
+    uint4 m;
+    m.x = ((b & 1u) ? 0x0000ffffu : 0u) | ((b & 2u) ? 0xffff0000u : 0u);
+    m.y = ((b & 4u) ? 0x0000ffffu : 0u) | ((b & 8u) ? 0xffff0000u : 0u);
+    m.z = ((b & 16u) ? 0x0000ffffu : 0u) | ((b & 32u) ? 0xffff0000u : 0u);
+    m.w = ((b & 64u) ? 0x0000ffffu : 0u) | ((b & 128u) ? 0xffff0000u : 0u);
+    return m;
+  }
+};
+struct F32T {
+  static constexpr int VEC = 4;
+  static constexpr int ES = 4;
+  static constexpr uint32_t NEG = 0xff800000u;
+  __device__ static __forceinline__ float get(const uint4& d, int e) {
+    const uint32_t w = e == 0 ? d.x : e == 1 ? d.y : e == 2 ? d.z : d.w;
+    return __uint_as_float(w);
+  }
+  __device__ static __forceinline__ float load1(const unsigned char* row, int64_t i) {
+    return reinterpret_cast<const float*>(row)[i];
+  }
+  __device__ static __forceinline__ uint4 mask_of(uint32_t b) {
+    uint4 m;
+    m.x = (b & 1u) ? ~0u : 0u;
+    m.y = (b & 2u) ? ~0u : 0u;
+    m.z = (b & 4u) ? ~0u : 0u;
+    m.w = (b & 8u) ? ~0u : 0u;
+    return m;
+  }
+};
+
+// ----------------------------------------------------------------------------------------------
+// Shared memory of the sampling kernel
+// ----------------------------------------------------------------------------------------------
+struct Smem {
+  int32_t h_key[HCAP];
+  uint32_t h_cnt[HCAP];
+  uint16_t u_slot[UCAP];
+  uint32_t bitmap[JMAX * NT / 4];  // one byte per body slot of the chunk, bit e = element e
+  uint4 masktab[256];
+  int16_t h_xi[HCAP];              // hash slot -> extras index
+  int32_t x_pos[UCAP];             // extras: penalised body entries and head/tail entries
+  float x_val[UCAP];
+  uint64_t sk[LCAP];               // candidate list / sort keys
+  float l_z[LCAP];                 // resolved list: z, weight, position in descending order
+  float l_w[LCAP];
+  int32_t l_p[LCAP];
+  uint64_t hist[256];
+  float red_f[2 * NW];
+  uint32_t red_u[NW];
+  uint64_t red_q[NW];
+  int32_t n_uniq;
+  int32_t n_list;
+  uint32_t flags;
+  int32_t bc_i[4];
+  float bc_f[4];
+  uint64_t bc_q[4];
+};
+static_assert(sizeof(Smem) <= 160 * 1024, "LDS of one workgroup exceeds a gfx950 CU");
+static_assert(4 * NT <= UCAP, "history staging does not fit the extras arrays");
+
+// ----------------------------------------------------------------------------------------------
+// Workgroup reductions and scans (fixed combination order: wave butterfly / Kogge-Stone, then
+// waves in index order), so results are bit-identical from run to run
+// ----------------------------------------------------------------------------------------------
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ int wave_min_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ int wave_max_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ float wave_incl_scan(float v) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float t = __shfl_up(v, o);
+    if (l >= o) v += t;
+  }
+  return v;
+}
+// bitonic sort of one 64-bit key per lane across the wave (descending or ascending by lane index)
+__device__ __forceinline__ uint64_t wave_sort_u64(uint64_t key, bool descending) {
+  const int l = lane_id();
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const uint64_t o = __shfl_xor(key, j);
+      const bool lower = (l & j) == 0;
+      const bool block_desc = ((l & k) == 0) == descending;
+      const bool take_max = lower == block_desc;
+      key = take_max ? (key > o ? key : o) : (key < o ? key : o);
+    }
+  }
+  return key;
+}
+
+__device__ __forceinline__ float block_max(float v, Smem& s) {
+  v = wave_max(v);
+  __syncthreads();
+  if (lane_id() == 0) s.red_f[wave_id()] = v;
+  __syncthreads();
+  float r = s.red_f[0];
+  for (int w = 1; w < NW; ++w) r = fmaxf(r, s.red_f[w]);
+  return r;
+}
+__device__ __forceinline__ float block_min(float v, Smem& s) { return -block_max(-v, s); }
+__device__ __forceinline__ uint32_t block_or(uint32_t v, Smem& s) {
+  v = wave_or(v);
+  __syncthreads();
+  if (lane_id() == 0) s.red_u[wave_id()] = v;
+  __syncthreads();
+  uint32_t r = 0;
+  for (int w = 0; w < NW; ++w) r |= s.red_u[w];
+  return r;
+}
+__device__ __forceinline__ int block_min_i(int v, Smem& s) {
+  v = wave_min_i(v);
+  __syncthreads();
+  if (lane_id() == 0) s.red_u[wave_id()] = (uint32_t)v;
+  __syncthreads();
+  int r = (int)s.red_u[0];
+  for (int w = 1; w < NW; ++w) r = min(r, (int)s.red_u[w]);
+  return r;
+}
+__device__ __forceinline__ int block_max_i(int v, Smem& s) {
+  v = wave_max_i(v);
+  __syncthreads();
+  if (lane_id() == 0) s.red_u[wave_id()] = (uint32_t)v;
+  __syncthreads();
+  int r = (int)s.red_u[0];
+  for (int w = 1; w < NW; ++w) r = max(r, (int)s.red_u[w]);
+  return r;
+}
+__device__ __forceinline__ int block_sum_i(int v, Smem& s) {
+  v = wave_sum_i(v);
+  __syncthreads();
+  if (lane_id() == 0) s.red_u[wave_id()] = (uint32_t)v;
+  __syncthreads();
+  int r = 0;
+  for (int w = 0; w < NW; ++w) r += (int)s.red_u[w];
+  return r;
+}
+__device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, Smem& s) {
+  v = wave_sum_u64(v);
+  __syncthreads();
+  if (lane_id() == 0) s.red_q[wave_id()] = v;
+  __syncthreads();
+  uint64_t r = 0;
+  for (int w = 0; w < NW; ++w) r += s.red_q[w];
+  return r;
+}
+// (mref, s) pairs: s is relative to 2^mref
+__device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float s2) {
+  const float M = fmaxf(m, m2);
+  s = s * rel2(m, M) + s2 * rel2(m2, M);
+  m = M;
+}
+__device__ __forceinline__ void block_lse(float& m, float& s, Smem& sm) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o), s2 = __shfl_xor(s, o);
+    lse_combine(m, s, m2, s2);
+  }
+  __syncthreads();
+  if (lane_id() == 0) {
+    sm.red_f[wave_id()] = m;
+    sm.red_f[NW + wave_id()] = s;
+  }
+  __syncthreads();
+  float M = sm.red_f[0], S = sm.red_f[NW];
+  for (int w = 1; w < NW; ++w) lse_combine(M, S, sm.red_f[w], sm.red_f[NW + w]);
+  m = M;
+  s = S;
+}
+
+// Exclusive scan over the NT threads in thread order.  *total is the last thread's exclusive prefix
+// plus its own value, i.e. exactly the value a thread-serial continuation of the scan would give.
+__device__ __forceinline__ float block_excl_scan(float v, Smem& s, float* total) {
+  const int l = lane_id();
+  float incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float t = __shfl_up(incl, o);
+    if (l >= o) incl += t;
+  }
+  float excl = __shfl_up(incl, 1);
+  if (l == 0) excl = 0.0f;
+  __syncthreads();
+  if (l == 63) s.red_f[wave_id()] = incl;
+  __syncthreads();
+  float off = 0.0f;
+  for (int w = 0; w < wave_id(); ++w) off += s.red_f[w];
+  const float e = off + excl;
+  if (threadIdx.x == NT - 1) s.bc_f[3] = e + v;
+  __syncthreads();
+  *total = s.bc_f[3];
+  __syncthreads();
+  return e;
+}
+
+// Lower bound of the K-th largest of one value per thread (absent threads pass -inf): one 256-bucket
+// histogram over [min, max] of the values; for the highest bucket c whose count together with all
+// higher buckets reaches K, the smallest value in buckets >= c has at least K values at or above it.
+// Returns -inf when fewer than K values exist.
+__device__ __forceinline__ float block_kth_bound(float tz, int K, Smem& s) {
+  const bool valid = tz > -INFINITY;
+  const float hi = block_max(valid ? tz : -INFINITY, s);
+  const float lo = block_min(valid ? tz : INFINITY, s);
+  if (!(hi > -INFINITY)) return -INFINITY;
+  const float width = hi - lo;
+  const float scale = (width > 0.0f && width < INFINITY) ? 256.0f / width : 0.0f;
+  uint32_t* h = reinterpret_cast<uint32_t*>(s.hist);
+  if (threadIdx.x < 256) h[threadIdx.x] = 0;
+  __syncthreads();
+  int b = 0;
+  if (valid) {
+    const float f = (tz - lo) * scale;
+    b = f >= 255.0f ? 255 : (f > 0.0f ? (int)f : 0);
+    atomicAdd(&h[b], 1u);
+  }
+  __syncthreads();
+  if (wave_id() == 0) {
+    // lane l holds buckets 255-4l .. 252-4l (descending); inclusive scan over lanes counts from the top
+    const int l = lane_id();
+    const uint32_t c0 = h[255 - 4 * l], c1 = h[254 - 4 * l], c2 = h[253 - 4 * l], c3 = h[252 - 4 * l];
+    uint32_t incl = c0 + c1 + c2 + c3;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = __shfl_up(incl, o);
+      if (l >= o) incl += t;
+    }
+    const uint32_t excl = incl - (c0 + c1 + c2 + c3);
+    const uint64_t hit = __ballot(incl >= (uint32_t)K);
+    const int first = hit ? __ffsll((unsigned long long)hit) - 1 : -1;
+    if (l == (first < 0 ? 0 : first)) {
+      int c = -1;
+      if (first >= 0) {
+        uint32_t cum = excl;
+        if ((cum += c0) >= (uint32_t)K) c = 255 - 4 * l;
+        else if ((cum += c1) >= (uint32_t)K) c = 254 - 4 * l;
+        else if ((cum += c2) >= (uint32_t)K) c = 253 - 4 * l;
+        else c = 252 - 4 * l;
+      }
+      s.bc_i[0] = c;
+    }
+  }
+  __syncthreads();
+  const int c = s.bc_i[0];
+  if (c < 0) return -INFINITY;
+  return block_min((valid && b >= c) ? tz : INFINITY, s);
+}
+
+// ----------------------------------------------------------------------------------------------
+// Row-group synchronisation through the workspace (P > 1).  The wait is bounded: after SPIN_LIMIT
+// polls it records an error in the group's sync block and continues, so a bug cannot hang the GPU.
+// ----------------------------------------------------------------------------------------------
+__device__ __forceinline__ void group_barrier(GroupSync* gs, int P) {
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(&gs->arrive, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t target = (old / (uint32_t)P + 1u) * (uint32_t)P;
+    uint32_t spins = 0;
+    while ((int32_t)(__hip_atomic_load(&gs->arrive, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > SPIN_LIMIT) {
+        __hip_atomic_fetch_or(&gs->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// ----------------------------------------------------------------------------------------------
+// Bitonic sort of s.sk[0, npad) (npad a power of two <= LCAP)
+// ----------------------------------------------------------------------------------------------
+__device__ void bitonic_sort(Smem& s, int npad, bool descending) {
+  __syncthreads();
+  for (int size = 2; size <= npad; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = threadIdx.x; i < (npad >> 1); i += NT) {
+        const int lo = 2 * stride * (i / stride) + (i % stride);
+        const int hi = lo + stride;
+        const bool up = ((lo & size) == 0) != descending;
+        const uint64_t x = s.sk[lo], y = s.sk[hi];
+        if ((x > y) == up) {
+          s.sk[lo] = y;
+          s.sk[hi] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__device__ __forceinline__ int next_pow2(int n) {
+  int p = 2;
+  while (p < n) p <<= 1;
+  return p;
+}
+
+// A threshold bx with canon(x r) >= bl  =>  x >= bx, for r > 0 (fl(x r) is monotone in x): the
+// quotient bl / r lowered by a relative 2^-20 plus the smallest normal, which covers the rounding of
+// both the quotient and the product.
+__device__ __forceinline__ float x_threshold(float bl, float r) {
+  if (!(bl > -INFINITY)) return -INFINITY;
+  const float q = (float)((double)bl / (double)r);
+  if (!isfinite(q)) return -INFINITY;  // no useful prefilter: every slot is checked exactly
+  return q - (fabsf(q) * 9.5367431640625e-07f + 1.1754943508222875e-38f);
+}
+
+// ----------------------------------------------------------------------------------------------
+// Per-row uniform state
+// ----------------------------------------------------------------------------------------------
+struct RowState {
+  int64_t row;
+  const unsigned char* rowp;
+  int V;
+  int head;            // elements before the first 16-byte boundary of the row
+  int64_t body_slots;  // 16-byte slots after head
+  int tail_lo;         // first element after the body
+  int64_t s0, s1;      // this chunk's body slots [s0, s1)
+  int c, P;
+  bool owns_head, owns_tail;
+  bool greedy;
+  float r;             // temperature reciprocal
+  int k;
+  bool k_on, minp_on, topp_on;
+  float p, minp;
+  bool pen_on;
+  float rep, freq, pres;
+  int64_t h_lo, h_hi;
+  float u;
+  uint32_t flags;
+};
+
+template <class DT>
+__device__ __forceinline__ void row_setup(const KArgs& a, int64_t row, int c, RowState& R) {
+  R.row = row;
+  R.c = c;
+  R.P = a.P;
+  R.V = (int)a.V;
+  R.rowp = a.logits + row * a.ld * DT::ES;
+  const uint64_t addr = reinterpret_cast<uint64_t>(R.rowp);
+  int head = (int)(((16u - (uint32_t)(addr & 15u)) & 15u) / DT::ES);
+  if (head > R.V) head = R.V;
+  R.head = head;
+  R.body_slots = (R.V - head) / DT::VEC;
+  R.tail_lo = head + (int)R.body_slots * DT::VEC;
+  R.s0 = (int64_t)c * a.chunk_slots;
+  if (R.s0 > R.body_slots) R.s0 = R.body_slots;
+  R.s1 = R.s0 + a.chunk_slots;
+  if (R.s1 > R.body_slots) R.s1 = R.body_slots;
+  R.owns_head = (c == 0);
+  R.owns_tail = (c == a.P - 1);
+
+  uint32_t flags = 0;
+  const DevParams& q = a.prm;
+  float T = q.temperature ? q.temperature[row] : 1.0f;
+  const int k = q.top_k ? q.top_k[row] : 0;
+  float p = q.top_p ? q.top_p[row] : 1.0f;
+  float mp = q.min_p ? q.min_p[row] : 0.0f;
+  float rep = q.rep ? q.rep[row] : 1.0f;
+  float freq = q.freq ? q.freq[row] : 0.0f;
+  float pres = q.pres ? q.pres[row] : 0.0f;
+  if (!isfinite(T)) { flags |= FLAG_BAD_PARAM; T = 1.0f; }
+  if (isnan(p)) { flags |= FLAG_BAD_PARAM; p = 1.0f; }
+  if (isnan(mp)) { flags |= FLAG_BAD_PARAM; mp = 0.0f; }
+  if (!(rep > 0.0f) || isinf(rep)) { flags |= FLAG_BAD_PARAM; rep = 1.0f; }
+  if (!isfinite(freq)) { flags |= FLAG_BAD_PARAM; freq = 0.0f; }
+  if (!isfinite(pres)) { flags |= FLAG_BAD_PARAM; pres = 0.0f; }
+  R.greedy = T < 1e-5f;
+  if (R.greedy) flags |= FLAG_GREEDY;
+  R.r = R.greedy ? 1.0f : (float)(1.0 / (double)T);
+  R.k = k;
+  R.k_on = !R.greedy && k > 0 && (int64_t)k < a.V;
+  R.minp_on = !R.greedy && mp > 0.0f;
+  R.minp = mp > 1.0f ? 1.0f : mp;
+  R.topp_on = !R.greedy && p < 1.0f;
+  R.p = p;
+  R.rep = rep;
+  R.freq = freq;
+  R.pres = pres;
+  R.pen_on = false;
+  R.h_lo = R.h_hi = 0;
+  if (q.hist_offsets) {
+    const int64_t lo = q.hist_offsets[row], hi = q.hist_offsets[row + 1];
+    if (lo < 0 || hi < lo || hi > q.hist_len) {
+      flags |= FLAG_BAD_PARAM;
+    } else if (hi > lo) {
+      R.pen_on = true;
+      R.h_lo = lo;
+      R.h_hi = hi;
+    }
+  }
+  R.u = a.uniforms ? a.uniforms[row] : 0.0f;
+  R.flags = flags;
+}
+
+template <class DT, int J>
+struct Chunk {
+  uint4 d[J];
+};
+
+// Double-precision per-row scalars, kept out of line so their polynomial constants never occupy
+// registers of the streaming loop.
+struct RowDoubles {
+  double L;        // log sum_v exp(z_v - m)
+  float zfull;     // sum_v exp(z_v - m)
+  float log_minp;  // fl32(log(min_p))
+  float t0;        // top-p candidate bound (p < 1 without top-k / min-p)
+};
+
+// sum_v 2^(z_v L2E - mref) = S  =>  log sum_v e^(z_v - m) = ln S - D ln 2 with D = m L2E - mref (the
+// exact offset of the reference, in double).  The elements below t0 = m + log((1 - p) Z / (2 V))
+// carry less than (1 - p) / 2 of the mass, so the nucleus lies above t0 (lowered by a relative 1e-4
+// to absorb rounding).
+__device__ __noinline__ RowDoubles row_doubles(float mref, float S, float m, float minp, float p, int V) {
+  RowDoubles o;
+  const double D = (double)m * (double)L2E - (double)mref;
+  o.L = log((double)S) - D * 0.6931471805599453;
+  o.zfull = (float)exp(o.L);
+  o.log_minp = minp > 0.0f ? (float)log((double)minp) : 0.0f;
+  o.t0 = -INFINITY;
+  if (p < 1.0f) {
+    const double t0 = (double)m + log((1.0 - (double)p) * 0.5 * (double)o.zfull / (double)V);
+    o.t0 = (float)(t0 - 1e-4 * (1.0 + fabs(t0)));
+  }
+  return o;
+}
+
+// ----------------------------------------------------------------------------------------------
+// Per-row context shared by the resolution stages
+// ----------------------------------------------------------------------------------------------
+struct RowCtx {
+  float m;         // max processed logit z of the row
+  double L;        // log sum_v exp(z_v - m) over the full vocabulary
+  float zfull;     // sum_v exp(z_v - m)
+  float tau_m;     // min-p threshold (-inf when off)
+  float row_beta;  // K-th largest per-thread maximum of the row
+  int n_ext;       // extras in LDS
+  int n_list;      // candidates in s.sk (at the leader: union over the chunks)
+  GroupSync* gsync;
+  ChunkStats* gstats;
+  GroupRes* gres;
+  uint64_t* ghist;
+  uint64_t* glists;
+};
+
+// The outputs the out-of-line stages write, passed by value so the kernel arguments themselves never
+// have their address taken (they stay in the kernarg segment and load through the scalar unit).
+struct OutArgs {
+  int32_t mode;
+  int32_t n_top;
+  int64_t V;
+  int32_t* out_top_ids;
+  float* out_top_logprobs;
+  float* out_probs;
+};
+
+struct Resolution {
+  float tau;    // kept set S = {finite z >= tau}
+  float zs;     // sum over S of exp(z - m)
+  float zmin;   // min z over S
+  int kept;     // |S|
+  int id;       // drawn (or greedy) token
+  float zid;    // its processed logit
+  int id_here;  // this workgroup writes out_ids / out_logprobs
+};
+
+// Iterate over the extras held in LDS (strided over threads).  BODY sees x and pos.
+#define FOR_EXTRAS(S, NX, BODY)                                                                 \
+  for (int xi_ = threadIdx.x; xi_ < (NX); xi_ += NT) {                                        \
+    const float x = (S).x_val[xi_];                                                             \
+    const int pos = (S).x_pos[xi_];                                                             \
+    BODY                                                                                        \
+  }
+
+// Re-read one body slot of the chunk from memory with the penalised entries masked to -inf (their
+// values are in the extras).  Used by the stages that run after the registers are released.
+template <class DT>
+__device__ __forceinline__ uint4 load_masked(const RowState& R, const Smem& s, int64_t slot) {
+  const uint4* body = reinterpret_cast<const uint4*>(R.rowp + (int64_t)R.head * DT::ES);
+  uint4 d = body[slot];
+  if (R.pen_on) {
+    const int sl = (int)(slot - R.s0);
+    const uint32_t byte = (s.bitmap[sl >> 2] >> ((sl & 3) * 8)) & 255u;
+    const uint4 mk = s.masktab[byte];
+    d.x = (d.x & ~mk.x) | (DT::NEG & mk.x);
+    d.y = (d.y & ~mk.y) | (DT::NEG & mk.y);
+    d.z = (d.z & ~mk.z) | (DT::NEG & mk.z);
+    d.w = (d.w & ~mk.w) | (DT::NEG & mk.w);
+  }
+  return d;
+}
+
+// Iterate over the chunk's body elements re-read from memory.  BODY sees x and pos.
+#define FOR_MEM_ELEMS(R, S, BODY)                                                               \
+  for (int64_t slot_ = (R).s0 + threadIdx.x; slot_ < (R).s1; slot_ += NT) {                    \
+    const uint4 d_ = load_masked<DT>((R), (S), slot_);                                          \
+    _Pragma("unroll") for (int e_ = 0; e_ < DT::VEC; ++e_) {                                    \
+      const float x = DT::get(d_, e_);                                                          \
+      const int pos = (R).head + (int)slot_ * DT::VEC + e_;                                     \
+      BODY                                                                                      \
+    }                                                                                           \
+  }
+
+__device__ __forceinline__ uint32_t hash_of(int id) { return ((uint32_t)id * 2654435761u) >> (32 - LOG2_HCAP); }
+
+// Count one occurrence of `id` (inc 0 registers the id without counting).  Distinct ids beyond UCAP
+// are counted in the table but not tracked: their logit keeps its unpenalised value (FLAG_LIMIT).
+__device__ __forceinline__ void hash_insert(Smem& s, int id, uint32_t inc) {
+  uint32_t h = hash_of(id);
+  for (int probe = 0; probe < HCAP; ++probe) {
+    const int prev = atomicCAS(&s.h_key[h], -1, id);
+    if (prev == -1) {
+      const int u = atomicAdd(&s.n_uniq, 1);
+      if (u < UCAP) s.u_slot[u] = (uint16_t)h;
+      else atomicOr(&s.flags, FLAG_LIMIT);
+      if (inc) atomicAdd(&s.h_cnt[h], inc);
+      return;
+    }
+    if (prev == id) {
+      if (inc) atomicAdd(&s.h_cnt[h], inc);
+      return;
+    }
+    h = (h + 1) & (HCAP - 1);
+  }
+  atomicOr(&s.flags, FLAG_LIMIT);
+}
+
+// The logit at any position of the row as the resolution sees it: the extras value for a tracked
+// penalised or head/tail entry, the raw value otherwise.
+template <class DT>
+__device__ __forceinline__ float x_at(const Smem& s, const RowState& R, int n_ext, int pos) {
+  const float raw = DT::load1(R.rowp, pos);
+  if (n_ext == 0) return raw;
+  bool look = pos < R.head || pos >= R.tail_lo;
+  if (!look && R.pen_on) {
+    const int64_t slot = (pos - R.head) / DT::VEC;
+    if (slot >= R.s0 && slot < R.s1) {
+      const int sl = (int)(slot - R.s0);
+      const int e = (pos - R.head) - (int)slot * DT::VEC;
+      look = (s.bitmap[sl >> 2] >> ((sl & 3) * 8 + e)) & 1u;
+    }
+  }
+  if (!look) return raw;
+  uint32_t h = hash_of(pos);
+  for (int probe = 0; probe < HCAP; ++probe) {
+    const int k = s.h_key[h];
+    if (k == pos) {
+      const int xi = s.h_xi[h];
+      return xi < n_ext ? s.x_val[xi] : raw;
+    }
+    if (k == -1) break;
+    h = (h + 1) & (HCAP - 1);
+  }
+  return raw;
+}
+
+// Gather the n_top-candidate list (or any list) above `bl` into s.sk; returns the count (may
+// exceed LCAP, in which case the list is incomplete).
+template <class DT>
+__device__ int gather_mem(Smem& s, const RowState& R, int n_ext, float bl, bool strict) {
+  __syncthreads();
+  if (threadIdx.x == 0) s.n_list = 0;
+  __syncthreads();
+  const float r = R.r;
+  FOR_MEM_ELEMS(R, s, {
+    const float z = canon(x, r);
+    if (z > -INFINITY && (strict ? z > bl : z >= bl)) {
+      const int idx = atomicAdd(&s.n_list, 1);
+      if (idx < LCAP) s.sk[idx] = cand_key(z, pos);
+    }
+  })
+  FOR_EXTRAS(s, n_ext, {
+    const float z = canon(x, r);
+    if (z > -INFINITY && (strict ? z > bl : z >= bl)) {
+      const int idx = atomicAdd(&s.n_list, 1);
+      if (idx < LCAP) s.sk[idx] = cand_key(z, pos);
+    }
+  })
+  __syncthreads();
+  return s.n_list;
+}
+
+// Union of the chunk lists at the leader (P > 1).  Every chunk passes its own count; returns the
+// total and whether any chunk (or the union) overflowed.  On return the leader holds the union in
+// s.sk[0, total) when there is no overflow.
+__device__ int union_lists(Smem& s, const RowState& R, const RowCtx& X, int n_own, bool& overflow) {
+  const int P = R.P, c = R.c;
+  if (threadIdx.x == 0) {
+    st_agent(&X.gstats[c].n_list, (int32_t)n_own);
+    st_agent(&X.gstats[c].overflow, (int32_t)overflow);
+  }
+  if (!overflow)
+    for (int i = threadIdx.x; i < n_own; i += NT) st_agent(&X.glists[(int64_t)c * LCAP + i], s.sk[i]);
+  group_barrier(X.gsync, P);
+  int tot = 0;
+  bool of = false;
+  for (int q = 0; q < P; ++q) {
+    tot += ld_agent(&X.gstats[q].n_list);
+    of = of || ld_agent(&X.gstats[q].overflow) != 0;
+  }
+  overflow = of || tot > LCAP;
+  if (!overflow && c == 0) {
+    int off = 0;
+    for (int q = 0; q < P; ++q) {
+      const int nq = ld_agent(&X.gstats[q].n_list);
+      if (q > 0)
+        for (int i = threadIdx.x; i < nq; i += NT) s.sk[off + i] = ld_agent(&X.glists[(int64_t)q * LCAP + i]);
+      off += nq;
+    }
+  }
+  // every chunk has read the counts before any of them reuses the slots
+  group_barrier(X.gsync, P);
+  return tot;
+}
+
+// Sort s.sk[0, n) descending (z desc, position asc) and write the n_top outputs of the row.
+__device__ void write_top_n(const OutArgs& a, Smem& s, const RowCtx& X, int64_t row, int n) {
+  const int npad = next_pow2(n);
+  for (int i = n + threadIdx.x; i < npad; i += NT) s.sk[i] = 0;
+  bitonic_sort(s, npad, true);
+  for (int t = threadIdx.x; t < a.n_top; t += NT) {
+    const int64_t o = row * a.n_top + t;
+    if (t < n) {
+      a.out_top_ids[o] = cand_pos(s.sk[t]);
+      a.out_top_logprobs[o] = (float)((double)cand_z(s.sk[t]) - (double)X.m - X.L);
+    } else {
+      a.out_top_ids[o] = -1;
+      a.out_top_logprobs[o] = -INFINITY;
+    }
+  }
+  __syncthreads();
+}
+
+// ----------------------------------------------------------------------------------------------
+// Radix selection over the chunk (re-read from memory) and the extras (general path).
+// Finds the largest key K such that the weight of eligible elements (finite z >= zlo) with
+// key(z) >= K reaches the target; weights are counts (wmode 0) or fixed-point masses
+// 2^32 * exp(z - m) (wmode 1).  A negative target means (-target) * (total eligible weight).
+// Returns false when the target is not reached.  Uniform across the chunks of a row.
+// ----------------------------------------------------------------------------------------------
+template <class DT>
+__device__ bool radix_select(Smem& s, const RowState& R, const RowCtx& X, float zlo, int wmode, double target,
+                             uint32_t& out_key) {
+  uint32_t prefix = 0;
+  uint64_t above = 0;
+  double tgt = target;
+  const float r = R.r, m = X.m;
+  const int P = R.P;
+#pragma unroll 1
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    __syncthreads();
+    if (threadIdx.x < 256) s.hist[threadIdx.x] = 0;
+    __syncthreads();
+    const uint32_t hi_mask = (shift == 24) ? 0u : (0xffffffffu << (shift + 8));
+    FOR_MEM_ELEMS(R, s, {
+      const float z = canon(x, r);
+      if (z > -INFINITY && z >= zlo) {
+        const uint32_t kz = f2key(z);
+        if ((kz & hi_mask) == (prefix & hi_mask)) {
+          const uint64_t wgt = wmode ? fixmass(__expf(z - m)) : 1ull;
+          atomicAdd((unsigned long long*)&s.hist[(kz >> shift) & 255u], (unsigned long long)wgt);
+        }
+      }
+    })
+    FOR_EXTRAS(s, X.n_ext, {
+      const float z = canon(x, r);
+      if (z > -INFINITY && z >= zlo) {
+        const uint32_t kz = f2key(z);
+        if ((kz & hi_mask) == (prefix & hi_mask)) {
+          const uint64_t wgt = wmode ? fixmass(__expf(z - m)) : 1ull;
+          atomicAdd((unsigned long long*)&s.hist[(kz >> shift) & 255u], (unsigned long long)wgt);
+        }
+      }
+    })
+    __syncthreads();
+    if (P > 1) {
+      if (threadIdx.x < 256) st_agent(&X.ghist[(int64_t)R.c * 256 + threadIdx.x], s.hist[threadIdx.x]);
+      group_barrier(X.gsync, P);
+      uint64_t v = 0;
+      if (threadIdx.x < 256)
+        for (int q = 0; q < P; ++q) v += ld_agent(&X.ghist[(int64_t)q * 256 + threadIdx.x]);
+      group_barrier(X.gsync, P);  // every chunk has read before anyone writes the next round
+      if (threadIdx.x < 256) s.hist[threadIdx.x] = v;
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+      if (tgt < 0) {  // the first round sees every eligible element: resolve the fractional target
+        uint64_t tt = 0;
+        for (int d = 0; d < 256; ++d) tt += s.hist[d];
+        tgt = (double)tt * (-tgt);
+      }
+      uint64_t cum = above;
+      int d = 255;
+      for (; d >= 0; --d) {
+        if ((double)(cum + s.hist[d]) >= tgt) break;
+        cum += s.hist[d];
+      }
+      s.bc_i[0] = d;
+      s.bc_q[0] = cum;
+      s.bc_q[1] = (uint64_t)__double_as_longlong(tgt);
+    }
+    __syncthreads();
+    const int d = s.bc_i[0];
+    above = s.bc_q[0];
+    tgt = __longlong_as_double((long long)s.bc_q[1]);
+    __syncthreads();
+    if (d < 0) return false;
+    prefix |= (uint32_t)d << shift;
+  }
+  out_key = prefix;
+  return true;
+}
+
+// ----------------------------------------------------------------------------------------------
+// List path for at most 64 candidates: one wave, one entry per lane, shuffles only (no barriers).
+// Same definitions as resolve_list below; the result lands in res of every lane of wave 0.
+// ----------------------------------------------------------------------------------------------
+__device__ __forceinline__ void resolve_list_wave(const OutArgs& a, Smem& s, const RowState& R, const RowCtx& X,
+                                                  Resolution& res) {
+  const int l = lane_id();
+  const int n = X.n_list;
+  const float m = X.m;
+  uint64_t key = l < n ? s.sk[l] : 0ull;
+  key = wave_sort_u64(key, true);  // descending z, then ascending position
+  const float z = l < n ? cand_z(key) : -INFINITY;
+  const int pos = l < n ? cand_pos(key) : -1;
+  const float w = l < n ? __expf(z - m) : 0.f;
+  int nS;
+  if (R.greedy) {
+    nS = 1;
+  } else {
+    float tau2 = X.tau_m;
+    if (R.k_on && R.k <= n) tau2 = fmaxf(tau2, __shfl(z, R.k - 1));
+    const bool in2 = l < n && z >= tau2;
+    const int n2 = __popcll(__ballot(in2));  // S2 is a prefix of the descending list
+    nS = n2;
+    if (R.topp_on) {
+      const float c = wave_incl_scan(in2 ? w : 0.f);
+      const float Z2 = (R.k_on || R.minp_on) ? __shfl(c, n2 - 1) : X.zfull;
+      const float target = R.p * Z2;
+      const uint64_t hit = __ballot(in2 && c >= target);
+      if (hit) {  // the nucleus closes at the end of that tie group
+        const float zc = __shfl(z, __ffsll((unsigned long long)hit) - 1);
+        nS = __popcll(__ballot(l < n2 && z >= zc));
+      }
+    }
+  }
+  res.kept = nS;
+  res.zmin = __shfl(z, nS - 1);
+  res.tau = res.zmin;
+  res.zs = __shfl(wave_incl_scan(l < nS ? w : 0.f), nS - 1);
+  res.id_here = 1;
+  if (a.mode == 0 && a.n_top > 0 && l < a.n_top) {
+    const int64_t o = R.row * a.n_top + l;
+    a.out_top_ids[o] = l < n ? pos : -1;
+    a.out_top_logprobs[o] = l < n ? (float)((double)z - (double)m - X.L) : -INFINITY;
+  }
+  if (R.greedy) {
+    res.id = __shfl(pos, 0);
+    res.zid = __shfl(z, 0);
+  } else if (a.mode == 0) {
+    // inverse CDF in ascending token id over the kept prefix
+    uint64_t k2 = l < nS ? (((uint64_t)(uint32_t)pos << 32) | (uint32_t)l) : ~0ull;
+    k2 = wave_sort_u64(k2, false);
+    const int src = l < nS ? (int)(uint32_t)k2 : 0;
+    const float ws = l < nS ? __shfl(w, src) : 0.f;
+    const float c2 = wave_incl_scan(ws);
+    const float t = R.u * __shfl(c2, nS - 1);
+    const uint64_t hit = __ballot(l < nS && c2 > t);
+    int sel;
+    if (hit) {
+      sel = __ffsll((unsigned long long)hit) - 1;
+    } else {  // rounding left the cumulative at u: the last positive weight
+      const uint64_t pz = __ballot(l < nS && ws > 0.f);
+      sel = pz ? 63 - __clzll((long long)pz) : -1;
+    }
+    if (sel >= 0) {
+      res.id = (int)(__shfl(k2, sel) >> 32);
+      res.zid = __shfl(z, __shfl(src, sel));
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------------------------
+// List path: exact resolution on the sorted candidate list (leader workgroup only)
+// ----------------------------------------------------------------------------------------------
+__device__ __noinline__ void resolve_list(const OutArgs a, Smem& s, const RowState R, const RowCtx X,
+                                          Resolution& res) {
+  const int n = X.n_list;
+  const float m = X.m;
+  const int npad = next_pow2(n);
+  for (int i = n + threadIdx.x; i < npad; i += NT) s.sk[i] = 0;  // key 0 sorts last
+  bitonic_sort(s, npad, true);  // descending z, then ascending position
+  for (int i = threadIdx.x; i < n; i += NT) {
+    const float z = cand_z(s.sk[i]);
+    s.l_z[i] = z;
+    s.l_p[i] = cand_pos(s.sk[i]);
+    s.l_w[i] = __expf(z - m);
+  }
+  __syncthreads();
+  // thread t owns entries [EPT t, EPT t + EPT) in every scan below (fixed structure); an entry's
+  // cumulative is the thread's exclusive prefix plus the serial sum of its own entries
+  const int i0 = EPT * (int)threadIdx.x;
+  float cm[EPT];
+  int nS;
+  if (R.greedy) {
+    nS = 1;
+  } else {
+    float tau2 = X.tau_m;
+    if (R.k_on && R.k <= n) tau2 = fmaxf(tau2, s.l_z[R.k - 1]);
+    int loc = 0;
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) loc += (i0 + q < n && s.l_z[i0 + q] >= tau2) ? 1 : 0;
+    const int n2 = block_sum_i(loc, s);  // S2 is a prefix of the descending list
+    nS = n2;
+    if (R.topp_on) {
+      float ts = 0.f;
+#pragma unroll
+      for (int q = 0; q < EPT; ++q) ts += (i0 + q < n2) ? s.l_w[i0 + q] : 0.f;
+      float tot;
+      float cum = block_excl_scan(ts, s, &tot);
+#pragma unroll
+      for (int q = 0; q < EPT; ++q) {
+        cum += (i0 + q < n2) ? s.l_w[i0 + q] : 0.f;
+        cm[q] = cum;
+        if (i0 + q == n2 - 1) s.bc_f[0] = cum;  // Z2: cumulative at the last S2 entry
+      }
+      __syncthreads();
+      const float Z2 = (R.k_on || R.minp_on) ? s.bc_f[0] : X.zfull;
+      const float target = R.p * Z2;
+      int first = INT32_MAX;
+#pragma unroll
+      for (int q = 0; q < EPT; ++q)
+        if (first == INT32_MAX && i0 + q < n2 && cm[q] >= target) first = i0 + q;
+      first = block_min_i(first, s);
+      if (first != INT32_MAX) {  // the nucleus closes at the end of that tie group
+        const float zc = s.l_z[first];
+        int cnt = 0;
+#pragma unroll
+        for (int q = 0; q < EPT; ++q) cnt += (i0 + q < n2 && s.l_z[i0 + q] >= zc) ? 1 : 0;
+        nS = block_sum_i(cnt, s);
+      }
+    }
+  }
+  res.kept = nS;
+  res.zmin = s.l_z[nS - 1];
+  res.tau = res.zmin;
+  {
+    float ts = 0.f;
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) ts += (i0 + q < nS) ? s.l_w[i0 + q] : 0.f;
+    float tot;
+    float cum = block_excl_scan(ts, s, &tot);
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      cum += (i0 + q < nS) ? s.l_w[i0 + q] : 0.f;
+      if (i0 + q == nS - 1) s.bc_f[1] = cum;
+    }
+    __syncthreads();
+    res.zs = s.bc_f[1];
+  }
+  res.id_here = 1;
+  if (R.greedy) {
+    res.id = s.l_p[0];
+    res.zid = s.l_z[0];
+  } else if (a.mode == 0) {
+    // inverse CDF in ascending token id over the kept prefix: sort (position, index) pairs
+    const int npS = next_pow2(nS);
+    __syncthreads();
+    for (int i = threadIdx.x; i < npS; i += NT)
+      s.sk[i] = i < nS ? (((uint64_t)(uint32_t)s.l_p[i] << 32) | (uint32_t)i) : ~0ull;
+    bitonic_sort(s, npS, false);
+    float wv[EPT];
+    float ts = 0.f;
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      wv[q] = (i0 + q < nS) ? s.l_w[(uint32_t)s.sk[i0 + q]] : 0.f;
+      ts += wv[q];
+    }
+    float tot;
+    float cum = block_excl_scan(ts, s, &tot);
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      cum += wv[q];
+      cm[q] = cum;
+      if (i0 + q == nS - 1) s.bc_f[2] = cum;  // the id-order total
+    }
+    __syncthreads();
+    const float t = R.u * s.bc_f[2];
+    int first = INT32_MAX;
+#pragma unroll
+    for (int q = 0; q < EPT; ++q)
+      if (first == INT32_MAX && i0 + q < nS && cm[q] > t) first = i0 + q;
+    first = block_min_i(first, s);
+    if (first == INT32_MAX) {  // rounding left the cumulative at u: the last positive weight
+      int last = -1;
+#pragma unroll
+      for (int q = 0; q < EPT; ++q)
+        if (i0 + q < nS && wv[q] > 0.f) last = i0 + q;
+      first = block_max_i(last, s);
+    }
+    if (first >= 0) {
+      const int di = (int)(uint32_t)s.sk[first];
+      res.id = s.l_p[di];
+      res.zid = s.l_z[di];
+    }
+  }
+  // top-n straight from the descending list
+  if (a.mode == 0 && a.n_top > 0) {
+    for (int t = threadIdx.x; t < a.n_top; t += NT) {
+      const int64_t o = R.row * a.n_top + t;
+      if (t < n) {
+        a.out_top_ids[o] = s.l_p[t];
+        a.out_top_logprobs[o] = (float)((double)s.l_z[t] - (double)m - X.L);
+      } else {
+        a.out_top_ids[o] = -1;
+        a.out_top_logprobs[o] = -INFINITY;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// ----------------------------------------------------------------------------------------------
+// General path (every chunk of the row): thresholds by radix selection, draw through an id-ordered
+// weight buffer in the workspace, top-n by a separate candidate list (selection for massive ties)
+// ----------------------------------------------------------------------------------------------
+template <class DT>
+__device__ __noinline__ void resolve_general(const OutArgs a, Smem& s, const RowState R, const RowCtx X,
+                                             Resolution& res) {
+  const float r = R.r, m = X.m;
+  const int P = R.P, c = R.c;
+  const bool leader = c == 0;
+  const int n_ext = X.n_ext;
+  float tau_star;
+  if (R.greedy) {
+    tau_star = m;
+  } else {
+    float tau2 = X.tau_m;
+    uint32_t kk = 0;
+    if (R.k_on && radix_select<DT>(s, R, X, -INFINITY, 0, (double)R.k, kk)) tau2 = fmaxf(tau2, key2f(kk));
+    tau_star = tau2;
+    if (R.topp_on && radix_select<DT>(s, R, X, tau2, 1, -(double)R.p, kk)) tau_star = fmaxf(tau_star, key2f(kk));
+  }
+  // kept count, min z and fixed-point mass of S = {finite z >= tau_star}; greedy argmax position
+  int kept = 0, best = INT32_MAX;
+  float zmin = INFINITY;
+  uint64_t zsx = 0;
+  FOR_MEM_ELEMS(R, s, {
+    const float z = canon(x, r);
+    if (z > -INFINITY && z >= tau_star) {
+      ++kept;
+      zmin = fminf(zmin, z);
+      zsx += fixmass(__expf(z - m));
+      if (z == m && pos < best) best = pos;
+    }
+  })
+  FOR_EXTRAS(s, n_ext, {
+    const float z = canon(x, r);
+    if (z > -INFINITY && z >= tau_star) {
+      ++kept;
+      zmin = fminf(zmin, z);
+      zsx += fixmass(__expf(z - m));
+      if (z == m && pos < best) best = pos;
+    }
+  })
+  kept = block_sum_i(kept, s);
+  zmin = block_min(zmin, s);
+  zsx = block_sum_u64(zsx, s);
+  best = block_min_i(best, s);
+  // draw: blocked scans in ascending id over this chunk's region [lo, hi), reading the logits back
+  const int64_t lo = R.owns_head ? 0 : (int64_t)R.head + R.s0 * DT::VEC;
+  const int64_t hi = R.owns_tail ? (int64_t)R.V : (int64_t)R.head + R.s1 * DT::VEC;
+  const bool draw = (a.mode == 0) && !R.greedy;
+  // 4 consecutive entries per thread per block.  An element's cumulative is
+  // run + (exclusive thread prefix + serial sum within the thread); the block total is the last
+  // thread's value of that expression, so a block whose total exceeds the target contains an element
+  // that does too.
+  float ctot = 0.f;
+  int clast = -1;
+  auto scan_find = [&](float target) -> int {
+    float run = 0.f;
+    int found = -1;
+    int lastp = -1;
+    for (int64_t b0 = lo; b0 < hi; b0 += 4 * NT) {
+      float w4[4];
+      float ts = 0.f;
+      int lp = -1;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t i = b0 + 4 * (int64_t)threadIdx.x + q;
+        float w = 0.f;
+        if (i < hi) {
+          const float z = canon(x_at<DT>(s, R, n_ext, (int)i), r);
+          w = (z > -INFINITY && z >= tau_star) ? __expf(z - m) : 0.f;
+        }
+        w4[q] = w;
+        ts += w;
+        if (w > 0.f) lp = (int)i;
+      }
+      float btot;
+      const float ex = block_excl_scan(ts, s, &btot);
+      lastp = max(lastp, block_max_i(lp, s));
+      if (found < 0 && run + btot > target) {
+        float cum = ex;
+        int f = INT32_MAX;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          cum += w4[q];
+          if (f == INT32_MAX && run + cum > target) f = (int)(b0 + 4 * (int64_t)threadIdx.x + q);
+        }
+        f = block_min_i(f, s);
+        found = (f == INT32_MAX) ? -1 : f;
+      }
+      run += btot;
+    }
+    ctot = run;
+    clast = lastp;
+    return found;
+  };
+  if (draw) (void)scan_find(INFINITY);
+  // per-chunk results, combined in chunk order (identical arithmetic in every chunk)
+  float cum_before = 0.f, row_tot = ctot;
+  int kept_row = kept, last_row = clast, best_row = best, c_star = -1;
+  float zmin_row = zmin;
+  uint64_t zsx_row = zsx;
+  if (P > 1) {
+    if (threadIdx.x == 0) {
+      st_agent(&X.gstats[c].w_total, ctot);
+      st_agent(&X.gstats[c].last_pos, (int32_t)clast);
+      st_agent(&X.gstats[c].n_keep, (int32_t)kept);
+      st_agent(&X.gstats[c].zmin, zmin);
+      st_agent(&X.gstats[c].zs_fix, zsx);
+      st_agent(&X.gstats[c].best, (int32_t)best);
+    }
+    group_barrier(X.gsync, P);
+    float cum = 0.f;
+    float cums[MAXP];
+    kept_row = 0;
+    zmin_row = INFINITY;
+    last_row = -1;
+    best_row = INT32_MAX;
+    zsx_row = 0;
+    for (int q = 0; q < P; ++q) {
+      cum = cum + ld_agent(&X.gstats[q].w_total);
+      cums[q] = cum;
+      kept_row += ld_agent(&X.gstats[q].n_keep);
+      zmin_row = fminf(zmin_row, ld_agent(&X.gstats[q].zmin));
+      last_row = max(last_row, (int)ld_agent(&X.gstats[q].last_pos));
+      best_row = min(best_row, (int)ld_agent(&X.gstats[q].best));
+      zsx_row += ld_agent(&X.gstats[q].zs_fix);
+    }
+    row_tot = cum;
+    const float tt = R.u * row_tot;
+    for (int q = 0; q < P; ++q)
+      if (c_star < 0 && cums[q] > tt) c_star = q;
+    cum_before = c > 0 ? cums[c - 1] : 0.f;
+    group_barrier(X.gsync, P);  // stats read before the top-n stage reuses them
+  } else {
+    c_star = (ctot > R.u * ctot) ? 0 : -1;
+  }
+  res.tau = tau_star;
+  res.kept = kept_row;
+  res.zmin = zmin_row;
+  res.zs = (float)((double)zsx_row / FIX_SCALE);
+  res.id_here = 0;
+  if (R.greedy) {
+    res.id = best_row;
+    res.zid = m;
+    res.kept = 1;
+    res.zmin = m;
+    res.tau = m;
+    res.zs = 1.0f;
+    res.id_here = leader;
+  } else if (draw) {
+    const float tt = R.u * row_tot;
+    int idf = -1;
+    if (c == c_star) {
+      idf = scan_find(tt - cum_before);
+      if (idf < 0) idf = clast;  // rounding inside the chunk: its last positive weight
+    } else if (c_star < 0 && clast >= 0 && clast == last_row) {
+      idf = clast;  // rounding beyond the row total: the row's last positive weight
+    }
+    if (idf >= 0) {
+      res.id = idf;
+      res.zid = canon(x_at<DT>(s, R, n_ext, idf), r);
+      res.id_here = 1;
+    }
+  }
+  // top-n: the n_top largest (z desc, position asc)
+  if (a.mode == 0 && a.n_top > 0) {
+    const int nt = a.n_top;
+    const float bl = X.row_beta;
+    bool tover = !(bl > -INFINITY);
+    int nl = tover ? 0 : gather_mem<DT>(s, R, n_ext, bl, false);
+    tover = tover || nl > LCAP;
+    if (P > 1) nl = union_lists(s, R, X, nl, tover);
+    if (tover) {
+      // selection: tau_n = n-th largest z, the entries strictly above it, then ties by position
+      uint32_t kk = 0;
+      const bool ok = radix_select<DT>(s, R, X, -INFINITY, 0, (double)nt, kk);
+      const float tau_n = ok ? key2f(kk) : -INFINITY;
+      int ngt = gather_mem<DT>(s, R, n_ext, tau_n, true);  // fewer than nt entries
+      if (P > 1) {
+        bool of2 = false;
+        ngt = union_lists(s, R, X, ngt, of2);
+      }
+      int last = -1;
+      for (int q = ngt; q < nt; ++q) {
+        int bp = INT32_MAX;
+        if (tau_n > -INFINITY) {
+          FOR_MEM_ELEMS(R, s, {
+            if (canon(x, r) == tau_n && pos > last && pos < bp) bp = pos;
+          })
+          FOR_EXTRAS(s, n_ext, {
+            if (canon(x, r) == tau_n && pos > last && pos < bp) bp = pos;
+          })
+        }
+        bp = block_min_i(bp, s);
+        if (P > 1) {
+          if (threadIdx.x == 0) st_agent(&X.gstats[c].last_pos, (int32_t)bp);
+          group_barrier(X.gsync, P);
+          int b2 = INT32_MAX;
+          for (int qq = 0; qq < P; ++qq) b2 = min(b2, (int)ld_agent(&X.gstats[qq].last_pos));
+          bp = b2;
+          group_barrier(X.gsync, P);
+        }
+        if (bp == INT32_MAX) break;
+        if (leader && threadIdx.x == 0) s.sk[q] = cand_key(tau_n, bp);
+        __syncthreads();
+        last = bp;
+        ngt = q + 1;
+      }
+      nl = ngt;
+    }
+    if (leader) write_top_n(a, s, X, R.row, min(nl, LCAP));
+  }
+  __syncthreads();
+}
+
+// ----------------------------------------------------------------------------------------------
+// Dense filtered distribution (albireo_topk_topp), written by every chunk from memory
+// ----------------------------------------------------------------------------------------------
+template <class DT>
+__device__ __noinline__ void dense_probs(const OutArgs a, Smem& s, const RowState R, const RowCtx X,
+                                         Resolution res, bool skip, bool broadcast) {
+  if (broadcast) {  // list path with P > 1: the leader resolved alone
+    if (R.c == 0 && threadIdx.x == 0) {
+      st_agent(&X.gres->tau, res.tau);
+      st_agent(&X.gres->zs, res.zs);
+      st_agent(&X.gres->id, (int32_t)res.id);
+    }
+    group_barrier(X.gsync, R.P);
+    res.tau = ld_agent(&X.gres->tau);
+    res.zs = ld_agent(&X.gres->zs);
+    res.id = ld_agent(&X.gres->id);
+    group_barrier(X.gsync, R.P);
+  }
+  float* orow = a.out_probs + R.row * a.V;
+  const float r = R.r, m = X.m;
+  const float inv = (skip || !(res.zs > 0.f)) ? 0.f : 1.0f / res.zs;
+  const float tau = res.tau;
+  const int id = res.id;
+  const bool greedy = R.greedy;
+  FOR_MEM_ELEMS(R, s, {
+    const float z = canon(x, r);
+    float pr = 0.f;
+    if (!skip) {
+      if (greedy) pr = (pos == id) ? 1.0f : 0.f;
+      else if (z > -INFINITY && z >= tau) pr = __expf(z - m) * inv;
+    }
+    orow[pos] = pr;
+  })
+  __threadfence_block();
+  __syncthreads();
+  FOR_EXTRAS(s, X.n_ext, {  // penalised body entries overwrite; head/tail entries are written here
+    const float z = canon(x, r);
+    float pr = 0.f;
+    if (!skip) {
+      if (greedy) pr = (pos == id) ? 1.0f : 0.f;
+      else if (z > -INFINITY && z >= tau) pr = __expf(z - m) * inv;
+    }
+    orow[pos] = pr;
+  })
+  __syncthreads();
+}
+
+// ----------------------------------------------------------------------------------------------
+// The sampling kernel (mode 0) / filtered-distribution kernel (mode 1)
+// ----------------------------------------------------------------------------------------------
+// One row chunk end to end.  MULTI selects the build for P > 1 chunks per row (cross-workgroup
+// exchanges through the workspace); the single-chunk build has none of that code.
+template <class DT, int J, bool MULTI>
+__device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, int64_t row, int c) {
+  const int P = MULTI ? a.P : 1;
+  const bool leader = (c == 0);
+  {
+    RowState R;
+    row_setup<DT>(a, row, c, R);
+    R.P = P;
+    const bool extras_any = R.pen_on || (R.owns_head && R.head > 0) || (R.owns_tail && R.tail_lo < R.V);
+
+    // ---------------- history ids first (so waiting for them never waits for the row) ----------------
+    // Issued unconditionally in straight-line code (a zero-size range when penalties are off reads
+    // nothing), so the copy to LDS below waits for these loads only, not for the row.
+    constexpr int HPT = 4;  // history ids per thread staged through registers; longer histories loop
+    int hreg[HPT];
+    const int nh = (int)(R.h_hi - R.h_lo);
+    {
+      const uint64_t hb = reinterpret_cast<uint64_t>(R.pen_on ? a.prm.hist_ids + R.h_lo : a.prm.hist_ids);
+      const uint32_t hb_lo = __builtin_amdgcn_readfirstlane((uint32_t)hb);
+      const uint32_t hb_hi = __builtin_amdgcn_readfirstlane((uint32_t)(hb >> 32));
+      const int hrec = __builtin_amdgcn_readfirstlane(!R.pen_on ? 0 : (nh < HPT * NT ? nh * 4 : HPT * NT * 4));
+      const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
+          reinterpret_cast<void*>(((uint64_t)hb_hi << 32) | hb_lo), (short)0, hrec, 0x00020000);
+#pragma unroll
+      for (int q = 0; q < HPT; ++q)
+        hreg[q] = __builtin_amdgcn_raw_buffer_load_b32(hrs, ((int)threadIdx.x + q * NT) * 4, 0, 0);
+    }
+
+    // ---------------- issue every load of the chunk ----------------
+    Chunk<DT, J> ch;
+    {
+      // one buffer resource per chunk (SGPRs), a 32-bit lane offset (one VGPR) and the per-slot
+      // offset in soffset, so no 64-bit addresses occupy VGPRs
+      const int nslots = (int)(R.s1 - R.s0);
+      // the descriptor must live in SGPRs: make its inputs visibly wave-uniform
+      const uint64_t cb = reinterpret_cast<uint64_t>(R.rowp + ((int64_t)R.head + R.s0 * DT::VEC) * DT::ES);
+      const uint32_t cb_lo = __builtin_amdgcn_readfirstlane((uint32_t)cb);
+      const uint32_t cb_hi = __builtin_amdgcn_readfirstlane((uint32_t)(cb >> 32));
+      const int nrec = __builtin_amdgcn_readfirstlane(nslots * 16);
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          reinterpret_cast<void*>(((uint64_t)cb_hi << 32) | cb_lo), (short)0, nrec, 0x00020000);
+      // Unconditional loads with the whole offset in the range-checked VGPR operand: slots past the
+      // chunk read as 0 without touching memory and are set to -inf when consumed (only the last,
+      // partly filled slots can be affected).
+      const int voff = (int)threadIdx.x * 16;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + j * NT * 16, 0, 0);
+        ch.d[j] = make_uint4(v[0], v[1], v[2], v[3]);
+      }
+    }
+    const int jfull = __builtin_amdgcn_readfirstlane((int)(R.s1 - R.s0) / NT);  // slots 0..jfull-1 all live
+    // history ids to LDS (x_pos is free until the extras are built)
+#pragma unroll
+    for (int q = 0; q < HPT; ++q) s.x_pos[threadIdx.x + q * NT] = hreg[q];
+
+    // ---------------- history counts, penalised-slot bitmap, extras ----------------
+    __syncthreads();  // LDS of the previous row is no longer in use
+    int n_ext = 0;
+    uint32_t ext_flags = 0;
+    if (extras_any) {
+      for (int i = threadIdx.x; i < HCAP; i += NT) {
+        s.h_key[i] = -1;
+        s.h_cnt[i] = 0;
+        s.h_xi[i] = INT16_MAX;
+      }
+      if (R.pen_on)
+        for (int i = threadIdx.x; i < JMAX * NT / 4; i += NT) s.bitmap[i] = 0;
+      if (threadIdx.x == 0) {
+        s.n_uniq = 0;
+        s.flags = 0;
+      }
+      __syncthreads();
+      if (R.owns_head)
+        for (int i = threadIdx.x; i < R.head; i += NT) hash_insert(s, i, 0);
+      if (R.owns_tail)
+        for (int i = R.tail_lo + threadIdx.x; i < R.V; i += NT) hash_insert(s, i, 0);
+      if (R.pen_on) {
+        auto count_id = [&](int id) {
+          if (id < 0 || id >= R.V) {
+            atomicOr(&s.flags, FLAG_BAD_INPUT);
+            return;
+          }
+          bool mine;
+          if (id < R.head) mine = R.owns_head;
+          else if (id >= R.tail_lo) mine = R.owns_tail;
+          else {
+            const int64_t slot = (id - R.head) / DT::VEC;
+            mine = slot >= R.s0 && slot < R.s1;
+          }
+          if (mine) hash_insert(s, id, 1u);
+        };
+        for (int i = threadIdx.x; i < nh && i < HPT * NT; i += NT) count_id(s.x_pos[i]);
+        const int32_t* hid = a.prm.hist_ids;
+        for (int64_t h = R.h_lo + HPT * NT + threadIdx.x; h < R.h_hi; h += NT) count_id(hid[h]);
+      }
+      __syncthreads();
+      n_ext = min(s.n_uniq, UCAP);
+      ext_flags = s.flags;
+      // bitmap bits for the tracked penalised body entries (exactly those have an extras entry)
+      if (R.pen_on) {
+        for (int xi = threadIdx.x; xi < n_ext; xi += NT) {
+          const int hs = s.u_slot[xi];
+          const int id = s.h_key[hs];
+          if (id >= R.head && id < R.tail_lo && s.h_cnt[hs] > 0) {
+            const int64_t slot = (id - R.head) / DT::VEC;
+            const int sl = (int)(slot - R.s0);
+            const int e = (id - R.head) - (int)slot * DT::VEC;
+            atomicOr(&s.bitmap[sl >> 2], 1u << ((sl & 3) * 8 + e));
+          }
+        }
+        __syncthreads();
+      }
+    }
+
+    // ---------------- online max / sum-exp over the registers (overlaps the loads) ----------------
+    // The reference starts finite: a -inf element then gives exp2(-inf) = 0 rather than NaN, and the
+    // first finite slot always moves the reference before anything is accumulated against it.
+    float xm = -INFINITY, mref = MREF0;
+    float acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
+    const float rr = R.r;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      if (j >= jfull) {  // wave-uniform: the partly filled tail slots
+        const bool dead = j * NT + (int)threadIdx.x >= (int)(R.s1 - R.s0);
+        ch.d[j].x = dead ? DT::NEG : ch.d[j].x;
+        ch.d[j].y = dead ? DT::NEG : ch.d[j].y;
+        ch.d[j].z = dead ? DT::NEG : ch.d[j].z;
+        ch.d[j].w = dead ? DT::NEG : ch.d[j].w;
+      }
+      if (R.pen_on) {
+        const int sl = j * NT + threadIdx.x;
+        const uint32_t byte = (s.bitmap[sl >> 2] >> ((sl & 3) * 8)) & 255u;
+        const uint4 mk = s.masktab[byte];
+        ch.d[j].x = (ch.d[j].x & ~mk.x) | (DT::NEG & mk.x);
+        ch.d[j].y = (ch.d[j].y & ~mk.y) | (DT::NEG & mk.y);
+        ch.d[j].z = (ch.d[j].z & ~mk.z) | (DT::NEG & mk.z);
+        ch.d[j].w = (ch.d[j].w & ~mk.w) | (DT::NEG & mk.w);
+      }
+      float v[DT::VEC];
+#pragma unroll
+      for (int e = 0; e < DT::VEC; ++e) v[e] = DT::get(ch.d[j], e);
+      float smax = v[0];
+#pragma unroll
+      for (int e = 1; e < DT::VEC; ++e) smax = fmaxf(smax, v[e]);
+      xm = fmaxf(xm, smax);
+      // sums run over the canonical z = fl32(x r) (exactly what the logprobs are defined on), as
+      // 2^(z L2E - mref) with a reference mref in log2 units
+      const float sref = (smax * rr) * L2E;
+      if (sref > mref + 32.0f) {  // move the reference lazily: exp2 arguments stay below 32
+        const float f = __builtin_amdgcn_exp2f(mref - sref);
+        acc0 *= f;
+        acc1 *= f;
+        acc2 *= f;
+        acc3 *= f;
+        mref = sref;
+      }
+#pragma unroll
+      for (int e = 0; e < DT::VEC; e += 4) {
+        acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 0] * rr, L2E, -mref));
+        acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 1] * rr, L2E, -mref));
+        acc2 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 2] * rr, L2E, -mref));
+        acc3 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 3] * rr, L2E, -mref));
+      }
+    }
+    float ssum = (acc0 + acc1) + (acc2 + acc3);
+    // The later passes re-extract the floats from the packed registers; this opaque redefinition
+    // keeps the compiler from holding every extracted value live across the passes instead.
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+      asm volatile("" : "+v"(ch.d[j].x), "+v"(ch.d[j].y), "+v"(ch.d[j].z), "+v"(ch.d[j].w));
+
+    // maximum of this thread's register elements (a subset of the row, so the K-th largest of these
+    // per-thread maxima bounds the K-th largest z of the row from below)
+    const float tmax_z = canon(xm, R.r);
+
+    // ---------------- extras: originals from memory, penalties ----------------
+    // Their order in LDS follows the atomic insertion order, so they are merged into the row sum
+    // through an order-independent fixed-point sum below (run-to-run bit-identical results).
+    float xmx = -INFINITY;
+    if (extras_any) {
+      for (int xi = threadIdx.x; xi < n_ext; xi += NT) {
+        const int hs = s.u_slot[xi];
+        const int id = s.h_key[hs];
+        const uint32_t cnt = s.h_cnt[hs];
+        float x = DT::load1(R.rowp, id);
+        if (cnt > 0) x = penalise(x, cnt, R.rep, R.freq, R.pres);
+        s.x_pos[xi] = id;
+        s.x_val[xi] = x;
+        s.h_xi[hs] = (int16_t)xi;
+        xmx = fmaxf(xmx, x);
+        if (x != x) ext_flags |= FLAG_BAD_INPUT;
+      }
+    }
+
+    // ---------------- workgroup reduction ----------------
+    float bm = mref, bs = ssum;
+    block_lse(bm, bs, s);
+    float bxm = block_max(xm, s);
+    if (extras_any) {
+      const float bxx = block_max(xmx, s);
+      ext_flags = block_or(ext_flags, s);
+      bxm = fmaxf(bxm, bxx);
+      // reference for the extras: at or above every extras term, so each term is <= 1
+      const float eref = fmaxf(bm, (bxx * rr) * L2E);
+      uint64_t fx = 0;
+      for (int xi = threadIdx.x; xi < n_ext; xi += NT)
+        fx += fixmass(__builtin_amdgcn_exp2f(__builtin_fmaf(s.x_val[xi] * rr, L2E, -eref)));
+      fx = block_sum_u64(fx, s);
+      if (eref > bm) {
+        bs = bs * rel2(bm, eref);
+        bm = eref;
+      }
+      bs += (float)((double)fx / FIX_SCALE) * rel2(eref, bm);
+    }
+    const uint32_t bflags = R.flags | ext_flags;
+    // K-th largest per-thread maximum: at least K elements are >= it, so it bounds the K-th largest
+    // z of the row from below (K covers top-k and top-n)
+    int Ksel = R.k_on ? R.k : 0;
+    if (a.mode == 0 && a.n_top > Ksel) Ksel = a.n_top;
+    float beta_sel = -INFINITY;
+    if (Ksel > 0 && Ksel <= NT) beta_sel = block_kth_bound(tmax_z, Ksel, s);
+
+    // ---------------- combine the chunks of the row (fixed chunk order) ----------------
+    float row_xm = bxm, row_mref = bm, row_s = bs, row_beta = beta_sel;
+    uint32_t row_flags = bflags;
+    if (P > 1) {
+      if (threadIdx.x == 0) {
+        st_agent(&X.gstats[c].xm, bxm);
+        st_agent(&X.gstats[c].mref, bm);
+        st_agent(&X.gstats[c].s, bs);
+        st_agent(&X.gstats[c].flags, bflags);
+        st_agent(&X.gstats[c].beta_sel, beta_sel);
+      }
+      group_barrier(X.gsync, P);
+      row_xm = -INFINITY;
+      row_mref = -INFINITY;
+      row_s = 0.f;
+      row_beta = -INFINITY;
+      row_flags = 0;
+      for (int q = 0; q < P; ++q) {
+        row_xm = fmaxf(row_xm, ld_agent(&X.gstats[q].xm));
+        lse_combine(row_mref, row_s, ld_agent(&X.gstats[q].mref), ld_agent(&X.gstats[q].s));
+        row_beta = fmaxf(row_beta, ld_agent(&X.gstats[q].beta_sel));
+        row_flags |= ld_agent(&X.gstats[q].flags);
+      }
+    }
+
+    // ---------------- row statistics ----------------
+    const float m = canon(row_xm, R.r);
+    X.m = m;
+    const RowDoubles RD = row_doubles(row_mref, row_s, m, R.minp_on ? R.minp : 0.0f,
+                                      (R.topp_on && !R.k_on && !R.minp_on) ? R.p : 1.0f, R.V);
+    X.L = RD.L;
+    X.zfull = RD.zfull;
+    X.row_beta = row_beta;
+    X.n_ext = n_ext;
+    if (!(m > -INFINITY)) row_flags |= FLAG_EMPTY;
+    const bool bad_vals = (m == INFINITY) || isnan(row_s) || isnan(m);
+    if (bad_vals) row_flags |= FLAG_BAD_INPUT;
+    const bool skip = (row_flags & FLAG_EMPTY) || bad_vals;
+
+    // ---------------- candidate bound ----------------
+    X.tau_m = R.minp_on ? __fadd_rn(m, RD.log_minp) : -INFINITY;
+    float beta_S = -INFINITY;
+    if (R.greedy) {
+      beta_S = m;
+    } else if (R.k_on || R.minp_on) {
+      beta_S = fmaxf(R.k_on ? row_beta : -INFINITY, X.tau_m);
+    } else if (R.topp_on && R.p <= 0.9999f) {
+      beta_S = RD.t0;
+    }
+    float beta_list = beta_S;
+    if (a.mode == 0 && a.n_top > 0) beta_list = fminf(beta_list, row_beta);
+    const bool no_bound = !(beta_list > -INFINITY);
+
+    // ---------------- gather candidates z >= beta_list into the LDS list ----------------
+    if (threadIdx.x == 0) s.n_list = 0;
+    __syncthreads();
+    if (!skip && !no_bound) {
+      const float r = R.r;
+      const float bl = beta_list;
+      // canon(x r) >= bl implies x >= bx for this bx (a few ulps below bl / r; fl(x r) is monotone in
+      // x), so a slot whose maximum is below bx holds no candidate
+      const float bx = x_threshold(bl, r);
+      const int pos0 = R.head + (int)(R.s0 + threadIdx.x) * DT::VEC;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        float v[DT::VEC];
+#pragma unroll
+        for (int e = 0; e < DT::VEC; ++e) v[e] = DT::get(ch.d[j], e);
+        float smax = v[0];
+#pragma unroll
+        for (int e = 1; e < DT::VEC; ++e) smax = fmaxf(smax, v[e]);
+        if (__ballot(smax >= bx)) {
+#pragma unroll
+          for (int e = 0; e < DT::VEC; ++e) {
+            const float z = canon(v[e], r);
+            const bool cand = v[e] >= bx && z >= bl;  // absent slots hold -inf and never qualify
+            const uint64_t mask = __ballot(cand);
+            if (mask) {
+              const int ldr = __ffsll((unsigned long long)mask) - 1;
+              int base = 0;
+              if (lane_id() == ldr) base = atomicAdd(&s.n_list, __popcll(mask));
+              base = __shfl(base, ldr);
+              const int idx = base + __popcll(mask & lanemask_lt());
+              if (cand && idx < LCAP) s.sk[idx] = cand_key(z, pos0 + (j * NT) * DT::VEC + e);
+            }
+          }
+        }
+      }
+      FOR_EXTRAS(s, n_ext, {
+        const float z = canon(x, r);
+        if (z >= bl) {
+          const int idx = atomicAdd(&s.n_list, 1);
+          if (idx < LCAP) s.sk[idx] = cand_key(z, pos);
+        }
+      })
+    }
+    __syncthreads();
+    int n_list = s.n_list;
+    bool overflow = !skip && (no_bound || n_list > LCAP || n_list == 0);
+    if (P > 1) n_list = union_lists(s, R, X, n_list, overflow);
+    X.n_list = n_list;
+
+    // ---------------- resolution ----------------
+    Resolution res;
+    res.tau = INFINITY;
+    res.zs = 0.f;
+    res.zmin = -INFINITY;
+    res.kept = 0;
+    res.id = -1;
+    res.zid = -INFINITY;
+    res.id_here = leader;
+    const OutArgs oa{a.mode, a.n_top, a.V, a.out_top_ids, a.out_top_logprobs, a.out_probs};
+    if (skip) {
+      // empty row or NaN / +inf values: nothing to resolve
+    } else if (!overflow) {
+      if (leader) {
+        if (X.n_list <= 64) {
+          if (wave_id() == 0) resolve_list_wave(oa, s, R, X, res);
+          if (a.mode == 1) {  // every thread needs the kept set for the dense output
+            if (threadIdx.x == 0) {
+              s.bc_f[0] = res.tau;
+              s.bc_f[1] = res.zs;
+              s.bc_i[0] = res.id;
+            }
+            __syncthreads();
+            res.tau = s.bc_f[0];
+            res.zs = s.bc_f[1];
+            res.id = s.bc_i[0];
+          }
+          __syncthreads();
+        } else {
+          resolve_list(oa, s, R, X, res);
+        }
+      }
+    } else {
+      resolve_general<DT>(oa, s, R, X, res);
+    }
+
+    // ---------------- per-row outputs ----------------
+    if (a.mode == 0) {
+      if (skip) {
+        if (leader) {
+          if (threadIdx.x == 0) {
+            a.out_ids[row] = -1;
+            a.out_logprobs[row] = -INFINITY;
+          }
+          for (int t = threadIdx.x; t < a.n_top; t += NT) {
+            a.out_top_ids[row * a.n_top + t] = -1;
+            a.out_top_logprobs[row * a.n_top + t] = -INFINITY;
+          }
+        }
+      } else if (res.id_here && threadIdx.x == 0) {
+        a.out_ids[row] = res.id;
+        a.out_logprobs[row] = res.id >= 0 ? (float)((double)res.zid - (double)m - X.L) : -INFINITY;
+      }
+    }
+    if (leader && threadIdx.x == 0) {
+      if (a.out_flags) a.out_flags[row] = row_flags;
+      if (a.mode == 1) {
+        if (a.out_threshold) a.out_threshold[row] = skip ? -INFINITY : res.zmin;
+        if (a.out_kept) a.out_kept[row] = skip ? 0 : res.kept;
+        if (a.out_log_norm) a.out_log_norm[row] = skip ? -INFINITY : (float)((double)m + log((double)res.zs));
+      }
+    }
+    if (a.mode == 1 && a.out_probs) dense_probs<DT>(oa, s, R, X, res, skip, P > 1 && !skip && !overflow);
+    __syncthreads();
+  }
+}
+
+// Single-chunk rows: one workgroup per row, no workspace.
+template <class DT, int J>
+__global__ __launch_bounds__(NT) void k_sample(KArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Smem& s = *reinterpret_cast<Smem*>(smem_raw);
+  if (threadIdx.x < 256) s.masktab[threadIdx.x] = DT::mask_of(threadIdx.x);
+  RowCtx X;
+  memset(&X, 0, sizeof X);
+  process_row<DT, J, false>(a, s, X, (int64_t)blockIdx.x, 0);
+}
+
+// Rows of P > 1 chunks: a persistent cooperative grid of row groups; the P workgroups of a group
+// process the group's rows in lockstep and exchange per-chunk results through the workspace.
+template <class DT, int J>
+__global__ __launch_bounds__(NT) void k_sample_multi(KArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Smem& s = *reinterpret_cast<Smem*>(smem_raw);
+
+  // block -> (group, chunk); with xcd_map the P chunks of a group sit on one XCD (consecutive
+  // workgroups are dispatched round-robin over the 8 XCDs)
+  int g, c;
+  if (a.xcd_map) {
+    const int b = blockIdx.x, xcd = b & 7, li = b >> 3;
+    g = (li / a.P) * 8 + xcd;
+    c = li % a.P;
+  } else {
+    g = blockIdx.x / a.P;
+    c = blockIdx.x % a.P;
+  }
+  RowCtx X;
+  memset(&X, 0, sizeof X);
+  {
+    unsigned char* wsg = a.ws + (int64_t)g * a.ws_group_bytes;
+    const WsLayout WL(a.P);
+    X.gsync = reinterpret_cast<GroupSync*>(wsg + WL.sync);
+    X.gstats = reinterpret_cast<ChunkStats*>(wsg + WL.stats);
+    X.gres = reinterpret_cast<GroupRes*>(wsg + WL.res);
+    X.ghist = reinterpret_cast<uint64_t*>(wsg + WL.hist);
+    X.glists = reinterpret_cast<uint64_t*>(wsg + WL.lists);
+  }
+  if (threadIdx.x < 256) s.masktab[threadIdx.x] = DT::mask_of(threadIdx.x);
+  for (int64_t row = g; row < a.B; row += a.n_groups) process_row<DT, J, true>(a, s, X, row, c);
+
+  // leave the group's counters at zero for the next call
+  if (threadIdx.x == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(&X.gsync->exit, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == (uint32_t)a.P - 1) {
+      __hip_atomic_store(&X.gsync->arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&X.gsync->exit, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+}  // namespace
+
+// ==============================================================================================
+// Standalone penalties: albireo_apply_penalties.  A workgroup handles one tile of one row: the
+// tile's history ids are counted in an LDS hash, a bit per tile element marks the penalised ones,
+// and the tile is streamed to the fp32 output (each element read and written by the same thread,
+// so the output may alias an fp32 input).
+// ==============================================================================================
+namespace {
+
+constexpr int PEN_NT = 256;
+constexpr int PEN_LOG2_HCAP = 13;
+constexpr int PEN_HCAP = 1 << PEN_LOG2_HCAP;
+constexpr int64_t PEN_TILE = 65536;  // elements per workgroup (8 KB bitmap)
+
+struct PenSmem {
+  int32_t h_key[PEN_HCAP];
+  uint32_t h_cnt[PEN_HCAP];
+  uint32_t bits[PEN_TILE / 32];
+  int32_t n_used;
+};
+
+__device__ __forceinline__ uint32_t pen_hash(int id) { return ((uint32_t)id * 2654435761u) >> (32 - PEN_LOG2_HCAP); }
+
+template <class DT>
+__global__ __launch_bounds__(PEN_NT) void k_penalties(const unsigned char* logits, int64_t V, int64_t ld,
+                                                      DevParams prm, float* out) {
+  __shared__ PenSmem s;
+  const int64_t row = blockIdx.y;
+  const int64_t t0 = (int64_t)blockIdx.x * PEN_TILE;
+  const int64_t t1 = min(V, t0 + PEN_TILE);
+  const unsigned char* rowp = logits + row * ld * DT::ES;
+  float rep = prm.rep ? prm.rep[row] : 1.0f;
+  float freq = prm.freq ? prm.freq[row] : 0.0f;
+  float pres = prm.pres ? prm.pres[row] : 0.0f;
+  if (!(rep > 0.0f) || isinf(rep)) rep = 1.0f;
+  if (!isfinite(freq)) freq = 0.0f;
+  if (!isfinite(pres)) pres = 0.0f;
+  int64_t lo = 0, hi = 0;
+  if (prm.hist_offsets) {
+    lo = prm.hist_offsets[row];
+    hi = prm.hist_offsets[row + 1];
+    if (lo < 0 || hi < lo || hi > prm.hist_len) lo = hi = 0;
+  }
+  const bool pen = hi > lo;
+  if (pen) {
+    for (int i = threadIdx.x; i < PEN_HCAP; i += PEN_NT) {
+      s.h_key[i] = -1;
+      s.h_cnt[i] = 0;
+    }
+    for (int i = threadIdx.x; i < PEN_TILE / 32; i += PEN_NT) s.bits[i] = 0;
+    if (threadIdx.x == 0) s.n_used = 0;
+    __syncthreads();
+    for (int64_t h = lo + threadIdx.x; h < hi; h += PEN_NT) {
+      const int id = prm.hist_ids[h];
+      if (id < t0 || id >= t1) continue;
+      uint32_t k = pen_hash(id);
+      for (int probe = 0; probe < PEN_HCAP; ++probe) {
+        const int prev = atomicCAS(&s.h_key[k], -1, id);
+        if (prev == -1) {
+          if (atomicAdd(&s.n_used, 1) >= (PEN_HCAP * 3) / 4) {  // keep probing chains short
+            s.h_key[k] = -2;                                    // tombstone: slot unusable
+            break;
+          }
+          atomicAdd(&s.h_cnt[k], 1u);
+          atomicOr(&s.bits[(id - t0) >> 5], 1u << ((id - t0) & 31));
+          break;
+        }
+        if (prev == id) {
+          atomicAdd(&s.h_cnt[k], 1u);
+          break;
+        }
+        k = (k + 1) & (PEN_HCAP - 1);
+      }
+    }
+    __syncthreads();
+  }
+  float* orow = out + row * V;
+  for (int64_t i = t0 + threadIdx.x; i < t1; i += PEN_NT) {
+    float x = DT::load1(rowp, i);
+    if (pen && ((s.bits[(i - t0) >> 5] >> ((i - t0) & 31)) & 1u)) {
+      uint32_t k = pen_hash((int)i);
+      uint32_t cnt = 0;
+      for (int probe = 0; probe < PEN_HCAP; ++probe) {
+        const int key = s.h_key[k];
+        if (key == (int)i) {
+          cnt = s.h_cnt[k];
+          break;
+        }
+        if (key == -1) break;
+        k = (k + 1) & (PEN_HCAP - 1);
+      }
+      if (cnt > 0) x = penalise(x, cnt, rep, freq, pres);
+    }
+    orow[i] = x;
+  }
+}
+
+// ==============================================================================================
+// Host side: geometry, capacity, workspace, launch
+// ==============================================================================================
+struct KernelInfo {
+  const void* fn;
+  int J;
+};
+
+template <class DT, int J>
+KernelInfo kinfo(bool multi) {
+  return {multi ? reinterpret_cast<const void*>(&k_sample_multi<DT, J>) : reinterpret_cast<const void*>(&k_sample<DT, J>), J};
+}
+
+template <class DT>
+KernelInfo pick_kernel(int64_t chunk_slots, bool multi) {
+#ifdef ALBIREO_DEV_ONE_J  // development builds: a single instantiation for quick compiles
+  (void)chunk_slots;
+  return kinfo<DT, ALBIREO_DEV_ONE_J>(multi);
+#else
+  if (chunk_slots <= 8 * NT) return kinfo<DT, 8>(multi);
+  if (chunk_slots <= 16 * NT) return kinfo<DT, 16>(multi);
+  if (chunk_slots <= 32 * NT) return kinfo<DT, 32>(multi);
+  return kinfo<DT, JMAX>(multi);
+#endif
+}
+
+struct Geometry {
+  int P;
+  int64_t chunk_slots;
+  KernelInfo k;
+  int n_groups;
+  int64_t group_bytes;
+  size_t smem;
+  bool ok;
+};
+
+struct DeviceCaps {
+  int cus = 0;
+  int blocks_per_cu = 0;
+};
+
+// Per (device, kernel) launch setup, done once: the dynamic-LDS attribute and the occupancy that
+// bounds the persistent grid.
+constexpr int MAX_DEV = 64;
+constexpr int MAX_FN = 64;
+std::mutex g_caps_mu;
+int g_cus[MAX_DEV];
+const void* g_fn[MAX_DEV][MAX_FN];
+int g_bpc[MAX_DEV][MAX_FN];
+
+hipError_t device_caps(int dev, const void* fn, size_t smem, DeviceCaps& out) {
+  std::lock_guard<std::mutex> lk(g_caps_mu);
+  if (dev < 0 || dev >= MAX_DEV) return hipErrorInvalidDevice;
+  if (g_cus[dev] == 0) {
+    hipDeviceProp_t p;
+    hipError_t e = hipGetDeviceProperties(&p, dev);
+    if (e != hipSuccess) return e;
+    g_cus[dev] = p.multiProcessorCount;
+  }
+  out.cus = g_cus[dev];
+  for (int i = 0; i < MAX_FN; ++i) {
+    if (g_fn[dev][i] == fn) {
+      out.blocks_per_cu = g_bpc[dev][i];
+      return hipSuccess;
+    }
+    if (g_fn[dev][i] == nullptr) {
+      hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      if (e != hipSuccess) return e;
+      int nb = 0;
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, NT, smem);
+      if (e != hipSuccess) return e;
+      g_fn[dev][i] = fn;
+      g_bpc[dev][i] = nb;
+      out.blocks_per_cu = nb;
+      return hipSuccess;
+    }
+  }
+  return hipErrorUnknown;
+}
+
+hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& G) {
+  const int VEC = dtype == ALBIREO_BF16 ? BF16T::VEC : F32T::VEC;
+  const int64_t max_body = V / VEC;
+  int64_t P = (max_body + (int64_t)JMAX * NT - 1) / ((int64_t)JMAX * NT);
+  if (P < 1) P = 1;
+  G.ok = P <= MAXP;
+  if (!G.ok) return hipSuccess;
+  G.P = (int)P;
+  G.chunk_slots = (max_body + P - 1) / P;
+  G.k = dtype == ALBIREO_BF16 ? pick_kernel<BF16T>(G.chunk_slots, G.P > 1) : pick_kernel<F32T>(G.chunk_slots, G.P > 1);
+  G.smem = sizeof(Smem);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  DeviceCaps caps;
+  e = device_caps(dev, G.k.fn, G.smem, caps);
+  if (e != hipSuccess) return e;
+  if (G.P == 1) {  // one workgroup per row, nothing in the workspace
+    G.n_groups = (int)B;
+    G.group_bytes = 0;
+    return hipSuccess;
+  }
+  int64_t cap_groups = (int64_t)caps.cus * (caps.blocks_per_cu > 0 ? caps.blocks_per_cu : 1) / G.P;
+  if (cap_groups < 1) cap_groups = 1;
+  G.n_groups = (int)(B < cap_groups ? B : cap_groups);
+  if (G.n_groups < 1) G.n_groups = 1;
+  G.group_bytes = WsLayout(G.P).total;
+  return hipSuccess;
+}
+
+size_t required_ws(const Geometry& G) { return (size_t)G.group_bytes * (size_t)G.n_groups; }
+
+albireo_status_t launch_sample(const KArgs& a0, const Geometry& G, hipStream_t stream) {
+  KArgs a = a0;
+  a.P = G.P;
+  a.n_groups = G.n_groups;
+  a.chunk_slots = G.chunk_slots;
+  a.ws_group_bytes = G.group_bytes;
+  const int grid = G.n_groups * G.P;
+  a.xcd_map = (G.P > 1 && grid % (8 * G.P) == 0) ? 1 : 0;
+  void* args[] = {&a};
+  hipError_t e;
+  if (G.P == 1) {
+    e = hipLaunchKernel(G.k.fn, dim3(grid), dim3(NT), args, G.smem, stream);
+  } else {
+    e = hipLaunchCooperativeKernel(G.k.fn, dim3(grid), dim3(NT), args, (unsigned int)G.smem, stream);
+  }
+  return e == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
+}
+
+DevParams dev_params(const albireo_params_t* p) {
+  DevParams d;
+  memset(&d, 0, sizeof d);
+  if (!p) return d;
+  d.temperature = p->temperature;
+  d.top_k = p->top_k;
+  d.top_p = p->top_p;
+  d.min_p = p->min_p;
+  d.rep = p->repetition_penalty;
+  d.freq = p->frequency_penalty;
+  d.pres = p->presence_penalty;
+  d.hist_offsets = p->hist_offsets;
+  d.hist_ids = p->hist_ids;
+  d.hist_len = p->hist_len;
+  return d;
+}
+
+albireo_status_t check_common(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
+                              const albireo_params_t* params) {
+  if (dtype != ALBIREO_F32 && dtype != ALBIREO_BF16) return ALBIREO_E_INVALID;
+  if (B < 0 || V <= 0 || ld < V) return ALBIREO_E_INVALID;
+  if (V >= ((int64_t)1 << 31) - 16 || B >= ((int64_t)1 << 31)) return ALBIREO_E_UNSUPPORTED;
+  if (B > 0 && !logits) return ALBIREO_E_INVALID;
+  const int es = dtype == ALBIREO_BF16 ? 2 : 4;
+  if (reinterpret_cast<uintptr_t>(logits) % es) return ALBIREO_E_INVALID;
+  if (params && params->hist_offsets) {
+    if (params->hist_len < 0) return ALBIREO_E_INVALID;
+    if (params->hist_len > 0 && !params->hist_ids) return ALBIREO_E_INVALID;
+  }
+  return ALBIREO_OK;
+}
+
+albireo_status_t check_ws(void* ws, size_t bytes, size_t need) {
+  if (need == 0) return ALBIREO_OK;
+  if (!ws || reinterpret_cast<uintptr_t>(ws) % 256) return ALBIREO_E_WORKSPACE;
+  if (bytes < need) return ALBIREO_E_WORKSPACE;
+  return ALBIREO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t albireo_workspace_size(int64_t B, int64_t V, albireo_dtype_t dtype, int32_t n_top) {
+  (void)n_top;
+  if (B <= 0 || V <= 0 || (dtype != ALBIREO_F32 && dtype != ALBIREO_BF16)) return 256;
+  if (V >= ((int64_t)1 << 31) - 16) return 0;
+  Geometry G;
+  if (make_geometry(B, V, dtype, G) != hipSuccess || !G.ok) return 0;
+  return required_ws(G);
+}
+
+albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
+                                const albireo_params_t* params, const float* uniforms, int32_t* out_ids,
+                                float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
+                                float* out_top_logprobs, uint32_t* out_flags, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream) {
+  albireo_status_t st = check_common(logits, dtype, B, V, ld, params);
+  if (st != ALBIREO_OK) return st;
+  if (n_top < 0 || n_top > ALBIREO_MAX_TOP_N) return ALBIREO_E_INVALID;
+  if (B == 0) return ALBIREO_OK;
+  if (!uniforms || !out_ids || !out_logprobs) return ALBIREO_E_INVALID;
+  if (n_top > 0 && (!out_top_ids || !out_top_logprobs)) return ALBIREO_E_INVALID;
+  Geometry G;
+  if (make_geometry(B, V, dtype, G) != hipSuccess) return ALBIREO_E_LAUNCH;
+  if (!G.ok) return ALBIREO_E_UNSUPPORTED;
+  st = check_ws(workspace, workspace_bytes, required_ws(G));
+  if (st != ALBIREO_OK) return st;
+  KArgs a;
+  memset(&a, 0, sizeof a);
+  a.logits = static_cast<const unsigned char*>(logits);
+  a.B = B;
+  a.V = V;
+  a.ld = ld;
+  a.prm = dev_params(params);
+  a.uniforms = uniforms;
+  a.out_ids = out_ids;
+  a.out_logprobs = out_logprobs;
+  a.n_top = n_top;
+  a.out_top_ids = out_top_ids;
+  a.out_top_logprobs = out_top_logprobs;
+  a.out_flags = out_flags;
+  a.mode = 0;
+  a.ws = static_cast<unsigned char*>(workspace);
+  return launch_sample(a, G, stream);
+}
+
+albireo_status_t albireo_topk_topp(const float* logits, int64_t B, int64_t V, int64_t ld,
+                                   const albireo_params_t* params, float* out_probs, float* out_threshold,
+                                   int32_t* out_kept, float* out_log_norm, uint32_t* out_flags,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  albireo_status_t st = check_common(logits, ALBIREO_F32, B, V, ld, nullptr);
+  if (st != ALBIREO_OK) return st;
+  if (B == 0) return ALBIREO_OK;
+  Geometry G;
+  if (make_geometry(B, V, ALBIREO_F32, G) != hipSuccess) return ALBIREO_E_LAUNCH;
+  if (!G.ok) return ALBIREO_E_UNSUPPORTED;
+  st = check_ws(workspace, workspace_bytes, required_ws(G));
+  if (st != ALBIREO_OK) return st;
+  KArgs a;
+  memset(&a, 0, sizeof a);
+  a.logits = reinterpret_cast<const unsigned char*>(logits);
+  a.B = B;
+  a.V = V;
+  a.ld = ld;
+  a.prm = dev_params(params);
+  // the filtered distribution uses temperature and the three filters only
+  a.prm.rep = a.prm.freq = a.prm.pres = nullptr;
+  a.prm.hist_offsets = nullptr;
+  a.prm.hist_ids = nullptr;
+  a.prm.hist_len = 0;
+  a.out_probs = out_probs;
+  a.out_threshold = out_threshold;
+  a.out_kept = out_kept;
+  a.out_log_norm = out_log_norm;
+  a.out_flags = out_flags;
+  a.mode = 1;
+  a.ws = static_cast<unsigned char*>(workspace);
+  return launch_sample(a, G, stream);
+}
+
+albireo_status_t albireo_apply_penalties(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V,
+                                         int64_t ld, const albireo_params_t* params, float* out_logits,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  albireo_status_t st = check_common(logits, dtype, B, V, ld, params);
+  if (st != ALBIREO_OK) return st;
+  if (B == 0) return ALBIREO_OK;
+  if (!out_logits) return ALBIREO_E_INVALID;
+  // aliasing is only defined for an fp32 input with ld == V (element-wise in place)
+  if (static_cast<const void*>(out_logits) == logits && !(dtype == ALBIREO_F32 && ld == V)) return ALBIREO_E_INVALID;
+  if (B > 65535) return ALBIREO_E_UNSUPPORTED;
+  const DevParams d = dev_params(params);
+  const dim3 grid((unsigned)((V + PEN_TILE - 1) / PEN_TILE), (unsigned)B);
+  if (dtype == ALBIREO_BF16)
+    hipLaunchKernelGGL(k_penalties<BF16T>, grid, dim3(PEN_NT), 0, stream,
+                       static_cast<const unsigned char*>(logits), V, ld, d, out_logits);
+  else
+    hipLaunchKernelGGL(k_penalties<F32T>, grid, dim3(PEN_NT), 0, stream,
+                       static_cast<const unsigned char*>(logits), V, ld, d, out_logits);
+  return hipGetLastError() == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
+}
+
+const char* albireo_status_string(albireo_status_t s) {
+  switch (s) {
+    case ALBIREO_OK: return "ok";
+    case ALBIREO_E_INVALID: return "invalid argument";
+    case ALBIREO_E_UNSUPPORTED: return "unsupported shape";
+    case ALBIREO_E_WORKSPACE: return "workspace missing, misaligned or too small";
+    case ALBIREO_E_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

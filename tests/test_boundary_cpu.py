@@ -1,0 +1,95 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, it exports every entry point the
+header declares, and argument errors come back as status codes before anything is launched."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "albireo.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:albireo_status_t|size_t|const char\*)\s+(albireo_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def alb():
+    lib = os.path.join(ROOT, "paper_2606_01927_amd", "libalbireo.so")
+    if not os.path.exists(lib):
+        pytest.skip("library not built")
+    import paper_2606_01927_amd
+
+    return paper_2606_01927_amd
+
+
+def test_header_declares_the_entry_points():
+    assert _declared() == sorted(["albireo_apply_penalties", "albireo_sample", "albireo_status_string",
+                                  "albireo_topk_topp", "albireo_workspace_size"])
+
+
+def test_library_exports_every_declared_symbol(alb):
+    lib = ctypes.CDLL(alb.LIB_PATH)
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_declared()) == set(alb.EXPORTED)
+
+
+def test_status_strings(alb):
+    for st in range(5):
+        assert alb.status_string(st)
+    assert alb.status_string(99) == "unknown status"
+
+
+def _sample(alb, **kw):
+    args = dict(logits=0x1000, dtype=alb.BF16, B=4, V=1000, ld=1000, params=None, uniforms=0x2000,
+                ids=0x3000, lps=0x4000, n_top=0, tids=None, tlps=None, flags=None, ws=None, wsb=0, stream=None)
+    args.update(kw)
+    f = alb.raw_call("albireo_sample")
+    return f(args["logits"], args["dtype"], args["B"], args["V"], args["ld"], args["params"], args["uniforms"],
+             args["ids"], args["lps"], args["n_top"], args["tids"], args["tlps"], args["flags"], args["ws"],
+             args["wsb"], args["stream"])
+
+
+def test_argument_errors_return_before_any_launch(alb):
+    E = alb.E_INVALID
+    assert _sample(alb, dtype=7) == E
+    assert _sample(alb, B=-1) == E
+    assert _sample(alb, V=0) == E
+    assert _sample(alb, ld=999) == E
+    assert _sample(alb, n_top=33) == E
+    assert _sample(alb, n_top=-1) == E
+    assert _sample(alb, logits=None) == E
+    assert _sample(alb, logits=0x1001) == E           # misaligned for bf16
+    assert _sample(alb, uniforms=None) == E
+    assert _sample(alb, ids=None) == E
+    assert _sample(alb, n_top=5) == E                  # top-n outputs missing
+    assert _sample(alb, V=1 << 31, ld=1 << 31) == alb.E_UNSUPPORTED
+    assert _sample(alb, B=0) == alb.OK                 # nothing to do, nothing launched
+
+
+def test_penalty_and_filter_entry_points_validate(alb):
+    pen = alb.raw_call("albireo_apply_penalties")
+    assert pen(0x1000, alb.BF16, 2, 100, 50, None, 0x2000, None, 0, None) == alb.E_INVALID     # ld < V
+    assert pen(0x1000, alb.BF16, 2, 100, 100, None, None, None, 0, None) == alb.E_INVALID     # no output
+    assert pen(0x1000, alb.BF16, 2, 100, 100, None, 0x1000, None, 0, None) == alb.E_INVALID   # bf16 alias
+    assert pen(0x1000, alb.F32, 0, 100, 100, None, 0x2000, None, 0, None) == alb.OK
+    tt = alb.raw_call("albireo_topk_topp")
+    assert tt(0x1002, 2, 100, 100, None, None, None, None, None, None, None, 0, None) == alb.E_INVALID
+    assert tt(0x1000, 0, 100, 100, None, None, None, None, None, None, None, 0, None) == alb.OK
+    # history length must be non-negative and come with ids
+    p = alb.Params()
+    p.hist_offsets = 0x5000
+    p.hist_ids = None
+    p.hist_len = 10
+    assert _sample(alb, params=ctypes.pointer(p)) == alb.E_INVALID
+    p.hist_len = -1
+    assert _sample(alb, params=ctypes.pointer(p)) == alb.E_INVALID
+
+
+def test_workspace_size_without_rows(alb):
+    assert alb.workspace_size(0, 1000, __import__("torch").bfloat16) == 256

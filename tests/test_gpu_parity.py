@@ -1,0 +1,233 @@
+"""GPU parity: the HIP sampling path through the C ABI against the CPU oracle on seeded inputs."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import workloads
+from tests.parity import BAND, TOL, compare_sample, np_
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_01927_amd as alb
+
+    return alb
+
+
+def _run(alb, w, n_top=None, offset_bytes=0):
+    import torch
+    from workloads.device import to_device
+
+    logits, u, p = to_device(w, row_offset_bytes=offset_bytes)
+    out = alb.sample(logits, u, p, n_top=w.n_top if n_top is None else n_top, V=w.V)
+    torch.cuda.synchronize()
+    return out
+
+
+# reduced sizes that still span several register slots, ragged tails and (for the wide fp32 case)
+# two chunks per row
+SMALL = [
+    (1, 4, 32000), (1, 16, 4099), (2, 64, 30011), (2, 32, 128256), (3, 32, 20011),
+    (3, 16, 152064), (4, 16, 60013), (4, 8, 100003), (5, 24, 40009), (5, 8, 170011),
+]
+
+
+@pytest.mark.parametrize("cfg,B,V", SMALL, ids=["c%d_B%d_V%d" % c for c in SMALL])
+def test_sample_reduced(cfg, B, V, lib, oracle_mod):
+    w = workloads.generate(cfg, B=B, V=V, H=min(2048, V // 4) if cfg in (3, 5) else None, variant=1)
+    _say("sample", cfg, B, V)
+    out = _run(lib, w)
+    ref = oracle_mod.sample(w)
+    rep = compare_sample(ref, out, n_top=w.n_top)
+    _say("  ", rep)
+    assert rep["band"] <= max(2, B // 8)
+
+
+FULL = [1, 2, 3, 4, 5]
+
+
+@pytest.mark.parametrize("cfg", FULL)
+def test_sample_full_size(cfg, lib, oracle_mod):
+    """The configuration at its full size in the launch the benchmark times; the oracle checks a
+    spread of rows one by one."""
+    w = workloads.generate(cfg)
+    _say("full config", cfg, w.B, w.V)
+    out = _run(lib, w)
+    rows = np.unique(np.linspace(0, w.B - 1, num=min(w.B, 48)).astype(np.int64))
+    ref = oracle_mod.sample(w, rows=rows)
+    rep = compare_sample(ref, out, rows=rows, n_top=w.n_top)
+    _say("  ", rep)
+
+
+def test_determinism_and_shard_invariance(lib):
+    """sec. 6.2: splitting the rows across workers, each consuming its slice of the pre-generated
+    uniforms, gives the single-worker result -- here bit-exact, logprobs included."""
+    import torch
+
+    w = workloads.generate(5, B=32, V=50021, H=512, ld=50024)  # rows 16-byte aligned in every slice
+    full = [np_(x) for x in _run(lib, w)]
+    again = [np_(x) for x in _run(lib, w)]
+    for a, b in zip(full, again):
+        assert np.array_equal(a, b)
+    for t in (2, 4, 8):
+        step = 32 // t
+        parts = [[np_(x) for x in _run(lib, w.row_slice(a, a + step))] for a in range(0, 32, step)]
+        for k in range(5):
+            assert np.array_equal(np.concatenate([p[k] for p in parts]), full[k]), (t, k)
+    torch.cuda.synchronize()
+
+
+def test_padding_rows_do_not_change_real_rows(lib):
+    w = workloads.generate(2, B=10, V=20011)
+    base = [np_(x) for x in _run(lib, w)]
+    pad = workloads.generate(2, B=6, V=20011, variant=7)
+    ww = w.row_slice(0, 10)
+    ww.B = 16
+    ww.logits = np.concatenate([w.logits, pad.logits])
+    ww.uniforms = np.concatenate([w.uniforms, pad.uniforms])
+    for f in ("temperature", "top_k", "top_p"):
+        setattr(ww, f, np.concatenate([getattr(w, f), getattr(pad, f)]))
+    got = [np_(x) for x in _run(lib, ww)]
+    for k in range(5):
+        assert np.array_equal(got[k][:10], base[k])
+
+
+@pytest.mark.parametrize("offset", [0, 2, 6, 12])
+@pytest.mark.parametrize("cfg,ld_pad", [(3, 13), (4, 7)])
+def test_strided_and_misaligned_rows(cfg, ld_pad, offset, lib, oracle_mod):
+    es = 2 if cfg in (2, 3, 5) else 4
+    if offset % es:
+        pytest.skip("offset not a multiple of the element size")
+    V = 9001
+    w = workloads.generate(cfg, B=8, V=V, ld=V + ld_pad, H=300 if cfg in (3, 5) else None)
+    _say("strided", cfg, ld_pad, offset)
+    out = _run(lib, w, offset_bytes=offset)
+    compare_sample(oracle_mod.sample(w), out, n_top=w.n_top)
+
+
+def _rowset(rows, dtype="f32", **params):
+    """Workload built from explicit rows (list of lists), same V for all."""
+    B = len(rows)
+    V = len(rows[0])
+    x = np.array([[(-np.inf if v == "-inf" else (np.inf if v == "inf" else (np.nan if v == "nan" else v)))
+                   for v in r] for r in rows], dtype=np.float32)
+    w = workloads.Workload(name="edge", B=B, V=V, dtype=dtype, ld=V,
+                           logits=workloads.to_bf16_bits(x) if dtype == "bf16" else x,
+                           uniforms=np.asarray(params.pop("u", np.linspace(0.05, 0.95, B)), np.float32))
+    for k, v in params.items():
+        setattr(w, k, v)
+    return w
+
+
+def test_edge_cases(lib, oracle_mod):
+    rng = np.random.default_rng(5)
+    V = 1000
+    base = rng.normal(0, 1, size=V).astype(np.float32)
+    rows, T, K, Pp, MP = [], [], [], [], []
+
+    def add(x, t=1.0, k=0, p=1.0, mp=0.0):
+        rows.append(list(x)); T.append(t); K.append(k); Pp.append(p); MP.append(mp)
+
+    allneg = np.full(V, -np.inf, np.float32)
+    add(allneg)                                   # empty row
+    ties = np.zeros(V, np.float32)
+    add(ties, t=0.0)                              # greedy, every entry tied: lowest id
+    add(ties, k=5)                                # top-k ties keep all
+    add(ties, p=0.3)                              # nucleus of all-equal mass
+    x = base.copy(); x[[10, 700]] = 9.0
+    add(x, t=0.0)                                 # greedy tie between two ids
+    add(x, k=1)                                   # top_k = 1 with a tied maximum
+    add(x, p=1e-7)                                # p -> 0 keeps the top group
+    add(base, mp=2.0)                             # min_p > 1 behaves as 1
+    add(base, t=1e6)                              # huge temperature
+    add(base, t=1e-4, k=3, p=0.5, mp=0.05)        # tiny temperature, all filters
+    y = base.copy(); y[::3] = -np.inf
+    add(y, p=0.9, k=50)                           # masked entries
+    add(y, k=V - 1)                               # top-k nearly off
+    add(base, k=V + 5)                            # top-k beyond V is off
+    add(base, p=-1.0)                             # p <= 0
+    z = base.copy(); z[17] = np.nan
+    add(z)                                        # NaN -> BAD_INPUT
+    w = _rowset(rows, temperature=np.array(T, np.float32), top_k=np.array(K, np.int32),
+                top_p=np.array(Pp, np.float32), min_p=np.array(MP, np.float32))
+    w.n_top = 7
+    out = _run(lib, w)
+    ref = oracle_mod.sample(w)
+    compare_sample(ref, out, n_top=7)
+
+
+def test_penalty_edge_cases(lib, oracle_mod):
+    rng = np.random.default_rng(6)
+    V = 3001
+    B = 6
+    x = rng.normal(0, 2, size=(B, V)).astype(np.float32)
+    hist = [
+        [0, 0, 0, 5, 5, V - 1],            # repeats and the last id
+        [V + 3, -1, 7],                     # out of range ids are skipped and flagged
+        list(range(0, V, 2)),               # half the vocabulary penalised
+        [],                                 # empty history
+        [42] * 500,                         # one id many times
+        list(rng.integers(0, V, size=2500)),
+    ]
+    offs = np.cumsum([0] + [len(h) for h in hist]).astype(np.int64)
+    w = workloads.Workload(name="pen", B=B, V=V, dtype="f32", ld=V, logits=x,
+                           uniforms=rng.random(B).astype(np.float32),
+                           repetition_penalty=np.array([1.3, 1.1, 0.0, 1.2, 2.0, 1.05], np.float32),
+                           frequency_penalty=np.array([0.5, 0.2, 0.1, 0.3, 0.01, np.inf], np.float32),
+                           presence_penalty=np.array([0.25, 0.1, -0.5, 0.1, 1.0, 0.2], np.float32),
+                           hist_offsets=offs, hist_ids=np.concatenate([np.array(h, np.int32) for h in hist]),
+                           temperature=np.array([0.9, 1.0, 0.0, 1.1, 0.7, 1.0], np.float32),
+                           top_k=np.array([0, 10, 0, 0, 50, 0], np.int32),
+                           top_p=np.array([0.9, 1.0, 1.0, 0.8, 0.95, 0.99], np.float32))
+    w.n_top = 5
+    out = _run(lib, w)
+    compare_sample(oracle_mod.sample(w), out, n_top=5)
+
+
+def test_topk_topp_dense(lib, oracle_mod):
+    import torch
+    from workloads.device import to_device
+
+    for cfg, B, V in [(1, 4, 32000), (4, 8, 100003), (2, 16, 20011)]:
+        w = workloads.generate(cfg, B=B, V=V)
+        if w.dtype == "bf16":
+            w.logits = (w.logits.astype(np.uint32) << 16).view(np.float32)
+            w.dtype = "f32"
+        _say("topk_topp", cfg, B, V)
+        logits, u, p = to_device(w)
+        pr, thr, kept, lnorm, flags = lib.topk_topp(logits, p, V=V)
+        torch.cuda.synchronize()
+        ref = oracle_mod.sample(w, probs=True, draw=False)
+        ok = ref["topp_margin"] >= BAND
+        assert np.array_equal(np_(kept)[ok], ref["kept"][ok])
+        assert np.array_equal(np_(thr)[ok].astype(np.float64), ref["threshold"][ok])
+        assert (np.abs(np_(lnorm)[ok] - ref["log_norm"][ok]) <= TOL).all()
+        d = np.abs(np_(pr)[ok].astype(np.float64) - ref["probs"][ok])
+        assert d.max() <= TOL, d.max()
+
+
+def test_apply_penalties_bit_exact(lib, oracle_mod):
+    import torch
+    from workloads.device import to_device
+
+    for cfg, B, V in [(3, 8, 20011), (5, 4, 170011)]:
+        w = workloads.generate(cfg, B=B, V=V, H=1000)
+        logits, u, p = to_device(w)
+        out = lib.apply_penalties(logits, p, V=V)
+        torch.cuda.synchronize()
+        ref = oracle_mod.sample(w, penalised=True)["penalised"]
+        assert np.array_equal(np_(out).view(np.uint32), ref.view(np.uint32))
