@@ -13,6 +13,7 @@ Prints one JSON line: rows/s (whole job), ms per step, the roofline entry of the
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -36,6 +37,47 @@ def algorithmic_bytes(w) -> int:
     b += w.B * 4 + w.B * 4      # ids + logprobs
     b += w.B * w.n_top * 8      # top-n ids + logprobs
     return int(b)
+
+
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_01927_amd", "csrc", "albireo.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sample_C3_B256_V152064_bf16_traffic.txt")
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the sampling kernel from the committed rocprofv3 --pmc summary
+    (FETCH_SIZE + WRITE_SIZE, each scaled by what the counter reads for a copy of known size), or
+    None when the summary is missing or was taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
+    except OSError:
+        return None
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib: int):
+    """One elementwise copy of a known size (mib MiB read, mib MiB written), launched before the
+    timed region so that a counter run of this script can scale FETCH_SIZE / WRITE_SIZE."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def cpu_baseline(w, seconds_target: float = 15.0) -> dict:
@@ -72,6 +114,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--config", type=int, default=3, help="workload index (3 is the headline one)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="launch one elementwise copy of this many MiB before the timed region (for "
+                         "scaling hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the sampling step of one rank's row-share; --gpus %d is not "
@@ -86,6 +131,8 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.calib_copy_mib > 0:
+        copy_calibration(args.calib_copy_mib)
     w = workloads.generate(args.config)
     logits0, u, p = to_device(w, device=dev)
     nbytes = logits0.numel() * logits0.element_size()
@@ -146,7 +193,8 @@ def main():
         "hbm_gbs": alg / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_of_peak": alg / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic() if args.config == 3 else None,
                      "kernel": "k_sample (one launch per step)", "algorithmic_bytes": alg,
                      "launch_us_avg": launch_us, "host_wall_us_per_step": wall * 1e6 / args.steps},
         "wall_s": wall,

@@ -23,6 +23,7 @@
 #include <string.h>
 
 #include <mutex>
+#include <utility>
 
 #include "albireo.h"
 
@@ -34,9 +35,8 @@ namespace {
 constexpr int NT = 512;           // threads per workgroup (2 waves per SIMD, 256 VGPRs each)
 constexpr int NW = NT / 64;       // waves per workgroup
 constexpr int JMAX = 38;          // 16-byte register slots per thread (152 VGPRs of row data)
-constexpr int LOG2_HCAP = 12;
-constexpr int HCAP = 1 << LOG2_HCAP;              // LDS hash slots for history counts
 constexpr int UCAP = ALBIREO_MAX_UNIQUE_HISTORY;  // tracked distinct ids (history + head/tail)
+constexpr int NWORDS = JMAX * NT / 4;             // presence bitmap words (one byte per register slot)
 constexpr int LCAP = 2048;        // candidate list capacity
 constexpr int EPT = LCAP / NT;    // list entries per thread in the list scans
 constexpr int MAXP = 8;           // chunks per row supported
@@ -148,9 +148,9 @@ __device__ __forceinline__ float key2f(uint32_t k) {
   return __uint_as_float(u);
 }
 // canonical processed logit: fl32(x * r) with -0 -> +0; -inf stays -inf (also when r == 0)
-__device__ __forceinline__ float canon(float x, float r) {
-  return (x == -INFINITY) ? -INFINITY : __fadd_rn(__fmul_rn(x, r), 0.0f);
-}
+// r is finite and positive (a malformed temperature is replaced), so x r keeps -inf and adding +0
+// turns -0 into +0
+__device__ __forceinline__ float canon(float x, float r) { return __fadd_rn(__fmul_rn(x, r), 0.0f); }
 // penalty overlay of one logit seen c > 0 times in the history
 __device__ __forceinline__ float penalise(float x, uint32_t c, float rep, float freq, float pres) {
   float v = (x > 0.0f) ? __fdiv_rn(x, rep) : __fmul_rn(x, rep);
@@ -232,13 +232,25 @@ struct F32T {
 // ----------------------------------------------------------------------------------------------
 // Shared memory of the sampling kernel
 // ----------------------------------------------------------------------------------------------
+// Compile-time loop: f(std::integral_constant<int, I>) for I = 0 .. N-1 as straight-line code, so a
+// register array indexed by I never gets a dynamic index (a rolled loop would put it in scratch).
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(static_cast<F&&>(f), std::make_integer_sequence<int, N>{});
+}
+
 struct Smem {
-  int32_t h_key[HCAP];
-  uint32_t h_cnt[HCAP];
-  uint16_t u_slot[UCAP];
-  uint32_t bitmap[JMAX * NT / 4];  // one byte per body slot of the chunk, bit e = element e
-  uint4 masktab[256];
-  int16_t h_xi[HCAP];              // hash slot -> extras index
+  alignas(16) uint32_t bitmap[NWORDS];  // one byte per body slot of the chunk, bit e = element e
+  alignas(16) uint16_t wpref[NWORDS];   // set bits in the bitmap words before each word
+  alignas(16) uint4 masktab[256];
+  alignas(16) uint32_t x_cnt[UCAP];     // history count of each extras entry
+  // per register slot and thread, the top 16 bits of the ordered key of the slot maximum (two slots
+  // per word, slot-pair major): the gather's first pass reads these instead of the registers
+  alignas(16) uint32_t scode[(JMAX + 1) / 2 * NT];
   int32_t x_pos[UCAP];             // extras: penalised body entries and head/tail entries
   float x_val[UCAP];
   uint64_t sk[LCAP];               // candidate list / sort keys
@@ -249,15 +261,21 @@ struct Smem {
   float red_f[2 * NW];
   uint32_t red_u[NW];
   uint64_t red_q[NW];
-  int32_t n_uniq;
+  int32_t n_body;  // extras entries of penalised body elements (position order); head/tail ones follow
+  int32_t n_ext;   // all extras entries
   int32_t n_list;
   uint32_t flags;
+  uint32_t ready;  // the row's penalty bitmap and hash are initialised (set by wave 0)
+  alignas(16) float wp[6][NW];       // per-wave partials of the workgroup reduction
+  alignas(16) uint32_t kh_cnt[256];  // K-th bound histogram: counts and minimum key per bucket
+  alignas(16) uint32_t kh_min[256];
+  uint64_t fxsum;                    // fixed-point mass of the extras
   int32_t bc_i[4];
   float bc_f[4];
   uint64_t bc_q[4];
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "LDS of one workgroup exceeds a gfx950 CU");
-static_assert(4 * NT <= UCAP, "history staging does not fit the extras arrays");
+static_assert(64 * 32 <= UCAP, "history staging does not fit the extras arrays");
 
 // ----------------------------------------------------------------------------------------------
 // Workgroup reductions and scans (fixed combination order: wave butterfly / Kogge-Stone, then
@@ -293,12 +311,31 @@ __device__ __forceinline__ uint32_t wave_or(uint32_t v) {
   for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o);
   return v;
 }
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, o));
+  return v;
+}
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
   return v;
 }
 
+__device__ __forceinline__ int wave_incl_scan_i(int v) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(v, o);
+    if (l >= o) v += t;
+  }
+  return v;
+}
 __device__ __forceinline__ float wave_incl_scan(float v) {
   const int l = lane_id();
 #pragma unroll
@@ -309,21 +346,6 @@ __device__ __forceinline__ float wave_incl_scan(float v) {
   return v;
 }
 // bitonic sort of one 64-bit key per lane across the wave (descending or ascending by lane index)
-__device__ __forceinline__ uint64_t wave_sort_u64(uint64_t key, bool descending) {
-  const int l = lane_id();
-#pragma unroll
-  for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const uint64_t o = __shfl_xor(key, j);
-      const bool lower = (l & j) == 0;
-      const bool block_desc = ((l & k) == 0) == descending;
-      const bool take_max = lower == block_desc;
-      key = take_max ? (key > o ? key : o) : (key < o ? key : o);
-    }
-  }
-  return key;
-}
 
 __device__ __forceinline__ float block_max(float v, Smem& s) {
   v = wave_max(v);
@@ -544,6 +566,9 @@ __device__ __forceinline__ float x_threshold(float bl, float r) {
 // ----------------------------------------------------------------------------------------------
 // Per-row uniform state
 // ----------------------------------------------------------------------------------------------
+// fl32(log(min_p)), evaluated in double
+__device__ __forceinline__ float log_minp_of(float minp) { return (float)log((double)minp); }
+
 struct RowState {
   int64_t row;
   const unsigned char* rowp;
@@ -566,8 +591,16 @@ struct RowState {
   uint32_t flags;
 };
 
+// Load of a wave-uniform, read-only value through the scalar unit (constant address space): it is
+// tracked apart from the vector loads, so waiting for it never waits for row data in flight.
+template <class T>
+__device__ __forceinline__ T sload(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)(p);
+}
+
+// Row geometry from the kernel arguments alone (no loads), so the row loads can start at once.
 template <class DT>
-__device__ __forceinline__ void row_setup(const KArgs& a, int64_t row, int c, RowState& R) {
+__device__ __forceinline__ void row_geometry(const KArgs& a, int64_t row, int c, RowState& R) {
   R.row = row;
   R.c = c;
   R.P = a.P;
@@ -585,16 +618,44 @@ __device__ __forceinline__ void row_setup(const KArgs& a, int64_t row, int c, Ro
   if (R.s1 > R.body_slots) R.s1 = R.body_slots;
   R.owns_head = (c == 0);
   R.owns_tail = (c == a.P - 1);
+}
 
-  uint32_t flags = 0;
+// Values of the per-row parameters whose arrays are NULL (feature off), read in their place so that
+// every parameter load is one unconditional scalar load.
+__constant__ float kParamDefaults[8] = {1.0f, 1.0f, 0.0f, 1.0f, 0.0f, 0.0f, 0.0f, 0.0f};  // T p min_p rep freq pres u
+__constant__ int32_t kZeroI32[2] = {0, 0};
+__constant__ int64_t kZeroI64[2] = {0, 0};
+
+struct RawParams {
+  float T, p, mp, rep, freq, pres, u;
+  int k;
+  int64_t lo, hi;
+};
+
+// Issue the row's parameter loads (scalar, no branches); the values are used later, so the loads are
+// in flight while the first row loads go out.
+__device__ __forceinline__ RawParams row_params_load(const KArgs& a, int64_t row) {
   const DevParams& q = a.prm;
-  float T = q.temperature ? q.temperature[row] : 1.0f;
-  const int k = q.top_k ? q.top_k[row] : 0;
-  float p = q.top_p ? q.top_p[row] : 1.0f;
-  float mp = q.min_p ? q.min_p[row] : 0.0f;
-  float rep = q.rep ? q.rep[row] : 1.0f;
-  float freq = q.freq ? q.freq[row] : 0.0f;
-  float pres = q.pres ? q.pres[row] : 0.0f;
+  RawParams rp;
+  rp.T = sload(q.temperature ? q.temperature + row : &kParamDefaults[0]);
+  rp.p = sload(q.top_p ? q.top_p + row : &kParamDefaults[1]);
+  rp.mp = sload(q.min_p ? q.min_p + row : &kParamDefaults[2]);
+  rp.rep = sload(q.rep ? q.rep + row : &kParamDefaults[3]);
+  rp.freq = sload(q.freq ? q.freq + row : &kParamDefaults[4]);
+  rp.pres = sload(q.pres ? q.pres + row : &kParamDefaults[5]);
+  rp.u = sload(a.uniforms ? a.uniforms + row : &kParamDefaults[6]);
+  rp.k = sload(q.top_k ? q.top_k + row : &kZeroI32[0]);
+  const int64_t* ho = q.hist_offsets ? q.hist_offsets + row : &kZeroI64[0];
+  rp.lo = sload(ho);
+  rp.hi = sload(ho + 1);
+  return rp;
+}
+
+// Per-row parameters, with malformed values replaced by their "off" value and flagged.
+__device__ __forceinline__ void row_params(const KArgs& a, RawParams rp, RowState& R) {
+  uint32_t flags = 0;
+  float T = rp.T, p = rp.p, mp = rp.mp, rep = rp.rep, freq = rp.freq, pres = rp.pres;
+  const int k = rp.k;
   if (!isfinite(T)) { flags |= FLAG_BAD_PARAM; T = 1.0f; }
   if (isnan(p)) { flags |= FLAG_BAD_PARAM; p = 1.0f; }
   if (isnan(mp)) { flags |= FLAG_BAD_PARAM; mp = 0.0f; }
@@ -615,9 +676,9 @@ __device__ __forceinline__ void row_setup(const KArgs& a, int64_t row, int c, Ro
   R.pres = pres;
   R.pen_on = false;
   R.h_lo = R.h_hi = 0;
-  if (q.hist_offsets) {
-    const int64_t lo = q.hist_offsets[row], hi = q.hist_offsets[row + 1];
-    if (lo < 0 || hi < lo || hi > q.hist_len) {
+  if (a.prm.hist_offsets) {
+    const int64_t lo = rp.lo, hi = rp.hi;
+    if (lo < 0 || hi < lo || hi > a.prm.hist_len) {
       flags |= FLAG_BAD_PARAM;
     } else if (hi > lo) {
       R.pen_on = true;
@@ -625,40 +686,117 @@ __device__ __forceinline__ void row_setup(const KArgs& a, int64_t row, int c, Ro
       R.h_hi = hi;
     }
   }
-  R.u = a.uniforms ? a.uniforms[row] : 0.0f;
+  R.u = rp.u;
   R.flags = flags;
 }
 
+typedef uint32_t u32x32 __attribute__((ext_vector_type(32)));
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+
+// A thread's register slots of the chunk (16 bytes each), stored as register tuples of at most 32
+// dwords -- 8-slot tuples, then a 4-slot and a 2-slot one -- so that a slot can also be read with a
+// wave-uniform run-time index: inside one tuple that is a handful of indexed register moves, where
+// an array of slots would need a chain of selects over every slot.
 template <class DT, int J>
 struct Chunk {
-  uint4 d[J];
+  static constexpr int NG = J / 8;             // 8-slot tuples
+  static constexpr bool H4 = (J % 8) >= 4;     // a 4-slot tuple after them
+  static constexpr bool H2 = (J % 4) >= 2;     // and a 2-slot tuple
+  static_assert(J % 2 == 0 && NG <= 4, "unsupported slot count");
+  u32x32 g[NG > 0 ? NG : 1];
+  u32x16 h;
+  u32x8 q;
+
+  template <int j>
+  __device__ __forceinline__ uint4 get() const {
+    if constexpr (j < 8 * NG) {
+      constexpr int o = 4 * (j % 8);
+      return make_uint4(g[j / 8][o], g[j / 8][o + 1], g[j / 8][o + 2], g[j / 8][o + 3]);
+    } else if constexpr (H4 && j < 8 * NG + 4) {
+      constexpr int o = 4 * (j - 8 * NG);
+      return make_uint4(h[o], h[o + 1], h[o + 2], h[o + 3]);
+    } else {
+      constexpr int o = 4 * (j - 8 * NG - (H4 ? 4 : 0));
+      return make_uint4(q[o], q[o + 1], q[o + 2], q[o + 3]);
+    }
+  }
+  template <int j>
+  __device__ __forceinline__ void set(uint4 v) {
+    if constexpr (j < 8 * NG) {
+      constexpr int o = 4 * (j % 8);
+      g[j / 8][o] = v.x;
+      g[j / 8][o + 1] = v.y;
+      g[j / 8][o + 2] = v.z;
+      g[j / 8][o + 3] = v.w;
+    } else if constexpr (H4 && j < 8 * NG + 4) {
+      constexpr int o = 4 * (j - 8 * NG);
+      h[o] = v.x;
+      h[o + 1] = v.y;
+      h[o + 2] = v.z;
+      h[o + 3] = v.w;
+    } else {
+      constexpr int o = 4 * (j - 8 * NG - (H4 ? 4 : 0));
+      q[o] = v.x;
+      q[o + 1] = v.y;
+      q[o + 2] = v.z;
+      q[o + 3] = v.w;
+    }
+  }
+  // slot j for a wave-uniform j in [0, J): a branch to its tuple, then indexed moves inside it
+  __device__ __forceinline__ uint4 pick(int j) const {
+    if (j < 8 * NG) {
+      const int o = 4 * (j & 7);
+      if (j < 8) return make_uint4(g[0][o], g[0][o + 1], g[0][o + 2], g[0][o + 3]);
+      if constexpr (NG > 1) {
+        if (j < 16) return make_uint4(g[1 % NG][o], g[1 % NG][o + 1], g[1 % NG][o + 2], g[1 % NG][o + 3]);
+      }
+      if constexpr (NG > 2) {
+        if (j < 24) return make_uint4(g[2 % NG][o], g[2 % NG][o + 1], g[2 % NG][o + 2], g[2 % NG][o + 3]);
+      }
+      if constexpr (NG > 3) return make_uint4(g[3 % NG][o], g[3 % NG][o + 1], g[3 % NG][o + 2], g[3 % NG][o + 3]);
+    }
+    if constexpr (H4) {
+      if (j < 8 * NG + 4) {
+        const int o = 4 * (j - 8 * NG);
+        return make_uint4(h[o], h[o + 1], h[o + 2], h[o + 3]);
+      }
+    }
+    if constexpr (H2) {
+      const int o = 4 * (j - 8 * NG - (H4 ? 4 : 0));
+      return make_uint4(q[o], q[o + 1], q[o + 2], q[o + 3]);
+    }
+    return make_uint4(0u, 0u, 0u, 0u);
+  }
 };
 
+
 // Double-precision per-row scalars, kept out of line so their polynomial constants never occupy
-// registers of the streaming loop.
+// registers of the streaming code.  Both are called where few registers are live: the first before any
+// load of the row is issued, the second after the row's registers are released.
 struct RowDoubles {
-  double L;        // log sum_v exp(z_v - m)
-  float zfull;     // sum_v exp(z_v - m)
-  float log_minp;  // fl32(log(min_p))
-  float t0;        // top-p candidate bound (p < 1 without top-k / min-p)
+  double L;     // log sum_v exp(z_v - m)
+  float zfull;  // sum_v exp(z_v - m)
 };
 
 // sum_v 2^(z_v L2E - mref) = S  =>  log sum_v e^(z_v - m) = ln S - D ln 2 with D = m L2E - mref (the
-// exact offset of the reference, in double).  The elements below t0 = m + log((1 - p) Z / (2 V))
-// carry less than (1 - p) / 2 of the mass, so the nucleus lies above t0 (lowered by a relative 1e-4
-// to absorb rounding).
-__device__ __noinline__ RowDoubles row_doubles(float mref, float S, float m, float minp, float p, int V) {
+// exact offset of the reference, in double).
+__device__ __noinline__ RowDoubles row_doubles(float mref, float S, float m) {
   RowDoubles o;
   const double D = (double)m * (double)L2E - (double)mref;
   o.L = log((double)S) - D * 0.6931471805599453;
   o.zfull = (float)exp(o.L);
-  o.log_minp = minp > 0.0f ? (float)log((double)minp) : 0.0f;
-  o.t0 = -INFINITY;
-  if (p < 1.0f) {
-    const double t0 = (double)m + log((1.0 - (double)p) * 0.5 * (double)o.zfull / (double)V);
-    o.t0 = (float)(t0 - 1e-4 * (1.0 + fabs(t0)));
-  }
   return o;
+}
+
+// Top-p candidate bound when top-p is the only filter: the elements below
+// t0 = m + log((1 - p) Z / (2 V)) carry less than (1 - p) / 2 of the mass together, so the nucleus
+// (whose complement below its last group holds at most 1 - p) lies at or above t0.  Evaluated in
+// fp32 and lowered by a relative 1e-4, far more than the fp32 rounding of ln Z and of the sum.
+__device__ __forceinline__ float topp_bound(float mref, float S, float m, float p, int V) {
+  const float lnZ = __logf(S) - __builtin_fmaf(m, L2E, -mref) * 0.693147182f;
+  const float t0 = m + lnZ + __logf((1.0f - p) * 0.5f / (float)V);
+  return t0 - 1e-4f * (1.0f + fabsf(t0));
 }
 
 // ----------------------------------------------------------------------------------------------
@@ -737,57 +875,29 @@ __device__ __forceinline__ uint4 load_masked(const RowState& R, const Smem& s, i
     }                                                                                           \
   }
 
-__device__ __forceinline__ uint32_t hash_of(int id) { return ((uint32_t)id * 2654435761u) >> (32 - LOG2_HCAP); }
-
-// Count one occurrence of `id` (inc 0 registers the id without counting).  Distinct ids beyond UCAP
-// are counted in the table but not tracked: their logit keeps its unpenalised value (FLAG_LIMIT).
-__device__ __forceinline__ void hash_insert(Smem& s, int id, uint32_t inc) {
-  uint32_t h = hash_of(id);
-  for (int probe = 0; probe < HCAP; ++probe) {
-    const int prev = atomicCAS(&s.h_key[h], -1, id);
-    if (prev == -1) {
-      const int u = atomicAdd(&s.n_uniq, 1);
-      if (u < UCAP) s.u_slot[u] = (uint16_t)h;
-      else atomicOr(&s.flags, FLAG_LIMIT);
-      if (inc) atomicAdd(&s.h_cnt[h], inc);
-      return;
-    }
-    if (prev == id) {
-      if (inc) atomicAdd(&s.h_cnt[h], inc);
-      return;
-    }
-    h = (h + 1) & (HCAP - 1);
-  }
-  atomicOr(&s.flags, FLAG_LIMIT);
+// Extras index of a row position in this chunk, or -1 when the position's value is in the registers
+// (or belongs to another chunk).  Penalised body elements are numbered by their rank among the set
+// bits of the presence bitmap (position order); the unaligned head / tail positions follow.
+template <class DT>
+__device__ __forceinline__ int extras_index(const Smem& s, const RowState& R, int pos) {
+  if (pos < R.head) return R.owns_head ? s.n_body + pos : -1;
+  if (pos >= R.tail_lo) return R.owns_tail ? s.n_body + (R.owns_head ? R.head : 0) + (pos - R.tail_lo) : -1;
+  if (!R.pen_on) return -1;
+  const int rel = pos - R.head;  // >= 0 here: a shift and a mask below
+  const int sl = rel / DT::VEC - (int)R.s0;
+  if ((unsigned)sl >= (unsigned)(R.s1 - R.s0)) return -1;
+  const int b = (sl & 3) * 8 + rel % DT::VEC;
+  const uint32_t word = s.bitmap[sl >> 2];
+  if (!((word >> b) & 1u)) return -1;
+  return (int)s.wpref[sl >> 2] + __popc(word & ((1u << b) - 1u));
 }
 
-// The logit at any position of the row as the resolution sees it: the extras value for a tracked
-// penalised or head/tail entry, the raw value otherwise.
+// The processed-before-temperature value x of a row position: the extras value where the position has
+// one, else the raw logit.
 template <class DT>
 __device__ __forceinline__ float x_at(const Smem& s, const RowState& R, int n_ext, int pos) {
-  const float raw = DT::load1(R.rowp, pos);
-  if (n_ext == 0) return raw;
-  bool look = pos < R.head || pos >= R.tail_lo;
-  if (!look && R.pen_on) {
-    const int64_t slot = (pos - R.head) / DT::VEC;
-    if (slot >= R.s0 && slot < R.s1) {
-      const int sl = (int)(slot - R.s0);
-      const int e = (pos - R.head) - (int)slot * DT::VEC;
-      look = (s.bitmap[sl >> 2] >> ((sl & 3) * 8 + e)) & 1u;
-    }
-  }
-  if (!look) return raw;
-  uint32_t h = hash_of(pos);
-  for (int probe = 0; probe < HCAP; ++probe) {
-    const int k = s.h_key[h];
-    if (k == pos) {
-      const int xi = s.h_xi[h];
-      return xi < n_ext ? s.x_val[xi] : raw;
-    }
-    if (k == -1) break;
-    h = (h + 1) & (HCAP - 1);
-  }
-  return raw;
+  const int u = n_ext > 0 ? extras_index<DT>(s, R, pos) : -1;
+  return u >= 0 ? s.x_val[u] : DT::load1(R.rowp, pos);
 }
 
 // Gather the n_top-candidate list (or any list) above `bl` into s.sk; returns the count (may
@@ -948,18 +1058,27 @@ __device__ bool radix_select(Smem& s, const RowState& R, const RowCtx& X, float 
 }
 
 // ----------------------------------------------------------------------------------------------
-// List path for at most 64 candidates: one wave, one entry per lane, shuffles only (no barriers).
-// Same definitions as resolve_list below; the result lands in res of every lane of wave 0.
-// ----------------------------------------------------------------------------------------------
-__device__ __forceinline__ void resolve_list_wave(const OutArgs& a, Smem& s, const RowState& R, const RowCtx& X,
-                                                  Resolution& res) {
+// Single-wave resolution of a candidate list of at most 64 entries (wave 0 of the leader).  Entries
+// are ordered by rank rather than by a sorting network: each lane counts the larger keys with
+// broadcast LDS reads and scatters its entry to its rank, which takes a few hundred cycles against
+// the long shuffle chains of a 64-lane sort.
+__device__ __forceinline__ Resolution resolve_small(const OutArgs& a, Smem& s, const RowState& R, const RowCtx& X,
+                                                    Resolution res) {
   const int l = lane_id();
   const int n = X.n_list;
   const float m = X.m;
-  uint64_t key = l < n ? s.sk[l] : 0ull;
-  key = wave_sort_u64(key, true);  // descending z, then ascending position
-  const float z = l < n ? cand_z(key) : -INFINITY;
-  const int pos = l < n ? cand_pos(key) : -1;
+  // rank in (z descending, position ascending): keys are distinct, padding keys (0) rank below all
+  const uint64_t key = l < n ? s.sk[l] : 0ull;
+  s.sk[l] = key;
+  int rank = 0;
+#pragma unroll 16
+  for (int i = 0; i < 64; ++i) rank += s.sk[i] > key ? 1 : 0;
+  if (l < n) {
+    s.l_z[rank] = cand_z(key);
+    s.l_p[rank] = cand_pos(key);
+  }
+  const float z = l < n ? s.l_z[l] : -INFINITY;
+  const int pos = l < n ? s.l_p[l] : -1;
   const float w = l < n ? __expf(z - m) : 0.f;
   int nS;
   if (R.greedy) {
@@ -995,11 +1114,19 @@ __device__ __forceinline__ void resolve_list_wave(const OutArgs& a, Smem& s, con
     res.id = __shfl(pos, 0);
     res.zid = __shfl(z, 0);
   } else if (a.mode == 0) {
-    // inverse CDF in ascending token id over the kept prefix
-    uint64_t k2 = l < nS ? (((uint64_t)(uint32_t)pos << 32) | (uint32_t)l) : ~0ull;
-    k2 = wave_sort_u64(k2, false);
-    const int src = l < nS ? (int)(uint32_t)k2 : 0;
-    const float ws = l < nS ? __shfl(w, src) : 0.f;
+    // inverse CDF in ascending token id over the kept prefix: rank the kept entries by position
+    const int kp = l < nS ? pos : INT32_MAX;
+    s.l_p[l] = kp;  // lanes >= nS pad with positions above every real one
+    int r2 = 0;
+#pragma unroll 16
+    for (int i = 0; i < 64; ++i) r2 += s.l_p[i] < kp ? 1 : 0;
+    if (l < nS) {
+      s.l_w[r2] = w;
+      s.sk[r2] = ((uint64_t)(uint32_t)pos << 32) | (uint32_t)l;
+    }
+    const float ws = l < nS ? s.l_w[l] : 0.f;
+    const uint64_t k2 = l < nS ? s.sk[l] : 0ull;
+    const int src = (int)(uint32_t)k2;
     const float c2 = wave_incl_scan(ws);
     const float t = R.u * __shfl(c2, nS - 1);
     const uint64_t hit = __ballot(l < nS && c2 > t);
@@ -1015,13 +1142,14 @@ __device__ __forceinline__ void resolve_list_wave(const OutArgs& a, Smem& s, con
       res.zid = __shfl(z, __shfl(src, sel));
     }
   }
+  return res;
 }
 
 // ----------------------------------------------------------------------------------------------
 // List path: exact resolution on the sorted candidate list (leader workgroup only)
 // ----------------------------------------------------------------------------------------------
-__device__ __noinline__ void resolve_list(const OutArgs a, Smem& s, const RowState R, const RowCtx X,
-                                          Resolution& res) {
+__device__ __noinline__ Resolution resolve_list(const OutArgs a, Smem& s, const RowState R, const RowCtx X,
+                                          Resolution res) {
   const int n = X.n_list;
   const float m = X.m;
   const int npad = next_pow2(n);
@@ -1155,6 +1283,7 @@ __device__ __noinline__ void resolve_list(const OutArgs a, Smem& s, const RowSta
     }
   }
   __syncthreads();
+  return res;
 }
 
 // ----------------------------------------------------------------------------------------------
@@ -1162,8 +1291,8 @@ __device__ __noinline__ void resolve_list(const OutArgs a, Smem& s, const RowSta
 // weight buffer in the workspace, top-n by a separate candidate list (selection for massive ties)
 // ----------------------------------------------------------------------------------------------
 template <class DT>
-__device__ __noinline__ void resolve_general(const OutArgs a, Smem& s, const RowState R, const RowCtx X,
-                                             Resolution& res) {
+__device__ __noinline__ Resolution resolve_general(const OutArgs a, Smem& s, const RowState R, const RowCtx X,
+                                             Resolution res) {
   const float r = R.r, m = X.m;
   const int P = R.P, c = R.c;
   const bool leader = c == 0;
@@ -1372,6 +1501,7 @@ __device__ __noinline__ void resolve_general(const OutArgs a, Smem& s, const Row
     if (leader) write_top_n(a, s, X, R.row, min(nl, LCAP));
   }
   __syncthreads();
+  return res;
 }
 
 // ----------------------------------------------------------------------------------------------
@@ -1421,6 +1551,240 @@ __device__ __noinline__ void dense_probs(const OutArgs a, Smem& s, const RowStat
   __syncthreads();
 }
 
+// Wait (bounded) until wave 0 has published the row's penalty state up to the given level
+// (1: presence bitmap, 2: extras numbering and cleared counts).
+__device__ __forceinline__ void wait_ready(Smem& s, uint32_t level) {
+  for (uint32_t n = 0; n < SPIN_LIMIT; ++n) {
+    if (__hip_atomic_load(&s.ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= level) return;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Whether a history id lies in this chunk (the chunk's body slots, or the head / tail it owns).
+template <class DT>
+__device__ __forceinline__ bool id_in_chunk(const RowState& R, int id) {
+  if (id < R.head) return R.owns_head;
+  if (id >= R.tail_lo) return R.owns_tail;
+  const int64_t slot = (id - R.head) / DT::VEC;
+  return slot >= R.s0 && slot < R.s1;
+}
+
+// Add one history occurrence to its extras entry: ids outside [0, V) (flagged by the presence build),
+// ids of other chunks and ids cut for capacity have none.
+template <class DT>
+__device__ __forceinline__ void count_history_id(Smem& s, const RowState& R, int id) {
+  if ((unsigned)id >= (unsigned)R.V) return;
+  const int u = extras_index<DT>(s, R, id);
+  if (u < 0) return;
+  atomicAdd(&s.x_cnt[u], 1u);
+  s.x_pos[u] = id;  // every counting thread of this id writes the same value
+}
+
+constexpr int HSTAGE = 3 * LCAP;  // history ids staged in LDS at once (the list arrays, unused until
+                                  // the candidate list is resolved)
+
+__device__ __forceinline__ int32_t* hist_stage(Smem& s) { return reinterpret_cast<int32_t*>(s.l_z); }
+static_assert(offsetof(Smem, l_w) == offsetof(Smem, l_z) + LCAP * 4 &&
+                  offsetof(Smem, l_p) == offsetof(Smem, l_w) + LCAP * 4,
+              "the history staging area spans l_z, l_w and l_p");
+
+// Stage history ids [b, b + n) (n <= HSTAGE) in LDS with direct-to-LDS loads: no registers are
+// involved, so nothing can be re-issued or moved behind the row loads.
+__device__ __forceinline__ void stage_history(Smem& s, const int32_t* hist_ids, int64_t b, int n) {
+  const uint64_t hb = reinterpret_cast<uint64_t>(hist_ids + b);
+  const uint32_t hb_lo = __builtin_amdgcn_readfirstlane((uint32_t)hb);
+  const uint32_t hb_hi = __builtin_amdgcn_readfirstlane((uint32_t)(hb >> 32));
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      reinterpret_cast<void*>(((uint64_t)hb_hi << 32) | hb_lo), (short)0, __builtin_amdgcn_readfirstlane(n * 4),
+      0x00020000);
+  int32_t* hst = hist_stage(s);
+  const int lane = lane_id();
+  const int nk = __builtin_amdgcn_readfirstlane((n + 63) / 64);
+  for (int k = 0; k < nk; ++k)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(hst + 64 * k), 4,
+                                             (lane + 64 * k) * 4, 0, 0, 0);
+}
+
+// Chunk-relative position of a row id's register element: (slot << 3) | element, or -1 when the id
+// is not a body element of this chunk.  32-bit arithmetic throughout (V < 2^31).
+template <class DT>
+__device__ __forceinline__ int body_code(const RowState& R, int id) {
+  const int rel = id - R.head;
+  if (rel < 0 || id >= R.tail_lo) return -1;
+  const int sl = rel / DT::VEC - (int)R.s0;  // rel >= 0: a shift
+  if ((unsigned)sl >= (unsigned)(R.s1 - R.s0)) return -1;
+  return (sl << 3) | (rel % DT::VEC);
+}
+
+// Wave 0, first: mark every penalised register element (a history id in the chunk's body) in the
+// presence bitmap and raise the flag to 1, which is all the other waves need before their online
+// pass.  When the history could name more distinct ids than the extras hold, only the lowest
+// positions keep their bit (the rest keep their raw value: penalties not applied, LIMIT flagged).
+// The first history batch was staged before this call.  Returns the flags found.
+template <class DT>
+__device__ __forceinline__ uint32_t build_presence(Smem& s, const RowState& R, const int32_t* hist_ids) {
+  const int lane = lane_id();
+  const int n_ht = (R.owns_head ? R.head : 0) + (R.owns_tail ? R.V - R.tail_lo : 0);
+  uint32_t flags = 0;
+  if (R.pen_on) {
+    uint4* bm4 = reinterpret_cast<uint4*>(s.bitmap);
+    for (int i = lane; i < NWORDS / 4; i += 64) bm4[i] = make_uint4(0u, 0u, 0u, 0u);
+    const int32_t* hst = hist_stage(s);
+    for (int64_t b = R.h_lo; b < R.h_hi; b += HSTAGE) {
+      const int n = (int)min<int64_t>(R.h_hi - b, HSTAGE);
+      if (b != R.h_lo) stage_history(s, hist_ids, b, n);
+#pragma unroll 4
+      for (int i = lane; i < n; i += 64) {
+        const int id = hst[i];
+        if ((unsigned)id >= (unsigned)R.V) {
+          flags = FLAG_BAD_INPUT;
+        } else {
+          const int code = body_code<DT>(R, id);
+          if (code >= 0) atomicOr(&s.bitmap[code >> 5], 1u << (code & 31));
+        }
+      }
+    }
+    flags = wave_or(flags);
+    const uint32_t cap = (uint32_t)(UCAP - n_ht);
+    if ((uint64_t)(R.h_hi - R.h_lo) > cap) {
+      // distinct body ids = set bits; each lane owns WPL consecutive words (position order)
+      constexpr int WPL = NWORDS / 64;
+      uint32_t cnt = 0;
+      for (int i = lane * WPL; i < (lane + 1) * WPL; ++i) cnt += __popc(s.bitmap[i]);
+      uint32_t incl = cnt;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+      }
+      if (__shfl(incl, 63) > cap) {
+        flags |= FLAG_LIMIT;
+        uint32_t before = incl - cnt;  // keep the lowest positions within the capacity
+        for (int i = lane * WPL; i < (lane + 1) * WPL; ++i) {
+          uint32_t wv = s.bitmap[i];
+          const uint32_t c = __popc(wv);
+          if (before + c > cap) {
+            uint32_t keep = before >= cap ? 0u : cap - before;
+            uint32_t out = 0;
+            while (keep > 0 && wv) {
+              const uint32_t lowbit = wv & (0u - wv);
+              out |= lowbit;
+              wv ^= lowbit;
+              --keep;
+            }
+            s.bitmap[i] = out;
+          }
+          before += c;
+        }
+      }
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  if (lane == 0) __hip_atomic_store(&s.ready, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  return flags;
+}
+
+// Extras index of a penalised body element from its body code (see extras_index).
+__device__ __forceinline__ int rank_of_code(const Smem& s, int code) {
+  const uint32_t word = s.bitmap[code >> 5];
+  const int b = code & 31;
+  if (!((word >> b) & 1u)) return -1;
+  return (int)s.wpref[code >> 5] + __popc(word & ((1u << b) - 1u));
+}
+
+// Wave 0, second: number the extras entries (penalised body elements by position, through the word
+// prefixes of the bitmap, then the unaligned head / tail positions the chunk owns), clear their
+// counts and raise the flag to 2.  A history longer than the staging area is also counted here;
+// otherwise every thread counts its share of the staged history after its online pass.
+template <class DT>
+__device__ __forceinline__ void build_ranks(Smem& s, const RowState& R, const int32_t* hist_ids, uint32_t flags) {
+  const int lane = lane_id();
+  const int n_head = R.owns_head ? R.head : 0;
+  const int n_ht = n_head + (R.owns_tail ? R.V - R.tail_lo : 0);
+  int n_body = 0;
+  if (R.pen_on) {
+    constexpr int WPL = NWORDS / 64;
+    static_assert(WPL * 64 == NWORDS && WPL % 4 == 0, "bitmap words do not split evenly over the lanes");
+    const uint4* own = reinterpret_cast<const uint4*>(s.bitmap + lane * WPL);
+    uint32_t cnt = 0;
+#pragma unroll 4
+    for (int i = 0; i < WPL / 4; ++i) {
+      const uint4 w = own[i];
+      cnt += __popc(w.x) + __popc(w.y) + __popc(w.z) + __popc(w.w);
+    }
+    uint32_t incl = cnt;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = __shfl_up(incl, o);
+      if (lane >= o) incl += t;
+    }
+    n_body = (int)__shfl(incl, 63);
+    uint32_t before = incl - cnt;
+    uint2* pref = reinterpret_cast<uint2*>(s.wpref + lane * WPL);  // 4 prefixes per 8-byte store
+#pragma unroll 4
+    for (int i = 0; i < WPL / 4; ++i) {
+      const uint4 w = own[i];
+      const uint32_t p0 = before;
+      const uint32_t p1 = p0 + __popc(w.x);
+      const uint32_t p2 = p1 + __popc(w.y);
+      const uint32_t p3 = p2 + __popc(w.z);
+      before = p3 + __popc(w.w);
+      pref[i] = make_uint2(p0 | (p1 << 16), p2 | (p3 << 16));
+    }
+  }
+  for (int i = lane; i < n_body + n_ht; i += 64) s.x_cnt[i] = 0u;
+  for (int i = lane; i < n_ht; i += 64) s.x_pos[n_body + i] = i < n_head ? i : R.tail_lo + (i - n_head);
+  if (lane == 0) {
+    s.n_body = n_body;
+    s.n_ext = n_body + n_ht;
+    s.flags = flags;
+  }
+  if (R.pen_on && R.h_hi - R.h_lo > HSTAGE) {  // long history: counted here, batch by batch
+    const int32_t* hst = hist_stage(s);
+    for (int64_t b = R.h_lo; b < R.h_hi; b += HSTAGE) {
+      const int n = (int)min<int64_t>(R.h_hi - b, HSTAGE);
+      stage_history(s, hist_ids, b, n);
+      for (int i = lane; i < n; i += 64) count_history_id<DT>(s, R, hst[i]);
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  if (lane == 0) __hip_atomic_store(&s.ready, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// K-th bound from the workgroup histogram of per-thread maxima: the bucket holding the K-th largest
+// (counting from the top bucket), then the smallest maximum at or above that bucket.  Every wave
+// evaluates it on the same LDS data, so no further barrier is needed.
+__device__ __forceinline__ float kth_from_hist(const Smem& s, int K) {
+  const int l = lane_id();
+  const uint32_t c0 = s.kh_cnt[255 - 4 * l], c1 = s.kh_cnt[254 - 4 * l], c2 = s.kh_cnt[253 - 4 * l],
+                 c3 = s.kh_cnt[252 - 4 * l];
+  const uint32_t own = c0 + c1 + c2 + c3;
+  uint32_t incl = own;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = __shfl_up(incl, o);
+    if (l >= o) incl += t;
+  }
+  const uint64_t hit = __ballot(incl >= (uint32_t)K);
+  if (!hit) return -INFINITY;
+  const int first = __ffsll((unsigned long long)hit) - 1;
+  int c = 0;
+  {
+    uint32_t cum = incl - own;
+    if ((cum += c0) >= (uint32_t)K) c = 255 - 4 * l;
+    else if ((cum += c1) >= (uint32_t)K) c = 254 - 4 * l;
+    else if ((cum += c2) >= (uint32_t)K) c = 253 - 4 * l;
+    else c = 252 - 4 * l;
+  }
+  c = __shfl(c, first);
+  uint32_t mk = 0xffffffffu;
+  if (255 - 4 * l >= c) mk = min(mk, s.kh_min[255 - 4 * l]);
+  if (254 - 4 * l >= c) mk = min(mk, s.kh_min[254 - 4 * l]);
+  if (253 - 4 * l >= c) mk = min(mk, s.kh_min[253 - 4 * l]);
+  if (252 - 4 * l >= c) mk = min(mk, s.kh_min[252 - 4 * l]);
+  return key2f(wave_min_u32(mk));
+}
+
 // ----------------------------------------------------------------------------------------------
 // The sampling kernel (mode 0) / filtered-distribution kernel (mode 1)
 // ----------------------------------------------------------------------------------------------
@@ -1432,156 +1796,137 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
   const bool leader = (c == 0);
   {
     RowState R;
-    row_setup<DT>(a, row, c, R);
+    row_geometry<DT>(a, row, c, R);
     R.P = P;
-    const bool extras_any = R.pen_on || (R.owns_head && R.head > 0) || (R.owns_tail && R.tail_lo < R.V);
 
-    // ---------------- history ids first (so waiting for them never waits for the row) ----------------
-    // Issued unconditionally in straight-line code (a zero-size range when penalties are off reads
-    // nothing), so the copy to LDS below waits for these loads only, not for the row.
-    constexpr int HPT = 4;  // history ids per thread staged through registers; longer histories loop
-    int hreg[HPT];
-    const int nh = (int)(R.h_hi - R.h_lo);
-    {
-      const uint64_t hb = reinterpret_cast<uint64_t>(R.pen_on ? a.prm.hist_ids + R.h_lo : a.prm.hist_ids);
-      const uint32_t hb_lo = __builtin_amdgcn_readfirstlane((uint32_t)hb);
-      const uint32_t hb_hi = __builtin_amdgcn_readfirstlane((uint32_t)(hb >> 32));
-      const int hrec = __builtin_amdgcn_readfirstlane(!R.pen_on ? 0 : (nh < HPT * NT ? nh * 4 : HPT * NT * 4));
-      const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
-          reinterpret_cast<void*>(((uint64_t)hb_hi << 32) | hb_lo), (short)0, hrec, 0x00020000);
-#pragma unroll
-      for (int q = 0; q < HPT; ++q)
-        hreg[q] = __builtin_amdgcn_raw_buffer_load_b32(hrs, ((int)threadIdx.x + q * NT) * 4, 0, 0);
-    }
-
-    // ---------------- issue every load of the chunk ----------------
+    // ---------------- row loads first ----------------
+    // The row loads depend on the kernel arguments only, so they go out before anything else.  They
+    // are software-pipelined with the online pass: slot j + PIPE is issued just before slot j is
+    // consumed, so each wave computes on its data as it arrives, with enough bytes in flight to hold
+    // the HBM stream.  Every issue is unconditional: a load under a branch would have its register
+    // merged at the join, which waits for the load.
     Chunk<DT, J> ch;
-    {
-      // one buffer resource per chunk (SGPRs), a 32-bit lane offset (one VGPR) and the per-slot
-      // offset in soffset, so no 64-bit addresses occupy VGPRs
-      const int nslots = (int)(R.s1 - R.s0);
-      // the descriptor must live in SGPRs: make its inputs visibly wave-uniform
-      const uint64_t cb = reinterpret_cast<uint64_t>(R.rowp + ((int64_t)R.head + R.s0 * DT::VEC) * DT::ES);
-      const uint32_t cb_lo = __builtin_amdgcn_readfirstlane((uint32_t)cb);
-      const uint32_t cb_hi = __builtin_amdgcn_readfirstlane((uint32_t)(cb >> 32));
-      const int nrec = __builtin_amdgcn_readfirstlane(nslots * 16);
-      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-          reinterpret_cast<void*>(((uint64_t)cb_hi << 32) | cb_lo), (short)0, nrec, 0x00020000);
-      // Unconditional loads with the whole offset in the range-checked VGPR operand: slots past the
-      // chunk read as 0 without touching memory and are set to -inf when consumed (only the last,
-      // partly filled slots can be affected).
-      const int voff = (int)threadIdx.x * 16;
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + j * NT * 16, 0, 0);
-        ch.d[j] = make_uint4(v[0], v[1], v[2], v[3]);
-      }
-    }
-    const int jfull = __builtin_amdgcn_readfirstlane((int)(R.s1 - R.s0) / NT);  // slots 0..jfull-1 all live
-    // history ids to LDS (x_pos is free until the extras are built)
-#pragma unroll
-    for (int q = 0; q < HPT; ++q) s.x_pos[threadIdx.x + q * NT] = hreg[q];
+    constexpr int PIPE = J < 8 ? J : 8;
+    const int nslots = (int)(R.s1 - R.s0);
+    // one buffer resource per chunk (SGPRs) and a 32-bit lane offset; its inputs are made visibly
+    // wave-uniform so the descriptor lives in SGPRs
+    const uint64_t cb = reinterpret_cast<uint64_t>(R.rowp + ((int64_t)R.head + R.s0 * DT::VEC) * DT::ES);
+    const uint32_t cb_lo = __builtin_amdgcn_readfirstlane((uint32_t)cb);
+    const uint32_t cb_hi = __builtin_amdgcn_readfirstlane((uint32_t)(cb >> 32));
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(((uint64_t)cb_hi << 32) | cb_lo), (short)0,
+        __builtin_amdgcn_readfirstlane(nslots * 16), 0x00020000);
+    const int voff = (int)threadIdx.x * 16;
+    // Unconditional loads with the whole offset in the range-checked VGPR operand: slots past the
+    // chunk read as 0 without touching memory and are set to -inf when consumed (only the last,
+    // partly filled slots can be affected).
+    auto issue = [&](auto jc) __attribute__((always_inline)) {
+      constexpr int j = decltype(jc)::value;
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + j * NT * 16, 0, 0);
+      ch.template set<j>(make_uint4(v[0], v[1], v[2], v[3]));
+    };
+    // the parameter loads (scalar) go out first, then the first row slots; the rest of the pipeline
+    // is issued once wave 0 has sent the history, so that the history is not queued behind the whole
+    // initial burst of row loads across the chip
+    constexpr int PIPE0 = PIPE < 2 ? PIPE : 2;
+    const RawParams rp = row_params_load(a, row);
+    static_for<PIPE0>(issue);
+    row_params(a, rp, R);
+    const bool extras_any = R.pen_on || (R.owns_head && R.head > 0) || (R.owns_tail && R.tail_lo < R.V);
+    const bool builder = extras_any && wave_id() == 0;
+    const int64_t n_hist = R.h_hi - R.h_lo;
 
-    // ---------------- history counts, penalised-slot bitmap, extras ----------------
-    __syncthreads();  // LDS of the previous row is no longer in use
-    int n_ext = 0;
-    uint32_t ext_flags = 0;
-    if (extras_any) {
-      for (int i = threadIdx.x; i < HCAP; i += NT) {
-        s.h_key[i] = -1;
-        s.h_cnt[i] = 0;
-        s.h_xi[i] = INT16_MAX;
-      }
-      if (R.pen_on)
-        for (int i = threadIdx.x; i < JMAX * NT / 4; i += NT) s.bitmap[i] = 0;
-      if (threadIdx.x == 0) {
-        s.n_uniq = 0;
-        s.flags = 0;
-      }
-      __syncthreads();
-      if (R.owns_head)
-        for (int i = threadIdx.x; i < R.head; i += NT) hash_insert(s, i, 0);
-      if (R.owns_tail)
-        for (int i = R.tail_lo + threadIdx.x; i < R.V; i += NT) hash_insert(s, i, 0);
-      if (R.pen_on) {
-        auto count_id = [&](int id) {
-          if (id < 0 || id >= R.V) {
-            atomicOr(&s.flags, FLAG_BAD_INPUT);
-            return;
-          }
-          bool mine;
-          if (id < R.head) mine = R.owns_head;
-          else if (id >= R.tail_lo) mine = R.owns_tail;
-          else {
-            const int64_t slot = (id - R.head) / DT::VEC;
-            mine = slot >= R.s0 && slot < R.s1;
-          }
-          if (mine) hash_insert(s, id, 1u);
-        };
-        for (int i = threadIdx.x; i < nh && i < HPT * NT; i += NT) count_id(s.x_pos[i]);
-        const int32_t* hid = a.prm.hist_ids;
-        for (int64_t h = R.h_lo + HPT * NT + threadIdx.x; h < R.h_hi; h += NT) count_id(hid[h]);
-      }
-      __syncthreads();
-      n_ext = min(s.n_uniq, UCAP);
-      ext_flags = s.flags;
-      // bitmap bits for the tracked penalised body entries (exactly those have an extras entry)
-      if (R.pen_on) {
-        for (int xi = threadIdx.x; xi < n_ext; xi += NT) {
-          const int hs = s.u_slot[xi];
-          const int id = s.h_key[hs];
-          if (id >= R.head && id < R.tail_lo && s.h_cnt[hs] > 0) {
-            const int64_t slot = (id - R.head) / DT::VEC;
-            const int sl = (int)(slot - R.s0);
-            const int e = (id - R.head) - (int)slot * DT::VEC;
-            atomicOr(&s.bitmap[sl >> 2], 1u << ((sl & 3) * 8 + e));
-          }
-        }
-        __syncthreads();
-      }
+    // ---------------- penalty state ----------------
+    // Wave 0 marks the penalised register elements in the presence bitmap and raises the LDS flag to 1
+    // (all the others need before their online pass), then numbers the extras entries and raises it to
+    // 2; every thread counts its share of the staged history after its online pass.
+    if (threadIdx.x == 0) {
+      s.ready = 0;
+      s.n_list = 0;
+      s.fxsum = 0;
     }
+    if (threadIdx.x < 256) {
+      s.kh_cnt[threadIdx.x] = 0u;
+      s.kh_min[threadIdx.x] = 0xffffffffu;
+    }
+    __syncthreads();  // LDS of the previous row is no longer in use; per-row LDS state is cleared
+    if (builder) {
+      if (R.pen_on) stage_history(s, a.prm.hist_ids, R.h_lo, (int)min<int64_t>(n_hist, HSTAGE));
+      const uint32_t bflags0 = build_presence<DT>(s, R, a.prm.hist_ids);
+      build_ranks<DT>(s, R, a.prm.hist_ids, bflags0);
+    }
+    // the rest of the pipeline's first slots (wave 0 after its penalty work, whose waits for the
+    // staged history would otherwise also wait for these)
+    static_for<PIPE - PIPE0>([&](auto jc) __attribute__((always_inline)) {
+      issue(std::integral_constant<int, decltype(jc)::value + PIPE0>{});
+    });
+    const int jfull = __builtin_amdgcn_readfirstlane(nslots / NT);  // slots 0..jfull-1 all live
+    if (R.pen_on) wait_ready(s, 1u);  // the masks below need the bitmap
 
-    // ---------------- online max / sum-exp over the registers (overlaps the loads) ----------------
+    // ---------------- online max / sum-exp over the registers ----------------
     // The reference starts finite: a -inf element then gives exp2(-inf) = 0 rather than NaN, and the
     // first finite slot always moves the reference before anything is accumulated against it.
     float xm = -INFINITY, mref = MREF0;
     float acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
     const float rr = R.r;
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
+    // the reference moves when a slot maximum x gives z L2E above mref + 32; xthr is that point in x
+    // units lowered by one (log2) unit, a cheap filter in front of the exact test
+    const float inv_c = 1.0f / (rr * L2E);
+    float xthr = (mref + 31.0f) * inv_c;
+    // the -inf pattern in a register, so that masking is one bit-select per word
+    uint32_t neg;
+    asm volatile("s_mov_b32 %0, %1" : "=s"(neg) : "i"(DT::NEG));
+    uint32_t code_lo = 0;  // slot-maximum code of the even slot of the current pair
+    static_for<J>([&](auto jc) __attribute__((always_inline)) {
+      constexpr int j = decltype(jc)::value;
+      if constexpr (j + PIPE < J) issue(std::integral_constant<int, j + PIPE>{});
       if (j >= jfull) {  // wave-uniform: the partly filled tail slots
-        const bool dead = j * NT + (int)threadIdx.x >= (int)(R.s1 - R.s0);
-        ch.d[j].x = dead ? DT::NEG : ch.d[j].x;
-        ch.d[j].y = dead ? DT::NEG : ch.d[j].y;
-        ch.d[j].z = dead ? DT::NEG : ch.d[j].z;
-        ch.d[j].w = dead ? DT::NEG : ch.d[j].w;
+        const bool dead = j * NT + (int)threadIdx.x >= nslots;
+        uint4 dj = ch.template get<j>();
+        dj.x = dead ? DT::NEG : dj.x;
+        dj.y = dead ? DT::NEG : dj.y;
+        dj.z = dead ? DT::NEG : dj.z;
+        dj.w = dead ? DT::NEG : dj.w;
+        ch.template set<j>(dj);
       }
       if (R.pen_on) {
         const int sl = j * NT + threadIdx.x;
         const uint32_t byte = (s.bitmap[sl >> 2] >> ((sl & 3) * 8)) & 255u;
         const uint4 mk = s.masktab[byte];
-        ch.d[j].x = (ch.d[j].x & ~mk.x) | (DT::NEG & mk.x);
-        ch.d[j].y = (ch.d[j].y & ~mk.y) | (DT::NEG & mk.y);
-        ch.d[j].z = (ch.d[j].z & ~mk.z) | (DT::NEG & mk.z);
-        ch.d[j].w = (ch.d[j].w & ~mk.w) | (DT::NEG & mk.w);
+        uint4 dj = ch.template get<j>();
+        dj.x = (neg & mk.x) | (dj.x & ~mk.x);
+        dj.y = (neg & mk.y) | (dj.y & ~mk.y);
+        dj.z = (neg & mk.z) | (dj.z & ~mk.z);
+        dj.w = (neg & mk.w) | (dj.w & ~mk.w);
+        ch.template set<j>(dj);
       }
+      const uint4 dcur = ch.template get<j>();
       float v[DT::VEC];
 #pragma unroll
-      for (int e = 0; e < DT::VEC; ++e) v[e] = DT::get(ch.d[j], e);
+      for (int e = 0; e < DT::VEC; ++e) v[e] = DT::get(dcur, e);
       float smax = v[0];
 #pragma unroll
       for (int e = 1; e < DT::VEC; ++e) smax = fmaxf(smax, v[e]);
       xm = fmaxf(xm, smax);
+      if constexpr (j % 2 == 0) {
+        code_lo = f2key(smax) >> 16;
+        if constexpr (j + 1 == J) s.scode[(j / 2) * NT + threadIdx.x] = code_lo;
+      } else {
+        s.scode[(j / 2) * NT + threadIdx.x] = code_lo | (f2key(smax) & 0xffff0000u);
+      }
       // sums run over the canonical z = fl32(x r) (exactly what the logprobs are defined on), as
       // 2^(z L2E - mref) with a reference mref in log2 units
-      const float sref = (smax * rr) * L2E;
-      if (sref > mref + 32.0f) {  // move the reference lazily: exp2 arguments stay below 32
-        const float f = __builtin_amdgcn_exp2f(mref - sref);
-        acc0 *= f;
-        acc1 *= f;
-        acc2 *= f;
-        acc3 *= f;
-        mref = sref;
+      if (smax > xthr) {
+        const float sref = (smax * rr) * L2E;
+        if (sref > mref + 32.0f) {  // move the reference lazily: exp2 arguments stay below 32
+          const float f = __builtin_amdgcn_exp2f(mref - sref);
+          acc0 *= f;
+          acc1 *= f;
+          acc2 *= f;
+          acc3 *= f;
+          mref = sref;
+          xthr = (mref + 31.0f) * inv_c;
+        }
       }
 #pragma unroll
       for (int e = 0; e < DT::VEC; e += 4) {
@@ -1590,51 +1935,114 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
         acc2 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 2] * rr, L2E, -mref));
         acc3 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 3] * rr, L2E, -mref));
       }
-    }
+    });
     float ssum = (acc0 + acc1) + (acc2 + acc3);
-    // The later passes re-extract the floats from the packed registers; this opaque redefinition
-    // keeps the compiler from holding every extracted value live across the passes instead.
-#pragma unroll
-    for (int j = 0; j < J; ++j)
-      asm volatile("" : "+v"(ch.d[j].x), "+v"(ch.d[j].y), "+v"(ch.d[j].z), "+v"(ch.d[j].w));
+
+    // this thread's share of the staged history into the counts (read after the barrier below)
+    if (R.pen_on && n_hist <= HSTAGE) {
+      wait_ready(s, 2u);
+      const int32_t* hst = hist_stage(s);
+      for (int i = threadIdx.x; i < (int)n_hist; i += NT) count_history_id<DT>(s, R, hst[i]);
+    }
 
     // maximum of this thread's register elements (a subset of the row, so the K-th largest of these
-    // per-thread maxima bounds the K-th largest z of the row from below)
+    // per-thread maxima bounds the K-th largest z of the row from below; K covers top-k and top-n)
     const float tmax_z = canon(xm, R.r);
-
-    // ---------------- extras: originals from memory, penalties ----------------
-    // Their order in LDS follows the atomic insertion order, so they are merged into the row sum
-    // through an order-independent fixed-point sum below (run-to-run bit-identical results).
-    float xmx = -INFINITY;
-    if (extras_any) {
-      for (int xi = threadIdx.x; xi < n_ext; xi += NT) {
-        const int hs = s.u_slot[xi];
-        const int id = s.h_key[hs];
-        const uint32_t cnt = s.h_cnt[hs];
-        float x = DT::load1(R.rowp, id);
-        if (cnt > 0) x = penalise(x, cnt, R.rep, R.freq, R.pres);
-        s.x_pos[xi] = id;
-        s.x_val[xi] = x;
-        s.h_xi[hs] = (int16_t)xi;
-        xmx = fmaxf(xmx, x);
-        if (x != x) ext_flags |= FLAG_BAD_INPUT;
-      }
-    }
+    int Ksel = R.k_on ? R.k : 0;
+    if (a.mode == 0 && a.n_top > Ksel) Ksel = a.n_top;
+    const bool want_kth = Ksel > 0 && Ksel <= NT;
 
     // ---------------- workgroup reduction ----------------
-    float bm = mref, bs = ssum;
-    block_lse(bm, bs, s);
-    float bxm = block_max(xm, s);
+    // Barrier A publishes every wave's partials (the history counts are complete then too), B the
+    // extras' maxima and the K-th bound histogram, C (rows with extras only) the extras' mass.  Every
+    // thread combines the partials in the same fixed order, so all hold identical row statistics.
+    {
+      const float wm = wave_max(mref);
+      const float wsum = wave_sum(ssum * rel2(mref, wm));
+      const float wxm = wave_max(xm);
+      const bool tv = tmax_z > -INFINITY;
+      const float thi = wave_max(tv ? tmax_z : -INFINITY);
+      const float tlo = wave_min(tv ? tmax_z : INFINITY);
+      if (lane_id() == 0) {
+        const int w = wave_id();
+        s.wp[0][w] = wm;
+        s.wp[1][w] = wsum;
+        s.wp[2][w] = wxm;
+        s.wp[3][w] = thi;
+        s.wp[4][w] = tlo;
+      }
+    }
+    __syncthreads();  // A
+    float bm = s.wp[0][0], bs = s.wp[1][0], bxm = s.wp[2][0], thi = s.wp[3][0], tlo = s.wp[4][0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) {
+      lse_combine(bm, bs, s.wp[0][w], s.wp[1][w]);
+      bxm = fmaxf(bxm, s.wp[2][w]);
+      thi = fmaxf(thi, s.wp[3][w]);
+      tlo = fminf(tlo, s.wp[4][w]);
+    }
+    if (want_kth && thi > -INFINITY && tmax_z > -INFINITY) {
+      const float width = thi - tlo;
+      const float scale = (width > 0.0f && width < INFINITY) ? 256.0f / width : 0.0f;
+      const float f = (tmax_z - tlo) * scale;
+      const int b = f >= 255.0f ? 255 : (f > 0.0f ? (int)f : 0);
+      atomicAdd(&s.kh_cnt[b], 1u);
+      atomicMin(&s.kh_min[b], f2key(tmax_z));
+    }
+    // extras: originals from memory with their penalties, entered into the row sum through an
+    // order-independent fixed-point sum
+    int n_ext = 0;
+    float xmx = -INFINITY;
     if (extras_any) {
-      const float bxx = block_max(xmx, s);
-      ext_flags = block_or(ext_flags, s);
+      n_ext = s.n_ext;
+      uint32_t myflags = 0;
+      for (int xi0 = threadIdx.x; xi0 < n_ext; xi0 += 4 * NT) {
+        int idv[4];
+        float xv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {  // all loads in flight before the first use
+          const int xi = xi0 + q * NT;
+          idv[q] = xi < n_ext ? s.x_pos[xi] : 0;
+          xv[q] = DT::load1(R.rowp, idv[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int xi = xi0 + q * NT;
+          if (xi < n_ext) {
+            const uint32_t cnt = s.x_cnt[xi];
+            float x = xv[q];
+            if (cnt > 0) x = penalise(x, cnt, R.rep, R.freq, R.pres);
+            s.x_val[xi] = x;
+            xmx = fmaxf(xmx, x);
+            if (x != x) myflags |= FLAG_BAD_INPUT;
+          }
+        }
+      }
+      if (myflags) atomicOr(&s.flags, myflags);
+      const float wx = wave_max(xmx);
+      if (lane_id() == 0) s.wp[5][wave_id()] = wx;
+    }
+    __syncthreads();  // B
+    uint32_t ext_flags = 0;
+    float eref = bm;
+    if (extras_any) {
+      ext_flags = s.flags;
+      float bxx = s.wp[5][0];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) bxx = fmaxf(bxx, s.wp[5][w]);
       bxm = fmaxf(bxm, bxx);
       // reference for the extras: at or above every extras term, so each term is <= 1
-      const float eref = fmaxf(bm, (bxx * rr) * L2E);
+      eref = fmaxf(bm, (bxx * rr) * L2E);
       uint64_t fx = 0;
       for (int xi = threadIdx.x; xi < n_ext; xi += NT)
         fx += fixmass(__builtin_amdgcn_exp2f(__builtin_fmaf(s.x_val[xi] * rr, L2E, -eref)));
-      fx = block_sum_u64(fx, s);
+      fx = wave_sum_u64(fx);
+      if (lane_id() == 0 && fx) atomicAdd(reinterpret_cast<unsigned long long*>(&s.fxsum), (unsigned long long)fx);
+    }
+    const float beta_sel = (want_kth && thi > -INFINITY) ? kth_from_hist(s, Ksel) : -INFINITY;
+    if (extras_any) {
+      __syncthreads();  // C
+      const uint64_t fx = s.fxsum;
       if (eref > bm) {
         bs = bs * rel2(bm, eref);
         bm = eref;
@@ -1642,12 +2050,6 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       bs += (float)((double)fx / FIX_SCALE) * rel2(eref, bm);
     }
     const uint32_t bflags = R.flags | ext_flags;
-    // K-th largest per-thread maximum: at least K elements are >= it, so it bounds the K-th largest
-    // z of the row from below (K covers top-k and top-n)
-    int Ksel = R.k_on ? R.k : 0;
-    if (a.mode == 0 && a.n_top > Ksel) Ksel = a.n_top;
-    float beta_sel = -INFINITY;
-    if (Ksel > 0 && Ksel <= NT) beta_sel = block_kth_bound(tmax_z, Ksel, s);
 
     // ---------------- combine the chunks of the row (fixed chunk order) ----------------
     float row_xm = bxm, row_mref = bm, row_s = bs, row_beta = beta_sel;
@@ -1677,10 +2079,6 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     // ---------------- row statistics ----------------
     const float m = canon(row_xm, R.r);
     X.m = m;
-    const RowDoubles RD = row_doubles(row_mref, row_s, m, R.minp_on ? R.minp : 0.0f,
-                                      (R.topp_on && !R.k_on && !R.minp_on) ? R.p : 1.0f, R.V);
-    X.L = RD.L;
-    X.zfull = RD.zfull;
     X.row_beta = row_beta;
     X.n_ext = n_ext;
     if (!(m > -INFINITY)) row_flags |= FLAG_EMPTY;
@@ -1689,50 +2087,75 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     const bool skip = (row_flags & FLAG_EMPTY) || bad_vals;
 
     // ---------------- candidate bound ----------------
-    X.tau_m = R.minp_on ? __fadd_rn(m, RD.log_minp) : -INFINITY;
+    X.tau_m = R.minp_on ? __fadd_rn(m, log_minp_of(R.minp)) : -INFINITY;
     float beta_S = -INFINITY;
     if (R.greedy) {
       beta_S = m;
     } else if (R.k_on || R.minp_on) {
       beta_S = fmaxf(R.k_on ? row_beta : -INFINITY, X.tau_m);
-    } else if (R.topp_on && R.p <= 0.9999f) {
-      beta_S = RD.t0;
+    } else if (R.topp_on && R.p <= 0.9999f && !skip) {
+      beta_S = topp_bound(row_mref, row_s, m, R.p, R.V);
     }
     float beta_list = beta_S;
     if (a.mode == 0 && a.n_top > 0) beta_list = fminf(beta_list, row_beta);
     const bool no_bound = !(beta_list > -INFINITY);
 
     // ---------------- gather candidates z >= beta_list into the LDS list ----------------
-    if (threadIdx.x == 0) s.n_list = 0;
-    __syncthreads();
+    // (the list counter was cleared at the start of the row)
     if (!skip && !no_bound) {
       const float r = R.r;
       const float bl = beta_list;
       // canon(x r) >= bl implies x >= bx for this bx (a few ulps below bl / r; fl(x r) is monotone in
-      // x), so a slot whose maximum is below bx holds no candidate
+      // x), so a slot whose maximum is below bx holds no candidate; the few that qualify are rare
+      // enough for one LDS atomic per candidate
       const float bx = x_threshold(bl, r);
-      const int pos0 = R.head + (int)(R.s0 + threadIdx.x) * DT::VEC;
+      const int pos_t = R.head + (int)(R.s0 + threadIdx.x) * DT::VEC;
+      // pass 1 from the slot-maximum codes the online pass left in LDS: the slots in which some lane
+      // may hold a candidate (a code at or above the bound's code: truncating a monotone key keeps
+      // smax >= bx => code(smax) >= code(bx))
+      const uint32_t tcode = f2key(bx) >> 16;
+      uint64_t whits = 0;
+      static_for<(J + 1) / 2>([&](auto ic) __attribute__((always_inline)) {
+        constexpr int i = decltype(ic)::value;
+        const uint32_t w = s.scode[i * NT + threadIdx.x];
+        whits |= (__ballot((w & 0xffffu) >= tcode) != 0ull ? 1ull : 0ull) << (2 * i);
+        if constexpr (2 * i + 1 < J) whits |= (__ballot((w >> 16) >= tcode) != 0ull ? 1ull : 0ull) << (2 * i + 1);
+      });
+      // pass 2 over those slots (few: the bound sits near the top of the row), four at a time: the
+      // slots are picked from the registers by their run-time index, each lane marks its candidates
+      // in a bit mask, and the batch takes one list claim per wave (a lane's place is its exclusive
+      // prefix of the candidate counts); the lanes then write their (usually one or none) entries.
+      constexpr int PB = 4;
+      while (whits) {
+        uint4 dd[PB];
+        int jj[PB];
 #pragma unroll
-      for (int j = 0; j < J; ++j) {
-        float v[DT::VEC];
+        for (int k = 0; k < PB; ++k) {
+          const int j = whits ? __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(whits)) : -1;
+          whits &= whits - 1;
+          jj[k] = j;
+          dd[k] = j >= 0 ? ch.pick(j) : make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG);
+        }
+        uint32_t cm = 0;  // bit 8 k + e: element e of batch slot k is a candidate
 #pragma unroll
-        for (int e = 0; e < DT::VEC; ++e) v[e] = DT::get(ch.d[j], e);
-        float smax = v[0];
+        for (int k = 0; k < PB; ++k)
 #pragma unroll
-        for (int e = 1; e < DT::VEC; ++e) smax = fmaxf(smax, v[e]);
-        if (__ballot(smax >= bx)) {
+          for (int e = 0; e < DT::VEC; ++e) cm |= (canon(DT::get(dd[k], e), r) >= bl ? 1u : 0u) << (8 * k + e);
+        const int c = __popc(cm);
+        const int incl = wave_incl_scan_i(c);
+        const int total = __shfl(incl, 63);
+        if (total > 0) {
+          int base = 0;
+          if (lane_id() == 0) base = atomicAdd(&s.n_list, total);
+          int idx = __builtin_amdgcn_readfirstlane(base) + incl - c;
 #pragma unroll
-          for (int e = 0; e < DT::VEC; ++e) {
-            const float z = canon(v[e], r);
-            const bool cand = v[e] >= bx && z >= bl;  // absent slots hold -inf and never qualify
-            const uint64_t mask = __ballot(cand);
-            if (mask) {
-              const int ldr = __ffsll((unsigned long long)mask) - 1;
-              int base = 0;
-              if (lane_id() == ldr) base = atomicAdd(&s.n_list, __popcll(mask));
-              base = __shfl(base, ldr);
-              const int idx = base + __popcll(mask & lanemask_lt());
-              if (cand && idx < LCAP) s.sk[idx] = cand_key(z, pos0 + (j * NT) * DT::VEC + e);
+          for (int k = 0; k < PB; ++k) {
+            uint32_t ck = (cm >> (8 * k)) & 0xffu;
+            while (ck) {
+              const int e = __ffs(ck) - 1;
+              ck &= ck - 1;
+              if (idx < LCAP) s.sk[idx] = cand_key(canon(DT::get(dd[k], e), r), pos_t + jj[k] * NT * DT::VEC + e);
+              ++idx;
             }
           }
         }
@@ -1745,7 +2168,13 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
         }
       })
     }
-    __syncthreads();
+    __syncthreads();  // D
+    // the full-vocabulary normaliser in double, now that the row's registers are released
+    {
+      const RowDoubles RD = row_doubles(row_mref, row_s, m);
+      X.L = RD.L;
+      X.zfull = RD.zfull;
+    }
     int n_list = s.n_list;
     bool overflow = !skip && (no_bound || n_list > LCAP || n_list == 0);
     if (P > 1) n_list = union_lists(s, R, X, n_list, overflow);
@@ -1766,7 +2195,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     } else if (!overflow) {
       if (leader) {
         if (X.n_list <= 64) {
-          if (wave_id() == 0) resolve_list_wave(oa, s, R, X, res);
+          if (wave_id() == 0) res = resolve_small(oa, s, R, X, res);
           if (a.mode == 1) {  // every thread needs the kept set for the dense output
             if (threadIdx.x == 0) {
               s.bc_f[0] = res.tau;
@@ -1778,13 +2207,12 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
             res.zs = s.bc_f[1];
             res.id = s.bc_i[0];
           }
-          __syncthreads();
         } else {
-          resolve_list(oa, s, R, X, res);
+          res = resolve_list(oa, s, R, X, res);
         }
       }
     } else {
-      resolve_general<DT>(oa, s, R, X, res);
+      res = resolve_general<DT>(oa, s, R, X, res);
     }
 
     // ---------------- per-row outputs ----------------
@@ -1814,7 +2242,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       }
     }
     if (a.mode == 1 && a.out_probs) dense_probs<DT>(oa, s, R, X, res, skip, P > 1 && !skip && !overflow);
-    __syncthreads();
+    if (MULTI) __syncthreads();  // the next row reuses LDS
   }
 }
 
