@@ -1551,8 +1551,9 @@ __device__ __noinline__ void dense_probs(const OutArgs a, Smem& s, const RowStat
   __syncthreads();
 }
 
-// Wait (bounded) until wave 0 has published the row's penalty state up to the given level
-// (1: presence bitmap, 2: extras numbering and cleared counts).
+// Wait (bounded) until the row's penalty state has reached the given level of the LDS counter: one
+// count per wave that has marked its share of the history, then one for wave 0's finished presence
+// bitmap, then one for its extras numbering and cleared counts.
 __device__ __forceinline__ void wait_ready(Smem& s, uint32_t level) {
   for (uint32_t n = 0; n < SPIN_LIMIT; ++n) {
     if (__hip_atomic_load(&s.ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= level) return;
@@ -1616,24 +1617,21 @@ __device__ __forceinline__ int body_code(const RowState& R, int id) {
   return (sl << 3) | (rel % DT::VEC);
 }
 
-// Wave 0, first: mark every penalised register element (a history id in the chunk's body) in the
-// presence bitmap and raise the flag to 1, which is all the other waves need before their online
-// pass.  When the history could name more distinct ids than the extras hold, only the lowest
-// positions keep their bit (the rest keep their raw value: penalties not applied, LIMIT flagged).
-// The first history batch was staged before this call.  Returns the flags found.
+// Wave 0, once every wave has marked its share of the history in the presence bitmap: mark the rest
+// of a history longer than the staging area, apply the capacity cut, and advance the flag (to 9), which
+// lets the other waves mask their registers.  When the history could name more distinct ids than the
+// extras hold, only the lowest positions keep their bit (the rest keep their raw value: penalties not
+// applied, LIMIT flagged).  Returns the flags found.
 template <class DT>
-__device__ __forceinline__ uint32_t build_presence(Smem& s, const RowState& R, const int32_t* hist_ids) {
+__device__ __forceinline__ uint32_t finish_presence(Smem& s, const RowState& R, const int32_t* hist_ids) {
   const int lane = lane_id();
   const int n_ht = (R.owns_head ? R.head : 0) + (R.owns_tail ? R.V - R.tail_lo : 0);
   uint32_t flags = 0;
   if (R.pen_on) {
-    uint4* bm4 = reinterpret_cast<uint4*>(s.bitmap);
-    for (int i = lane; i < NWORDS / 4; i += 64) bm4[i] = make_uint4(0u, 0u, 0u, 0u);
     const int32_t* hst = hist_stage(s);
-    for (int64_t b = R.h_lo; b < R.h_hi; b += HSTAGE) {
+    for (int64_t b = R.h_lo + HSTAGE; b < R.h_hi; b += HSTAGE) {  // long histories only
       const int n = (int)min<int64_t>(R.h_hi - b, HSTAGE);
-      if (b != R.h_lo) stage_history(s, hist_ids, b, n);
-#pragma unroll 4
+      stage_history(s, hist_ids, b, n);
       for (int i = lane; i < n; i += 64) {
         const int id = hst[i];
         if ((unsigned)id >= (unsigned)R.V) {
@@ -1680,7 +1678,7 @@ __device__ __forceinline__ uint32_t build_presence(Smem& s, const RowState& R, c
     }
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  if (lane == 0) __hip_atomic_store(&s.ready, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  if (lane == 0) atomicAdd(&s.ready, 1u);
   return flags;
 }
 
@@ -1694,7 +1692,7 @@ __device__ __forceinline__ int rank_of_code(const Smem& s, int code) {
 
 // Wave 0, second: number the extras entries (penalised body elements by position, through the word
 // prefixes of the bitmap, then the unaligned head / tail positions the chunk owns), clear their
-// counts and raise the flag to 2.  A history longer than the staging area is also counted here;
+// counts and advance the flag (to 10 when penalties are on).  A history longer than the staging area is also counted here;
 // otherwise every thread counts its share of the staged history after its online pass.
 template <class DT>
 __device__ __forceinline__ void build_ranks(Smem& s, const RowState& R, const int32_t* hist_ids, uint32_t flags) {
@@ -1737,7 +1735,7 @@ __device__ __forceinline__ void build_ranks(Smem& s, const RowState& R, const in
   if (lane == 0) {
     s.n_body = n_body;
     s.n_ext = n_body + n_ht;
-    s.flags = flags;
+    if (flags) atomicOr(&s.flags, flags);
   }
   if (R.pen_on && R.h_hi - R.h_lo > HSTAGE) {  // long history: counted here, batch by batch
     const int32_t* hst = hist_stage(s);
@@ -1748,7 +1746,7 @@ __device__ __forceinline__ void build_ranks(Smem& s, const RowState& R, const in
     }
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  if (lane == 0) __hip_atomic_store(&s.ready, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  if (lane == 0) atomicAdd(&s.ready, 1u);
 }
 
 // K-th bound from the workgroup histogram of per-thread maxima: the bucket holding the K-th largest
@@ -1826,8 +1824,8 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       ch.template set<j>(make_uint4(v[0], v[1], v[2], v[3]));
     };
     // the parameter loads (scalar) go out first, then the first row slots; the rest of the pipeline
-    // is issued once wave 0 has sent the history, so that the history is not queued behind the whole
-    // initial burst of row loads across the chip
+    // is issued once the history has been sent, so that it is not queued behind the whole initial
+    // burst of row loads across the chip
     constexpr int PIPE0 = PIPE < 2 ? PIPE : 2;
     const RawParams rp = row_params_load(a, row);
     static_for<PIPE0>(issue);
@@ -1837,31 +1835,79 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     const int64_t n_hist = R.h_hi - R.h_lo;
 
     // ---------------- penalty state ----------------
-    // Wave 0 marks the penalised register elements in the presence bitmap and raises the LDS flag to 1
-    // (all the others need before their online pass), then numbers the extras entries and raises it to
-    // 2; every thread counts its share of the staged history after its online pass.
+    // Every wave marks its share of the history in the presence bitmap of penalised register elements
+    // (and stages it in LDS for the counts) and advances an LDS counter; at 8, wave 0 applies the
+    // capacity rule and advances it to 9, which is all the waves need before their online pass, then
+    // numbers the extras entries (10).  Every thread counts its share of the staged history after its
+    // online pass.
+    // this wave's share of the (staged part of the) history, into registers ahead of the barrier so
+    // that it is not queued behind the row loads: positions c * 2048 + wave * 256 + q * 64 + lane;
+    // unconditional loads over a zero-size range when penalties are off
+    constexpr int HQ = HSTAGE / (4 * NT);
+    const int n_stage = (int)min<int64_t>(n_hist, HSTAGE);
+    int hq[HQ * 4];
+    {
+      const uint64_t hb = reinterpret_cast<uint64_t>(a.prm.hist_ids + (R.pen_on ? R.h_lo : 0));
+      const uint32_t hb_lo = __builtin_amdgcn_readfirstlane((uint32_t)hb);
+      const uint32_t hb_hi = __builtin_amdgcn_readfirstlane((uint32_t)(hb >> 32));
+      const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
+          reinterpret_cast<void*>(((uint64_t)hb_hi << 32) | hb_lo), (short)0,
+          __builtin_amdgcn_readfirstlane(R.pen_on ? n_stage * 4 : 0), 0x00020000);
+      const int hoff = (wave_id() * 256 + lane_id()) * 4;
+#pragma unroll
+      for (int t = 0; t < HQ * 4; ++t)
+        hq[t] = __builtin_amdgcn_raw_buffer_load_b32(hrs, hoff + ((t >> 2) * 2048 + (t & 3) * 64) * 4, 0, 0);
+    }
     if (threadIdx.x == 0) {
       s.ready = 0;
       s.n_list = 0;
       s.fxsum = 0;
+      s.flags = 0;
     }
     if (threadIdx.x < 256) {
       s.kh_cnt[threadIdx.x] = 0u;
       s.kh_min[threadIdx.x] = 0xffffffffu;
     }
-    __syncthreads();  // LDS of the previous row is no longer in use; per-row LDS state is cleared
-    if (builder) {
-      if (R.pen_on) stage_history(s, a.prm.hist_ids, R.h_lo, (int)min<int64_t>(n_hist, HSTAGE));
-      const uint32_t bflags0 = build_presence<DT>(s, R, a.prm.hist_ids);
-      build_ranks<DT>(s, R, a.prm.hist_ids, bflags0);
+    if (R.pen_on) {
+      uint4* bm4 = reinterpret_cast<uint4*>(s.bitmap);
+      for (int i = threadIdx.x; i < NWORDS / 4; i += NT) bm4[i] = make_uint4(0u, 0u, 0u, 0u);
     }
-    // the rest of the pipeline's first slots (wave 0 after its penalty work, whose waits for the
-    // staged history would otherwise also wait for these)
+    __syncthreads();  // LDS of the previous row is no longer in use; per-row LDS state is cleared
+    // the rest of the pipeline's first slots
     static_for<PIPE - PIPE0>([&](auto jc) __attribute__((always_inline)) {
       issue(std::integral_constant<int, decltype(jc)::value + PIPE0>{});
     });
+    if (R.pen_on) {
+      int32_t* hst = hist_stage(s);
+      uint32_t bad = 0;
+#pragma unroll
+      for (int t = 0; t < HQ * 4; ++t) {
+        const int i = (t >> 2) * 2048 + wave_id() * 256 + (t & 3) * 64 + lane_id();
+        if (i < n_stage) {
+          const int id = hq[t];
+          if ((unsigned)id >= (unsigned)R.V) {
+            bad = FLAG_BAD_INPUT;
+          } else {
+            const int code = body_code<DT>(R, id);
+            if (code >= 0) atomicOr(&s.bitmap[code >> 5], 1u << (code & 31));
+          }
+          hst[i] = id;
+        }
+      }
+      bad = wave_or(bad);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      if (lane_id() == 0) {
+        if (bad) atomicOr(&s.flags, bad);
+        atomicAdd(&s.ready, 1u);
+      }
+    }
+    if (builder) {
+      if (R.pen_on) wait_ready(s, (uint32_t)NW);
+      const uint32_t bflags0 = finish_presence<DT>(s, R, a.prm.hist_ids);
+      build_ranks<DT>(s, R, a.prm.hist_ids, bflags0);
+    }
     const int jfull = __builtin_amdgcn_readfirstlane(nslots / NT);  // slots 0..jfull-1 all live
-    if (R.pen_on) wait_ready(s, 1u);  // the masks below need the bitmap
+    if (R.pen_on) wait_ready(s, (uint32_t)NW + 1u);  // the masks below need the finished bitmap
 
     // ---------------- online max / sum-exp over the registers ----------------
     // The reference starts finite: a -inf element then gives exp2(-inf) = 0 rather than NaN, and the
@@ -1940,7 +1986,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
 
     // this thread's share of the staged history into the counts (read after the barrier below)
     if (R.pen_on && n_hist <= HSTAGE) {
-      wait_ready(s, 2u);
+      wait_ready(s, (uint32_t)NW + 2u);
       const int32_t* hst = hist_stage(s);
       for (int i = threadIdx.x; i < (int)n_hist; i += NT) count_history_id<DT>(s, R, hst[i]);
     }
