@@ -278,72 +278,109 @@ static_assert(sizeof(Smem) <= 160 * 1024, "LDS of one workgroup exceeds a gfx950
 static_assert(64 * 32 <= UCAP, "history staging does not fit the extras arrays");
 
 // ----------------------------------------------------------------------------------------------
-// Workgroup reductions and scans (fixed combination order: wave butterfly / Kogge-Stone, then
-// waves in index order), so results are bit-identical from run to run
+// Wave reductions and scans on DPP: row shifts within the 16-lane rows, then the broadcasts of lanes
+// 15 and 31 into the following rows, and a total read from lane 63.  Each step costs a few VALU
+// cycles where an LDS permute would cost a round trip.  The combination order is fixed by the lane
+// layout, so results are bit-identical from run to run and every lane receives the same total.
 // ----------------------------------------------------------------------------------------------
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+constexpr int DPP_ROW_SHR = 0x110, DPP_WAVE_SHR1 = 0x138, DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143;
+
+// v from the lane the control names; lanes without a source (or outside ROWS) get `old`
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWS, 0xf, false);
+}
+// inclusive scan in lane order under op, whose identity is id
+template <class Op>
+__device__ __forceinline__ uint32_t wave_scan_bits(uint32_t v, uint32_t id, Op op) {
+  v = op(v, dpp_mov<DPP_ROW_SHR + 1>(id, v));
+  v = op(v, dpp_mov<DPP_ROW_SHR + 2>(id, v));
+  v = op(v, dpp_mov<DPP_ROW_SHR + 4>(id, v));
+  v = op(v, dpp_mov<DPP_ROW_SHR + 8>(id, v));
+  v = op(v, dpp_mov<DPP_ROW_BCAST15, 0xa>(id, v));
+  v = op(v, dpp_mov<DPP_ROW_BCAST31, 0xc>(id, v));
   return v;
 }
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+// value of lane i (i wave-uniform)
+__device__ __forceinline__ uint32_t lane_u32(uint32_t v, int i) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, __builtin_amdgcn_readfirstlane(i));
 }
-__device__ __forceinline__ int wave_min_i(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ int wave_max_i(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ int wave_sum_i(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o);
-  return v;
-}
-__device__ __forceinline__ float wave_min(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, o));
-  return v;
-}
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+__device__ __forceinline__ int lane_i32(int v, int i) { return (int)lane_u32((uint32_t)v, i); }
+__device__ __forceinline__ float lane_f32(float v, int i) { return __uint_as_float(lane_u32(__float_as_uint(v), i)); }
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int i) {
+  return ((uint64_t)lane_u32((uint32_t)(v >> 32), i) << 32) | lane_u32((uint32_t)v, i);
 }
 
-__device__ __forceinline__ int wave_incl_scan_i(int v) {
-  const int l = lane_id();
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int t = __shfl_up(v, o);
-    if (l >= o) v += t;
+struct OpFmax {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
   }
-  return v;
+};
+struct OpFmin {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const {
+    return __float_as_uint(fminf(__uint_as_float(a), __uint_as_float(b)));
+  }
+};
+struct OpFadd {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  }
+};
+struct OpAdd {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a + b; }
+};
+struct OpOr {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a | b; }
+};
+struct OpMinU {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return min(a, b); }
+};
+struct OpMinI {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return (uint32_t)min((int)a, (int)b); }
+};
+struct OpMaxI {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return (uint32_t)max((int)a, (int)b); }
+};
+
+__device__ __forceinline__ float wave_max(float v) {
+  return __uint_as_float(lane_u32(wave_scan_bits(__float_as_uint(v), __float_as_uint(-INFINITY), OpFmax{}), 63));
 }
+__device__ __forceinline__ float wave_min(float v) {
+  return __uint_as_float(lane_u32(wave_scan_bits(__float_as_uint(v), __float_as_uint(INFINITY), OpFmin{}), 63));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  return __uint_as_float(lane_u32(wave_scan_bits(__float_as_uint(v), 0u, OpFadd{}), 63));
+}
+__device__ __forceinline__ int wave_min_i(int v) {
+  return (int)lane_u32(wave_scan_bits((uint32_t)v, 0x7fffffffu, OpMinI{}), 63);
+}
+__device__ __forceinline__ int wave_max_i(int v) {
+  return (int)lane_u32(wave_scan_bits((uint32_t)v, 0x80000000u, OpMaxI{}), 63);
+}
+__device__ __forceinline__ int wave_sum_i(int v) { return (int)lane_u32(wave_scan_bits((uint32_t)v, 0u, OpAdd{}), 63); }
+__device__ __forceinline__ uint32_t wave_or(uint32_t v) { return lane_u32(wave_scan_bits(v, 0u, OpOr{}), 63); }
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+  return lane_u32(wave_scan_bits(v, 0xffffffffu, OpMinU{}), 63);
+}
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ uint64_t dpp_mov64(uint64_t v) {
+  const uint32_t lo = dpp_mov<CTRL, ROWS>(0u, (uint32_t)v);
+  const uint32_t hi = dpp_mov<CTRL, ROWS>(0u, (uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+  v += dpp_mov64<DPP_ROW_SHR + 1>(v);
+  v += dpp_mov64<DPP_ROW_SHR + 2>(v);
+  v += dpp_mov64<DPP_ROW_SHR + 4>(v);
+  v += dpp_mov64<DPP_ROW_SHR + 8>(v);
+  v += dpp_mov64<DPP_ROW_BCAST15, 0xa>(v);
+  v += dpp_mov64<DPP_ROW_BCAST31, 0xc>(v);
+  return lane_u64(v, 63);
+}
+__device__ __forceinline__ int wave_incl_scan_i(int v) { return (int)wave_scan_bits((uint32_t)v, 0u, OpAdd{}); }
+__device__ __forceinline__ uint32_t wave_incl_scan_u(uint32_t v) { return wave_scan_bits(v, 0u, OpAdd{}); }
 __device__ __forceinline__ float wave_incl_scan(float v) {
-  const int l = lane_id();
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const float t = __shfl_up(v, o);
-    if (l >= o) v += t;
-  }
-  return v;
+  return __uint_as_float(wave_scan_bits(__float_as_uint(v), 0u, OpFadd{}));
 }
 // bitonic sort of one 64-bit key per lane across the wave (descending or ascending by lane index)
 
@@ -408,36 +445,13 @@ __device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float 
   s = s * rel2(m, M) + s2 * rel2(m2, M);
   m = M;
 }
-__device__ __forceinline__ void block_lse(float& m, float& s, Smem& sm) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float m2 = __shfl_xor(m, o), s2 = __shfl_xor(s, o);
-    lse_combine(m, s, m2, s2);
-  }
-  __syncthreads();
-  if (lane_id() == 0) {
-    sm.red_f[wave_id()] = m;
-    sm.red_f[NW + wave_id()] = s;
-  }
-  __syncthreads();
-  float M = sm.red_f[0], S = sm.red_f[NW];
-  for (int w = 1; w < NW; ++w) lse_combine(M, S, sm.red_f[w], sm.red_f[NW + w]);
-  m = M;
-  s = S;
-}
 
 // Exclusive scan over the NT threads in thread order.  *total is the last thread's exclusive prefix
 // plus its own value, i.e. exactly the value a thread-serial continuation of the scan would give.
 __device__ __forceinline__ float block_excl_scan(float v, Smem& s, float* total) {
   const int l = lane_id();
-  float incl = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const float t = __shfl_up(incl, o);
-    if (l >= o) incl += t;
-  }
-  float excl = __shfl_up(incl, 1);
-  if (l == 0) excl = 0.0f;
+  const float incl = wave_incl_scan(v);
+  const float excl = __uint_as_float(dpp_mov<DPP_WAVE_SHR1>(0u, __float_as_uint(incl)));
   __syncthreads();
   if (l == 63) s.red_f[wave_id()] = incl;
   __syncthreads();
@@ -451,57 +465,6 @@ __device__ __forceinline__ float block_excl_scan(float v, Smem& s, float* total)
   return e;
 }
 
-// Lower bound of the K-th largest of one value per thread (absent threads pass -inf): one 256-bucket
-// histogram over [min, max] of the values; for the highest bucket c whose count together with all
-// higher buckets reaches K, the smallest value in buckets >= c has at least K values at or above it.
-// Returns -inf when fewer than K values exist.
-__device__ __forceinline__ float block_kth_bound(float tz, int K, Smem& s) {
-  const bool valid = tz > -INFINITY;
-  const float hi = block_max(valid ? tz : -INFINITY, s);
-  const float lo = block_min(valid ? tz : INFINITY, s);
-  if (!(hi > -INFINITY)) return -INFINITY;
-  const float width = hi - lo;
-  const float scale = (width > 0.0f && width < INFINITY) ? 256.0f / width : 0.0f;
-  uint32_t* h = reinterpret_cast<uint32_t*>(s.hist);
-  if (threadIdx.x < 256) h[threadIdx.x] = 0;
-  __syncthreads();
-  int b = 0;
-  if (valid) {
-    const float f = (tz - lo) * scale;
-    b = f >= 255.0f ? 255 : (f > 0.0f ? (int)f : 0);
-    atomicAdd(&h[b], 1u);
-  }
-  __syncthreads();
-  if (wave_id() == 0) {
-    // lane l holds buckets 255-4l .. 252-4l (descending); inclusive scan over lanes counts from the top
-    const int l = lane_id();
-    const uint32_t c0 = h[255 - 4 * l], c1 = h[254 - 4 * l], c2 = h[253 - 4 * l], c3 = h[252 - 4 * l];
-    uint32_t incl = c0 + c1 + c2 + c3;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t t = __shfl_up(incl, o);
-      if (l >= o) incl += t;
-    }
-    const uint32_t excl = incl - (c0 + c1 + c2 + c3);
-    const uint64_t hit = __ballot(incl >= (uint32_t)K);
-    const int first = hit ? __ffsll((unsigned long long)hit) - 1 : -1;
-    if (l == (first < 0 ? 0 : first)) {
-      int c = -1;
-      if (first >= 0) {
-        uint32_t cum = excl;
-        if ((cum += c0) >= (uint32_t)K) c = 255 - 4 * l;
-        else if ((cum += c1) >= (uint32_t)K) c = 254 - 4 * l;
-        else if ((cum += c2) >= (uint32_t)K) c = 253 - 4 * l;
-        else c = 252 - 4 * l;
-      }
-      s.bc_i[0] = c;
-    }
-  }
-  __syncthreads();
-  const int c = s.bc_i[0];
-  if (c < 0) return -INFINITY;
-  return block_min((valid && b >= c) ? tz : INFINITY, s);
-}
 
 // ----------------------------------------------------------------------------------------------
 // Row-group synchronisation through the workspace (P > 1).  The wait is bounded: after SPIN_LIMIT
@@ -1058,88 +1021,142 @@ __device__ bool radix_select(Smem& s, const RowState& R, const RowCtx& X, float 
 }
 
 // ----------------------------------------------------------------------------------------------
-// Single-wave resolution of a candidate list of at most 64 entries (wave 0 of the leader).  Entries
-// are ordered by rank rather than by a sorting network: each lane counts the larger keys with
-// broadcast LDS reads and scatters its entry to its rank, which takes a few hundred cycles against
-// the long shuffle chains of a 64-lane sort.
+// Single-wave resolution of a candidate list of at most 2 * 64 entries (wave 0 of the leader): lane l
+// holds entries l and l + 64.  Entries are ordered by rank rather than by a sorting network: each
+// entry counts the larger keys with broadcast LDS reads and is scattered to its rank, a few hundred
+// cycles against the long exchange chains of a sort.  Quantities indexed by a list position i are
+// read from lane i % 64 of half i / 64.
+constexpr int SMALL_LIST = 128;
+
+// rank of each of this lane's two keys among the first nr keys of arr (broadcast reads); with one
+// half in use only the first key is ranked
+template <class T, class Less>
+__device__ __forceinline__ void rank2(const T* arr, int nr, bool two, const T (&k)[2], int (&r)[2], Less less) {
+  r[0] = 0;
+  r[1] = 0;
+  if (two) {
+#pragma unroll 8
+    for (int i = 0; i < nr; ++i) {
+      const T v = arr[i];
+      r[0] += less(k[0], v) ? 1 : 0;
+      r[1] += less(k[1], v) ? 1 : 0;
+    }
+  } else {
+#pragma unroll 16
+    for (int i = 0; i < nr; ++i) r[0] += less(k[0], arr[i]) ? 1 : 0;
+  }
+}
+__device__ __forceinline__ float at2f(const float (&v)[2], int i) {
+  return i < 64 ? lane_f32(v[0], i) : lane_f32(v[1], i - 64);
+}
+__device__ __forceinline__ int first_of2(uint64_t b0, uint64_t b1) {
+  return b0 ? __ffsll((unsigned long long)b0) - 1 : (b1 ? 64 + __ffsll((unsigned long long)b1) - 1 : -1);
+}
+
 __device__ __forceinline__ Resolution resolve_small(const OutArgs& a, Smem& s, const RowState& R, const RowCtx& X,
                                                     Resolution res) {
   const int l = lane_id();
   const int n = X.n_list;
+  const bool two = n > 64;
+  const int nr = two ? 128 : 64;
   const float m = X.m;
   // rank in (z descending, position ascending): keys are distinct, padding keys (0) rank below all
-  const uint64_t key = l < n ? s.sk[l] : 0ull;
-  s.sk[l] = key;
-  int rank = 0;
-#pragma unroll 16
-  for (int i = 0; i < 64; ++i) rank += s.sk[i] > key ? 1 : 0;
-  if (l < n) {
-    s.l_z[rank] = cand_z(key);
-    s.l_p[rank] = cand_pos(key);
+  uint64_t key[2];
+  int rk[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) key[q] = l + 64 * q < n ? s.sk[l + 64 * q] : 0ull;
+  s.sk[l] = key[0];
+  s.sk[l + 64] = key[1];
+  rank2(s.sk, nr, two, key, rk, [](uint64_t k, uint64_t v) { return v > k; });
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+    if (l + 64 * q < n) {
+      s.l_z[rk[q]] = cand_z(key[q]);
+      s.l_p[rk[q]] = cand_pos(key[q]);
+    }
+  float z[2], w[2];
+  int pos[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const bool in = l + 64 * q < n;
+    z[q] = in ? s.l_z[l + 64 * q] : -INFINITY;
+    pos[q] = in ? s.l_p[l + 64 * q] : -1;
+    w[q] = in ? __expf(z[q] - m) : 0.f;
   }
-  const float z = l < n ? s.l_z[l] : -INFINITY;
-  const int pos = l < n ? s.l_p[l] : -1;
-  const float w = l < n ? __expf(z - m) : 0.f;
   int nS;
   if (R.greedy) {
     nS = 1;
   } else {
     float tau2 = X.tau_m;
-    if (R.k_on && R.k <= n) tau2 = fmaxf(tau2, __shfl(z, R.k - 1));
-    const bool in2 = l < n && z >= tau2;
-    const int n2 = __popcll(__ballot(in2));  // S2 is a prefix of the descending list
+    if (R.k_on && R.k <= n) tau2 = fmaxf(tau2, at2f(z, R.k - 1));
+    const bool in0 = l < n && z[0] >= tau2, in1 = l + 64 < n && z[1] >= tau2;
+    const int n2 = __popcll(__ballot(in0)) + __popcll(__ballot(in1));  // S2 is a prefix of the list
     nS = n2;
     if (R.topp_on) {
-      const float c = wave_incl_scan(in2 ? w : 0.f);
-      const float Z2 = (R.k_on || R.minp_on) ? __shfl(c, n2 - 1) : X.zfull;
+      float c[2];
+      c[0] = wave_incl_scan(in0 ? w[0] : 0.f);
+      c[1] = lane_f32(c[0], 63) + wave_incl_scan(in1 ? w[1] : 0.f);
+      const float Z2 = (R.k_on || R.minp_on) ? at2f(c, n2 - 1) : X.zfull;
       const float target = R.p * Z2;
-      const uint64_t hit = __ballot(in2 && c >= target);
-      if (hit) {  // the nucleus closes at the end of that tie group
-        const float zc = __shfl(z, __ffsll((unsigned long long)hit) - 1);
-        nS = __popcll(__ballot(l < n2 && z >= zc));
+      const int first = first_of2(__ballot(in0 && c[0] >= target), __ballot(in1 && c[1] >= target));
+      if (first >= 0) {  // the nucleus closes at the end of that tie group
+        const float zc = at2f(z, first);
+        nS = __popcll(__ballot(l < n2 && z[0] >= zc)) + __popcll(__ballot(l + 64 < n2 && z[1] >= zc));
       }
     }
   }
   res.kept = nS;
-  res.zmin = __shfl(z, nS - 1);
+  res.zmin = at2f(z, nS - 1);
   res.tau = res.zmin;
-  res.zs = __shfl(wave_incl_scan(l < nS ? w : 0.f), nS - 1);
+  {
+    float c[2];
+    c[0] = wave_incl_scan(l < nS ? w[0] : 0.f);
+    c[1] = lane_f32(c[0], 63) + wave_incl_scan(l + 64 < nS ? w[1] : 0.f);
+    res.zs = at2f(c, nS - 1);
+  }
   res.id_here = 1;
-  if (a.mode == 0 && a.n_top > 0 && l < a.n_top) {
+  if (a.mode == 0 && a.n_top > 0 && l < a.n_top) {  // n_top <= 64: the first half
     const int64_t o = R.row * a.n_top + l;
-    a.out_top_ids[o] = l < n ? pos : -1;
-    a.out_top_logprobs[o] = l < n ? (float)((double)z - (double)m - X.L) : -INFINITY;
+    a.out_top_ids[o] = l < n ? pos[0] : -1;
+    a.out_top_logprobs[o] = l < n ? (float)((double)z[0] - (double)m - X.L) : -INFINITY;
   }
   if (R.greedy) {
-    res.id = __shfl(pos, 0);
-    res.zid = __shfl(z, 0);
+    res.id = lane_i32(pos[0], 0);
+    res.zid = lane_f32(z[0], 0);
   } else if (a.mode == 0) {
     // inverse CDF in ascending token id over the kept prefix: rank the kept entries by position
-    const int kp = l < nS ? pos : INT32_MAX;
-    s.l_p[l] = kp;  // lanes >= nS pad with positions above every real one
-    int r2 = 0;
-#pragma unroll 16
-    for (int i = 0; i < 64; ++i) r2 += s.l_p[i] < kp ? 1 : 0;
-    if (l < nS) {
-      s.l_w[r2] = w;
-      s.sk[r2] = ((uint64_t)(uint32_t)pos << 32) | (uint32_t)l;
+    int kp[2], r2[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) kp[q] = l + 64 * q < nS ? pos[q] : INT32_MAX;  // padding sorts last
+    s.l_p[l] = kp[0];
+    s.l_p[l + 64] = kp[1];
+    rank2(s.l_p, nr, two, kp, r2, [](int k, int v) { return v < k; });
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+      if (l + 64 * q < nS) {
+        s.l_w[r2[q]] = w[q];
+        s.sk[r2[q]] = ((uint64_t)(uint32_t)pos[q] << 32) | (uint32_t)(l + 64 * q);
+      }
+    float ws[2], c2[2];
+    uint64_t k2[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const bool in = l + 64 * q < nS;
+      ws[q] = in ? s.l_w[l + 64 * q] : 0.f;
+      k2[q] = in ? s.sk[l + 64 * q] : 0ull;
     }
-    const float ws = l < nS ? s.l_w[l] : 0.f;
-    const uint64_t k2 = l < nS ? s.sk[l] : 0ull;
-    const int src = (int)(uint32_t)k2;
-    const float c2 = wave_incl_scan(ws);
-    const float t = R.u * __shfl(c2, nS - 1);
-    const uint64_t hit = __ballot(l < nS && c2 > t);
-    int sel;
-    if (hit) {
-      sel = __ffsll((unsigned long long)hit) - 1;
-    } else {  // rounding left the cumulative at u: the last positive weight
-      const uint64_t pz = __ballot(l < nS && ws > 0.f);
-      sel = pz ? 63 - __clzll((long long)pz) : -1;
+    c2[0] = wave_incl_scan(ws[0]);
+    c2[1] = lane_f32(c2[0], 63) + wave_incl_scan(ws[1]);
+    const float t = R.u * at2f(c2, nS - 1);
+    int sel = first_of2(__ballot(l < nS && c2[0] > t), __ballot(l + 64 < nS && c2[1] > t));
+    if (sel < 0) {  // rounding left the cumulative at u: the last positive weight
+      const uint64_t p0 = __ballot(l < nS && ws[0] > 0.f), p1 = __ballot(l + 64 < nS && ws[1] > 0.f);
+      sel = p1 ? 64 + 63 - __clzll((long long)p1) : (p0 ? 63 - __clzll((long long)p0) : -1);
     }
     if (sel >= 0) {
-      res.id = (int)(__shfl(k2, sel) >> 32);
-      res.zid = __shfl(z, __shfl(src, sel));
+      const uint64_t ks = sel < 64 ? lane_u64(k2[0], sel) : lane_u64(k2[1], sel - 64);
+      res.id = (int)(ks >> 32);
+      res.zid = at2f(z, (int)(uint32_t)ks);
     }
   }
   return res;
@@ -1649,13 +1666,8 @@ __device__ __forceinline__ uint32_t finish_presence(Smem& s, const RowState& R, 
       constexpr int WPL = NWORDS / 64;
       uint32_t cnt = 0;
       for (int i = lane * WPL; i < (lane + 1) * WPL; ++i) cnt += __popc(s.bitmap[i]);
-      uint32_t incl = cnt;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t t = __shfl_up(incl, o);
-        if (lane >= o) incl += t;
-      }
-      if (__shfl(incl, 63) > cap) {
+      const uint32_t incl = wave_incl_scan_u(cnt);
+      if (lane_u32(incl, 63) > cap) {
         flags |= FLAG_LIMIT;
         uint32_t before = incl - cnt;  // keep the lowest positions within the capacity
         for (int i = lane * WPL; i < (lane + 1) * WPL; ++i) {
@@ -1710,13 +1722,8 @@ __device__ __forceinline__ void build_ranks(Smem& s, const RowState& R, const in
       const uint4 w = own[i];
       cnt += __popc(w.x) + __popc(w.y) + __popc(w.z) + __popc(w.w);
     }
-    uint32_t incl = cnt;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t t = __shfl_up(incl, o);
-      if (lane >= o) incl += t;
-    }
-    n_body = (int)__shfl(incl, 63);
+    const uint32_t incl = wave_incl_scan_u(cnt);
+    n_body = (int)lane_u32(incl, 63);
     uint32_t before = incl - cnt;
     uint2* pref = reinterpret_cast<uint2*>(s.wpref + lane * WPL);  // 4 prefixes per 8-byte store
 #pragma unroll 4
@@ -1757,12 +1764,7 @@ __device__ __forceinline__ float kth_from_hist(const Smem& s, int K) {
   const uint32_t c0 = s.kh_cnt[255 - 4 * l], c1 = s.kh_cnt[254 - 4 * l], c2 = s.kh_cnt[253 - 4 * l],
                  c3 = s.kh_cnt[252 - 4 * l];
   const uint32_t own = c0 + c1 + c2 + c3;
-  uint32_t incl = own;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t t = __shfl_up(incl, o);
-    if (l >= o) incl += t;
-  }
+  const uint32_t incl = wave_incl_scan_u(own);
   const uint64_t hit = __ballot(incl >= (uint32_t)K);
   if (!hit) return -INFINITY;
   const int first = __ffsll((unsigned long long)hit) - 1;
@@ -1774,7 +1776,7 @@ __device__ __forceinline__ float kth_from_hist(const Smem& s, int K) {
     else if ((cum += c2) >= (uint32_t)K) c = 253 - 4 * l;
     else c = 252 - 4 * l;
   }
-  c = __shfl(c, first);
+  c = lane_i32(c, first);
   uint32_t mk = 0xffffffffu;
   if (255 - 4 * l >= c) mk = min(mk, s.kh_min[255 - 4 * l]);
   if (254 - 4 * l >= c) mk = min(mk, s.kh_min[254 - 4 * l]);
@@ -2189,7 +2191,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
           for (int e = 0; e < DT::VEC; ++e) cm |= (canon(DT::get(dd[k], e), r) >= bl ? 1u : 0u) << (8 * k + e);
         const int c = __popc(cm);
         const int incl = wave_incl_scan_i(c);
-        const int total = __shfl(incl, 63);
+        const int total = lane_i32(incl, 63);
         if (total > 0) {
           int base = 0;
           if (lane_id() == 0) base = atomicAdd(&s.n_list, total);
@@ -2240,7 +2242,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       // empty row or NaN / +inf values: nothing to resolve
     } else if (!overflow) {
       if (leader) {
-        if (X.n_list <= 64) {
+        if (X.n_list <= SMALL_LIST) {
           if (wave_id() == 0) res = resolve_small(oa, s, R, X, res);
           if (a.mode == 1) {  // every thread needs the kept set for the dense output
             if (threadIdx.x == 0) {
