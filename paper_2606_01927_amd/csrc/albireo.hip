@@ -35,6 +35,13 @@ namespace {
 constexpr int NT = 512;           // threads per workgroup (2 waves per SIMD, 256 VGPRs each)
 constexpr int NW = NT / 64;       // waves per workgroup
 constexpr int JMAX = 38;          // 16-byte register slots per thread (152 VGPRs of row data)
+// Instantiated slot counts: a chunk of n slots runs on the smallest J with n <= J * NT, so a
+// single-chunk row of that kernel has more than (previous size) * NT slots (less one for the
+// unaligned head) and every thread's first live_slots_min(J) slots are live.
+constexpr int JSIZES[4] = {8, 16, 32, JMAX};
+__host__ __device__ constexpr int live_slots_min(int J) {
+  return J == JSIZES[3] ? JSIZES[2] : J == JSIZES[2] ? JSIZES[1] : J == JSIZES[1] ? JSIZES[0] : 0;
+}
 constexpr int UCAP = ALBIREO_MAX_UNIQUE_HISTORY;  // tracked distinct ids (history + head/tail)
 constexpr int NWORDS = JMAX * NT / 4;             // presence bitmap words (one byte per register slot)
 constexpr int LCAP = 2048;        // candidate list capacity
@@ -141,7 +148,7 @@ struct WsLayout {
 // order-preserving 32-bit key of a float (larger float -> larger key); -inf maps above 0
 __device__ __forceinline__ uint32_t f2key(float f) {
   const uint32_t u = __float_as_uint(f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);  // negative: ~u, else u | sign bit
 }
 __device__ __forceinline__ float key2f(uint32_t k) {
   const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
@@ -1598,6 +1605,8 @@ __device__ __forceinline__ void count_history_id(Smem& s, const RowState& R, int
   s.x_pos[u] = id;  // every counting thread of this id writes the same value
 }
 
+// s_waitcnt immediate for vmcnt(0) alone (expcnt and lgkmcnt at their maxima)
+constexpr int WAIT_VM0 = 0x0F70;
 constexpr int HSTAGE = 3 * LCAP;  // history ids staged in LDS at once (the list arrays, unused until
                                   // the candidate list is resolved)
 
@@ -1658,6 +1667,8 @@ __device__ __forceinline__ uint32_t finish_presence(Smem& s, const RowState& R, 
           if (code >= 0) atomicOr(&s.bitmap[code >> 5], 1u << (code & 31));
         }
       }
+      // the direct-to-LDS loads are complete here, so the publication below waits for LDS only
+      __builtin_amdgcn_s_waitcnt(WAIT_VM0);
     }
     flags = wave_or(flags);
     const uint32_t cap = (uint32_t)(UCAP - n_ht);
@@ -1689,7 +1700,7 @@ __device__ __forceinline__ uint32_t finish_presence(Smem& s, const RowState& R, 
       }
     }
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");  // LDS only: row loads stay in flight
   if (lane == 0) atomicAdd(&s.ready, 1u);
   return flags;
 }
@@ -1751,8 +1762,9 @@ __device__ __forceinline__ void build_ranks(Smem& s, const RowState& R, const in
       stage_history(s, hist_ids, b, n);
       for (int i = lane; i < n; i += 64) count_history_id<DT>(s, R, hst[i]);
     }
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0);  // as in finish_presence
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");  // LDS only: row loads stay in flight
   if (lane == 0) atomicAdd(&s.ready, 1u);
 }
 
@@ -1807,6 +1819,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     // merged at the join, which waits for the load.
     Chunk<DT, J> ch;
     constexpr int PIPE = J < 8 ? J : 8;
+    constexpr int JLO = MULTI ? 0 : live_slots_min(J);
     const int nslots = (int)(R.s1 - R.s0);
     // one buffer resource per chunk (SGPRs) and a 32-bit lane offset; its inputs are made visibly
     // wave-uniform so the descriptor lives in SGPRs
@@ -1897,7 +1910,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
         }
       }
       bad = wave_or(bad);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");  // LDS only: row loads stay in flight
       if (lane_id() == 0) {
         if (bad) atomicOr(&s.flags, bad);
         atomicAdd(&s.ready, 1u);
@@ -1924,48 +1937,56 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     // the -inf pattern in a register, so that masking is one bit-select per word
     uint32_t neg;
     asm volatile("s_mov_b32 %0, %1" : "=s"(neg) : "i"(DT::NEG));
-    uint32_t code_lo = 0;  // slot-maximum code of the even slot of the current pair
-    static_for<J>([&](auto jc) __attribute__((always_inline)) {
-      constexpr int j = decltype(jc)::value;
-      if constexpr (j + PIPE < J) issue(std::integral_constant<int, j + PIPE>{});
-      if (j >= jfull) {  // wave-uniform: the partly filled tail slots
-        const bool dead = j * NT + (int)threadIdx.x >= nslots;
-        uint4 dj = ch.template get<j>();
-        dj.x = dead ? DT::NEG : dj.x;
-        dj.y = dead ? DT::NEG : dj.y;
-        dj.z = dead ? DT::NEG : dj.z;
-        dj.w = dead ? DT::NEG : dj.w;
-        ch.template set<j>(dj);
-      }
-      if (R.pen_on) {
-        const int sl = j * NT + threadIdx.x;
-        const uint32_t byte = (s.bitmap[sl >> 2] >> ((sl & 3) * 8)) & 255u;
-        const uint4 mk = s.masktab[byte];
-        uint4 dj = ch.template get<j>();
-        dj.x = (neg & mk.x) | (dj.x & ~mk.x);
-        dj.y = (neg & mk.y) | (dj.y & ~mk.y);
-        dj.z = (neg & mk.z) | (dj.z & ~mk.z);
-        dj.w = (neg & mk.w) | (dj.w & ~mk.w);
-        ch.template set<j>(dj);
-      }
-      const uint4 dcur = ch.template get<j>();
-      float v[DT::VEC];
+    // slots are taken in pairs: one reference test and one running-maximum update per pair
+    static_for<J / 2>([&](auto pc) __attribute__((always_inline)) {
+      constexpr int j0 = 2 * decltype(pc)::value;
+      if constexpr (j0 + PIPE < J) issue(std::integral_constant<int, j0 + PIPE>{});
+      if constexpr (j0 + 1 + PIPE < J) issue(std::integral_constant<int, j0 + 1 + PIPE>{});
+      float v[2][DT::VEC], sm[2];
+      static_for<2>([&](auto hc) __attribute__((always_inline)) {
+        constexpr int h = decltype(hc)::value;
+        constexpr int j = j0 + h;
+        // only slots at or past JLO can be partly filled (the host picks J so that the first JLO
+        // slots of every thread are live)
+        if constexpr (j >= JLO) {
+          if (j >= jfull) {  // wave-uniform: the partly filled tail slots
+            const bool dead = j * NT + (int)threadIdx.x >= nslots;
+            uint4 dj = ch.template get<j>();
+            dj.x = dead ? DT::NEG : dj.x;
+            dj.y = dead ? DT::NEG : dj.y;
+            dj.z = dead ? DT::NEG : dj.z;
+            dj.w = dead ? DT::NEG : dj.w;
+            ch.template set<j>(dj);
+          }
+        }
+        if (R.pen_on) {
+          const int sl = j * NT + threadIdx.x;
+          const uint32_t byte = (s.bitmap[sl >> 2] >> ((sl & 3) * 8)) & 255u;
+          const uint4 mk = s.masktab[byte];
+          uint4 dj = ch.template get<j>();
+          dj.x = (neg & mk.x) | (dj.x & ~mk.x);
+          dj.y = (neg & mk.y) | (dj.y & ~mk.y);
+          dj.z = (neg & mk.z) | (dj.z & ~mk.z);
+          dj.w = (neg & mk.w) | (dj.w & ~mk.w);
+          ch.template set<j>(dj);
+        }
+        const uint4 dcur = ch.template get<j>();
 #pragma unroll
-      for (int e = 0; e < DT::VEC; ++e) v[e] = DT::get(dcur, e);
-      float smax = v[0];
+        for (int e = 0; e < DT::VEC; ++e) v[h][e] = DT::get(dcur, e);
+        float mx = v[h][0];
 #pragma unroll
-      for (int e = 1; e < DT::VEC; ++e) smax = fmaxf(smax, v[e]);
-      xm = fmaxf(xm, smax);
-      if constexpr (j % 2 == 0) {
-        code_lo = f2key(smax) >> 16;
-        if constexpr (j + 1 == J) s.scode[(j / 2) * NT + threadIdx.x] = code_lo;
-      } else {
-        s.scode[(j / 2) * NT + threadIdx.x] = code_lo | (f2key(smax) & 0xffff0000u);
-      }
+        for (int e = 1; e < DT::VEC; ++e) mx = fmaxf(mx, v[h][e]);
+        sm[h] = mx;
+      });
+      xm = fmaxf(xm, fmaxf(sm[0], sm[1]));
+      // 16-bit slot-maximum codes, two per word (slot-pair-major)
+      if constexpr (j0 + 1 < J)
+        s.scode[(j0 / 2) * NT + threadIdx.x] = __builtin_amdgcn_perm(f2key(sm[1]), f2key(sm[0]), 0x07060302u);
       // sums run over the canonical z = fl32(x r) (exactly what the logprobs are defined on), as
       // 2^(z L2E - mref) with a reference mref in log2 units
-      if (smax > xthr) {
-        const float sref = (smax * rr) * L2E;
+      const float pm = fmaxf(sm[0], sm[1]);
+      if (pm > xthr) {
+        const float sref = (pm * rr) * L2E;
         if (sref > mref + 32.0f) {  // move the reference lazily: exp2 arguments stay below 32
           const float f = __builtin_amdgcn_exp2f(mref - sref);
           acc0 *= f;
@@ -1977,12 +1998,14 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
         }
       }
 #pragma unroll
-      for (int e = 0; e < DT::VEC; e += 4) {
-        acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 0] * rr, L2E, -mref));
-        acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 1] * rr, L2E, -mref));
-        acc2 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 2] * rr, L2E, -mref));
-        acc3 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[e + 3] * rr, L2E, -mref));
-      }
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e = 0; e < DT::VEC; e += 4) {
+          acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 0] * rr, L2E, -mref));
+          acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 1] * rr, L2E, -mref));
+          acc2 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 2] * rr, L2E, -mref));
+          acc3 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 3] * rr, L2E, -mref));
+        }
     });
     float ssum = (acc0 + acc1) + (acc2 + acc3);
 
@@ -2464,10 +2487,10 @@ KernelInfo pick_kernel(int64_t chunk_slots, bool multi) {
   (void)chunk_slots;
   return kinfo<DT, ALBIREO_DEV_ONE_J>(multi);
 #else
-  if (chunk_slots <= 8 * NT) return kinfo<DT, 8>(multi);
-  if (chunk_slots <= 16 * NT) return kinfo<DT, 16>(multi);
-  if (chunk_slots <= 32 * NT) return kinfo<DT, 32>(multi);
-  return kinfo<DT, JMAX>(multi);
+  if (chunk_slots <= (int64_t)JSIZES[0] * NT) return kinfo<DT, JSIZES[0]>(multi);
+  if (chunk_slots <= (int64_t)JSIZES[1] * NT) return kinfo<DT, JSIZES[1]>(multi);
+  if (chunk_slots <= (int64_t)JSIZES[2] * NT) return kinfo<DT, JSIZES[2]>(multi);
+  return kinfo<DT, JSIZES[3]>(multi);
 #endif
 }
 
@@ -2535,6 +2558,12 @@ hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& 
   G.P = (int)P;
   G.chunk_slots = (max_body + P - 1) / P;
   G.k = dtype == ALBIREO_BF16 ? pick_kernel<BF16T>(G.chunk_slots, G.P > 1) : pick_kernel<F32T>(G.chunk_slots, G.P > 1);
+  // the single-chunk kernel skips the dead-slot test below live_slots_min(J) (always true for the
+  // size pick_kernel chose; a build restricted to one size can miss it for small rows)
+  if (G.P == 1 && max_body - 1 < (int64_t)live_slots_min(G.k.J) * NT) {
+    G.ok = false;
+    return hipSuccess;
+  }
   G.smem = sizeof(Smem);
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
