@@ -1028,142 +1028,241 @@ __device__ bool radix_select(Smem& s, const RowState& R, const RowCtx& X, float 
 }
 
 // ----------------------------------------------------------------------------------------------
-// Single-wave resolution of a candidate list of at most 2 * 64 entries (wave 0 of the leader): lane l
-// holds entries l and l + 64.  Entries are ordered by rank rather than by a sorting network: each
-// entry counts the larger keys with broadcast LDS reads and is scattered to its rank, a few hundred
-// cycles against the long exchange chains of a sort.  Quantities indexed by a list position i are
-// read from lane i % 64 of half i / 64.
+// Workgroup resolution of a candidate list of at most 2 * 64 entries, by counting instead of
+// sorting.  Every wave holds entries l and l + 64 in lane l and accumulates, over every NW-th list
+// entry, how many entries lie strictly above each of its own (larger z) and their mass; the totals
+// meet in LDS.  Then, with K, p, u of the row:
+//   S2 (top-k, ties kept)  = entries with fewer than K entries strictly above, z >= the min-p bound;
+//   kept (top-p)           = S2 entries whose mass strictly above is below p Z2 (so whole tie groups
+//                            enter in descending z until the cumulative mass reaches p Z2; the top
+//                            group always enters);
+//   drawn                  = the kept entry whose id-ordered exclusive prefix of kept mass is at or
+//                            below u times the kept mass, with its own mass ending above it.
+// Masses are fixed point (2^24 per unit, round to nearest; every weight exp(z - m) <= 1), so every
+// sum is exact and independent of the order in which the gather left the entries.
+// ----------------------------------------------------------------------------------------------
 constexpr int SMALL_LIST = 128;
+constexpr float WFIX = 16777216.0f;        // 2^24
+constexpr double WFIX40 = 1099511627776.0;  // 2^40 (kept mass reported as a float)
+__device__ __forceinline__ uint32_t wfix(float w) { return (uint32_t)__builtin_fmaf(w, WFIX, 0.5f); }
 
-// rank of each of this lane's two keys among the first nr keys of arr (broadcast reads); with one
-// half in use only the first key is ranked
-template <class T, class Less>
-__device__ __forceinline__ void rank2(const T* arr, int nr, bool two, const T (&k)[2], int (&r)[2], Less less) {
-  r[0] = 0;
-  r[1] = 0;
-  if (two) {
-#pragma unroll 8
-    for (int i = 0; i < nr; ++i) {
-      const T v = arr[i];
-      r[0] += less(k[0], v) ? 1 : 0;
-      r[1] += less(k[1], v) ? 1 : 0;
+// LDS totals of the counting resolver, in the general path's histogram (unused by this path)
+struct CountArrays {
+  uint32_t* above;  // entries strictly above
+  uint32_t* mass;   // their mass
+  uint32_t* lower;  // kept mass at lower ids
+  uint32_t* ties;   // entries of equal z at lower ids (top-n ranks)
+};
+__device__ __forceinline__ CountArrays count_arrays(Smem& s) {
+  uint32_t* b = reinterpret_cast<uint32_t*>(s.hist);
+  return {b, b + SMALL_LIST, b + 2 * SMALL_LIST, b + 3 * SMALL_LIST};
+}
+static_assert(sizeof(Smem::hist) >= 4 * SMALL_LIST * sizeof(uint32_t), "counting totals do not fit");
+__device__ __forceinline__ void clear_count_arrays(Smem& s) {  // any thread set covering 0..127
+  if (threadIdx.x < SMALL_LIST) reinterpret_cast<uint4*>(s.hist)[threadIdx.x] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// one lane's entries: z, position, fixed-point weight, presence
+struct Entries {
+  float z[2];
+  int pos[2];
+  uint32_t wf[2];
+  float w[2];
+  bool in[2];
+};
+
+// accumulate over list entries i = first, first + NW, ... < n (NQ halves in use; TIE: also count
+// equal z at lower ids)
+template <int NQ, bool TIE>
+__device__ __forceinline__ void count_above(const Smem& s, int n, float m, const Entries& E, uint32_t (&c)[2],
+                                            uint32_t (&g)[2], uint32_t (&t)[2]) {
+  for (int i = wave_id(); i < n; i += NW) {
+    const uint64_t k = s.sk[i];
+    const float zi = cand_z(k);
+    const uint32_t wi = wfix(__expf(zi - m));
+    const int pi = cand_pos(k);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const bool gt = zi > E.z[q];
+      c[q] += gt ? 1u : 0u;
+      g[q] += gt ? wi : 0u;
+      if constexpr (TIE) t[q] += (zi == E.z[q] && pi < E.pos[q]) ? 1u : 0u;
     }
-  } else {
-#pragma unroll 16
-    for (int i = 0; i < nr; ++i) r[0] += less(k[0], arr[i]) ? 1 : 0;
   }
 }
-__device__ __forceinline__ float at2f(const float (&v)[2], int i) {
-  return i < 64 ? lane_f32(v[0], i) : lane_f32(v[1], i - 64);
-}
-__device__ __forceinline__ int first_of2(uint64_t b0, uint64_t b1) {
-  return b0 ? __ffsll((unsigned long long)b0) - 1 : (b1 ? 64 + __ffsll((unsigned long long)b1) - 1 : -1);
+
+// accumulate the kept mass at lower ids over kept entries i = first, first + NW, ... < n
+template <int NQ>
+__device__ __forceinline__ void mass_below(const Smem& s, int n, float m, const Entries& E, uint64_t k0,
+                                           uint64_t k1, uint32_t (&x)[2]) {
+  for (int i = wave_id(); i < n; i += NW) {
+    const uint64_t bits = i < 64 ? k0 : k1;
+    if (!((bits >> (i & 63)) & 1ull)) continue;  // wave-uniform
+    const uint64_t k = s.sk[i];
+    const uint32_t wi = wfix(__expf(cand_z(k) - m));
+    const int pi = cand_pos(k);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) x[q] += pi < E.pos[q] ? wi : 0u;
+  }
 }
 
-__device__ __forceinline__ Resolution resolve_small(const OutArgs& a, Smem& s, const RowState& R, const RowCtx& X,
+// Every thread of the workgroup calls this (it holds barriers).  The counting is spread over all
+// waves; wave 0 decides the kept set, and the waves then split the id-ordered mass of the draw.
+// Every thread receives res.id / res.zid; in mode 1 also the kept set's tau, zs, zmin and size.
+__device__ __forceinline__ Resolution resolve_count(const OutArgs& a, Smem& s, const RowState& R, const RowCtx& X,
                                                     Resolution res) {
   const int l = lane_id();
   const int n = X.n_list;
   const bool two = n > 64;
-  const int nr = two ? 128 : 64;
   const float m = X.m;
-  // rank in (z descending, position ascending): keys are distinct, padding keys (0) rank below all
-  uint64_t key[2];
-  int rk[2];
-#pragma unroll
-  for (int q = 0; q < 2; ++q) key[q] = l + 64 * q < n ? s.sk[l + 64 * q] : 0ull;
-  s.sk[l] = key[0];
-  s.sk[l + 64] = key[1];
-  rank2(s.sk, nr, two, key, rk, [](uint64_t k, uint64_t v) { return v > k; });
-#pragma unroll
-  for (int q = 0; q < 2; ++q)
-    if (l + 64 * q < n) {
-      s.l_z[rk[q]] = cand_z(key[q]);
-      s.l_p[rk[q]] = cand_pos(key[q]);
-    }
-  float z[2], w[2];
-  int pos[2];
+  const CountArrays A = count_arrays(s);
+  Entries E;
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
-    const bool in = l + 64 * q < n;
-    z[q] = in ? s.l_z[l + 64 * q] : -INFINITY;
-    pos[q] = in ? s.l_p[l + 64 * q] : -1;
-    w[q] = in ? __expf(z[q] - m) : 0.f;
+    const int e = l + 64 * q;
+    E.in[q] = e < n;
+    const uint64_t k = E.in[q] ? s.sk[e] : 0ull;
+    E.z[q] = E.in[q] ? cand_z(k) : -INFINITY;
+    E.pos[q] = E.in[q] ? cand_pos(k) : INT32_MAX;
+    E.w[q] = E.in[q] ? __expf(E.z[q] - m) : 0.f;
+    E.wf[q] = E.in[q] ? wfix(E.w[q]) : 0u;
   }
-  int nS;
-  if (R.greedy) {
-    nS = 1;
-  } else {
-    float tau2 = X.tau_m;
-    if (R.k_on && R.k <= n) tau2 = fmaxf(tau2, at2f(z, R.k - 1));
-    const bool in0 = l < n && z[0] >= tau2, in1 = l + 64 < n && z[1] >= tau2;
-    const int n2 = __popcll(__ballot(in0)) + __popcll(__ballot(in1));  // S2 is a prefix of the list
-    nS = n2;
-    if (R.topp_on) {
-      float c[2];
-      c[0] = wave_incl_scan(in0 ? w[0] : 0.f);
-      c[1] = lane_f32(c[0], 63) + wave_incl_scan(in1 ? w[1] : 0.f);
-      const float Z2 = (R.k_on || R.minp_on) ? at2f(c, n2 - 1) : X.zfull;
-      const float target = R.p * Z2;
-      const int first = first_of2(__ballot(in0 && c[0] >= target), __ballot(in1 && c[1] >= target));
-      if (first >= 0) {  // the nucleus closes at the end of that tie group
-        const float zc = at2f(z, first);
-        nS = __popcll(__ballot(l < n2 && z[0] >= zc)) + __popcll(__ballot(l + 64 < n2 && z[1] >= zc));
-      }
-    }
-  }
-  res.kept = nS;
-  res.zmin = at2f(z, nS - 1);
-  res.tau = res.zmin;
+  const bool rank_top = a.mode == 0 && a.n_top > 0;
   {
-    float c[2];
-    c[0] = wave_incl_scan(l < nS ? w[0] : 0.f);
-    c[1] = lane_f32(c[0], 63) + wave_incl_scan(l + 64 < nS ? w[1] : 0.f);
-    res.zs = at2f(c, nS - 1);
-  }
-  res.id_here = 1;
-  if (a.mode == 0 && a.n_top > 0 && l < a.n_top) {  // n_top <= 64: the first half
-    const int64_t o = R.row * a.n_top + l;
-    a.out_top_ids[o] = l < n ? pos[0] : -1;
-    a.out_top_logprobs[o] = l < n ? (float)((double)z[0] - (double)m - X.L) : -INFINITY;
-  }
-  if (R.greedy) {
-    res.id = lane_i32(pos[0], 0);
-    res.zid = lane_f32(z[0], 0);
-  } else if (a.mode == 0) {
-    // inverse CDF in ascending token id over the kept prefix: rank the kept entries by position
-    int kp[2], r2[2];
-#pragma unroll
-    for (int q = 0; q < 2; ++q) kp[q] = l + 64 * q < nS ? pos[q] : INT32_MAX;  // padding sorts last
-    s.l_p[l] = kp[0];
-    s.l_p[l + 64] = kp[1];
-    rank2(s.l_p, nr, two, kp, r2, [](int k, int v) { return v < k; });
-#pragma unroll
-    for (int q = 0; q < 2; ++q)
-      if (l + 64 * q < nS) {
-        s.l_w[r2[q]] = w[q];
-        s.sk[r2[q]] = ((uint64_t)(uint32_t)pos[q] << 32) | (uint32_t)(l + 64 * q);
-      }
-    float ws[2], c2[2];
-    uint64_t k2[2];
+    uint32_t c[2] = {0u, 0u}, g[2] = {0u, 0u}, t[2] = {0u, 0u};
+    if (two) {
+      if (rank_top) count_above<2, true>(s, n, m, E, c, g, t);
+      else count_above<2, false>(s, n, m, E, c, g, t);
+    } else {
+      if (rank_top) count_above<1, true>(s, n, m, E, c, g, t);
+      else count_above<1, false>(s, n, m, E, c, g, t);
+    }
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const bool in = l + 64 * q < nS;
-      ws[q] = in ? s.l_w[l + 64 * q] : 0.f;
-      k2[q] = in ? s.sk[l + 64 * q] : 0ull;
+      const int e = l + 64 * q;
+      if (E.in[q]) {
+        if (c[q]) atomicAdd(&A.above[e], c[q]);
+        if (g[q]) atomicAdd(&A.mass[e], g[q]);
+        if (t[q]) atomicAdd(&A.ties[e], t[q]);
+      }
     }
-    c2[0] = wave_incl_scan(ws[0]);
-    c2[1] = lane_f32(c2[0], 63) + wave_incl_scan(ws[1]);
-    const float t = R.u * at2f(c2, nS - 1);
-    int sel = first_of2(__ballot(l < nS && c2[0] > t), __ballot(l + 64 < nS && c2[1] > t));
-    if (sel < 0) {  // rounding left the cumulative at u: the last positive weight
-      const uint64_t p0 = __ballot(l < nS && ws[0] > 0.f), p1 = __ballot(l + 64 < nS && ws[1] > 0.f);
-      sel = p1 ? 64 + 63 - __clzll((long long)p1) : (p0 ? 63 - __clzll((long long)p0) : -1);
+  }
+  __syncthreads();
+  const bool draw = a.mode == 0 && !R.greedy;
+  bool kept[2] = {false, false};
+  if (wave_id() == 0) {
+    uint32_t C[2], G[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      C[q] = E.in[q] ? A.above[l + 64 * q] : 0xffffffffu;
+      G[q] = E.in[q] ? A.mass[l + 64 * q] : 0xffffffffu;
     }
-    if (sel >= 0) {
-      const uint64_t ks = sel < 64 ? lane_u64(k2[0], sel) : lane_u64(k2[1], sel - 64);
-      res.id = (int)(ks >> 32);
-      res.zid = at2f(z, (int)(uint32_t)ks);
+    if (R.greedy) {  // the argmax with the lowest id
+      const int pmin = wave_min_i(min(C[0] == 0u ? E.pos[0] : INT32_MAX, C[1] == 0u ? E.pos[1] : INT32_MAX));
+#pragma unroll
+      for (int q = 0; q < 2; ++q) kept[q] = E.in[q] && C[q] == 0u && E.pos[q] == pmin;
+    } else {
+      bool s2[2];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) s2[q] = E.in[q] && (!R.k_on || C[q] < (uint32_t)R.k) && E.z[q] >= X.tau_m;
+      kept[0] = s2[0];
+      kept[1] = s2[1];
+      if (R.topp_on) {
+        // G < p Z2 for an integer G is G < ceil(p Z2)
+        const double Z2 = (R.k_on || R.minp_on)
+                              ? (double)(uint32_t)wave_sum_i((int)((s2[0] ? E.wf[0] : 0u) + (s2[1] ? E.wf[1] : 0u)))
+                              : (double)X.zfull * (double)WFIX;
+        const double tg = ceil((double)R.p * Z2);
+        const uint32_t target = tg <= 0.0 ? 0u : (tg >= 4294967295.0 ? 0xffffffffu : (uint32_t)tg);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) kept[q] = s2[q] && (G[q] == 0u || G[q] < target);
+      }
+    }
+    const uint64_t kb0 = __ballot(kept[0]), kb1 = __ballot(kept[1]);
+    if (rank_top) {  // the n_top largest (ties -> lower id); padding past the list
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        if (E.in[q]) {
+          const uint32_t r = C[q] + A.ties[l + 64 * q];
+          if (r < (uint32_t)a.n_top) {
+            const int64_t o = R.row * a.n_top + r;
+            a.out_top_ids[o] = E.pos[q];
+            a.out_top_logprobs[o] = (float)((double)E.z[q] - (double)m - X.L);
+          }
+        }
+      if (l >= n && l < a.n_top) {
+        const int64_t o = R.row * a.n_top + l;
+        a.out_top_ids[o] = -1;
+        a.out_top_logprobs[o] = -INFINITY;
+      }
+    }
+    if (R.greedy) {
+      const int sel = kb0 ? __ffsll((unsigned long long)kb0) - 1 : 64 + __ffsll((unsigned long long)kb1) - 1;
+      res.id = sel < 64 ? lane_i32(E.pos[0], sel) : lane_i32(E.pos[1], sel - 64);
+      res.zid = sel < 64 ? lane_f32(E.z[0], sel) : lane_f32(E.z[1], sel - 64);
+    }
+    if (a.mode == 1) {
+      res.kept = __popcll(kb0) + __popcll(kb1);
+      res.zmin = wave_min(fminf(kept[0] ? E.z[0] : INFINITY, kept[1] ? E.z[1] : INFINITY));
+      uint64_t w40 = 0;
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        if (kept[q]) w40 += (uint64_t)__builtin_fma((double)E.w[q], WFIX40, 0.5);
+      res.zs = (float)((double)wave_sum_u64(w40) / WFIX40);
+    }
+    if (l == 0) {
+      s.bc_q[0] = kb0;
+      s.bc_q[1] = kb1;
+      if (a.mode == 1) {
+        s.bc_f[0] = res.zmin;
+        s.bc_f[1] = res.zs;
+        s.bc_i[1] = res.kept;
+      }
+      s.bc_i[0] = res.id;
+    }
+  }
+  if (draw || a.mode == 1) __syncthreads();  // kept set (and mode 1 results) published
+  if (wave_id() != 0 && (draw || a.mode == 1)) {
+    const uint64_t kb0 = s.bc_q[0], kb1 = s.bc_q[1];
+    kept[0] = E.in[0] && ((kb0 >> l) & 1ull);
+    kept[1] = E.in[1] && ((kb1 >> l) & 1ull);
+    if (a.mode == 1) {
+      res.zmin = s.bc_f[0];
+      res.zs = s.bc_f[1];
+      res.kept = s.bc_i[1];
+      res.id = s.bc_i[0];
+    }
+  }
+  res.tau = res.zmin;
+  res.id_here = 1;
+  if (draw) {
+    // the draw, in ascending id over the kept entries: the waves split the id-ordered mass
+    const uint64_t kb0 = __ballot(kept[0]), kb1 = __ballot(kept[1]);
+    {
+      uint32_t x[2] = {0u, 0u};
+      if (two) mass_below<2>(s, n, m, E, kb0, kb1, x);
+      else mass_below<1>(s, n, m, E, kb0, kb1, x);
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        if (kept[q] && x[q]) atomicAdd(&A.lower[l + 64 * q], x[q]);
+    }
+    __syncthreads();
+    if (wave_id() == 0) {
+      const uint32_t total = (uint32_t)wave_sum_i((int)((kept[0] ? E.wf[0] : 0u) + (kept[1] ? E.wf[1] : 0u)));
+      uint32_t tf = (uint32_t)((double)R.u * (double)total);
+      if (tf >= total) tf = total - 1u;
+      bool hit[2];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const uint32_t lo = kept[q] ? A.lower[l + 64 * q] : 0u;
+        hit[q] = kept[q] && lo <= tf && tf - lo < E.wf[q];
+      }
+      const uint64_t h0 = __ballot(hit[0]), h1 = __ballot(hit[1]);
+      if (h0 | h1) {
+        const int sel = h0 ? __ffsll((unsigned long long)h0) - 1 : 64 + __ffsll((unsigned long long)h1) - 1;
+        res.id = sel < 64 ? lane_i32(E.pos[0], sel) : lane_i32(E.pos[1], sel - 64);
+        res.zid = sel < 64 ? lane_f32(E.z[0], sel) : lane_f32(E.z[1], sel - 64);
+      }
     }
   }
   return res;
@@ -2044,6 +2143,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       }
     }
     __syncthreads();  // A
+    clear_count_arrays(s);  // totals of the counting resolver (read after barrier D)
     float bm = s.wp[0][0], bs = s.wp[1][0], bxm = s.wp[2][0], thi = s.wp[3][0], tlo = s.wp[4][0];
 #pragma unroll
     for (int w = 1; w < NW; ++w) {
@@ -2266,18 +2366,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     } else if (!overflow) {
       if (leader) {
         if (X.n_list <= SMALL_LIST) {
-          if (wave_id() == 0) res = resolve_small(oa, s, R, X, res);
-          if (a.mode == 1) {  // every thread needs the kept set for the dense output
-            if (threadIdx.x == 0) {
-              s.bc_f[0] = res.tau;
-              s.bc_f[1] = res.zs;
-              s.bc_i[0] = res.id;
-            }
-            __syncthreads();
-            res.tau = s.bc_f[0];
-            res.zs = s.bc_f[1];
-            res.id = s.bc_i[0];
-          }
+          res = resolve_count(oa, s, R, X, res);  // every thread holds the result
         } else {
           res = resolve_list(oa, s, R, X, res);
         }
