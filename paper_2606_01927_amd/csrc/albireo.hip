@@ -106,7 +106,7 @@ struct GroupSync {
   uint32_t pad[61];
 };
 struct ChunkStats {  // published by every chunk workgroup of a row
-  float xm;          // max x over the chunk
+  float xm;          // max of the products x r over the chunk
   float mref;        // reference of s (log2 units)
   float s;           // sum of 2^(z*L2E - mref)
   uint32_t flags;
@@ -521,16 +521,6 @@ __device__ __forceinline__ int next_pow2(int n) {
   int p = 2;
   while (p < n) p <<= 1;
   return p;
-}
-
-// A threshold bx with canon(x r) >= bl  =>  x >= bx, for r > 0 (fl(x r) is monotone in x): the
-// quotient bl / r lowered by a relative 2^-20 plus the smallest normal, which covers the rounding of
-// both the quotient and the product.
-__device__ __forceinline__ float x_threshold(float bl, float r) {
-  if (!(bl > -INFINITY)) return -INFINITY;
-  const float q = (float)((double)bl / (double)r);
-  if (!isfinite(q)) return -INFINITY;  // no useful prefilter: every slot is checked exactly
-  return q - (fabsf(q) * 9.5367431640625e-07f + 1.1754943508222875e-38f);
 }
 
 // ----------------------------------------------------------------------------------------------
@@ -2026,13 +2016,22 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     // ---------------- online max / sum-exp over the registers ----------------
     // The reference starts finite: a -inf element then gives exp2(-inf) = 0 rather than NaN, and the
     // first finite slot always moves the reference before anything is accumulated against it.
-    float xm = -INFINITY, mref = MREF0;
+    // Maxima are taken over the products x r (the processed logits before the +0 that canonicalises
+    // -0), which the sums need anyway; being results of arithmetic they need no quieting before a
+    // max.  fl(x r) is monotone in x, so these are the products of the x maxima.
+    float xm = -INFINITY, mref = MREF0;  // xm: this thread's maximum product
+    // The thread's best slot pair so far (its data, pair index; xm is its maximum) and the largest
+    // maximum of its other pairs: the gather tests the best pair from this copy, and only a thread
+    // whose other pairs may reach the bound goes through the slot-by-slot pass.
+    uint4 bd0 = make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG), bd1 = bd0;
+    int bj = 0;
+    float b2 = -INFINITY;
     float acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
     const float rr = R.r;
-    // the reference moves when a slot maximum x gives z L2E above mref + 32; xthr is that point in x
+    // the reference moves when a pair maximum gives z L2E above mref + 32; zthr is that point in z
     // units lowered by one (log2) unit, a cheap filter in front of the exact test
-    const float inv_c = 1.0f / (rr * L2E);
-    float xthr = (mref + 31.0f) * inv_c;
+    constexpr float INV_L2E = 0.693147180559945309f;
+    float zthr = (mref + 31.0f) * INV_L2E;
     // the -inf pattern in a register, so that masking is one bit-select per word
     uint32_t neg;
     asm volatile("s_mov_b32 %0, %1" : "=s"(neg) : "i"(DT::NEG));
@@ -2042,6 +2041,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       if constexpr (j0 + PIPE < J) issue(std::integral_constant<int, j0 + PIPE>{});
       if constexpr (j0 + 1 + PIPE < J) issue(std::integral_constant<int, j0 + 1 + PIPE>{});
       float v[2][DT::VEC], sm[2];
+      uint4 dc[2];
       static_for<2>([&](auto hc) __attribute__((always_inline)) {
         constexpr int h = decltype(hc)::value;
         constexpr int j = j0 + h;
@@ -2070,22 +2070,41 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
           ch.template set<j>(dj);
         }
         const uint4 dcur = ch.template get<j>();
+        dc[h] = dcur;
 #pragma unroll
-        for (int e = 0; e < DT::VEC; ++e) v[h][e] = DT::get(dcur, e);
+        for (int e = 0; e < DT::VEC; ++e) v[h][e] = DT::get(dcur, e) * rr;
         float mx = v[h][0];
 #pragma unroll
         for (int e = 1; e < DT::VEC; ++e) mx = fmaxf(mx, v[h][e]);
         sm[h] = mx;
       });
-      xm = fmaxf(xm, fmaxf(sm[0], sm[1]));
+      const float pm = fmaxf(sm[0], sm[1]);
+      {
+        const bool nb = pm > xm;  // ties keep the earlier pair and count toward b2
+        const float t = nb ? xm : pm;
+        b2 = t > b2 ? t : b2;
+        xm = nb ? pm : xm;
+        bj = nb ? j0 / 2 : bj;
+        bd0.x = nb ? dc[0].x : bd0.x;
+        bd0.y = nb ? dc[0].y : bd0.y;
+        bd0.z = nb ? dc[0].z : bd0.z;
+        bd0.w = nb ? dc[0].w : bd0.w;
+        bd1.x = nb ? dc[1].x : bd1.x;
+        bd1.y = nb ? dc[1].y : bd1.y;
+        bd1.z = nb ? dc[1].z : bd1.z;
+        bd1.w = nb ? dc[1].w : bd1.w;
+        // keep the updates here: left to itself the compiler sinks them into the gather, keeping
+        // every pair maximum live (and spilled) across the reduction
+        asm volatile("" : "+v"(b2), "+v"(xm), "+v"(bj), "+v"(bd0.x), "+v"(bd0.y), "+v"(bd0.z), "+v"(bd0.w),
+                     "+v"(bd1.x), "+v"(bd1.y), "+v"(bd1.z), "+v"(bd1.w));
+      }
       // 16-bit slot-maximum codes, two per word (slot-pair-major)
       if constexpr (j0 + 1 < J)
         s.scode[(j0 / 2) * NT + threadIdx.x] = __builtin_amdgcn_perm(f2key(sm[1]), f2key(sm[0]), 0x07060302u);
       // sums run over the canonical z = fl32(x r) (exactly what the logprobs are defined on), as
       // 2^(z L2E - mref) with a reference mref in log2 units
-      const float pm = fmaxf(sm[0], sm[1]);
-      if (pm > xthr) {
-        const float sref = (pm * rr) * L2E;
+      if (pm > zthr) {
+        const float sref = pm * L2E;
         if (sref > mref + 32.0f) {  // move the reference lazily: exp2 arguments stay below 32
           const float f = __builtin_amdgcn_exp2f(mref - sref);
           acc0 *= f;
@@ -2093,17 +2112,17 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
           acc2 *= f;
           acc3 *= f;
           mref = sref;
-          xthr = (mref + 31.0f) * inv_c;
+          zthr = (mref + 31.0f) * INV_L2E;
         }
       }
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int e = 0; e < DT::VEC; e += 4) {
-          acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 0] * rr, L2E, -mref));
-          acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 1] * rr, L2E, -mref));
-          acc2 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 2] * rr, L2E, -mref));
-          acc3 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 3] * rr, L2E, -mref));
+          acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 0], L2E, -mref));
+          acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 1], L2E, -mref));
+          acc2 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 2], L2E, -mref));
+          acc3 += __builtin_amdgcn_exp2f(__builtin_fmaf(v[h][e + 3], L2E, -mref));
         }
     });
     float ssum = (acc0 + acc1) + (acc2 + acc3);
@@ -2117,7 +2136,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
 
     // maximum of this thread's register elements (a subset of the row, so the K-th largest of these
     // per-thread maxima bounds the K-th largest z of the row from below; K covers top-k and top-n)
-    const float tmax_z = canon(xm, R.r);
+    const float tmax_z = xm + 0.0f;  // canonical (-0 -> +0)
     int Ksel = R.k_on ? R.k : 0;
     if (a.mode == 0 && a.n_top > Ksel) Ksel = a.n_top;
     const bool want_kth = Ksel > 0 && Ksel <= NT;
@@ -2201,7 +2220,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       float bxx = s.wp[5][0];
 #pragma unroll
       for (int w = 1; w < NW; ++w) bxx = fmaxf(bxx, s.wp[5][w]);
-      bxm = fmaxf(bxm, bxx);
+      bxm = fmaxf(bxm, bxx * rr);  // the extras' maximum as a product
       // reference for the extras: at or above every extras term, so each term is <= 1
       eref = fmaxf(bm, (bxx * rr) * L2E);
       uint64_t fx = 0;
@@ -2248,7 +2267,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     }
 
     // ---------------- row statistics ----------------
-    const float m = canon(row_xm, R.r);
+    const float m = row_xm + 0.0f;  // the maxima are products already
     X.m = m;
     X.row_beta = row_beta;
     X.n_ext = n_ext;
@@ -2276,42 +2295,17 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     if (!skip && !no_bound) {
       const float r = R.r;
       const float bl = beta_list;
-      // canon(x r) >= bl implies x >= bx for this bx (a few ulps below bl / r; fl(x r) is monotone in
-      // x), so a slot whose maximum is below bx holds no candidate; the few that qualify are rare
-      // enough for one LDS atomic per candidate
-      const float bx = x_threshold(bl, r);
+      // a candidate is an element whose product x r is >= bl (canon only turns -0 into +0)
       const int pos_t = R.head + (int)(R.s0 + threadIdx.x) * DT::VEC;
-      // pass 1 from the slot-maximum codes the online pass left in LDS: the slots in which some lane
-      // may hold a candidate (a code at or above the bound's code: truncating a monotone key keeps
-      // smax >= bx => code(smax) >= code(bx))
-      const uint32_t tcode = f2key(bx) >> 16;
-      uint64_t whits = 0;
-      static_for<(J + 1) / 2>([&](auto ic) __attribute__((always_inline)) {
-        constexpr int i = decltype(ic)::value;
-        const uint32_t w = s.scode[i * NT + threadIdx.x];
-        whits |= (__ballot((w & 0xffffu) >= tcode) != 0ull ? 1ull : 0ull) << (2 * i);
-        if constexpr (2 * i + 1 < J) whits |= (__ballot((w >> 16) >= tcode) != 0ull ? 1ull : 0ull) << (2 * i + 1);
-      });
-      // pass 2 over those slots (few: the bound sits near the top of the row), four at a time: the
-      // slots are picked from the registers by their run-time index, each lane marks its candidates
-      // in a bit mask, and the batch takes one list claim per wave (a lane's place is its exclusive
-      // prefix of the candidate counts); the lanes then write their (usually one or none) entries.
-      constexpr int PB = 4;
-      while (whits) {
-        uint4 dd[PB];
-        int jj[PB];
+      // the best pair, from its register copy: one list claim per wave, each lane's place being its
+      // exclusive prefix of the candidate counts
+      {
+        uint32_t cm = 0;  // bit e: element e of the pair (slot 2 bj, then 2 bj + 1)
 #pragma unroll
-        for (int k = 0; k < PB; ++k) {
-          const int j = whits ? __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(whits)) : -1;
-          whits &= whits - 1;
-          jj[k] = j;
-          dd[k] = j >= 0 ? ch.pick(j) : make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG);
+        for (int e = 0; e < DT::VEC; ++e) {
+          cm |= (canon(DT::get(bd0, e), r) >= bl ? 1u : 0u) << e;
+          cm |= (canon(DT::get(bd1, e), r) >= bl ? 1u : 0u) << (DT::VEC + e);
         }
-        uint32_t cm = 0;  // bit 8 k + e: element e of batch slot k is a candidate
-#pragma unroll
-        for (int k = 0; k < PB; ++k)
-#pragma unroll
-          for (int e = 0; e < DT::VEC; ++e) cm |= (canon(DT::get(dd[k], e), r) >= bl ? 1u : 0u) << (8 * k + e);
         const int c = __popc(cm);
         const int incl = wave_incl_scan_i(c);
         const int total = lane_i32(incl, 63);
@@ -2319,14 +2313,75 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
           int base = 0;
           if (lane_id() == 0) base = atomicAdd(&s.n_list, total);
           int idx = __builtin_amdgcn_readfirstlane(base) + incl - c;
+          const int pb = pos_t + 2 * bj * NT * DT::VEC;
+          while (cm) {
+            const int b = __ffs(cm) - 1;
+            cm &= cm - 1;
+            const int e = b % DT::VEC;
+            const float x = b < DT::VEC ? DT::get(bd0, e) : DT::get(bd1, e);
+            if (idx < LCAP) s.sk[idx] = cand_key(canon(x, r), pb + (b < DT::VEC ? 0 : NT * DT::VEC) + e);
+            ++idx;
+          }
+        }
+      }
+      // the other pairs of threads whose second-best pair maximum reaches the bound: pass 1 from the
+      // slot-maximum codes the online pass left in LDS (a code at or above the bound's code:
+      // truncating a monotone key keeps smax >= bl => code(smax) >= code(bl)), pass 2 from the
+      // registers
+      const bool more = b2 >= bl;
+      if (__ballot(more)) {
+        const uint32_t tcode = f2key(bl) >> 16;
+        uint64_t whits = 0;
+        // an opaque copy of the thread index, so that the code addresses are not shared with the
+        // online pass's stores (which would keep them live, spilled, across the pass)
+        int tid = (int)threadIdx.x;
+        asm volatile("" : "+v"(tid));
+        static_for<(J + 1) / 2>([&](auto ic) __attribute__((always_inline)) {
+          constexpr int i = decltype(ic)::value;
+          const uint32_t w = s.scode[i * NT + tid];
+          const bool lane_on = more && bj != i;  // word i holds the codes of pair i
+          whits |= (__ballot(lane_on && (w & 0xffffu) >= tcode) != 0ull ? 1ull : 0ull) << (2 * i);
+          if constexpr (2 * i + 1 < J)
+            whits |= (__ballot(lane_on && (w >> 16) >= tcode) != 0ull ? 1ull : 0ull) << (2 * i + 1);
+        });
+        // four slots at a time: picked from the registers by their run-time index, each lane marks its
+        // candidates in a bit mask (never in its best pair, already listed), and the batch takes one list
+        // claim per wave; the lanes then write their (usually one or none) entries
+        constexpr int PB = 4;
+        while (whits) {
+          uint4 dd[PB];
+          int jj[PB];
 #pragma unroll
           for (int k = 0; k < PB; ++k) {
-            uint32_t ck = (cm >> (8 * k)) & 0xffu;
-            while (ck) {
-              const int e = __ffs(ck) - 1;
-              ck &= ck - 1;
-              if (idx < LCAP) s.sk[idx] = cand_key(canon(DT::get(dd[k], e), r), pos_t + jj[k] * NT * DT::VEC + e);
-              ++idx;
+            const int j = whits ? __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(whits)) : -1;
+            whits &= whits - 1;
+            jj[k] = j;
+            dd[k] = j >= 0 ? ch.pick(j) : make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG);
+          }
+          uint32_t cm = 0;  // bit 8 k + e: element e of batch slot k is a candidate
+#pragma unroll
+          for (int k = 0; k < PB; ++k) {
+            const bool use = more && (jj[k] >> 1) != bj;
+#pragma unroll
+            for (int e = 0; e < DT::VEC; ++e)
+              cm |= (use && canon(DT::get(dd[k], e), r) >= bl ? 1u : 0u) << (8 * k + e);
+          }
+          const int c = __popc(cm);
+          const int incl = wave_incl_scan_i(c);
+          const int total = lane_i32(incl, 63);
+          if (total > 0) {
+            int base = 0;
+            if (lane_id() == 0) base = atomicAdd(&s.n_list, total);
+            int idx = __builtin_amdgcn_readfirstlane(base) + incl - c;
+#pragma unroll
+            for (int k = 0; k < PB; ++k) {
+              uint32_t ck = (cm >> (8 * k)) & 0xffu;
+              while (ck) {
+                const int e = __ffs(ck) - 1;
+                ck &= ck - 1;
+                if (idx < LCAP) s.sk[idx] = cand_key(canon(DT::get(dd[k], e), r), pos_t + jj[k] * NT * DT::VEC + e);
+                ++idx;
+              }
             }
           }
         }
