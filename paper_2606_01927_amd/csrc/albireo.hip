@@ -280,6 +280,8 @@ struct Smem {
   int32_t bc_i[4];
   float bc_f[4];
   uint64_t bc_q[4];
+  uint16_t first_u[4 * NT];  // extras entry of a thread's first occurrence of an id in the early
+                             // count, or 0xffff
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "LDS of one workgroup exceeds a gfx950 CU");
 static_assert(64 * 32 <= UCAP, "history staging does not fit the extras arrays");
@@ -1934,6 +1936,14 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     const RawParams rp = row_params_load(a, row);
     static_for<PIPE0>(issue);
     row_params(a, rp, R);
+    // the unaligned head / tail elements this chunk owns (the extras entries after the penalised
+    // body ones), loaded now and staged after the online pass: one unconditional load per thread
+    const int n_head0 = R.owns_head ? R.head : 0;
+    const int n_ht0 = n_head0 + (R.owns_tail ? R.V - R.tail_lo : 0);
+    const float xht = DT::load1(
+        R.rowp, (int)threadIdx.x < n_ht0 ? ((int)threadIdx.x < n_head0 ? (int)threadIdx.x
+                                                                       : R.tail_lo + ((int)threadIdx.x - n_head0))
+                                         : 0);
     const bool extras_any = R.pen_on || (R.owns_head && R.head > 0) || (R.owns_tail && R.tail_lo < R.V);
     const bool builder = extras_any && wave_id() == 0;
     const int64_t n_hist = R.h_hi - R.h_lo;
@@ -2035,9 +2045,39 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     // the -inf pattern in a register, so that masking is one bit-select per word
     uint32_t neg;
     asm volatile("s_mov_b32 %0, %1" : "=s"(neg) : "i"(DT::NEG));
+    // Penalised rows with short histories count them in the middle of the online pass and load the
+    // original value of each first occurrence there, so the loads complete under the stream; the
+    // values are staged in LDS after the pass.  (The original of a penalised element is its raw
+    // logit, which the registers hold only masked.)
+    constexpr int PCOUNT = J / 4;  // pair at which the count runs
+    const bool count_early = R.pen_on && n_hist <= 4 * NT;
+    int fid[4] = {0, 0, 0, 0};
+    float fv[4];
     // slots are taken in pairs: one reference test and one running-maximum update per pair
     static_for<J / 2>([&](auto pc) __attribute__((always_inline)) {
       constexpr int j0 = 2 * decltype(pc)::value;
+      if constexpr (j0 / 2 == PCOUNT) {
+        if (count_early) {
+          wait_ready(s, (uint32_t)NW + 2u);
+          const int32_t* hst = hist_stage(s);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int i = (int)threadIdx.x + q * NT;
+            const int id = i < (int)n_hist ? hst[i] : -1;
+            const int u = (unsigned)id < (unsigned)R.V ? extras_index<DT>(s, R, id) : -1;
+            uint32_t first = 0xffffu;
+            if (u >= 0) {
+              if (atomicAdd(&s.x_cnt[u], 1u) == 0u) first = (uint32_t)u;
+              s.x_pos[u] = id;  // every counting thread of this id writes the same value
+            }
+            s.first_u[q * NT + threadIdx.x] = (uint16_t)first;
+            fid[q] = first != 0xffffu ? id : 0;
+          }
+        }
+        // unconditional loads: a load under a branch is merged at its join, which waits for it
+#pragma unroll
+        for (int q = 0; q < 4; ++q) fv[q] = DT::load1(R.rowp, fid[q]);
+      }
       if constexpr (j0 + PIPE < J) issue(std::integral_constant<int, j0 + PIPE>{});
       if constexpr (j0 + 1 + PIPE < J) issue(std::integral_constant<int, j0 + 1 + PIPE>{});
       float v[2][DT::VEC], sm[2];
@@ -2127,12 +2167,23 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     });
     float ssum = (acc0 + acc1) + (acc2 + acc3);
 
-    // this thread's share of the staged history into the counts (read after the barrier below)
-    if (R.pen_on && n_hist <= HSTAGE) {
+    // this thread's share of the staged history into the counts (read after the barrier below),
+    // unless counted in the pass; the originals of the extras entries into LDS where all of them are
+    // known here (rows without penalties, and rows counted in the pass)
+    if (R.pen_on && n_hist <= HSTAGE && !count_early) {
       wait_ready(s, (uint32_t)NW + 2u);
       const int32_t* hst = hist_stage(s);
       for (int i = threadIdx.x; i < (int)n_hist; i += NT) count_history_id<DT>(s, R, hst[i]);
     }
+    const bool staged = !R.pen_on || count_early;
+    if (count_early) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t u = s.first_u[q * NT + threadIdx.x];
+        if (u != 0xffffu) s.x_val[u] = fv[q];
+      }
+    }
+    if (staged && (int)threadIdx.x < n_ht0) s.x_val[(R.pen_on ? s.n_body : 0) + (int)threadIdx.x] = xht;
 
     // maximum of this thread's register elements (a subset of the row, so the K-th largest of these
     // per-thread maxima bounds the K-th largest z of the row from below; K covers top-k and top-n)
@@ -2189,11 +2240,20 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       for (int xi0 = threadIdx.x; xi0 < n_ext; xi0 += 4 * NT) {
         int idv[4];
         float xv[4];
+        if (staged) {  // originals staged in LDS before the barrier
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {  // all loads in flight before the first use
-          const int xi = xi0 + q * NT;
-          idv[q] = xi < n_ext ? s.x_pos[xi] : 0;
-          xv[q] = DT::load1(R.rowp, idv[q]);
+          for (int q = 0; q < 4; ++q) {
+            const int xi = xi0 + q * NT;
+            xv[q] = xi < n_ext ? s.x_val[xi] : 0.f;
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {  // all loads in flight before the first use
+            const int xi = xi0 + q * NT;
+            const int pq = xi < n_ext ? s.x_pos[xi] : 0;
+            idv[q] = (unsigned)pq < (unsigned)R.V ? pq : 0;  // defensive: only in-row reads
+            xv[q] = DT::load1(R.rowp, idv[q]);
+          }
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
