@@ -2391,40 +2391,32 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       const bool more = b2 >= bl;
       if (__ballot(more)) {
         const uint32_t tcode = f2key(bl) >> 16;
-        uint64_t whits = 0;
         // an opaque copy of the thread index, so that the code addresses are not shared with the
         // online pass's stores (which would keep them live, spilled, across the pass)
         int tid = (int)threadIdx.x;
         asm volatile("" : "+v"(tid));
-        static_for<(J + 1) / 2>([&](auto ic) __attribute__((always_inline)) {
+        // per lane, the pairs other than its best whose larger slot code reaches the bound's code
+        // (word i holds the codes of pair i); the wave takes their union
+        uint32_t pm = 0;
+        static_for<J / 2>([&](auto ic) __attribute__((always_inline)) {
           constexpr int i = decltype(ic)::value;
           const uint32_t w = s.scode[i * NT + tid];
-          const bool lane_on = more && bj != i;  // word i holds the codes of pair i
-          whits |= (__ballot(lane_on && (w & 0xffffu) >= tcode) != 0ull ? 1ull : 0ull) << (2 * i);
-          if constexpr (2 * i + 1 < J)
-            whits |= (__ballot(lane_on && (w >> 16) >= tcode) != 0ull ? 1ull : 0ull) << (2 * i + 1);
+          pm |= (max(w & 0xffffu, w >> 16) >= tcode ? 1u : 0u) << i;
         });
-        // four slots at a time: picked from the registers by their run-time index, each lane marks its
-        // candidates in a bit mask (never in its best pair, already listed), and the batch takes one list
-        // claim per wave; the lanes then write their (usually one or none) entries
-        constexpr int PB = 4;
-        while (whits) {
-          uint4 dd[PB];
-          int jj[PB];
+        pm = more ? pm & ~(1u << bj) : 0u;
+        uint32_t wpm = wave_or(pm);
+        // one pair at a time, picked from the registers by its run-time index; the lanes that flagged
+        // it mark their candidates in a bit mask and the wave takes one list claim
+        while (wpm) {
+          const int i = __builtin_ctz(wpm);
+          wpm &= wpm - 1;
+          const uint4 p0 = ch.pick(2 * i), p1 = ch.pick(2 * i + 1);
+          const bool use = (pm >> i) & 1u;
+          uint32_t cm = 0;  // bit e: element e of the pair (slot 2 i, then 2 i + 1)
 #pragma unroll
-          for (int k = 0; k < PB; ++k) {
-            const int j = whits ? __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(whits)) : -1;
-            whits &= whits - 1;
-            jj[k] = j;
-            dd[k] = j >= 0 ? ch.pick(j) : make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG);
-          }
-          uint32_t cm = 0;  // bit 8 k + e: element e of batch slot k is a candidate
-#pragma unroll
-          for (int k = 0; k < PB; ++k) {
-            const bool use = more && (jj[k] >> 1) != bj;
-#pragma unroll
-            for (int e = 0; e < DT::VEC; ++e)
-              cm |= (use && canon(DT::get(dd[k], e), r) >= bl ? 1u : 0u) << (8 * k + e);
+          for (int e = 0; e < DT::VEC; ++e) {
+            cm |= (use && canon(DT::get(p0, e), r) >= bl ? 1u : 0u) << e;
+            cm |= (use && canon(DT::get(p1, e), r) >= bl ? 1u : 0u) << (DT::VEC + e);
           }
           const int c = __popc(cm);
           const int incl = wave_incl_scan_i(c);
@@ -2433,15 +2425,14 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
             int base = 0;
             if (lane_id() == 0) base = atomicAdd(&s.n_list, total);
             int idx = __builtin_amdgcn_readfirstlane(base) + incl - c;
-#pragma unroll
-            for (int k = 0; k < PB; ++k) {
-              uint32_t ck = (cm >> (8 * k)) & 0xffu;
-              while (ck) {
-                const int e = __ffs(ck) - 1;
-                ck &= ck - 1;
-                if (idx < LCAP) s.sk[idx] = cand_key(canon(DT::get(dd[k], e), r), pos_t + jj[k] * NT * DT::VEC + e);
-                ++idx;
-              }
+            const int pp = pos_t + 2 * i * NT * DT::VEC;
+            while (cm) {
+              const int b = __ffs(cm) - 1;
+              cm &= cm - 1;
+              const int e = b % DT::VEC;
+              const float x = b < DT::VEC ? DT::get(p0, e) : DT::get(p1, e);
+              if (idx < LCAP) s.sk[idx] = cand_key(canon(x, r), pp + (b < DT::VEC ? 0 : NT * DT::VEC) + e);
+              ++idx;
             }
           }
         }
