@@ -1040,9 +1040,9 @@ __device__ __forceinline__ uint32_t wfix(float w) { return (uint32_t)__builtin_f
 
 // LDS totals of the counting resolver, in the general path's histogram (unused by this path)
 struct CountArrays {
-  uint32_t* above;  // entries strictly above
+  uint32_t* above;  // entries strictly above (larger z)
   uint32_t* mass;   // their mass
-  uint32_t* lower;  // kept mass at lower ids
+  uint32_t* lower;  // entries at lower ids (the rank in ascending id)
   uint32_t* ties;   // entries of equal z at lower ids (top-n ranks)
 };
 __device__ __forceinline__ CountArrays count_arrays(Smem& s) {
@@ -1063,44 +1063,37 @@ struct Entries {
   bool in[2];
 };
 
-// accumulate over list entries i = first, first + NW, ... < n (NQ halves in use; TIE: also count
-// equal z at lower ids)
+// Accumulate over list entries i = first, first + NW, ... < n (NQ halves in use; TIE: also count
+// equal z at lower ids).  Entry i is read from lane i % 64 of this wave's own registers (every wave
+// holds the whole list).
 template <int NQ, bool TIE>
-__device__ __forceinline__ void count_above(const Smem& s, int n, float m, const Entries& E, uint32_t (&c)[2],
-                                            uint32_t (&g)[2], uint32_t (&t)[2]) {
+__device__ __forceinline__ void count_above(int n, const Entries& E, uint32_t (&c)[2], uint32_t (&g)[2],
+                                            uint32_t (&lo)[2], uint32_t (&t)[2]) {
   for (int i = wave_id(); i < n; i += NW) {
-    const uint64_t k = s.sk[i];
-    const float zi = cand_z(k);
-    const uint32_t wi = wfix(__expf(zi - m));
-    const int pi = cand_pos(k);
+    const int h = i >> 6, ln = i & 63;
+    const float zi = h ? lane_f32(E.z[1], ln) : lane_f32(E.z[0], ln);
+    const uint32_t wi = h ? lane_u32(E.wf[1], ln) : lane_u32(E.wf[0], ln);
+    const int pi = h ? lane_i32(E.pos[1], ln) : lane_i32(E.pos[0], ln);
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const bool gt = zi > E.z[q];
       c[q] += gt ? 1u : 0u;
       g[q] += gt ? wi : 0u;
+      lo[q] += pi < E.pos[q] ? 1u : 0u;
       if constexpr (TIE) t[q] += (zi == E.z[q] && pi < E.pos[q]) ? 1u : 0u;
     }
   }
 }
 
-// accumulate the kept mass at lower ids over kept entries i = first, first + NW, ... < n
-template <int NQ>
-__device__ __forceinline__ void mass_below(const Smem& s, int n, float m, const Entries& E, uint64_t k0,
-                                           uint64_t k1, uint32_t (&x)[2]) {
-  for (int i = wave_id(); i < n; i += NW) {
-    const uint64_t bits = i < 64 ? k0 : k1;
-    if (!((bits >> (i & 63)) & 1ull)) continue;  // wave-uniform
-    const uint64_t k = s.sk[i];
-    const uint32_t wi = wfix(__expf(cand_z(k) - m));
-    const int pi = cand_pos(k);
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) x[q] += pi < E.pos[q] ? wi : 0u;
-  }
+// index of the first set bit over two 64-bit halves (-1 when none)
+__device__ __forceinline__ int first_of2(uint64_t b0, uint64_t b1) {
+  return b0 ? __ffsll((unsigned long long)b0) - 1 : (b1 ? 64 + __ffsll((unsigned long long)b1) - 1 : -1);
 }
 
-// Every thread of the workgroup calls this (it holds barriers).  The counting is spread over all
-// waves; wave 0 decides the kept set, and the waves then split the id-ordered mass of the draw.
-// Every thread receives res.id / res.zid; in mode 1 also the kept set's tau, zs, zmin and size.
+// Every thread of the workgroup calls this (it holds a barrier).  The counting is spread over all
+// waves; wave 0 then decides the kept set and draws in ascending id: it scatters the kept masses to
+// their id ranks and takes an exact (integer) prefix scan.  In mode 0, wave 0 receives res.id /
+// res.zid; in mode 1 every thread receives the kept set's tau, zs, zmin, size (and the greedy id).
 __device__ __forceinline__ Resolution resolve_count(const OutArgs& a, Smem& s, const RowState& R, const RowCtx& X,
                                                     Resolution res) {
   const int l = lane_id();
@@ -1121,13 +1114,13 @@ __device__ __forceinline__ Resolution resolve_count(const OutArgs& a, Smem& s, c
   }
   const bool rank_top = a.mode == 0 && a.n_top > 0;
   {
-    uint32_t c[2] = {0u, 0u}, g[2] = {0u, 0u}, t[2] = {0u, 0u};
+    uint32_t c[2] = {0u, 0u}, g[2] = {0u, 0u}, lo[2] = {0u, 0u}, t[2] = {0u, 0u};
     if (two) {
-      if (rank_top) count_above<2, true>(s, n, m, E, c, g, t);
-      else count_above<2, false>(s, n, m, E, c, g, t);
+      if (rank_top) count_above<2, true>(n, E, c, g, lo, t);
+      else count_above<2, false>(n, E, c, g, lo, t);
     } else {
-      if (rank_top) count_above<1, true>(s, n, m, E, c, g, t);
-      else count_above<1, false>(s, n, m, E, c, g, t);
+      if (rank_top) count_above<1, true>(n, E, c, g, lo, t);
+      else count_above<1, false>(n, E, c, g, lo, t);
     }
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -1135,20 +1128,21 @@ __device__ __forceinline__ Resolution resolve_count(const OutArgs& a, Smem& s, c
       if (E.in[q]) {
         if (c[q]) atomicAdd(&A.above[e], c[q]);
         if (g[q]) atomicAdd(&A.mass[e], g[q]);
+        if (lo[q]) atomicAdd(&A.lower[e], lo[q]);
         if (t[q]) atomicAdd(&A.ties[e], t[q]);
       }
     }
   }
   __syncthreads();
-  const bool draw = a.mode == 0 && !R.greedy;
-  bool kept[2] = {false, false};
   if (wave_id() == 0) {
-    uint32_t C[2], G[2];
+    uint32_t C[2], G[2], Q[2];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       C[q] = E.in[q] ? A.above[l + 64 * q] : 0xffffffffu;
       G[q] = E.in[q] ? A.mass[l + 64 * q] : 0xffffffffu;
+      Q[q] = E.in[q] ? A.lower[l + 64 * q] : 0u;
     }
+    bool kept[2];
     if (R.greedy) {  // the argmax with the lowest id
       const int pmin = wave_min_i(min(C[0] == 0u ? E.pos[0] : INT32_MAX, C[1] == 0u ? E.pos[1] : INT32_MAX));
 #pragma unroll
@@ -1192,6 +1186,33 @@ __device__ __forceinline__ Resolution resolve_count(const OutArgs& a, Smem& s, c
       const int sel = kb0 ? __ffsll((unsigned long long)kb0) - 1 : 64 + __ffsll((unsigned long long)kb1) - 1;
       res.id = sel < 64 ? lane_i32(E.pos[0], sel) : lane_i32(E.pos[1], sel - 64);
       res.zid = sel < 64 ? lane_f32(E.z[0], sel) : lane_f32(E.z[1], sel - 64);
+    } else if (a.mode == 0) {
+      // the draw, in ascending id over the kept entries: every entry goes to its id rank (ranks are
+      // distinct: positions are), carrying its kept mass, and the cumulative of the kept masses in
+      // that order is an integer prefix scan; the drawn entry is the one whose cumulative first
+      // exceeds u times the kept mass
+      uint32_t* dw = A.mass;  // reused: wave 0 alone reads and writes it from here on
+      int32_t* dp = reinterpret_cast<int32_t*>(A.ties);
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        if (E.in[q]) {
+          dw[Q[q]] = kept[q] ? E.wf[q] : 0u;
+          dp[Q[q]] = l + 64 * q;  // the entry, by its lane and half
+        }
+      uint32_t wk[2], cu[2];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) wk[q] = l + 64 * q < n ? dw[l + 64 * q] : 0u;
+      cu[0] = wave_incl_scan_u(wk[0]);
+      cu[1] = lane_u32(cu[0], 63) + wave_incl_scan_u(wk[1]);
+      const uint32_t total = two ? lane_u32(cu[1], 63) : lane_u32(cu[0], 63);
+      uint32_t tf = (uint32_t)((double)R.u * (double)total);
+      if (tf >= total) tf = total - 1u;
+      const int r = first_of2(__ballot(cu[0] > tf), __ballot(l + 64 < n && cu[1] > tf));
+      if (r >= 0) {
+        const int e = dp[r];
+        res.id = e < 64 ? lane_i32(E.pos[0], e) : lane_i32(E.pos[1], e - 64);
+        res.zid = e < 64 ? lane_f32(E.z[0], e) : lane_f32(E.z[1], e - 64);
+      }
     }
     if (a.mode == 1) {
       res.kept = __popcll(kb0) + __popcll(kb1);
@@ -1201,62 +1222,23 @@ __device__ __forceinline__ Resolution resolve_count(const OutArgs& a, Smem& s, c
       for (int q = 0; q < 2; ++q)
         if (kept[q]) w40 += (uint64_t)__builtin_fma((double)E.w[q], WFIX40, 0.5);
       res.zs = (float)((double)wave_sum_u64(w40) / WFIX40);
-    }
-    if (l == 0) {
-      s.bc_q[0] = kb0;
-      s.bc_q[1] = kb1;
-      if (a.mode == 1) {
+      if (l == 0) {
         s.bc_f[0] = res.zmin;
         s.bc_f[1] = res.zs;
         s.bc_i[1] = res.kept;
+        s.bc_i[0] = res.id;
       }
-      s.bc_i[0] = res.id;
     }
   }
-  if (draw || a.mode == 1) __syncthreads();  // kept set (and mode 1 results) published
-  if (wave_id() != 0 && (draw || a.mode == 1)) {
-    const uint64_t kb0 = s.bc_q[0], kb1 = s.bc_q[1];
-    kept[0] = E.in[0] && ((kb0 >> l) & 1ull);
-    kept[1] = E.in[1] && ((kb1 >> l) & 1ull);
-    if (a.mode == 1) {
-      res.zmin = s.bc_f[0];
-      res.zs = s.bc_f[1];
-      res.kept = s.bc_i[1];
-      res.id = s.bc_i[0];
-    }
+  if (a.mode == 1) {  // every thread needs the kept set for the dense output
+    __syncthreads();
+    res.zmin = s.bc_f[0];
+    res.zs = s.bc_f[1];
+    res.kept = s.bc_i[1];
+    res.id = s.bc_i[0];
   }
   res.tau = res.zmin;
   res.id_here = 1;
-  if (draw) {
-    // the draw, in ascending id over the kept entries: the waves split the id-ordered mass
-    const uint64_t kb0 = __ballot(kept[0]), kb1 = __ballot(kept[1]);
-    {
-      uint32_t x[2] = {0u, 0u};
-      if (two) mass_below<2>(s, n, m, E, kb0, kb1, x);
-      else mass_below<1>(s, n, m, E, kb0, kb1, x);
-#pragma unroll
-      for (int q = 0; q < 2; ++q)
-        if (kept[q] && x[q]) atomicAdd(&A.lower[l + 64 * q], x[q]);
-    }
-    __syncthreads();
-    if (wave_id() == 0) {
-      const uint32_t total = (uint32_t)wave_sum_i((int)((kept[0] ? E.wf[0] : 0u) + (kept[1] ? E.wf[1] : 0u)));
-      uint32_t tf = (uint32_t)((double)R.u * (double)total);
-      if (tf >= total) tf = total - 1u;
-      bool hit[2];
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const uint32_t lo = kept[q] ? A.lower[l + 64 * q] : 0u;
-        hit[q] = kept[q] && lo <= tf && tf - lo < E.wf[q];
-      }
-      const uint64_t h0 = __ballot(hit[0]), h1 = __ballot(hit[1]);
-      if (h0 | h1) {
-        const int sel = h0 ? __ffsll((unsigned long long)h0) - 1 : 64 + __ffsll((unsigned long long)h1) - 1;
-        res.id = sel < 64 ? lane_i32(E.pos[0], sel) : lane_i32(E.pos[1], sel - 64);
-        res.zid = sel < 64 ? lane_f32(E.z[0], sel) : lane_f32(E.z[1], sel - 64);
-      }
-    }
-  }
   return res;
 }
 
