@@ -2272,14 +2272,20 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       if (lane_id() == 0 && fx) atomicAdd(reinterpret_cast<unsigned long long*>(&s.fxsum), (unsigned long long)fx);
     }
     const float beta_sel = (want_kth && thi > -INFINITY) ? kth_from_hist(s, Ksel) : -INFINITY;
-    if (extras_any) {
-      __syncthreads();  // C
+    // The extras' mass joins the row sum behind barrier C only where something before the gather
+    // needs the sum (the chunk exchange, the top-p-only bound); otherwise after barrier D.
+    const bool fx_late = extras_any && !(P > 1 || (!R.greedy && !R.k_on && !R.minp_on && R.topp_on));
+    auto fold_extras = [&](float& m2, float& s2) {
       const uint64_t fx = s.fxsum;
-      if (eref > bm) {
-        bs = bs * rel2(bm, eref);
-        bm = eref;
+      if (eref > m2) {
+        s2 = s2 * rel2(m2, eref);
+        m2 = eref;
       }
-      bs += (float)((double)fx / FIX_SCALE) * rel2(eref, bm);
+      s2 += (float)((double)fx / FIX_SCALE) * rel2(eref, m2);
+    };
+    if (extras_any && !fx_late) {
+      __syncthreads();  // C
+      fold_extras(bm, bs);
     }
     const uint32_t bflags = R.flags | ext_flags;
 
@@ -2428,6 +2434,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       })
     }
     __syncthreads();  // D
+    if (fx_late) fold_extras(row_mref, row_s);  // P == 1 here: the row's own sums
     // the full-vocabulary normaliser in double, now that the row's registers are released
     {
       const RowDoubles RD = row_doubles(row_mref, row_s, m);
