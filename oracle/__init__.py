@@ -66,6 +66,14 @@ def _load(path: str = _LIB):
         lib.oracle_sample.argtypes = [ctypes.POINTER(_In), ctypes.POINTER(_Out), ctypes.c_int]
         lib.oracle_sample.restype = ctypes.c_int
         lib.oracle_max_threads.restype = ctypes.c_int
+        lib.oracle_philox4x32_10.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        lib.oracle_philox4x32_10.restype = None
+        lib.oracle_philox_uniforms.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p,
+                                               ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_philox_uniforms.restype = None
+        lib.oracle_backfill.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                        ctypes.c_int64]
+        lib.oracle_backfill.restype = None
         _libs[path] = lib
     return _libs[path]
 
@@ -138,6 +146,36 @@ def sample(w, nthreads: int = 0, probs: bool = False, penalised: bool = False, d
     return o
 
 
+def philox4x32_10(counter, key, lib_path: str = _LIB) -> np.ndarray:
+    """Philox-4x32-10 of a 4-word counter under a 2-word key (O-11): four uint32 words."""
+    c = np.ascontiguousarray(counter, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    assert c.shape == (4,) and k.shape == (2,)
+    out = np.zeros(4, np.uint32)
+    _load(lib_path).oracle_philox4x32_10(c.ctypes.data, k.ctypes.data, out.ctypes.data)
+    return out
+
+
+def philox_uniforms(seed: int, step: int, seq_ids=None, B: int = None, lib_path: str = _LIB) -> np.ndarray:
+    """The per-row uniforms of O-11: row i uses sequence id seq_ids[i] (the row index when None)."""
+    if seq_ids is not None:
+        seq = np.ascontiguousarray(seq_ids, dtype=np.int64)
+        B = seq.size
+    out = np.zeros(B, np.float32)
+    _load(lib_path).oracle_philox_uniforms(ctypes.c_uint64(seed & (2**64 - 1)), ctypes.c_uint64(step & (2**64 - 1)),
+                                           None if seq_ids is None else seq.ctypes.data, B, out.ctypes.data)
+    return out
+
+
+def backfill(ids, dest, next_tokens, lib_path: str = _LIB) -> np.ndarray:
+    """O-12: a copy of next_tokens with row i's id written to slot dest[i] where that slot exists."""
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    dest = np.ascontiguousarray(dest, dtype=np.int32)
+    out = np.array(next_tokens, dtype=np.int32, copy=True)
+    _load(lib_path).oracle_backfill(ids.ctypes.data, dest.ctypes.data, ids.size, out.ctypes.data, out.size)
+    return out
+
+
 class Variant:
     """The oracle's interface bound to another build of the same source (used by the mutation test,
     which compiles deliberately broken copies and checks that the pins reject them)."""
@@ -149,3 +187,12 @@ class Variant:
 
     def sample(self, w, **kw):
         return sample(w, lib_path=self.lib_path, **kw)
+
+    def philox4x32_10(self, counter, key):
+        return philox4x32_10(counter, key, lib_path=self.lib_path)
+
+    def philox_uniforms(self, seed, step, seq_ids=None, B=None):
+        return philox_uniforms(seed, step, seq_ids, B, lib_path=self.lib_path)
+
+    def backfill(self, ids, dest, next_tokens):
+        return backfill(ids, dest, next_tokens, lib_path=self.lib_path)

@@ -367,3 +367,64 @@ int oracle_max_threads(void) {
   return 1;
 #endif
 }
+
+/*
+ * O-11 Device random numbers (the paper's deterministic random numbers, sec. 6.2 "Deterministic random
+ * number generation": every worker must draw what a single worker would; the paper pre-generates them,
+ * the "next" step generates them from a counter instead).  The generator is Philox-4x32 with 10 rounds
+ * as published by Salmon, Moraes, Dror and Shaw ("Parallel random numbers: as easy as 1, 2, 3",
+ * SC 2011): a round multiplies counter words 0 and 2 by the constants 0xD2511F53 and 0xCD9E8D57 into
+ * 64-bit products and recombines the halves with words 1 and 3 and the key; the key advances by the
+ * Weyl constants 0x9E3779B9 and 0xBB67AE85 between rounds.
+ * The uniform of a row: counter (lo(step), hi(step), lo(seq), hi(seq)), key (lo(seed), hi(seed)),
+ * u = (word0 >> 8) * 2^-24, a float in [0, 1).
+ */
+void oracle_philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4]) {
+  uint32_t c[4] = {ctr_in[0], ctr_in[1], ctr_in[2], ctr_in[3]};
+  uint32_t k[2] = {key_in[0], key_in[1]};
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k[0] += 0x9E3779B9u;
+      k[1] += 0xBB67AE85u;
+    }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)c[0];
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)c[2];
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    const uint32_t n0 = hi1 ^ c[1] ^ k[0];
+    const uint32_t n2 = hi0 ^ c[3] ^ k[1];
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+  }
+  out[0] = c[0];
+  out[1] = c[1];
+  out[2] = c[2];
+  out[3] = c[3];
+}
+
+void oracle_philox_uniforms(uint64_t seed, uint64_t step, const int64_t* seq_ids, int64_t B, float* out) {
+  const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  for (int64_t i = 0; i < B; ++i) {
+    const uint64_t seq = seq_ids ? (uint64_t)seq_ids[i] : (uint64_t)i;
+    const uint32_t ctr[4] = {(uint32_t)step, (uint32_t)(step >> 32), (uint32_t)seq, (uint32_t)(seq >> 32)};
+    uint32_t w[4];
+    oracle_philox4x32_10(ctr, key, w);
+    out[i] = (float)((double)(w[0] >> 8) * (1.0 / 16777216.0));
+  }
+}
+
+/*
+ * O-12 Early-feedback backfill (sec. 5, "Early-feedback backfill" and "Input processing"): the next
+ * iteration's last-token tensor X_T is laid out by the scheduler before sampling ends; the sampler
+ * then writes each scheduled sequence's new token into its slot.  Row i's id goes to slot dest[i] when
+ * 0 <= dest[i] < n_next; other rows (padding, sequences not scheduled next) are skipped.  Slots named
+ * by no row keep their contents.
+ */
+void oracle_backfill(const int32_t* ids, const int32_t* dest, int64_t B, int32_t* next_tokens, int64_t n_next) {
+  for (int64_t i = 0; i < B; ++i) {
+    const int64_t d = dest[i];
+    if (d >= 0 && d < n_next) next_tokens[d] = ids[i];
+  }
+}

@@ -15,6 +15,7 @@ import pytest
 
 import oracle
 from tests import test_oracle_pins as pins
+from tests import test_oracle_rng_backfill as rng_pins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "albireo_oracle.c")
 
@@ -38,13 +39,24 @@ MUTANTS = [
     ("draw ignores the kept set", "if (!inS[v]) continue;", "if (0) continue;"),
     ("greedy takes the highest id", "const int32_t id = ord[0].id;",
      "int32_t id = ord[0].id; for (int64_t q = 1; q < V && ord[q].z == ord[0].z; ++q) id = ord[q].id;"),
+    ("Philox multipliers swapped", "const uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)c[0];",
+     "const uint64_t p0 = (uint64_t)0xCD9E8D57u * (uint64_t)c[0];"),
+    ("Philox key not advanced", "k[1] += 0xBB67AE85u;", "k[1] += 0u;"),
+    ("Philox halves crossed", "const uint32_t n0 = hi1 ^ c[1] ^ k[0];", "const uint32_t n0 = hi0 ^ c[1] ^ k[0];"),
+    ("uniform from 23 bits", "out[i] = (float)((double)(w[0] >> 8) * (1.0 / 16777216.0));",
+     "out[i] = (float)((double)(w[0] >> 9) * (1.0 / 16777216.0));"),
+    ("step low word only", "const uint32_t ctr[4] = {(uint32_t)step, (uint32_t)(step >> 32),",
+     "const uint32_t ctr[4] = {(uint32_t)step, 0u,"),
+    ("backfill skips slot 0", "if (d >= 0 && d < n_next) next_tokens[d] = ids[i];",
+     "if (d > 0 && d < n_next) next_tokens[d] = ids[i];"),
 ]
 
 
 def _pin_calls():
     """(name, callable) for every pin test, with its parametrisations expanded."""
     calls = []
-    for name, fn in inspect.getmembers(pins, inspect.isfunction):
+    members = inspect.getmembers(pins, inspect.isfunction) + inspect.getmembers(rng_pins, inspect.isfunction)
+    for name, fn in members:
         if not name.startswith("test_"):
             continue
         params = getattr(fn, "pytestmark", [])
