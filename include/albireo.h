@@ -145,6 +145,60 @@ albireo_status_t albireo_topk_topp(const float* logits, int64_t B, int64_t V, in
                                    int32_t* out_kept, float* out_log_norm, uint32_t* out_flags,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * One decoding step's extras for albireo_sample_step (host struct, read during the call only).
+ *
+ * Device random numbers replace the caller's uniforms.  The paper pre-generates the random numbers of
+ * a request on every GPU so that each worker's draws match a single worker's (sec. 6.2, "Deterministic
+ * random number generation"); here they come from a counter-based generator instead, so any worker
+ * produces the same number for the same row without storing or exchanging them.  The uniform of row
+ * i is Philox-4x32 with 10 rounds (Salmon et al., SC 2011) of the counter (step, seq_ids[i]), four
+ * 32-bit words low word first, under the key seed: the top 24 bits of the first output word times
+ * 2^-24, in [0, 1).
+ *
+ * Early-feedback backfill (sec. 5, "Early-feedback backfill" and "Input processing"): the next
+ * iteration's last-token tensor X_T is laid out by the scheduler before sampling ends, and each
+ * scheduled sequence's new token is written into its slot by the sampler.  When next_tokens is not
+ * NULL, the sampled id of row i is also written to next_tokens[backfill_dest[i]] whenever
+ * 0 <= backfill_dest[i] < next_len (an EMPTY row writes -1); rows with any other value (padding rows,
+ * sequences not scheduled next) write nothing, and slots no row names keep their contents.  Two rows
+ * naming the same slot leave one of their ids there (which one is unspecified).
+ */
+typedef struct {
+  uint64_t seed;                /* generator key                                                   */
+  uint64_t step;                /* decoding step (counter words 0-1)                               */
+  const int64_t* seq_ids;       /* [B] device sequence ids (counter words 2-3), or NULL: row index  */
+  int32_t* next_tokens;         /* [next_len] device, or NULL: no backfill                         */
+  const int32_t* backfill_dest; /* [B] device slot of each row in next_tokens (needed with it)      */
+  int64_t next_len;             /* [host value] number of slots in next_tokens                     */
+} albireo_step_t;
+
+/*
+ * albireo_sample with the uniforms generated on the device and the optional backfill, in the same
+ * launch.  step [host] must not be NULL.  Every other argument is as for albireo_sample, and the
+ * results equal albireo_sample's on the uniforms albireo_philox_uniforms returns for the same
+ * (seed, step, seq_ids).
+ */
+albireo_status_t albireo_sample_step(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
+                                     const albireo_params_t* params, const albireo_step_t* step, int32_t* out_ids,
+                                     float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
+                                     float* out_top_logprobs, uint32_t* out_flags, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The device uniforms alone: out_uniforms[i] (device, [B] fp32) = the uniform described above for
+ * (seed, step, seq_ids[i]) (seq_ids NULL: i).  No workspace.
+ */
+albireo_status_t albireo_philox_uniforms(uint64_t seed, uint64_t step, const int64_t* seq_ids, int64_t B,
+                                         float* out_uniforms, hipStream_t stream);
+
+/*
+ * The backfill alone: next_tokens[dest[i]] = ids[i] for every row i with 0 <= dest[i] < next_len
+ * (ids, dest: [B] device; next_tokens: [next_len] device).  No workspace.
+ */
+albireo_status_t albireo_backfill(const int32_t* ids, const int32_t* dest, int64_t B, int32_t* next_tokens,
+                                  int64_t next_len, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* albireo_status_string(albireo_status_t status);
 

@@ -38,6 +38,13 @@ class _Params(ctypes.Structure):
     ]
 
 
+class _Step(ctypes.Structure):
+    _fields_ = [
+        ("seed", ctypes.c_uint64), ("step", ctypes.c_uint64), ("seq_ids", ctypes.c_void_p),
+        ("next_tokens", ctypes.c_void_p), ("backfill_dest", ctypes.c_void_p), ("next_len", ctypes.c_int64),
+    ]
+
+
 _vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
 _lib.albireo_workspace_size.argtypes = [_i64, _i64, ctypes.c_int, _i32]
 _lib.albireo_workspace_size.restype = _sz
@@ -50,11 +57,18 @@ _lib.albireo_apply_penalties.restype = ctypes.c_int
 _lib.albireo_topk_topp.argtypes = [_vp, _i64, _i64, _i64, ctypes.POINTER(_Params), _vp, _vp, _vp, _vp, _vp,
                                    _vp, _sz, _vp]
 _lib.albireo_topk_topp.restype = ctypes.c_int
+_lib.albireo_sample_step.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Params),
+                                     ctypes.POINTER(_Step), _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.albireo_sample_step.restype = ctypes.c_int
+_lib.albireo_philox_uniforms.argtypes = [ctypes.c_uint64, ctypes.c_uint64, _vp, _i64, _vp, _vp]
+_lib.albireo_philox_uniforms.restype = ctypes.c_int
+_lib.albireo_backfill.argtypes = [_vp, _vp, _i64, _vp, _i64, _vp]
+_lib.albireo_backfill.restype = ctypes.c_int
 _lib.albireo_status_string.argtypes = [ctypes.c_int]
 _lib.albireo_status_string.restype = ctypes.c_char_p
 
-EXPORTED = ("albireo_workspace_size", "albireo_sample", "albireo_apply_penalties", "albireo_topk_topp",
-            "albireo_status_string")
+EXPORTED = ("albireo_workspace_size", "albireo_sample", "albireo_sample_step", "albireo_philox_uniforms",
+            "albireo_backfill", "albireo_apply_penalties", "albireo_topk_topp", "albireo_status_string")
 
 
 class AlbireoError(RuntimeError):
@@ -214,6 +228,80 @@ class PreparedSample:
         st = self.fn(logits_ptr, self.dt, self.B, self.V, self.ld, *self.tail)
         if st != OK:
             raise AlbireoError(st, "albireo_sample")
+
+
+def sample_step(logits: torch.Tensor, seed: int, step: int, seq_ids: Optional[torch.Tensor] = None,
+                params: Optional[SamplingParams] = None, n_top: int = 0, V: Optional[int] = None,
+                next_tokens: Optional[torch.Tensor] = None, backfill_dest: Optional[torch.Tensor] = None,
+                workspace: Optional[Workspace] = None, stream=None, out=None):
+    """albireo_sample_step: uniforms generated on the device from (seed, step, seq_ids), and the sampled
+    ids optionally backfilled into next_tokens at backfill_dest.  Returns what sample() returns."""
+    dev = logits.device
+    B, V, ld = _rows(logits, V)
+    if seq_ids is not None and (seq_ids.dtype != torch.int64 or seq_ids.device != dev or seq_ids.numel() < B):
+        raise ValueError("seq_ids must be an int64 [B] tensor on the logits' device")
+    if next_tokens is not None:
+        if next_tokens.dtype != torch.int32 or next_tokens.device != dev or not next_tokens.is_contiguous():
+            raise ValueError("next_tokens must be a contiguous int32 tensor on the logits' device")
+        if backfill_dest is None or backfill_dest.dtype != torch.int32 or backfill_dest.device != dev \
+                or backfill_dest.numel() < B:
+            raise ValueError("backfill_dest must be an int32 [B] tensor on the logits' device")
+    if out is None:
+        ids = torch.empty(B, dtype=torch.int32, device=dev)
+        lps = torch.empty(B, dtype=torch.float32, device=dev)
+        tids = torch.empty((B, n_top), dtype=torch.int32, device=dev)
+        tlps = torch.empty((B, n_top), dtype=torch.float32, device=dev)
+        flags = torch.empty(B, dtype=torch.int32, device=dev)
+    else:
+        ids, lps, tids, tlps, flags = out
+    dt = _dtype_code(logits)
+    ws = _ws_for(dev, workspace)
+    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)))
+    prm = _params(params, dev)
+    stp = _Step(seed=seed & (2**64 - 1), step=step & (2**64 - 1),
+                seq_ids=seq_ids.data_ptr() if seq_ids is not None else None,
+                next_tokens=next_tokens.data_ptr() if next_tokens is not None else None,
+                backfill_dest=backfill_dest.data_ptr() if next_tokens is not None else None,
+                next_len=next_tokens.numel() if next_tokens is not None else 0)
+    st = _lib.albireo_sample_step(logits.data_ptr(), dt, B, V, ld, ctypes.byref(prm) if prm else None,
+                                  ctypes.byref(stp), ids.data_ptr(), lps.data_ptr(), n_top,
+                                  tids.data_ptr() if n_top else None, tlps.data_ptr() if n_top else None,
+                                  flags.data_ptr(), wptr, wbytes, _stream(stream))
+    if st != OK:
+        raise AlbireoError(st, "albireo_sample_step")
+    return ids, lps, tids, tlps, flags
+
+
+def philox_uniforms(seed: int, step: int, seq_ids: Optional[torch.Tensor] = None, B: Optional[int] = None,
+                    device=None, stream=None) -> torch.Tensor:
+    """albireo_philox_uniforms: float32 [B] uniforms for (seed, step, seq_ids) (seq_ids None: row index)."""
+    if seq_ids is not None:
+        if seq_ids.dtype != torch.int64 or not seq_ids.is_contiguous():
+            raise ValueError("seq_ids must be a contiguous int64 tensor")
+        B = seq_ids.numel()
+        device = seq_ids.device
+    out = torch.empty(B, dtype=torch.float32, device=device)
+    st = _lib.albireo_philox_uniforms(seed & (2**64 - 1), step & (2**64 - 1),
+                                      seq_ids.data_ptr() if seq_ids is not None else None, B,
+                                      out.data_ptr() if B else None, _stream(stream))
+    if st != OK:
+        raise AlbireoError(st, "albireo_philox_uniforms")
+    return out
+
+
+def backfill(ids: torch.Tensor, dest: torch.Tensor, next_tokens: torch.Tensor, stream=None) -> torch.Tensor:
+    """albireo_backfill: next_tokens[dest[i]] = ids[i] where the slot exists (in place; returned)."""
+    for t, name in ((ids, "ids"), (dest, "dest"), (next_tokens, "next_tokens")):
+        if t.dtype != torch.int32 or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous int32 tensor" % name)
+    B = ids.numel()
+    if dest.numel() < B:
+        raise ValueError("dest must have one slot per id")
+    st = _lib.albireo_backfill(ids.data_ptr(), dest.data_ptr(), B, next_tokens.data_ptr(), next_tokens.numel(),
+                               _stream(stream))
+    if st != OK:
+        raise AlbireoError(st, "albireo_backfill")
+    return next_tokens
 
 
 def apply_penalties(logits: torch.Tensor, params: SamplingParams, V: Optional[int] = None, out=None,

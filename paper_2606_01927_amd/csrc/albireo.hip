@@ -87,6 +87,14 @@ struct KArgs {
   float* out_threshold;
   int32_t* out_kept;
   float* out_log_norm;
+  // device random numbers: the uniform of a row from (seed, step, its sequence id) instead of uniforms
+  int32_t rng_on;
+  uint64_t rng_seed, rng_step;
+  const int64_t* seq_ids;  // NULL: the row index
+  // early-feedback backfill: the sampled id of row r also goes to next_tokens[backfill_dest[r]]
+  int32_t* next_tokens;
+  const int32_t* backfill_dest;
+  int64_t next_len;
   int32_t mode;          // 0: sample, 1: topk_topp
   int32_t P;             // chunks per row
   int32_t n_groups;      // persistent row groups (grid = n_groups * P)
@@ -588,10 +596,38 @@ __constant__ float kParamDefaults[8] = {1.0f, 1.0f, 0.0f, 1.0f, 0.0f, 0.0f, 0.0f
 __constant__ int32_t kZeroI32[2] = {0, 0};
 __constant__ int64_t kZeroI64[2] = {0, 0};
 
+// ----------------------------------------------------------------------------------------------
+// Counter-based uniforms: Philox-4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC 2011).  Each
+// round forms the 64-bit products of counter words 0 and 2 with two fixed odd multipliers, and the
+// new counter is (high half of the second product ^ word 1 ^ key 0, its low half, high half of the
+// first product ^ word 3 ^ key 1, its low half); the key advances by two Weyl constants per round.
+// A row's uniform: counter (step, sequence id) as four 32-bit words (low word first), key = seed, and
+// the top 24 bits of the first output word scaled by 2^-24, so u lies in [0, 1) on a 2^-24 grid.
+// Every argument here is wave-uniform, so the rounds run on the scalar unit.
+// ----------------------------------------------------------------------------------------------
+__host__ __device__ __forceinline__ float philox_uniform(uint64_t seed, uint64_t step, uint64_t seq) {
+  constexpr uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+  uint32_t c0 = (uint32_t)step, c1 = (uint32_t)(step >> 32), c2 = (uint32_t)seq, c3 = (uint32_t)(seq >> 32);
+  uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t a0 = (uint64_t)M0 * c0, a1 = (uint64_t)M1 * c2;
+    const uint32_t n0 = (uint32_t)(a1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(a0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)a1;
+    c3 = (uint32_t)a0;
+    c0 = n0;
+    c2 = n2;
+    k0 += W0;
+    k1 += W1;
+  }
+  return (float)(c0 >> 8) * (1.0f / 16777216.0f);
+}
+
 struct RawParams {
   float T, p, mp, rep, freq, pres, u;
   int k;
-  int64_t lo, hi;
+  int64_t lo, hi, seq;
 };
 
 // Issue the row's parameter loads (scalar, no branches); the values are used later, so the loads are
@@ -610,6 +646,7 @@ __device__ __forceinline__ RawParams row_params_load(const KArgs& a, int64_t row
   const int64_t* ho = q.hist_offsets ? q.hist_offsets + row : &kZeroI64[0];
   rp.lo = sload(ho);
   rp.hi = sload(ho + 1);
+  rp.seq = a.seq_ids ? sload(a.seq_ids + row) : row;
   return rp;
 }
 
@@ -648,7 +685,7 @@ __device__ __forceinline__ void row_params(const KArgs& a, RawParams rp, RowStat
       R.h_hi = hi;
     }
   }
-  R.u = rp.u;
+  R.u = a.rng_on ? philox_uniform(a.rng_seed, a.rng_step, (uint64_t)rp.seq) : rp.u;
   R.flags = flags;
 }
 
@@ -2487,6 +2524,11 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
         a.out_ids[row] = res.id;
         a.out_logprobs[row] = res.id >= 0 ? (float)((double)res.zid - (double)m - X.L) : -INFINITY;
       }
+      // early-feedback backfill into the next iteration's token slots (an empty row sends -1)
+      if (a.next_tokens && threadIdx.x == 0 && (skip ? leader : res.id_here)) {
+        const int32_t d = a.backfill_dest[row];
+        if (d >= 0 && (int64_t)d < a.next_len) a.next_tokens[d] = skip ? -1 : res.id;
+      }
     }
     if (leader && threadIdx.x == 0) {
       if (a.out_flags) a.out_flags[row] = row_flags;
@@ -2577,6 +2619,23 @@ struct PenSmem {
 };
 
 __device__ __forceinline__ uint32_t pen_hash(int id) { return ((uint32_t)id * 2654435761u) >> (32 - PEN_LOG2_HCAP); }
+
+// The uniforms alone (one thread per row), for callers that sample elsewhere.
+__global__ __launch_bounds__(256) void k_philox_uniforms(uint64_t seed, uint64_t step, const int64_t* seq_ids,
+                                                         int64_t B, float* out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < B) out[i] = philox_uniform(seed, step, seq_ids ? (uint64_t)seq_ids[i] : (uint64_t)i);
+}
+
+// The backfill alone (one thread per row).
+__global__ __launch_bounds__(256) void k_backfill(const int32_t* ids, const int32_t* dest, int64_t B,
+                                                  int32_t* next_tokens, int64_t next_len) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < B) {
+    const int32_t d = dest[i];
+    if (d >= 0 && (int64_t)d < next_len) next_tokens[d] = ids[i];
+  }
+}
 
 template <class DT>
 __global__ __launch_bounds__(PEN_NT) void k_penalties(const unsigned char* logits, int64_t V, int64_t ld,
@@ -2873,6 +2932,71 @@ albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64
   a.mode = 0;
   a.ws = static_cast<unsigned char*>(workspace);
   return launch_sample(a, G, stream);
+}
+
+albireo_status_t albireo_sample_step(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
+                                     const albireo_params_t* params, const albireo_step_t* step, int32_t* out_ids,
+                                     float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
+                                     float* out_top_logprobs, uint32_t* out_flags, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+  albireo_status_t st = check_common(logits, dtype, B, V, ld, params);
+  if (st != ALBIREO_OK) return st;
+  if (!step || n_top < 0 || n_top > ALBIREO_MAX_TOP_N) return ALBIREO_E_INVALID;
+  if (step->next_tokens && (!step->backfill_dest || step->next_len < 0)) return ALBIREO_E_INVALID;
+  if (B == 0) return ALBIREO_OK;
+  if (!out_ids || !out_logprobs) return ALBIREO_E_INVALID;
+  if (n_top > 0 && (!out_top_ids || !out_top_logprobs)) return ALBIREO_E_INVALID;
+  Geometry G;
+  if (make_geometry(B, V, dtype, G) != hipSuccess) return ALBIREO_E_LAUNCH;
+  if (!G.ok) return ALBIREO_E_UNSUPPORTED;
+  st = check_ws(workspace, workspace_bytes, required_ws(G));
+  if (st != ALBIREO_OK) return st;
+  KArgs a;
+  memset(&a, 0, sizeof a);
+  a.logits = static_cast<const unsigned char*>(logits);
+  a.B = B;
+  a.V = V;
+  a.ld = ld;
+  a.prm = dev_params(params);
+  a.rng_on = 1;
+  a.rng_seed = step->seed;
+  a.rng_step = step->step;
+  a.seq_ids = step->seq_ids;
+  a.next_tokens = step->next_tokens;
+  a.backfill_dest = step->backfill_dest;
+  a.next_len = step->next_len;
+  a.out_ids = out_ids;
+  a.out_logprobs = out_logprobs;
+  a.n_top = n_top;
+  a.out_top_ids = out_top_ids;
+  a.out_top_logprobs = out_top_logprobs;
+  a.out_flags = out_flags;
+  a.mode = 0;
+  a.ws = static_cast<unsigned char*>(workspace);
+  return launch_sample(a, G, stream);
+}
+
+albireo_status_t albireo_philox_uniforms(uint64_t seed, uint64_t step, const int64_t* seq_ids, int64_t B,
+                                         float* out_uniforms, hipStream_t stream) {
+  if (B < 0) return ALBIREO_E_INVALID;
+  if (B == 0) return ALBIREO_OK;
+  if (!out_uniforms) return ALBIREO_E_INVALID;
+  const int64_t blocks = (B + 255) / 256;
+  if (blocks > 0x7fffffff) return ALBIREO_E_UNSUPPORTED;
+  hipLaunchKernelGGL(k_philox_uniforms, dim3((unsigned)blocks), dim3(256), 0, stream, seed, step, seq_ids, B,
+                     out_uniforms);
+  return hipGetLastError() == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
+}
+
+albireo_status_t albireo_backfill(const int32_t* ids, const int32_t* dest, int64_t B, int32_t* next_tokens,
+                                  int64_t next_len, hipStream_t stream) {
+  if (B < 0 || next_len < 0) return ALBIREO_E_INVALID;
+  if (B == 0) return ALBIREO_OK;
+  if (!ids || !dest || !next_tokens) return ALBIREO_E_INVALID;
+  const int64_t blocks = (B + 255) / 256;
+  if (blocks > 0x7fffffff) return ALBIREO_E_UNSUPPORTED;
+  hipLaunchKernelGGL(k_backfill, dim3((unsigned)blocks), dim3(256), 0, stream, ids, dest, B, next_tokens, next_len);
+  return hipGetLastError() == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
 }
 
 albireo_status_t albireo_topk_topp(const float* logits, int64_t B, int64_t V, int64_t ld,

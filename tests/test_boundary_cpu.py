@@ -28,7 +28,8 @@ def alb():
 
 
 def test_header_declares_the_entry_points():
-    assert _declared() == sorted(["albireo_apply_penalties", "albireo_sample", "albireo_status_string",
+    assert _declared() == sorted(["albireo_apply_penalties", "albireo_backfill", "albireo_philox_uniforms",
+                                  "albireo_sample", "albireo_sample_step", "albireo_status_string",
                                   "albireo_topk_topp", "albireo_workspace_size"])
 
 
@@ -93,3 +94,32 @@ def test_penalty_and_filter_entry_points_validate(alb):
 
 def test_workspace_size_without_rows(alb):
     assert alb.workspace_size(0, 1000, __import__("torch").bfloat16) == 256
+
+
+def test_step_rng_and_backfill_entry_points_validate(alb):
+    step_fn = alb.raw_call("albireo_sample_step")
+
+    def call(st, **kw):
+        a = dict(logits=0x1000, dtype=alb.BF16, B=4, V=1000, ld=1000, ids=0x3000, lps=0x4000, n_top=0)
+        a.update(kw)
+        return step_fn(a["logits"], a["dtype"], a["B"], a["V"], a["ld"], None, st, a["ids"], a["lps"], a["n_top"],
+                       None, None, None, None, 0, None)
+
+    assert call(None) == alb.E_INVALID                           # no step struct
+    st = alb._Step(seed=1, step=2, seq_ids=None, next_tokens=0x6000, backfill_dest=None, next_len=8)
+    assert call(ctypes.pointer(st)) == alb.E_INVALID             # backfill without destinations
+    st.backfill_dest = 0x7000
+    st.next_len = -1
+    assert call(ctypes.pointer(st)) == alb.E_INVALID             # negative slot count
+    st.next_len = 8
+    assert call(ctypes.pointer(st), B=0) == alb.OK               # nothing to do, nothing launched
+    assert call(ctypes.pointer(st), ids=None) == alb.E_INVALID
+    rng = alb.raw_call("albireo_philox_uniforms")
+    assert rng(1, 2, None, -1, 0x1000, None) == alb.E_INVALID
+    assert rng(1, 2, None, 5, None, None) == alb.E_INVALID
+    assert rng(1, 2, None, 0, None, None) == alb.OK
+    bf = alb.raw_call("albireo_backfill")
+    assert bf(0x1000, 0x2000, -1, 0x3000, 4, None) == alb.E_INVALID
+    assert bf(0x1000, None, 3, 0x3000, 4, None) == alb.E_INVALID
+    assert bf(0x1000, 0x2000, 3, 0x3000, -1, None) == alb.E_INVALID
+    assert bf(None, None, 0, None, 0, None) == alb.OK
