@@ -107,6 +107,44 @@ def cpu_baseline(w, seconds_target: float = 15.0) -> dict:
             "sample": "%d rows of the B=256 V=152064 bf16 workload (%.1f s)" % (rows_done, el)}
 
 
+def step_extras(alb, w, copies, p, ws, stream, reps: int = 50) -> dict:
+    """Per-call times (HIP events on the launch stream) of the decoding-step extras on the same
+    workload: sampling with device-generated uniforms and the fused backfill (one launch), and the
+    standalone generator and scatter kernels for the same B."""
+    import torch
+
+    dev = copies[0].device
+    B, V = w.B, w.V
+    seq = torch.arange(B, dtype=torch.int64, device=dev) * 7919 + 13
+    nxt = torch.zeros(B, dtype=torch.int32, device=dev)
+    dest = torch.randperm(B, device=dev).to(torch.int32)
+    ids = torch.zeros(B, dtype=torch.int32, device=dev)
+    outs = (ids, torch.empty(B, dtype=torch.float32, device=dev),
+            torch.empty((B, w.n_top), dtype=torch.int32, device=dev),
+            torch.empty((B, w.n_top), dtype=torch.float32, device=dev), torch.empty(B, dtype=torch.int32, device=dev))
+
+    def timed(fn):
+        for i in range(5):
+            fn(i)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(reps):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    t_step = timed(lambda i: alb.sample_step(copies[i % len(copies)], 2026, i, seq, p, n_top=w.n_top, V=V,
+                                             next_tokens=nxt, backfill_dest=dest, workspace=ws, stream=stream,
+                                             out=outs))
+    t_rng = timed(lambda i: alb.philox_uniforms(2026, i, seq, stream=stream))
+    t_bf = timed(lambda i: alb.backfill(ids, dest, nxt, stream=stream))
+    return {"sample_step_us": t_step, "philox_uniforms_us": t_rng, "backfill_us": t_bf,
+            "note": "sample_step = sampling with device uniforms and the fused backfill, one launch"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -114,6 +152,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--config", type=int, default=3, help="workload index (3 is the headline one)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the timing of the step extras (device uniforms, backfill) after the main loop")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="launch one elementwise copy of this many MiB before the timed region (for "
                          "scaling hardware byte counters)")
@@ -199,6 +239,8 @@ def main():
                      "launch_us_avg": launch_us, "host_wall_us_per_step": wall * 1e6 / args.steps},
         "wall_s": wall,
     }
+    if not args.no_extras:
+        res["step_extras"] = step_extras(alb, w, copies, p, ws, stream)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res))
