@@ -141,8 +141,19 @@ def step_extras(alb, w, copies, p, ws, stream, reps: int = 50) -> dict:
                                              out=outs))
     t_rng = timed(lambda i: alb.philox_uniforms(2026, i, seq, stream=stream))
     t_bf = timed(lambda i: alb.backfill(ids, dest, nxt, stream=stream))
-    return {"sample_step_us": t_step, "philox_uniforms_us": t_rng, "backfill_us": t_bf,
-            "note": "sample_step = sampling with device uniforms and the fused backfill, one launch"}
+    res = {"sample_step_us": t_step, "philox_uniforms_us": t_rng, "backfill_us": t_bf,
+           "note": "sample_step = sampling with device uniforms and the fused backfill, one launch"}
+    # the same rows as one worker of t = 8 receives them from the all-to-all: [t][B][V / t] blocks
+    t = 8
+    L = alb.shard_len_for(V, t, copies[0].dtype)
+    if L * t == V and copies[0].stride(0) == V:
+        recvs = [c.view(B, t, L).permute(1, 0, 2).contiguous() for c in copies]
+        uni = torch.rand(B, device=dev)
+        res["sample_sharded_t8_us"] = timed(
+            lambda i: alb.sample_sharded(recvs[i % len(recvs)], V=V, uniforms=uni, params=p, n_top=w.n_top,
+                                         workspace=ws, stream=stream, out=outs))
+        del recvs
+    return res
 
 
 def main():

@@ -186,6 +186,41 @@ albireo_status_t albireo_sample_step(const void* logits, albireo_dtype_t dtype, 
                                      size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * The all-to-all receive layout (host struct, read during the call only).  Before sampling, each of t
+ * workers holds a vocabulary shard [s, V/t] of the whole batch; the all-to-all that replaces the gather
+ * (sec. 6.1, Eq. opt_sample, the exchange written g-hat; sec. 6.2, "Efficient logit exchange") sends
+ * every worker the shard columns of its own s/t rows, so worker j receives t blocks [s/t, V/t], one
+ * from each worker, one after another.  This struct describes such a buffer so that it can be sampled
+ * in place, with no repack:
+ * element v of row i lies at
+ *     logits + (v / shard_len) * shard_stride + i * ld + (v % shard_len)        (elements)
+ * The packed receive buffer [t][B][shard_len] has shard_stride = B * shard_len and ld = shard_len.
+ * The number of blocks is ceil(V / shard_len); the last block may be partly used (a worker's padded
+ * vocabulary columns past V are never read).
+ */
+typedef struct {
+  int64_t shard_len;    /* vocabulary columns per block (elements), > 0                       */
+  int64_t shard_stride; /* elements from the start of one block to the next, >= shard_len     */
+} albireo_shards_t;
+
+/*
+ * albireo_sample / albireo_sample_step on logits in the layout `shards` describes.  Exactly one of
+ * `uniforms` (as albireo_sample) and `step` (as albireo_sample_step) is given.  The row's 16-byte
+ * slots must each lie inside one block: logits 16-byte aligned, and shard_len, shard_stride and ld
+ * times the element size multiples of 16 (else ALBIREO_E_UNSUPPORTED).  ld >= min(shard_len, V).
+ * The results, including the reduction order, equal albireo_sample's on the same rows stored
+ * row-major with 16-byte aligned rows.  Batch padding rows (sec. 6.2, "Batch padding": the batch is
+ * padded to a multiple of t and the padded outputs are discarded before the backfill) are sampled
+ * like any other row; a backfill slot of -1 keeps their ids out of the next iteration.
+ */
+albireo_status_t albireo_sample_sharded(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
+                                        const albireo_shards_t* shards, const albireo_params_t* params,
+                                        const float* uniforms, const albireo_step_t* step, int32_t* out_ids,
+                                        float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
+                                        float* out_top_logprobs, uint32_t* out_flags, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
+/*
  * The device uniforms alone: out_uniforms[i] (device, [B] fp32) = the uniform described above for
  * (seed, step, seq_ids[i]) (seq_ids NULL: i).  No workspace.
  */

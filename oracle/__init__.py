@@ -74,6 +74,9 @@ def _load(path: str = _LIB):
         lib.oracle_backfill.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                         ctypes.c_int64]
         lib.oracle_backfill.restype = None
+        lib.oracle_receive_rows.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
+                                            ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_receive_rows.restype = None
         _libs[path] = lib
     return _libs[path]
 
@@ -176,6 +179,18 @@ def backfill(ids, dest, next_tokens, lib_path: str = _LIB) -> np.ndarray:
     return out
 
 
+def receive_rows(buf, B: int, V: int, ld: int, L: int, S: int, lib_path: str = _LIB) -> np.ndarray:
+    """O-13: the [B, V] rows held in an all-to-all receive buffer (flat array of bf16 bit patterns or
+    fp32) with blocks of L columns, S elements apart, row stride ld inside a block."""
+    buf = np.ascontiguousarray(buf).reshape(-1)
+    assert buf.dtype in (np.uint16, np.float32)
+    out = np.zeros((B, V), buf.dtype)
+    if B and V:
+        assert (V - 1) // L * S + (B - 1) * ld + min(L, V) - 1 < buf.size
+    _load(lib_path).oracle_receive_rows(buf.ctypes.data, buf.itemsize, B, V, ld, L, S, out.ctypes.data)
+    return out
+
+
 class Variant:
     """The oracle's interface bound to another build of the same source (used by the mutation test,
     which compiles deliberately broken copies and checks that the pins reject them)."""
@@ -196,3 +211,6 @@ class Variant:
 
     def backfill(self, ids, dest, next_tokens):
         return backfill(ids, dest, next_tokens, lib_path=self.lib_path)
+
+    def receive_rows(self, buf, B, V, ld, L, S):
+        return receive_rows(buf, B, V, ld, L, S, lib_path=self.lib_path)

@@ -428,3 +428,23 @@ void oracle_backfill(const int32_t* ids, const int32_t* dest, int64_t B, int32_t
     if (d >= 0 && d < n_next) next_tokens[d] = ids[i];
   }
 }
+
+/*
+ * O-13 Rows of the all-to-all receive layout (sec. 6.1, Eq. opt_sample: the exchange written g-hat
+ * turns the workers' vocabulary shards into row shards before Sample; sec. 6.2, "Efficient logit
+ * exchange").  Worker j receives from every worker w the columns of w's vocabulary shard for j's
+ * rows, one block after another, so element v of its row i lies in block v / L at column v % L:
+ *     rows[i][v] = buf[(v / L) * S + i * ld + v % L]            (elements of es bytes)
+ * L = columns per block, S = elements between block starts, ld = row stride inside a block.  Sampling
+ * then runs on these rows unchanged (O-0 to O-10).
+ */
+void oracle_receive_rows(const void* buf, int32_t es, int64_t B, int64_t V, int64_t ld, int64_t L, int64_t S,
+                         void* rows) {
+  const unsigned char* src = (const unsigned char*)buf;
+  unsigned char* dst = (unsigned char*)rows;
+  for (int64_t i = 0; i < B; ++i)
+    for (int64_t v = 0; v < V; ++v) {
+      const int64_t at = (v / L) * S + i * ld + v % L;
+      memcpy(dst + (i * V + v) * es, src + at * es, (size_t)es);
+    }
+}

@@ -45,6 +45,10 @@ class _Step(ctypes.Structure):
     ]
 
 
+class _Shards(ctypes.Structure):
+    _fields_ = [("shard_len", ctypes.c_int64), ("shard_stride", ctypes.c_int64)]
+
+
 _vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
 _lib.albireo_workspace_size.argtypes = [_i64, _i64, ctypes.c_int, _i32]
 _lib.albireo_workspace_size.restype = _sz
@@ -60,6 +64,10 @@ _lib.albireo_topk_topp.restype = ctypes.c_int
 _lib.albireo_sample_step.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Params),
                                      ctypes.POINTER(_Step), _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.albireo_sample_step.restype = ctypes.c_int
+_lib.albireo_sample_sharded.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Shards),
+                                        ctypes.POINTER(_Params), _vp, ctypes.POINTER(_Step), _vp, _vp, _i32, _vp,
+                                        _vp, _vp, _vp, _sz, _vp]
+_lib.albireo_sample_sharded.restype = ctypes.c_int
 _lib.albireo_philox_uniforms.argtypes = [ctypes.c_uint64, ctypes.c_uint64, _vp, _i64, _vp, _vp]
 _lib.albireo_philox_uniforms.restype = ctypes.c_int
 _lib.albireo_backfill.argtypes = [_vp, _vp, _i64, _vp, _i64, _vp]
@@ -67,7 +75,8 @@ _lib.albireo_backfill.restype = ctypes.c_int
 _lib.albireo_status_string.argtypes = [ctypes.c_int]
 _lib.albireo_status_string.restype = ctypes.c_char_p
 
-EXPORTED = ("albireo_workspace_size", "albireo_sample", "albireo_sample_step", "albireo_philox_uniforms",
+EXPORTED = ("albireo_workspace_size", "albireo_sample", "albireo_sample_step", "albireo_sample_sharded",
+            "albireo_philox_uniforms",
             "albireo_backfill", "albireo_apply_penalties", "albireo_topk_topp", "albireo_status_string")
 
 
@@ -230,14 +239,7 @@ class PreparedSample:
             raise AlbireoError(st, "albireo_sample")
 
 
-def sample_step(logits: torch.Tensor, seed: int, step: int, seq_ids: Optional[torch.Tensor] = None,
-                params: Optional[SamplingParams] = None, n_top: int = 0, V: Optional[int] = None,
-                next_tokens: Optional[torch.Tensor] = None, backfill_dest: Optional[torch.Tensor] = None,
-                workspace: Optional[Workspace] = None, stream=None, out=None):
-    """albireo_sample_step: uniforms generated on the device from (seed, step, seq_ids), and the sampled
-    ids optionally backfilled into next_tokens at backfill_dest.  Returns what sample() returns."""
-    dev = logits.device
-    B, V, ld = _rows(logits, V)
+def _step_arg(dev, B, seed, step, seq_ids, next_tokens, backfill_dest):
     if seq_ids is not None and (seq_ids.dtype != torch.int64 or seq_ids.device != dev or seq_ids.numel() < B):
         raise ValueError("seq_ids must be an int64 [B] tensor on the logits' device")
     if next_tokens is not None:
@@ -246,29 +248,98 @@ def sample_step(logits: torch.Tensor, seed: int, step: int, seq_ids: Optional[to
         if backfill_dest is None or backfill_dest.dtype != torch.int32 or backfill_dest.device != dev \
                 or backfill_dest.numel() < B:
             raise ValueError("backfill_dest must be an int32 [B] tensor on the logits' device")
-    if out is None:
-        ids = torch.empty(B, dtype=torch.int32, device=dev)
-        lps = torch.empty(B, dtype=torch.float32, device=dev)
-        tids = torch.empty((B, n_top), dtype=torch.int32, device=dev)
-        tlps = torch.empty((B, n_top), dtype=torch.float32, device=dev)
-        flags = torch.empty(B, dtype=torch.int32, device=dev)
-    else:
-        ids, lps, tids, tlps, flags = out
+    return _Step(seed=seed & (2**64 - 1), step=step & (2**64 - 1),
+                 seq_ids=seq_ids.data_ptr() if seq_ids is not None else None,
+                 next_tokens=next_tokens.data_ptr() if next_tokens is not None else None,
+                 backfill_dest=backfill_dest.data_ptr() if next_tokens is not None else None,
+                 next_len=next_tokens.numel() if next_tokens is not None else 0)
+
+
+def _outs(B, n_top, dev, out):
+    if out is not None:
+        return out
+    return (torch.empty(B, dtype=torch.int32, device=dev), torch.empty(B, dtype=torch.float32, device=dev),
+            torch.empty((B, n_top), dtype=torch.int32, device=dev),
+            torch.empty((B, n_top), dtype=torch.float32, device=dev), torch.empty(B, dtype=torch.int32, device=dev))
+
+
+def sample_step(logits: torch.Tensor, seed: int, step: int, seq_ids: Optional[torch.Tensor] = None,
+                params: Optional[SamplingParams] = None, n_top: int = 0, V: Optional[int] = None,
+                next_tokens: Optional[torch.Tensor] = None, backfill_dest: Optional[torch.Tensor] = None,
+                workspace: Optional[Workspace] = None, stream=None, out=None):
+    """albireo_sample_step: uniforms generated on the device from (seed, step, seq_ids), and the sampled
+    ids optionally backfilled into next_tokens at backfill_dest.  Returns what sample() returns."""
+    dev = logits.device
+    B, V, ld = _rows(logits, V)
+    stp = _step_arg(dev, B, seed, step, seq_ids, next_tokens, backfill_dest)
+    ids, lps, tids, tlps, flags = _outs(B, n_top, dev, out)
     dt = _dtype_code(logits)
     ws = _ws_for(dev, workspace)
     wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)))
     prm = _params(params, dev)
-    stp = _Step(seed=seed & (2**64 - 1), step=step & (2**64 - 1),
-                seq_ids=seq_ids.data_ptr() if seq_ids is not None else None,
-                next_tokens=next_tokens.data_ptr() if next_tokens is not None else None,
-                backfill_dest=backfill_dest.data_ptr() if next_tokens is not None else None,
-                next_len=next_tokens.numel() if next_tokens is not None else 0)
     st = _lib.albireo_sample_step(logits.data_ptr(), dt, B, V, ld, ctypes.byref(prm) if prm else None,
                                   ctypes.byref(stp), ids.data_ptr(), lps.data_ptr(), n_top,
                                   tids.data_ptr() if n_top else None, tlps.data_ptr() if n_top else None,
                                   flags.data_ptr(), wptr, wbytes, _stream(stream))
     if st != OK:
         raise AlbireoError(st, "albireo_sample_step")
+    return ids, lps, tids, tlps, flags
+
+
+def shard_len_for(V: int, t: int, dtype: torch.dtype) -> int:
+    """Columns per vocabulary shard when V is split over t workers: ceil(V / t) rounded up to whole
+    16-byte slots, the block length albireo_sample_sharded accepts (the last shard is partly used)."""
+    vec = 16 // torch.empty((), dtype=dtype).element_size()
+    per = (V + t - 1) // t
+    return (per + vec - 1) // vec * vec
+
+
+def padded_batch(s: int, t: int) -> int:
+    """Batch size after batch padding: the smallest multiple of t that holds s rows (sec. 6.2,
+    "Batch padding")."""
+    if s < 0 or t <= 0:
+        raise ValueError("need s >= 0 and t > 0")
+    return -(-s // t) * t
+
+
+def sample_sharded(recv: torch.Tensor, V: Optional[int] = None, uniforms: Optional[torch.Tensor] = None,
+                   seed: Optional[int] = None, step: int = 0, seq_ids: Optional[torch.Tensor] = None,
+                   params: Optional[SamplingParams] = None, n_top: int = 0,
+                   next_tokens: Optional[torch.Tensor] = None, backfill_dest: Optional[torch.Tensor] = None,
+                   workspace: Optional[Workspace] = None, stream=None, out=None):
+    """albireo_sample_sharded on an all-to-all receive buffer recv [t, B, shard_len] (unit stride along
+    the last axis; recv.stride(0) is the block stride and recv.stride(1) the row stride): row i is the
+    concatenation of recv[0, i], recv[1, i], ... cut at V (default t * shard_len).  Give uniforms
+    (as sample()) or seed (as sample_step(), with step, seq_ids and the optional backfill)."""
+    if recv.dim() != 3 or recv.stride(2) != 1:
+        raise ValueError("recv must be a 3-D tensor [t, B, shard_len] with unit stride along the last axis")
+    if (uniforms is None) == (seed is None):
+        raise ValueError("give exactly one of uniforms and seed")
+    dev = recv.device
+    t, B, L = recv.shape
+    V = t * L if V is None else V
+    if not (t - 1) * L < V <= t * L:
+        raise ValueError("V must lie in ((t - 1) * shard_len, t * shard_len]")
+    stp = None
+    if seed is not None:
+        stp = _step_arg(dev, B, seed, step, seq_ids, next_tokens, backfill_dest)
+    elif uniforms.dtype != torch.float32 or uniforms.device != dev or uniforms.numel() < B:
+        raise ValueError("uniforms must be a float32 [B] tensor on the logits' device")
+    ids, lps, tids, tlps, flags = _outs(B, n_top, dev, out)
+    dt = _dtype_code(recv)
+    ws = _ws_for(dev, workspace)
+    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)))
+    prm = _params(params, dev)
+    shards = _Shards(shard_len=L, shard_stride=recv.stride(0))
+    st = _lib.albireo_sample_sharded(recv.data_ptr(), dt, B, V, recv.stride(1), ctypes.byref(shards),
+                                     ctypes.byref(prm) if prm else None,
+                                     uniforms.data_ptr() if uniforms is not None else None,
+                                     ctypes.byref(stp) if stp is not None else None, ids.data_ptr(),
+                                     lps.data_ptr(), n_top, tids.data_ptr() if n_top else None,
+                                     tlps.data_ptr() if n_top else None, flags.data_ptr(), wptr, wbytes,
+                                     _stream(stream))
+    if st != OK:
+        raise AlbireoError(st, "albireo_sample_sharded")
     return ids, lps, tids, tlps, flags
 
 

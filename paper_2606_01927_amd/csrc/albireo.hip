@@ -95,6 +95,11 @@ struct KArgs {
   int32_t* next_tokens;
   const int32_t* backfill_dest;
   int64_t next_len;
+  // all-to-all receive layout: the row is split into blocks of seg_sps 16-byte slots, block b of row i
+  // starting seg_gap bytes after the end of block b - 1 (the kernels built for it only)
+  uint32_t seg_sps, seg_magic;  // slots per block; floor((2^32 - 1) / seg_sps)
+  uint32_t seg_ntq, seg_ntr;    // NT = seg_ntq * seg_sps + seg_ntr
+  int64_t seg_gap;
   int32_t mode;          // 0: sample, 1: topk_topp
   int32_t P;             // chunks per row
   int32_t n_groups;      // persistent row groups (grid = n_groups * P)
@@ -559,6 +564,9 @@ struct RowState {
   int64_t h_lo, h_hi;
   float u;
   uint32_t flags;
+  bool seg;            // the row is laid out in blocks (all-to-all receive layout)
+  uint32_t sps, smagic;
+  int64_t sgap;
 };
 
 // Load of a wave-uniform, read-only value through the scalar unit (constant address space): it is
@@ -568,9 +576,39 @@ __device__ __forceinline__ T sload(const T* p) {
   return *(const __attribute__((address_space(4))) T*)(p);
 }
 
-// Row geometry from the kernel arguments alone (no loads), so the row loads can start at once.
+// Block of a body slot in the blocked layout: the reciprocal-multiplier estimate is low by at most
+// one for q < 2^31, which the remainder test corrects.
+__device__ __forceinline__ uint32_t seg_of(const RowState& R, uint32_t q) {
+  uint32_t g = __umulhi(q, R.smagic);
+  if (q - g * R.sps >= R.sps) ++g;
+  return g;
+}
+// Address of a row position (bytes), in either layout.
 template <class DT>
+__device__ __forceinline__ const unsigned char* pos_ptr(const RowState& R, int64_t pos) {
+  const unsigned char* p = R.rowp + pos * DT::ES;
+  if (R.seg) p += (int64_t)seg_of(R, (uint32_t)(pos / DT::VEC)) * R.sgap;
+  return p;
+}
+template <class DT>
+__device__ __forceinline__ float load_pos(const RowState& R, int64_t pos) {
+  return DT::load1(pos_ptr<DT>(R, pos), 0);
+}
+// Byte offset of a body slot from the row's first element (the blocked layout has no head).
+template <class DT>
+__device__ __forceinline__ int64_t slot_off(const RowState& R, int64_t slot) {
+  int64_t o = ((int64_t)R.head + slot * DT::VEC) * DT::ES;
+  if (R.seg) o += (int64_t)seg_of(R, (uint32_t)slot) * R.sgap;
+  return o;
+}
+
+// Row geometry from the kernel arguments alone (no loads), so the row loads can start at once.
+template <class DT, bool SEG = false>
 __device__ __forceinline__ void row_geometry(const KArgs& a, int64_t row, int c, RowState& R) {
+  R.seg = SEG;
+  R.sps = a.seg_sps;
+  R.smagic = a.seg_magic;
+  R.sgap = a.seg_gap;
   R.row = row;
   R.c = c;
   R.P = a.P;
@@ -849,8 +887,7 @@ struct Resolution {
 // values are in the extras).  Used by the stages that run after the registers are released.
 template <class DT>
 __device__ __forceinline__ uint4 load_masked(const RowState& R, const Smem& s, int64_t slot) {
-  const uint4* body = reinterpret_cast<const uint4*>(R.rowp + (int64_t)R.head * DT::ES);
-  uint4 d = body[slot];
+  uint4 d = *reinterpret_cast<const uint4*>(R.rowp + slot_off<DT>(R, slot));
   if (R.pen_on) {
     const int sl = (int)(slot - R.s0);
     const uint32_t byte = (s.bitmap[sl >> 2] >> ((sl & 3) * 8)) & 255u;
@@ -896,7 +933,7 @@ __device__ __forceinline__ int extras_index(const Smem& s, const RowState& R, in
 template <class DT>
 __device__ __forceinline__ float x_at(const Smem& s, const RowState& R, int n_ext, int pos) {
   const int u = n_ext > 0 ? extras_index<DT>(s, R, pos) : -1;
-  return u >= 0 ? s.x_val[u] : DT::load1(R.rowp, pos);
+  return u >= 0 ? s.x_val[u] : load_pos<DT>(R, pos);
 }
 
 // Gather the n_top-candidate list (or any list) above `bl` into s.sk; returns the count (may
@@ -1912,13 +1949,13 @@ __device__ __forceinline__ float kth_from_hist(const Smem& s, int K) {
 // ----------------------------------------------------------------------------------------------
 // One row chunk end to end.  MULTI selects the build for P > 1 chunks per row (cross-workgroup
 // exchanges through the workspace); the single-chunk build has none of that code.
-template <class DT, int J, bool MULTI>
+template <class DT, int J, bool MULTI, bool SEG>
 __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, int64_t row, int c) {
   const int P = MULTI ? a.P : 1;
   const bool leader = (c == 0);
   {
     RowState R;
-    row_geometry<DT>(a, row, c, R);
+    row_geometry<DT, SEG>(a, row, c, R);
     R.P = P;
 
     // ---------------- row loads first ----------------
@@ -1933,19 +1970,46 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     const int nslots = (int)(R.s1 - R.s0);
     // one buffer resource per chunk (SGPRs) and a 32-bit lane offset; its inputs are made visibly
     // wave-uniform so the descriptor lives in SGPRs
-    const uint64_t cb = reinterpret_cast<uint64_t>(R.rowp + ((int64_t)R.head + R.s0 * DT::VEC) * DT::ES);
+    const int64_t off_s0 = slot_off<DT>(R, R.s0);
+    const uint64_t cb = reinterpret_cast<uint64_t>(R.rowp + off_s0);
     const uint32_t cb_lo = __builtin_amdgcn_readfirstlane((uint32_t)cb);
     const uint32_t cb_hi = __builtin_amdgcn_readfirstlane((uint32_t)(cb >> 32));
+    // bytes from the chunk's first slot to the end of its last (the host keeps this below 2^31)
+    const uint32_t span = SEG ? (nslots > 0 ? (uint32_t)(slot_off<DT>(R, R.s1 - 1) + 16 - off_s0) : 0u)
+                              : (uint32_t)nslots * 16u;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         reinterpret_cast<void*>(((uint64_t)cb_hi << 32) | cb_lo), (short)0,
-        __builtin_amdgcn_readfirstlane(nslots * 16), 0x00020000);
+        __builtin_amdgcn_readfirstlane(span), 0x00020000);
     const int voff = (int)threadIdx.x * 16;
+    // Blocked layout: each thread tracks its slot's place in its block (sr) and the slot's byte
+    // offset from the chunk base (soff), advanced by NT slots per issue; offsets grow with the slot,
+    // so slots past the chunk still land past the range and read as 0.  The host checks that the
+    // offsets of all J slots stay below 2^32.
+    uint32_t sr = 0, soff = 0;
+    const uint32_t sgap = (uint32_t)R.sgap, sps = a.seg_sps, ntr = a.seg_ntr;
+    const uint32_t step0 = (uint32_t)NT * 16u + a.seg_ntq * sgap, step1 = step0 + sgap;
+    if constexpr (SEG) {
+      const uint32_t q0 = (uint32_t)R.s0 + threadIdx.x;
+      const uint32_t g0 = seg_of(R, q0);
+      sr = q0 - g0 * sps;
+      soff = (uint32_t)voff + (g0 - seg_of(R, (uint32_t)R.s0)) * sgap;
+    }
     // Unconditional loads with the whole offset in the range-checked VGPR operand: slots past the
     // chunk read as 0 without touching memory and are set to -inf when consumed (only the last,
-    // partly filled slots can be affected).
+    // partly filled slots can be affected).  Slots are issued in order j = 0, 1, ..., J - 1.
     auto issue = [&](auto jc) __attribute__((always_inline)) {
       constexpr int j = decltype(jc)::value;
-      const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + j * NT * 16, 0, 0);
+      uint32_t off = (uint32_t)(voff + j * NT * 16);
+      if constexpr (SEG) {
+        if constexpr (j > 0) {
+          sr += ntr;
+          const bool w = sr >= sps;
+          sr = w ? sr - sps : sr;
+          soff += w ? step1 : step0;
+        }
+        off = soff;
+      }
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0);
       ch.template set<j>(make_uint4(v[0], v[1], v[2], v[3]));
     };
     // the parameter loads (scalar) go out first, then the first row slots; the rest of the pipeline
@@ -1959,8 +2023,8 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
     // body ones), loaded now and staged after the online pass: one unconditional load per thread
     const int n_head0 = R.owns_head ? R.head : 0;
     const int n_ht0 = n_head0 + (R.owns_tail ? R.V - R.tail_lo : 0);
-    const float xht = DT::load1(
-        R.rowp, (int)threadIdx.x < n_ht0 ? ((int)threadIdx.x < n_head0 ? (int)threadIdx.x
+    const float xht = load_pos<DT>(
+        R, (int)threadIdx.x < n_ht0 ? ((int)threadIdx.x < n_head0 ? (int)threadIdx.x
                                                                        : R.tail_lo + ((int)threadIdx.x - n_head0))
                                          : 0);
     const bool extras_any = R.pen_on || (R.owns_head && R.head > 0) || (R.owns_tail && R.tail_lo < R.V);
@@ -2095,7 +2159,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
         }
         // unconditional loads: a load under a branch is merged at its join, which waits for it
 #pragma unroll
-        for (int q = 0; q < 4; ++q) fv[q] = DT::load1(R.rowp, fid[q]);
+        for (int q = 0; q < 4; ++q) fv[q] = load_pos<DT>(R, fid[q]);
       }
       if constexpr (j0 + PIPE < J) issue(std::integral_constant<int, j0 + PIPE>{});
       if constexpr (j0 + 1 + PIPE < J) issue(std::integral_constant<int, j0 + 1 + PIPE>{});
@@ -2271,7 +2335,7 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
             const int xi = xi0 + q * NT;
             const int pq = xi < n_ext ? s.x_pos[xi] : 0;
             idv[q] = (unsigned)pq < (unsigned)R.V ? pq : 0;  // defensive: only in-row reads
-            xv[q] = DT::load1(R.rowp, idv[q]);
+            xv[q] = load_pos<DT>(R, idv[q]);
           }
         }
 #pragma unroll
@@ -2544,19 +2608,19 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
 }
 
 // Single-chunk rows: one workgroup per row, no workspace.
-template <class DT, int J>
+template <class DT, int J, bool SEG>
 __global__ __launch_bounds__(NT) void k_sample(KArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Smem& s = *reinterpret_cast<Smem*>(smem_raw);
   if (threadIdx.x < 256) s.masktab[threadIdx.x] = DT::mask_of(threadIdx.x);
   RowCtx X;
   memset(&X, 0, sizeof X);
-  process_row<DT, J, false>(a, s, X, (int64_t)blockIdx.x, 0);
+  process_row<DT, J, false, SEG>(a, s, X, (int64_t)blockIdx.x, 0);
 }
 
 // Rows of P > 1 chunks: a persistent cooperative grid of row groups; the P workgroups of a group
 // process the group's rows in lockstep and exchange per-chunk results through the workspace.
-template <class DT, int J>
+template <class DT, int J, bool SEG>
 __global__ __launch_bounds__(NT) void k_sample_multi(KArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Smem& s = *reinterpret_cast<Smem*>(smem_raw);
@@ -2584,7 +2648,7 @@ __global__ __launch_bounds__(NT) void k_sample_multi(KArgs a) {
     X.glists = reinterpret_cast<uint64_t*>(wsg + WL.lists);
   }
   if (threadIdx.x < 256) s.masktab[threadIdx.x] = DT::mask_of(threadIdx.x);
-  for (int64_t row = g; row < a.B; row += a.n_groups) process_row<DT, J, true>(a, s, X, row, c);
+  for (int64_t row = g; row < a.B; row += a.n_groups) process_row<DT, J, true, SEG>(a, s, X, row, c);
 
   // leave the group's counters at zero for the next call
   if (threadIdx.x == 0) {
@@ -2719,21 +2783,27 @@ struct KernelInfo {
   int J;
 };
 
+template <class DT, int J, bool SEG>
+KernelInfo kinfo1(bool multi) {
+  return {multi ? reinterpret_cast<const void*>(&k_sample_multi<DT, J, SEG>)
+                : reinterpret_cast<const void*>(&k_sample<DT, J, SEG>),
+          J};
+}
 template <class DT, int J>
-KernelInfo kinfo(bool multi) {
-  return {multi ? reinterpret_cast<const void*>(&k_sample_multi<DT, J>) : reinterpret_cast<const void*>(&k_sample<DT, J>), J};
+KernelInfo kinfo(bool multi, bool seg) {
+  return seg ? kinfo1<DT, J, true>(multi) : kinfo1<DT, J, false>(multi);
 }
 
 template <class DT>
-KernelInfo pick_kernel(int64_t chunk_slots, bool multi) {
+KernelInfo pick_kernel(int64_t chunk_slots, bool multi, bool seg) {
 #ifdef ALBIREO_DEV_ONE_J  // development builds: a single instantiation for quick compiles
   (void)chunk_slots;
-  return kinfo<DT, ALBIREO_DEV_ONE_J>(multi);
+  return kinfo<DT, ALBIREO_DEV_ONE_J>(multi, seg);
 #else
-  if (chunk_slots <= (int64_t)JSIZES[0] * NT) return kinfo<DT, JSIZES[0]>(multi);
-  if (chunk_slots <= (int64_t)JSIZES[1] * NT) return kinfo<DT, JSIZES[1]>(multi);
-  if (chunk_slots <= (int64_t)JSIZES[2] * NT) return kinfo<DT, JSIZES[2]>(multi);
-  return kinfo<DT, JSIZES[3]>(multi);
+  if (chunk_slots <= (int64_t)JSIZES[0] * NT) return kinfo<DT, JSIZES[0]>(multi, seg);
+  if (chunk_slots <= (int64_t)JSIZES[1] * NT) return kinfo<DT, JSIZES[1]>(multi, seg);
+  if (chunk_slots <= (int64_t)JSIZES[2] * NT) return kinfo<DT, JSIZES[2]>(multi, seg);
+  return kinfo<DT, JSIZES[3]>(multi, seg);
 #endif
 }
 
@@ -2791,7 +2861,7 @@ hipError_t device_caps(int dev, const void* fn, size_t smem, DeviceCaps& out) {
   return hipErrorUnknown;
 }
 
-hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& G) {
+hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& G, bool seg = false) {
   const int VEC = dtype == ALBIREO_BF16 ? BF16T::VEC : F32T::VEC;
   const int64_t max_body = V / VEC;
   int64_t P = (max_body + (int64_t)JMAX * NT - 1) / ((int64_t)JMAX * NT);
@@ -2800,7 +2870,8 @@ hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& 
   if (!G.ok) return hipSuccess;
   G.P = (int)P;
   G.chunk_slots = (max_body + P - 1) / P;
-  G.k = dtype == ALBIREO_BF16 ? pick_kernel<BF16T>(G.chunk_slots, G.P > 1) : pick_kernel<F32T>(G.chunk_slots, G.P > 1);
+  G.k = dtype == ALBIREO_BF16 ? pick_kernel<BF16T>(G.chunk_slots, G.P > 1, seg)
+                              : pick_kernel<F32T>(G.chunk_slots, G.P > 1, seg);
   // the single-chunk kernel skips the dead-slot test below live_slots_min(J) (always true for the
   // size pick_kernel chose; a build restricted to one size can miss it for small rows)
   if (G.P == 1 && max_body - 1 < (int64_t)live_slots_min(G.k.J) * NT) {
@@ -2886,6 +2957,97 @@ albireo_status_t check_ws(void* ws, size_t bytes, size_t need) {
   return ALBIREO_OK;
 }
 
+// The blocked (all-to-all receive) layout: checks that need no device.
+albireo_status_t check_shards(const void* logits, albireo_dtype_t dtype, int64_t V, int64_t ld,
+                              const albireo_shards_t& sh) {
+  const int64_t es = dtype == ALBIREO_BF16 ? 2 : 4;
+  const int64_t L = sh.shard_len, S = sh.shard_stride;
+  if (L <= 0 || S < 0 || ld < 0) return ALBIREO_E_INVALID;
+  if (ld < (L < V ? L : V)) return ALBIREO_E_INVALID;
+  const int64_t t = (V + L - 1) / L;
+  if (t > 1 && S < L) return ALBIREO_E_INVALID;  // blocks of one row must not overlap
+  // every 16-byte slot inside one block: aligned base, row stride, block stride and block length
+  if (reinterpret_cast<uintptr_t>(logits) % 16 || (L * es) % 16 || (S * es) % 16 || (ld * es) % 16)
+    return ALBIREO_E_UNSUPPORTED;
+  if (L * es / 16 > ((int64_t)1 << 31) || (t > 1 && (S - L) * es > ((int64_t)1 << 31))) return ALBIREO_E_UNSUPPORTED;
+  return ALBIREO_OK;
+}
+
+// The blocked layout's kernel arguments (after check_shards), once the kernel size is known.
+albireo_status_t shard_args(albireo_dtype_t dtype, int64_t V, const albireo_shards_t& sh, const Geometry& G,
+                            KArgs& a) {
+  const int64_t es = dtype == ALBIREO_BF16 ? 2 : 4;
+  const int64_t L = sh.shard_len, S = sh.shard_stride;
+  const int64_t t = (V + L - 1) / L;
+  const int64_t sps = L * es / 16;
+  const int64_t gap = t > 1 ? (S - L) * es : 0;
+  // the lane offsets of all J slots a workgroup issues stay below 2^31
+  const int64_t issued = (int64_t)G.k.J * NT;
+  if (issued * 16 + (issued / sps + 1) * gap >= ((int64_t)1 << 31)) return ALBIREO_E_UNSUPPORTED;
+  a.seg_sps = (uint32_t)sps;
+  a.seg_magic = (uint32_t)(0xffffffffull / (uint64_t)sps);
+  a.seg_ntq = (uint32_t)(NT / sps);
+  a.seg_ntr = (uint32_t)(NT % sps);
+  a.seg_gap = gap;
+  return ALBIREO_OK;
+}
+
+// albireo_sample / albireo_sample_step / albireo_sample_sharded: shards NULL is the row-major layout;
+// exactly one of uniforms and step is given.
+albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
+                             const albireo_shards_t* shards, const albireo_params_t* params, const float* uniforms,
+                             const albireo_step_t* step, int32_t* out_ids, float* out_logprobs, int32_t n_top,
+                             int32_t* out_top_ids, float* out_top_logprobs, uint32_t* out_flags, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  // the row-major checks; the blocked layout has its own stride rules (below)
+  albireo_status_t st = check_common(logits, dtype, B, V, shards ? V : ld, params);
+  if (st != ALBIREO_OK) return st;
+  if (n_top < 0 || n_top > ALBIREO_MAX_TOP_N) return ALBIREO_E_INVALID;
+  if (step && step->next_tokens && (!step->backfill_dest || step->next_len < 0)) return ALBIREO_E_INVALID;
+  if (B == 0) return ALBIREO_OK;
+  if ((!uniforms && !step) || !out_ids || !out_logprobs) return ALBIREO_E_INVALID;
+  if (n_top > 0 && (!out_top_ids || !out_top_logprobs)) return ALBIREO_E_INVALID;
+  if (shards) {
+    st = check_shards(logits, dtype, V, ld, *shards);
+    if (st != ALBIREO_OK) return st;
+  }
+  Geometry G;
+  if (make_geometry(B, V, dtype, G, shards != nullptr) != hipSuccess) return ALBIREO_E_LAUNCH;
+  if (!G.ok) return ALBIREO_E_UNSUPPORTED;
+  KArgs a;
+  memset(&a, 0, sizeof a);
+  if (shards) {
+    st = shard_args(dtype, V, *shards, G, a);
+    if (st != ALBIREO_OK) return st;
+  }
+  st = check_ws(workspace, workspace_bytes, required_ws(G));
+  if (st != ALBIREO_OK) return st;
+  a.logits = static_cast<const unsigned char*>(logits);
+  a.B = B;
+  a.V = V;
+  a.ld = ld;
+  a.prm = dev_params(params);
+  a.uniforms = uniforms;
+  if (step) {
+    a.rng_on = 1;
+    a.rng_seed = step->seed;
+    a.rng_step = step->step;
+    a.seq_ids = step->seq_ids;
+    a.next_tokens = step->next_tokens;
+    a.backfill_dest = step->backfill_dest;
+    a.next_len = step->next_len;
+  }
+  a.out_ids = out_ids;
+  a.out_logprobs = out_logprobs;
+  a.n_top = n_top;
+  a.out_top_ids = out_top_ids;
+  a.out_top_logprobs = out_top_logprobs;
+  a.out_flags = out_flags;
+  a.mode = 0;
+  a.ws = static_cast<unsigned char*>(workspace);
+  return launch_sample(a, G, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -2904,34 +3066,8 @@ albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64
                                 float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
                                 float* out_top_logprobs, uint32_t* out_flags, void* workspace,
                                 size_t workspace_bytes, hipStream_t stream) {
-  albireo_status_t st = check_common(logits, dtype, B, V, ld, params);
-  if (st != ALBIREO_OK) return st;
-  if (n_top < 0 || n_top > ALBIREO_MAX_TOP_N) return ALBIREO_E_INVALID;
-  if (B == 0) return ALBIREO_OK;
-  if (!uniforms || !out_ids || !out_logprobs) return ALBIREO_E_INVALID;
-  if (n_top > 0 && (!out_top_ids || !out_top_logprobs)) return ALBIREO_E_INVALID;
-  Geometry G;
-  if (make_geometry(B, V, dtype, G) != hipSuccess) return ALBIREO_E_LAUNCH;
-  if (!G.ok) return ALBIREO_E_UNSUPPORTED;
-  st = check_ws(workspace, workspace_bytes, required_ws(G));
-  if (st != ALBIREO_OK) return st;
-  KArgs a;
-  memset(&a, 0, sizeof a);
-  a.logits = static_cast<const unsigned char*>(logits);
-  a.B = B;
-  a.V = V;
-  a.ld = ld;
-  a.prm = dev_params(params);
-  a.uniforms = uniforms;
-  a.out_ids = out_ids;
-  a.out_logprobs = out_logprobs;
-  a.n_top = n_top;
-  a.out_top_ids = out_top_ids;
-  a.out_top_logprobs = out_top_logprobs;
-  a.out_flags = out_flags;
-  a.mode = 0;
-  a.ws = static_cast<unsigned char*>(workspace);
-  return launch_sample(a, G, stream);
+  return sample_impl(logits, dtype, B, V, ld, nullptr, params, uniforms, nullptr, out_ids, out_logprobs, n_top,
+                     out_top_ids, out_top_logprobs, out_flags, workspace, workspace_bytes, stream);
 }
 
 albireo_status_t albireo_sample_step(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
@@ -2939,41 +3075,20 @@ albireo_status_t albireo_sample_step(const void* logits, albireo_dtype_t dtype, 
                                      float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
                                      float* out_top_logprobs, uint32_t* out_flags, void* workspace,
                                      size_t workspace_bytes, hipStream_t stream) {
-  albireo_status_t st = check_common(logits, dtype, B, V, ld, params);
-  if (st != ALBIREO_OK) return st;
-  if (!step || n_top < 0 || n_top > ALBIREO_MAX_TOP_N) return ALBIREO_E_INVALID;
-  if (step->next_tokens && (!step->backfill_dest || step->next_len < 0)) return ALBIREO_E_INVALID;
-  if (B == 0) return ALBIREO_OK;
-  if (!out_ids || !out_logprobs) return ALBIREO_E_INVALID;
-  if (n_top > 0 && (!out_top_ids || !out_top_logprobs)) return ALBIREO_E_INVALID;
-  Geometry G;
-  if (make_geometry(B, V, dtype, G) != hipSuccess) return ALBIREO_E_LAUNCH;
-  if (!G.ok) return ALBIREO_E_UNSUPPORTED;
-  st = check_ws(workspace, workspace_bytes, required_ws(G));
-  if (st != ALBIREO_OK) return st;
-  KArgs a;
-  memset(&a, 0, sizeof a);
-  a.logits = static_cast<const unsigned char*>(logits);
-  a.B = B;
-  a.V = V;
-  a.ld = ld;
-  a.prm = dev_params(params);
-  a.rng_on = 1;
-  a.rng_seed = step->seed;
-  a.rng_step = step->step;
-  a.seq_ids = step->seq_ids;
-  a.next_tokens = step->next_tokens;
-  a.backfill_dest = step->backfill_dest;
-  a.next_len = step->next_len;
-  a.out_ids = out_ids;
-  a.out_logprobs = out_logprobs;
-  a.n_top = n_top;
-  a.out_top_ids = out_top_ids;
-  a.out_top_logprobs = out_top_logprobs;
-  a.out_flags = out_flags;
-  a.mode = 0;
-  a.ws = static_cast<unsigned char*>(workspace);
-  return launch_sample(a, G, stream);
+  if (!step) return ALBIREO_E_INVALID;
+  return sample_impl(logits, dtype, B, V, ld, nullptr, params, nullptr, step, out_ids, out_logprobs, n_top,
+                     out_top_ids, out_top_logprobs, out_flags, workspace, workspace_bytes, stream);
+}
+
+albireo_status_t albireo_sample_sharded(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
+                                        const albireo_shards_t* shards, const albireo_params_t* params,
+                                        const float* uniforms, const albireo_step_t* step, int32_t* out_ids,
+                                        float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
+                                        float* out_top_logprobs, uint32_t* out_flags, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  if (!shards || (uniforms == nullptr) == (step == nullptr)) return ALBIREO_E_INVALID;
+  return sample_impl(logits, dtype, B, V, ld, shards, params, uniforms, step, out_ids, out_logprobs, n_top,
+                     out_top_ids, out_top_logprobs, out_flags, workspace, workspace_bytes, stream);
 }
 
 albireo_status_t albireo_philox_uniforms(uint64_t seed, uint64_t step, const int64_t* seq_ids, int64_t B,

@@ -29,7 +29,8 @@ def alb():
 
 def test_header_declares_the_entry_points():
     assert _declared() == sorted(["albireo_apply_penalties", "albireo_backfill", "albireo_philox_uniforms",
-                                  "albireo_sample", "albireo_sample_step", "albireo_status_string",
+                                  "albireo_sample", "albireo_sample_sharded", "albireo_sample_step",
+                                  "albireo_status_string",
                                   "albireo_topk_topp", "albireo_workspace_size"])
 
 
@@ -123,3 +124,39 @@ def test_step_rng_and_backfill_entry_points_validate(alb):
     assert bf(0x1000, None, 3, 0x3000, 4, None) == alb.E_INVALID
     assert bf(0x1000, 0x2000, 3, 0x3000, -1, None) == alb.E_INVALID
     assert bf(None, None, 0, None, 0, None) == alb.OK
+
+
+def test_sharded_entry_point_validates(alb):
+    fn = alb.raw_call("albireo_sample_sharded")
+    st = alb._Step(seed=1, step=2, seq_ids=None, next_tokens=None, backfill_dest=None, next_len=0)
+
+    def call(shards, uniforms=0x5000, step=None, **kw):
+        a = dict(logits=0x10000, dtype=alb.BF16, B=4, V=1000, ld=256, ids=0x3000, lps=0x4000)
+        a.update(kw)
+        sh = None if shards is None else ctypes.pointer(alb._Shards(*shards))
+        return fn(a["logits"], a["dtype"], a["B"], a["V"], a["ld"], sh, None, uniforms, step, a["ids"], a["lps"],
+                  0, None, None, None, None, 0, None)
+
+    assert call(None) == alb.E_INVALID                                   # no layout
+    assert call((256, 1024), uniforms=None) == alb.E_INVALID             # neither uniforms nor step
+    assert call((256, 1024), step=ctypes.pointer(st)) == alb.E_INVALID   # both
+    assert call((0, 1024)) == alb.E_INVALID                              # empty blocks
+    assert call((256, 128)) == alb.E_INVALID                             # blocks of a row overlap
+    assert call((256, 1024), ld=100) == alb.E_INVALID                    # rows overlap inside a block
+    assert call((252, 1024)) == alb.E_UNSUPPORTED                        # a 16-byte slot crosses blocks
+    assert call((256, 1028)) == alb.E_UNSUPPORTED                        # misaligned block stride
+    assert call((256, 1024), logits=0x10008) == alb.E_UNSUPPORTED        # misaligned base
+    assert call((256, 1024), ld=260) == alb.E_UNSUPPORTED                # misaligned row stride
+    assert call((256, 1024), B=0) == alb.OK                              # nothing to do, nothing launched
+    assert call((256, 1024), ids=None) == alb.E_INVALID
+
+
+def test_batch_padding_and_shard_length(alb):
+    import torch
+
+    assert [alb.padded_batch(s, 8) for s in (0, 1, 8, 9, 250, 256)] == [0, 8, 8, 16, 256, 256]
+    assert alb.shard_len_for(152064, 8, torch.bfloat16) == 19008
+    assert alb.shard_len_for(32000, 8, torch.bfloat16) == 4000
+    assert alb.shard_len_for(32001, 8, torch.bfloat16) == 4008    # ceil(V / t), whole 16-byte slots
+    assert alb.shard_len_for(32001, 8, torch.float32) == 4004
+    assert alb.shard_len_for(10, 3, torch.float32) == 4

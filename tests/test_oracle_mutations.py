@@ -15,6 +15,7 @@ import pytest
 
 import oracle
 from tests import test_oracle_pins as pins
+from tests import test_oracle_receive_layout as layout_pins
 from tests import test_oracle_rng_backfill as rng_pins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "albireo_oracle.c")
@@ -49,13 +50,20 @@ MUTANTS = [
      "const uint32_t ctr[4] = {(uint32_t)step, 0u,"),
     ("backfill skips slot 0", "if (d >= 0 && d < n_next) next_tokens[d] = ids[i];",
      "if (d > 0 && d < n_next) next_tokens[d] = ids[i];"),
+    ("block stride taken as the row stride", "const int64_t at = (v / L) * S + i * ld + v % L;",
+     "const int64_t at = (v / L) * ld + i * ld + v % L;"),
+    ("row stride taken as the block length", "const int64_t at = (v / L) * S + i * ld + v % L;",
+     "const int64_t at = (v / L) * S + i * L + v % L;"),
+    ("column taken modulo the row stride", "const int64_t at = (v / L) * S + i * ld + v % L;",
+     "const int64_t at = (v / L) * S + i * ld + v % ld;"),
 ]
 
 
 def _pin_calls():
     """(name, callable) for every pin test, with its parametrisations expanded."""
     calls = []
-    members = inspect.getmembers(pins, inspect.isfunction) + inspect.getmembers(rng_pins, inspect.isfunction)
+    members = (inspect.getmembers(pins, inspect.isfunction) + inspect.getmembers(rng_pins, inspect.isfunction)
+               + inspect.getmembers(layout_pins, inspect.isfunction))
     for name, fn in members:
         if not name.startswith("test_"):
             continue
