@@ -46,6 +46,7 @@ class _In(ctypes.Structure):
         ("min_p", ctypes.c_void_p), ("rep", ctypes.c_void_p), ("freq", ctypes.c_void_p),
         ("pres", ctypes.c_void_p), ("hist_offsets", ctypes.c_void_p), ("hist_ids", ctypes.c_void_p),
         ("hist_len", ctypes.c_int64), ("uniforms", ctypes.c_void_p), ("n_top", ctypes.c_int32),
+        ("prompt_offsets", ctypes.c_void_p), ("prompt_ids", ctypes.c_void_p), ("prompt_len", ctypes.c_int64),
     ]
 
 
@@ -120,6 +121,12 @@ def sample(w, nthreads: int = 0, probs: bool = False, penalised: bool = False, d
     if ho is not None:
         hist_len = 0 if w.hist_ids is None else int(np.asarray(w.hist_ids).size)
         hi = c(w.hist_ids if hist_len else np.zeros(1, np.int32), np.int32)
+    po = c(getattr(w, "prompt_offsets", None), np.int64)
+    pi = None
+    prompt_len = 0
+    if po is not None:
+        prompt_len = 0 if w.prompt_ids is None else int(np.asarray(w.prompt_ids).size)
+        pi = c(w.prompt_ids if prompt_len else np.zeros(1, np.int32), np.int32)
     inp = _In(
         logits=_ptr(logits), is_bf16=1 if w.dtype == "bf16" else 0, B=B, V=V, ld=w.ld,
         temperature=_ptr(c(w.temperature, np.float32)), top_k=_ptr(c(w.top_k, np.int32)),
@@ -127,7 +134,8 @@ def sample(w, nthreads: int = 0, probs: bool = False, penalised: bool = False, d
         rep=_ptr(c(w.repetition_penalty, np.float32)), freq=_ptr(c(w.frequency_penalty, np.float32)),
         pres=_ptr(c(w.presence_penalty, np.float32)), hist_offsets=_ptr(ho),
         hist_ids=_ptr(hi), hist_len=hist_len,
-        uniforms=_ptr(c(w.uniforms, np.float32)) if draw else None, n_top=n_top)
+        uniforms=_ptr(c(w.uniforms, np.float32)) if draw else None, n_top=n_top,
+        prompt_offsets=_ptr(po), prompt_ids=_ptr(pi), prompt_len=prompt_len)
     o = dict(
         ids=np.zeros(B, np.int32), logprobs=np.zeros(B, np.float64),
         top_ids=np.zeros((B, n_top), np.int32), top_logprobs=np.zeros((B, n_top), np.float64),
@@ -179,6 +187,21 @@ def backfill(ids, dest, next_tokens, lib_path: str = _LIB) -> np.ndarray:
     return out
 
 
+def penalty_state(prompt_ids, output_ids, V: int) -> dict:
+    """O-15: a sequence's penalty state after its prompt and outputs: {id: (output count, in prompt)}
+    over the distinct ids of both that lie in [0, V)."""
+    st = {}
+    for t in np.asarray(prompt_ids, dtype=np.int64).ravel():
+        if 0 <= t < V:
+            c, _ = st.get(int(t), (0, False))
+            st[int(t)] = (c, True)
+    for t in np.asarray(output_ids, dtype=np.int64).ravel():
+        if 0 <= t < V:
+            c, f = st.get(int(t), (0, False))
+            st[int(t)] = (c + 1, f)
+    return st
+
+
 def receive_rows(buf, B: int, V: int, ld: int, L: int, S: int, lib_path: str = _LIB) -> np.ndarray:
     """O-13: the [B, V] rows held in an all-to-all receive buffer (flat array of bf16 bit patterns or
     fp32) with blocks of L columns, S elements apart, row stride ld inside a block."""
@@ -211,6 +234,9 @@ class Variant:
 
     def backfill(self, ids, dest, next_tokens):
         return backfill(ids, dest, next_tokens, lib_path=self.lib_path)
+
+    def penalty_state(self, prompt_ids, output_ids, V):
+        return penalty_state(prompt_ids, output_ids, V)
 
     def receive_rows(self, buf, B, V, ld, L, S):
         return receive_rows(buf, B, V, ld, L, S, lib_path=self.lib_path)

@@ -16,6 +16,8 @@
  *        frequency / presence: the OpenAI API definition the paper cites):
  *          for every v with count c_v > 0:  x = x > 0 ? x / rep : x * rep;
  *                                           x = x - fl(freq * c_v);  x = x - pres      (all fp32)
+ *        O-14: with a prompt history as well, the repetition penalty covers every id of the prompt or
+ *        the output, and the frequency and presence terms count the output only (c_v = output count).
  *   O-2  temperature T < 1e-5  => greedy: the lowest id among the maxima of x; logprobs use T = 1.
  *   O-3  r = (float)(1 / (double)T);  z_v = fl32(x_v * r), -0 -> +0, -inf stays -inf.
  *   O-4  m = max finite z;  L = log sum exp(z - m)  (double);  logprob_v = z_v - m - L.
@@ -64,6 +66,10 @@ typedef struct {
   int64_t hist_len; /* entries in hist_ids */
   const float* uniforms; /* [B] or NULL (then no draw: topk/topp only) */
   int32_t n_top;
+  /* O-14: a prompt history per row; when given, hist_* holds the row's output tokens only */
+  const int64_t* prompt_offsets; /* [B+1] or NULL */
+  const int32_t* prompt_ids;
+  int64_t prompt_len;
 } oracle_in;
 
 typedef struct {
@@ -132,28 +138,51 @@ static void sample_row(const oracle_in* in, const oracle_out* out, int64_t i, fl
   if (!isfinite(freq)) { flags |= OR_BAD_PARAM; freq = 0.0f; }
   if (!isfinite(pres)) { flags |= OR_BAD_PARAM; pres = 0.0f; }
 
-  /* ---- O-1: penalties ---- */
+  /* ---- O-1: penalties (O-14: with a prompt history, the repetition penalty covers the tokens of
+   * the prompt and of the output, the frequency and presence penalties the output tokens only; inS
+   * marks the prompt tokens here and is reused for the kept set below) ---- */
+  int have_c = 0, have_p = 0;
   if (in->hist_offsets) {
     int64_t lo = in->hist_offsets[i], hi = in->hist_offsets[i + 1];
     if (lo < 0 || hi < lo || hi > in->hist_len) {
       flags |= OR_BAD_PARAM;
     } else {
+      have_c = 1;
       memset(cnt, 0, sizeof(int64_t) * (size_t)V);
       for (int64_t h = lo; h < hi; ++h) {
         int32_t id = in->hist_ids[h];
         if (id < 0 || (int64_t)id >= V) { flags |= OR_BAD_INPUT; continue; }
         cnt[id] += 1;
       }
-      for (int64_t v = 0; v < V; ++v) {
-        if (cnt[v] == 0) continue;
-        float xv = x[v];
-        if (xv > 0.0f) xv = xv / rep;
-        else xv = xv * rep;
-        float fc = freq * (float)cnt[v];
+    }
+  }
+  if (in->prompt_offsets) {
+    int64_t lo = in->prompt_offsets[i], hi = in->prompt_offsets[i + 1];
+    if (lo < 0 || hi < lo || hi > in->prompt_len) {
+      flags |= OR_BAD_PARAM;
+    } else {
+      have_p = 1;
+      memset(inS, 0, (size_t)V);
+      for (int64_t h = lo; h < hi; ++h) {
+        int32_t id = in->prompt_ids[h];
+        if (id < 0 || (int64_t)id >= V) { flags |= OR_BAD_INPUT; continue; }
+        inS[id] = 1;
+      }
+    }
+  }
+  if (have_c || have_p) {
+    for (int64_t v = 0; v < V; ++v) {
+      const int64_t c = have_c ? cnt[v] : 0;
+      if (c == 0 && !(have_p && inS[v])) continue;
+      float xv = x[v];
+      if (xv > 0.0f) xv = xv / rep;
+      else xv = xv * rep;
+      if (c > 0) {
+        float fc = freq * (float)c;
         xv = xv - fc;
         xv = xv - pres;
-        x[v] = xv;
       }
+      x[v] = xv;
     }
   }
   if (out->penalised) memcpy(out->penalised + i * V, x, sizeof(float) * (size_t)V);

@@ -15,6 +15,7 @@ import pytest
 
 import oracle
 from tests import test_oracle_pins as pins
+from tests import test_oracle_penalty_state as state_pins
 from tests import test_oracle_receive_layout as layout_pins
 from tests import test_oracle_rng_backfill as rng_pins
 
@@ -24,7 +25,9 @@ MUTANTS = [
     ("presence penalty dropped", "xv = xv - pres;", "xv = xv;"),
     ("frequency penalty sign", "xv = xv - fc;", "xv = xv + fc;"),
     ("repetition operand transposed", "if (xv > 0.0f) xv = xv / rep;", "if (xv > 0.0f) xv = xv * rep;"),
-    ("frequency ignores the count", "float fc = freq * (float)cnt[v];", "float fc = freq;"),
+    ("frequency ignores the count", "float fc = freq * (float)c;", "float fc = freq;"),
+    ("presence applied to prompt-only ids", "      if (c > 0) {\n        float fc", "      if (1) {\n        float fc"),
+    ("prompt ids not penalised", "if (c == 0 && !(have_p && inS[v])) continue;", "if (c == 0) continue;"),
     ("non-strict inverse CDF", "if (C > u) {", "if (C >= u) {"),
     ("top-p not renormalised over S2", "c = c + gm / Z2;", "c = c + gm / sum;"),
     ("top-k off by one", "tau_k = ord[k - 1].z;", "tau_k = ord[k].z;"),
@@ -63,7 +66,8 @@ def _pin_calls():
     """(name, callable) for every pin test, with its parametrisations expanded."""
     calls = []
     members = (inspect.getmembers(pins, inspect.isfunction) + inspect.getmembers(rng_pins, inspect.isfunction)
-               + inspect.getmembers(layout_pins, inspect.isfunction))
+               + inspect.getmembers(layout_pins, inspect.isfunction)
+               + inspect.getmembers(state_pins, inspect.isfunction))
     for name, fn in members:
         if not name.startswith("test_"):
             continue

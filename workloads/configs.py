@@ -50,6 +50,9 @@ class Workload:
     hist_offsets: Optional[np.ndarray] = None  # [B + 1] int64
     hist_ids: Optional[np.ndarray] = None  # [hist_offsets[B]] int32
     n_top: int = 0
+    # a prompt history per row; when given, hist_* holds the output tokens only
+    prompt_offsets: Optional[np.ndarray] = None  # [B + 1] int64
+    prompt_ids: Optional[np.ndarray] = None  # [prompt_offsets[B]] int32
 
     def row_slice(self, lo: int, hi: int) -> "Workload":
         """Rows ``lo:hi`` as a workload of their own (histories re-based to start at 0)."""
@@ -65,6 +68,10 @@ class Workload:
             o = self.hist_offsets[lo:hi + 1]
             d.hist_ids = self.hist_ids[o[0]:o[-1]]
             d.hist_offsets = (o - o[0]).astype(np.int64)
+        if self.prompt_offsets is not None:
+            o = self.prompt_offsets[lo:hi + 1]
+            d.prompt_ids = self.prompt_ids[o[0]:o[-1]]
+            d.prompt_offsets = (o - o[0]).astype(np.int64)
         return d
 
     @property
