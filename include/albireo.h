@@ -72,7 +72,7 @@ typedef enum {
                                      extra ids are ignored                                        */
 
 #define ALBIREO_MAX_TOP_N 32
-#define ALBIREO_MAX_UNIQUE_HISTORY 3072
+#define ALBIREO_MAX_UNIQUE_HISTORY 2048
 
 /*
  * Per-row sampling metadata (the paper's per-sequence metadata, sec. 3 Challenge 3 and sec. 6.2).

@@ -7,7 +7,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "albireo.hip")
+SRCS = [os.path.join(HERE, "csrc", "albireo.hip"), os.path.join(HERE, "csrc", "split.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libalbireo.so")
 
@@ -23,7 +23,7 @@ HIPCC_FLAGS = [
 def build(out: str = LIB, extra=()) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = [hipcc, *HIPCC_FLAGS, *extra, "-I", INCLUDE, SRC, "-o", tmp]
+    cmd = [hipcc, *HIPCC_FLAGS, *extra, "-I", INCLUDE, *SRCS, "-o", tmp]
     subprocess.check_call(cmd)
     os.replace(tmp, out)
     return out

@@ -1,0 +1,1518 @@
+// split.hip -- the split-row kernel of the per-sequence sampling step (sec. 6.1, Eq. opt_sample: every
+// worker runs the unchanged per-row sampling computation on its rows; the computation is the one of
+// the workload of sec. 8.1: penalties, temperature, top-k, top-p, min-p, greedy, and the draw).
+//
+// A row of the [B, V] logits is cut into P chunks of at most CSLOTS 16-byte slots (16384 bf16 or
+// 8192 fp32 logits).  One 256-thread workgroup per chunk
+//   * issues one 16-byte load per slot into registers, all up front;
+//   * applies the penalty overlay: the chunk's history ids go into an LDS presence bitmap, a word
+//     prefix count numbers them, their counts are accumulated by number, and every penalised element
+//     leaves the registers (masked to -inf) for a small LDS "extras" list that holds its new value;
+//   * reduces the chunk to its max, a sum of exponentials relative to a reference, and, for rows with
+//     a top-k / min-p / top-n bound, a short candidate list sorted in descending order (the bound is a
+//     provable lower limit of the chunk's K-th largest value, taken from the per-thread maxima).
+// The workgroups of a row never wait for each other.  Each publishes its results in the workspace and
+// bumps the row's arrival counter; the last to arrive resolves the row: log-sum-exp over the chunks
+// in chunk order, top-n and the top-k threshold by ranking the staged list heads, then min-p, the
+// nucleus and the inverse-CDF draw in ascending token id on the (small) kept set.  Rows whose kept set
+// has no small bound (top-p alone, no filter) or whose lists overflow take a slower general path in
+// the same workgroup over the chunks' processed values (radix selection by count and by mass).
+//
+// Many small workgroups per row keep every CU streaming while other chunks run their reductions.
+// Everything that combines values across threads, waves or chunks does so in a fixed order or in
+// integers, so the results depend only on the row's values, V, the dtype and the row's alignment.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <utility>
+
+#include "albireo.h"
+#include "split.h"
+
+namespace {
+
+#include "common.h"
+
+constexpr int CT = 256;                          // threads per chunk workgroup
+constexpr int CW = CT / 64;                      // waves per workgroup
+constexpr int CJ = 8;                            // 16-byte register slots per thread
+constexpr int CSLOTS = CT * CJ;                  // body slots per chunk at most
+constexpr int BMW = ((CSLOTS + 2) * 8 + 31) / 32;  // bitmap words (one bit per element, +1 slot each side)
+constexpr int XCAP = ALBIREO_MAX_UNIQUE_HISTORY;  // distinct penalised positions tracked per chunk
+constexpr int LCAPC = 512;                       // candidate list capacity of a chunk
+constexpr int MSTAGE = 2048;                     // list entries the resolving workgroup stages in LDS
+constexpr int MCAP = 512;                        // kept-set capacity of the list resolution
+constexpr int MAXPC = 64;                        // chunks per row
+constexpr int HXN = 16;                          // plain head (threads 0-7) and tail (8-15) extras
+constexpr double LN2 = 0.6931471805599453;
+
+constexpr uint32_t PUB_DENSE = 1u << 30;   // the chunk wrote its processed values to the dense row
+constexpr uint32_t PUB_FINITE = 1u << 29;  // the chunk holds a finite processed value
+
+// What one chunk publishes for the row's resolution (32 bytes).
+struct ChunkPub {
+  float zmax;      // max processed value z of the chunk (+inf in rows with a bad input)
+  float mref;      // reference of s (log2 units)
+  float s;         // sum of 2^(z L2E - mref) over the chunk
+  uint32_t flags;  // FLAG_BAD_INPUT, FLAG_LIMIT, PUB_*
+  int32_t argpos;  // greedy rows: lowest position of zmax
+  int32_t n_list;  // sorted candidates in the chunk's list
+  float qk;        // z of list entry ceil(k / P) - 1 (-inf if the list is shorter)
+  float qn;        // z of list entry ceil(n_top / P) - 1
+};
+static_assert(sizeof(ChunkPub) == 32, "chunk record layout");
+
+struct SArgs {
+  const unsigned char* logits;
+  int64_t B, V, ld;
+  DevParams prm;
+  const float* uniforms;
+  int32_t* out_ids;
+  float* out_logprobs;
+  int32_t n_top;
+  int32_t* out_top_ids;
+  float* out_top_logprobs;
+  uint32_t* out_flags;
+  int32_t rng_on;
+  uint64_t rng_seed, rng_step;
+  const int64_t* seq_ids;
+  int32_t* next_tokens;
+  const int32_t* backfill_dest;
+  int64_t next_len;
+  uint32_t seg_sps, seg_magic;  // blocked layout: slots per block, floor((2^32 - 1) / seg_sps)
+  int64_t seg_gap;              // bytes between the end of a block and the start of the next
+  int32_t P;
+  int32_t xcd_map;
+  int64_t chunk_slots;
+  int64_t grid;
+  uint32_t* ctr;     // [B] arrival counters (zero between calls)
+  ChunkPub* pub;     // [B * P]
+  uint64_t* lists;   // [B * P * LCAPC]
+  float* dense;      // [B * V]
+};
+
+struct SRow {
+  int64_t row;
+  const unsigned char* rowp;
+  int V, head, tail_lo, c, P;
+  int64_t body_slots, s0, s1;
+  bool greedy, kon, minp_on, topp_on, pen_on;
+  float r, p, minp, rep, freq, pres;
+  int k;
+  int64_t h_lo, h_hi;
+  uint32_t flags;
+};
+
+// LDS of one workgroup: the chunk phase and the resolution phase share the same bytes.
+struct SSm {
+  union {
+    struct {
+      uint32_t bitmap[BMW];        // presence of the chunk's positions in the row's history
+      uint16_t wpref[BMW + 1];     // set bits in the bitmap words before each word
+      uint32_t xval[XCAP];         // per penalised position: its count, then its new value
+      uint64_t list[LCAPC];        // candidate keys
+    } c;
+    struct {
+      uint64_t key[MSTAGE];        // staged list prefixes / kept set keys and weights
+      ChunkPub pub[MAXPC];
+      int32_t off[MAXPC + 1];
+      int32_t cnt[MAXPC];
+      int32_t cut[MAXPC];
+    } m;
+  };
+  int32_t hx_pos[HXN];
+  float hx_val[HXN];
+  float wred[3][CW];
+  uint64_t qred[CW];
+  int32_t n_list;
+  uint32_t flags;
+  int32_t bc_i[4];
+  float bc_f[4];
+  uint64_t bc_q[2];
+  int32_t top_id[ALBIREO_MAX_TOP_N];
+  float top_lp[ALBIREO_MAX_TOP_N];
+};
+static_assert(sizeof(SSm) <= 20 * 1024, "LDS of a chunk workgroup exceeds an eighth of a gfx950 CU");
+
+// Hide the register slots' contents from the optimiser between passes, so that it unpacks the slots
+// again in every pass instead of keeping all unpacked (or scaled) values of the previous one alive.
+template <int N>
+__device__ __forceinline__ void reload_barrier(uint4 (&d)[N]) {
+  static_for<N>([&](auto J) {
+    constexpr int j = decltype(J)::value;
+    uint32_t x = d[j].x, y = d[j].y, z = d[j].z, w = d[j].w;
+    asm volatile("" : "+v"(x), "+v"(y), "+v"(z), "+v"(w));
+    d[j] = make_uint4(x, y, z, w);
+  });
+}
+
+// Element e of a 16-byte slot, the slot taken by value (so that a run-time e selects among register
+// values and never turns the register slots into addressable memory).
+template <class DT>
+__device__ __forceinline__ float elem(uint4 d, int e) {
+  if constexpr (DT::VEC == 8) {
+    const int h = e >> 1;
+    uint32_t w = d.x;
+    w = h == 1 ? d.y : w;
+    w = h == 2 ? d.z : w;
+    w = h == 3 ? d.w : w;
+    return (e & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
+  } else {
+    uint32_t w = d.x;
+    w = e == 1 ? d.y : w;
+    w = e == 2 ? d.z : w;
+    w = e == 3 ? d.w : w;
+    return __uint_as_float(w);
+  }
+}
+
+// ----------------------------------------------------------------------------------------------
+// Workgroup reductions (4 waves; fixed combination order)
+// ----------------------------------------------------------------------------------------------
+__device__ __forceinline__ int blk_sum_i(int v, SSm& s) {
+  v = wave_sum_i(v);
+  __syncthreads();
+  if (lane_id() == 0) s.bc_i[wave_id()] = v;
+  __syncthreads();
+  return s.bc_i[0] + s.bc_i[1] + s.bc_i[2] + s.bc_i[3];
+}
+__device__ __forceinline__ int blk_min_i(int v, SSm& s) {
+  v = wave_min_i(v);
+  __syncthreads();
+  if (lane_id() == 0) s.bc_i[wave_id()] = v;
+  __syncthreads();
+  return min(min(s.bc_i[0], s.bc_i[1]), min(s.bc_i[2], s.bc_i[3]));
+}
+__device__ __forceinline__ int blk_max_i(int v, SSm& s) {
+  v = wave_max_i(v);
+  __syncthreads();
+  if (lane_id() == 0) s.bc_i[wave_id()] = v;
+  __syncthreads();
+  return max(max(s.bc_i[0], s.bc_i[1]), max(s.bc_i[2], s.bc_i[3]));
+}
+__device__ __forceinline__ uint32_t blk_or(uint32_t v, SSm& s) {
+  v = wave_or(v);
+  __syncthreads();
+  if (lane_id() == 0) s.bc_i[wave_id()] = (int)v;
+  __syncthreads();
+  return (uint32_t)(s.bc_i[0] | s.bc_i[1] | s.bc_i[2] | s.bc_i[3]);
+}
+__device__ __forceinline__ uint64_t blk_sum_u64(uint64_t v, SSm& s) {
+  v = wave_sum_u64(v);
+  __syncthreads();
+  if (lane_id() == 0) s.qred[wave_id()] = v;
+  __syncthreads();
+  return s.qred[0] + s.qred[1] + s.qred[2] + s.qred[3];
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t w = ((uint64_t)(uint32_t)__shfl_xor((int)(v >> 32), o) << 32) | (uint32_t)__shfl_xor((int)v, o);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+__device__ __forceinline__ uint64_t blk_max_u64(uint64_t v, SSm& s) {
+  v = wave_max_u64(v);
+  __syncthreads();
+  if (lane_id() == 0) s.qred[wave_id()] = v;
+  __syncthreads();
+  uint64_t r = s.qred[0];
+  for (int w = 1; w < CW; ++w) r = s.qred[w] > r ? s.qred[w] : r;
+  return r;
+}
+// exclusive prefix of v over the threads in thread order; *total = sum over all threads
+__device__ __forceinline__ int blk_excl_scan_i(int v, SSm& s, int* total) {
+  const int incl = wave_incl_scan_i(v);
+  __syncthreads();
+  if (lane_id() == 63) s.bc_i[wave_id()] = incl;
+  __syncthreads();
+  int off = 0;
+  for (int w = 0; w < wave_id(); ++w) off += s.bc_i[w];
+  *total = s.bc_i[0] + s.bc_i[1] + s.bc_i[2] + s.bc_i[3];
+  return off + incl - v;
+}
+__device__ __forceinline__ uint64_t blk_excl_scan_u64(uint64_t v, SSm& s, uint64_t* total) {
+  // inclusive scan in lane order on DPP, 64-bit
+  uint64_t incl = v;
+  incl += dpp_mov64<DPP_ROW_SHR + 1>(incl);
+  incl += dpp_mov64<DPP_ROW_SHR + 2>(incl);
+  incl += dpp_mov64<DPP_ROW_SHR + 4>(incl);
+  incl += dpp_mov64<DPP_ROW_SHR + 8>(incl);
+  incl += dpp_mov64<DPP_ROW_BCAST15, 0xa>(incl);
+  incl += dpp_mov64<DPP_ROW_BCAST31, 0xc>(incl);
+  __syncthreads();
+  if (lane_id() == 63) s.qred[wave_id()] = incl;
+  __syncthreads();
+  uint64_t off = 0;
+  for (int w = 0; w < wave_id(); ++w) off += s.qred[w];
+  *total = s.qred[0] + s.qred[1] + s.qred[2] + s.qred[3];
+  return off + incl - v;
+}
+
+// (mref, s) pairs: s is relative to 2^mref
+__device__ __forceinline__ void lse_add(float& m, float& s, float m2, float s2) {
+  const float M = fmaxf(m, m2);
+  s = s * rel2(m, M) + s2 * rel2(m2, M);
+  m = M;
+}
+
+// fixed-point mass of a kept value: 2^((z - m) L2E) in units of 2^-32
+__device__ __forceinline__ uint64_t mass_of(float z, float m) {
+  const float w = __builtin_amdgcn_exp2f(__fmul_rn(__fsub_rn(z, m), L2E));
+  return (uint64_t)((double)w * FIX_SCALE);
+}
+
+// ----------------------------------------------------------------------------------------------
+// Row geometry and parameters
+// ----------------------------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t seg_block(const SArgs& a, uint32_t q) {
+  uint32_t g = __umulhi(q, a.seg_magic);
+  if (q - g * a.seg_sps >= a.seg_sps) ++g;
+  return g;
+}
+template <class DT, bool SEG>
+__device__ __forceinline__ const uint4* slot_ptr(const SArgs& a, const SRow& R, int64_t slot) {
+  int64_t off = ((int64_t)R.head + slot * DT::VEC) * DT::ES;
+  if constexpr (SEG) off += (int64_t)seg_block(a, (uint32_t)slot) * a.seg_gap;
+  return reinterpret_cast<const uint4*>(R.rowp + off);
+}
+template <class DT, bool SEG>
+__device__ __forceinline__ float load_elem(const SArgs& a, const SRow& R, int64_t pos) {
+  int64_t off = pos * DT::ES;
+  if constexpr (SEG) off += (int64_t)seg_block(a, (uint32_t)(pos / DT::VEC)) * a.seg_gap;
+  return DT::load1(R.rowp + off, 0);
+}
+
+template <class DT, bool SEG>
+__device__ __forceinline__ void row_setup(const SArgs& a, int64_t row, int c, SRow& R) {
+  R.row = row;
+  R.c = c;
+  R.P = a.P;
+  R.V = (int)a.V;
+  R.rowp = a.logits + row * a.ld * DT::ES;
+  int head = 0;
+  if constexpr (!SEG) {
+    const uint64_t addr = reinterpret_cast<uint64_t>(R.rowp);
+    head = (int)(((16u - (uint32_t)(addr & 15u)) & 15u) / DT::ES);
+    if (head > R.V) head = R.V;
+  }
+  R.head = head;
+  R.body_slots = (R.V - head) / DT::VEC;
+  R.tail_lo = head + (int)R.body_slots * DT::VEC;
+  R.s0 = (int64_t)c * a.chunk_slots;
+  if (R.s0 > R.body_slots) R.s0 = R.body_slots;
+  R.s1 = R.s0 + a.chunk_slots;
+  if (R.s1 > R.body_slots) R.s1 = R.body_slots;
+
+  const DevParams& q = a.prm;
+  float T = sload(q.temperature ? q.temperature + row : &kParamDefaults[0]);
+  float p = sload(q.top_p ? q.top_p + row : &kParamDefaults[1]);
+  float mp = sload(q.min_p ? q.min_p + row : &kParamDefaults[2]);
+  float rep = sload(q.rep ? q.rep + row : &kParamDefaults[3]);
+  float freq = sload(q.freq ? q.freq + row : &kParamDefaults[4]);
+  float pres = sload(q.pres ? q.pres + row : &kParamDefaults[5]);
+  const int k = sload(q.top_k ? q.top_k + row : &kZeroI32[0]);
+  const int64_t* ho = q.hist_offsets ? q.hist_offsets + row : &kZeroI64[0];
+  const int64_t lo = sload(ho), hi = sload(ho + 1);
+  uint32_t flags = 0;
+  if (!isfinite(T)) { flags |= FLAG_BAD_PARAM; T = 1.0f; }
+  if (isnan(p)) { flags |= FLAG_BAD_PARAM; p = 1.0f; }
+  if (isnan(mp)) { flags |= FLAG_BAD_PARAM; mp = 0.0f; }
+  if (!(rep > 0.0f) || isinf(rep)) { flags |= FLAG_BAD_PARAM; rep = 1.0f; }
+  if (!isfinite(freq)) { flags |= FLAG_BAD_PARAM; freq = 0.0f; }
+  if (!isfinite(pres)) { flags |= FLAG_BAD_PARAM; pres = 0.0f; }
+  R.greedy = T < 1e-5f;
+  if (R.greedy) flags |= FLAG_GREEDY;
+  R.r = R.greedy ? 1.0f : (float)(1.0 / (double)T);
+  R.k = k;
+  R.kon = !R.greedy && k > 0 && (int64_t)k < a.V;
+  R.minp_on = !R.greedy && mp > 0.0f;
+  R.minp = mp > 1.0f ? 1.0f : mp;
+  R.topp_on = !R.greedy && p < 1.0f;
+  R.p = p;
+  R.rep = rep;
+  R.freq = freq;
+  R.pres = pres;
+  R.pen_on = false;
+  R.h_lo = R.h_hi = 0;
+  if (q.hist_offsets) {
+    if (lo < 0 || hi < lo || hi > q.hist_len) {
+      flags |= FLAG_BAD_PARAM;
+    } else if (hi > lo) {
+      R.pen_on = true;
+      R.h_lo = lo;
+      R.h_hi = hi;
+    }
+  }
+  R.flags = flags;
+}
+
+// first and one-past-last row position of chunk c
+__device__ __forceinline__ int chunk_lo(const SArgs& a, const SRow& R, int c, int vec) {
+  if (c == 0) return 0;
+  int64_t s = (int64_t)c * a.chunk_slots;
+  if (s > R.body_slots) s = R.body_slots;
+  return R.head + (int)s * vec;
+}
+__device__ __forceinline__ int chunk_hi(const SArgs& a, const SRow& R, int c, int vec) {
+  if (c == R.P - 1) return R.V;
+  int64_t s = (int64_t)(c + 1) * a.chunk_slots;
+  if (s > R.body_slots) s = R.body_slots;
+  return R.head + (int)s * vec;
+}
+
+// Row position of the penalised extras entry of rank i (the i-th set bit of the bitmap).
+__device__ __forceinline__ int pos_of_rank(const SSm& s, int nwords, int64_t e_base, int i) {
+  int lo = 0, hi = nwords - 1;
+  while (lo < hi) {  // last word whose prefix count is <= i
+    const int mid = (lo + hi + 1) >> 1;
+    if ((int)s.c.wpref[mid] <= i) lo = mid;
+    else hi = mid - 1;
+  }
+  uint32_t w = s.c.bitmap[lo];
+  for (int q = i - (int)s.c.wpref[lo]; q > 0; --q) w &= w - 1;
+  return (int)(e_base + lo * 32 + __builtin_ctz(w));
+}
+
+// ----------------------------------------------------------------------------------------------
+// Resolution of a row by its last chunk workgroup
+// ----------------------------------------------------------------------------------------------
+struct RowTot {
+  float m;       // max z of the row
+  double L;      // log sum_v exp(z_v - m)
+  uint32_t flags;
+  bool empty, dense_any;
+  int argpos;
+};
+
+// Entries of the chunk lists that the resolving workgroup loads together with the chunk records (one
+// round trip): entries [0, E) of every chunk's list, SPQ per thread.  Entries past a list's end read 0
+// (the workspace is zero there), and no valid key is 0.
+constexpr int SPQ = 8;
+struct Spec {
+  uint64_t v[SPQ];
+  int E;
+  bool on;
+};
+
+// Stage into s.m.key the list entries i < imax of every chunk with z >= zthr, from the speculative
+// registers (sp.on) or from the lists themselves.  The order is arbitrary (ranks are counted).  For the
+// check of ties cut off at imax, s.m.cut[c] gets 1 (and s.m.cnt[c] the value's bits) when chunk c's
+// list goes on past imax and its entry imax - 1 passes.  Returns the count, or -1 above cap.
+__device__ int stage_entries(const SArgs& a, const SRow& R, SSm& s, const Spec& sp, float zthr, int imax, int cap) {
+  const int P = R.P, t = threadIdx.x;
+  if (t == 0) s.bc_i[2] = 0;
+  if (t < P) s.m.cut[t] = 0;
+  __syncthreads();
+  auto take = [&](uint64_t key, int c, int i) {
+    if (key != 0 && i < imax && cand_z(key) >= zthr) {
+      const int idx = atomicAdd(&s.bc_i[2], 1);
+      if (idx < cap) s.m.key[idx] = key;
+      if (i == imax - 1 && s.m.pub[c].n_list > imax) {
+        s.m.cut[c] = 1;
+        s.m.cnt[c] = __float_as_int(cand_z(key));  // its value, for the tie test
+      }
+    }
+  };
+  if (sp.on && imax <= sp.E) {
+#pragma unroll
+    for (int q = 0; q < SPQ; ++q) {
+      const int f = t + q * CT;
+      if (f < P * sp.E) {
+        const int c = f / sp.E;
+        take(sp.v[q], c, f - c * sp.E);
+      }
+    }
+  } else {
+    const uint64_t* base = a.lists + (R.row * P) * (int64_t)LCAPC;
+    int emax = 0;
+    for (int c = 0; c < P; ++c) emax = max(emax, min(s.m.pub[c].n_list, imax));
+    for (int f = t; f < P * emax; f += CT) {
+      const int c = f / emax, i = f - c * emax;
+      if (i < s.m.pub[c].n_list) take(ld_agent(base + (int64_t)c * LCAPC + i), c, i);
+    }
+  }
+  __syncthreads();
+  const int n = s.bc_i[2];
+  __syncthreads();
+  return n <= cap ? n : -1;
+}
+
+// Number of entries of arr[0, n) greater than key: one branch-free pass whose loads pipeline.
+__device__ __forceinline__ int count_above(const uint64_t* arr, int n, uint64_t key) {
+  int r = 0;
+#pragma unroll 8
+  for (int j = 0; j < n; ++j) r += arr[j] > key ? 1 : 0;
+  return r;
+}
+
+// Iterate over the values of chunk c's view: its dense processed row, or its candidate list.
+template <class F>
+__device__ __forceinline__ void for_view(const SArgs& a, const SRow& R, const SSm& s, int c, int vec, F&& f) {
+  const ChunkPub& pc = s.m.pub[c];
+  if (pc.flags & PUB_DENSE) {
+    const float* drow = a.dense + R.row * a.V;
+    const int lo = chunk_lo(a, R, c, vec), hi = chunk_hi(a, R, c, vec);
+    for (int p = lo + (int)threadIdx.x; p < hi; p += CT) f(ld_agent(drow + p), p);
+  } else {
+    const uint64_t* lst = a.lists + (R.row * R.P + c) * (int64_t)LCAPC;
+    for (int i = (int)threadIdx.x; i < pc.n_list; i += CT) {
+      const uint64_t key = ld_agent(lst + i);
+      f(cand_z(key), cand_pos(key));
+    }
+  }
+}
+
+// General path, radix selection by count: the order key of the K-th largest finite value (counting
+// duplicates), or 0 when there are fewer than K.
+__device__ __forceinline__ uint32_t gp_kth_key(const SArgs& a, const SRow& R, SSm& s, int vec, int K) {
+  uint32_t* hc = reinterpret_cast<uint32_t*>(s.m.key);
+  uint32_t prefix = 0, pmask = 0;
+  int remaining = K;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = threadIdx.x; b < 256; b += CT) hc[b] = 0;
+    __syncthreads();
+    for (int c = 0; c < R.P; ++c)
+      for_view(a, R, s, c, vec, [&](float z, int) {
+        if (z > -INFINITY && z == z) {
+          const uint32_t kk = f2key(z);
+          if ((kk & pmask) == prefix) atomicAdd(&hc[(kk >> shift) & 255u], 1u);
+        }
+      });
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const int l = threadIdx.x;  // lane l holds buckets 255 - 4l .. 252 - 4l (descending)
+      uint32_t b4[4], sum = 0;
+      for (int q = 0; q < 4; ++q) { b4[q] = hc[255 - 4 * l - q]; sum += b4[q]; }
+      const uint32_t incl = wave_incl_scan_u(sum);
+      const uint32_t excl = incl - sum;
+      const uint64_t hit = __ballot(incl >= (uint32_t)remaining);
+      if (hit == 0) {
+        if (l == 0) s.bc_i[0] = -1;
+      } else if (l == __builtin_ctzll(hit)) {
+        uint32_t cum = excl;
+        int q = 0;
+        while (q < 3 && cum + b4[q] < (uint32_t)remaining) { cum += b4[q]; ++q; }
+        s.bc_i[0] = 255 - 4 * l - q;
+        s.bc_i[1] = remaining - (int)cum;
+      }
+    }
+    __syncthreads();
+    const int b = s.bc_i[0];
+    if (b < 0) return 0u;
+    remaining = s.bc_i[1];
+    prefix |= (uint32_t)b << shift;
+    pmask |= 255u << shift;
+    __syncthreads();
+  }
+  return prefix;
+}
+
+// General path, radix selection by mass: the order key of the nucleus' closing group among the values
+// z >= tau2 (the first group, in descending order, at which the cumulative mass reaches target), or 0
+// when the cumulative mass never reaches it.
+__device__ __forceinline__ uint32_t gp_topp_key(const SArgs& a, const SRow& R, SSm& s, int vec, float tau2, float m,
+                                double target) {
+  uint64_t* hm = s.m.key;  // 256 masses
+  uint32_t prefix = 0, pmask = 0;
+  double above = 0.0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = threadIdx.x; b < 256; b += CT) hm[b] = 0;
+    __syncthreads();
+    for (int c = 0; c < R.P; ++c)
+      for_view(a, R, s, c, vec, [&](float z, int) {
+        if (z > -INFINITY && z >= tau2) {
+          const uint32_t kk = f2key(z);
+          if ((kk & pmask) == prefix) atomicAdd(reinterpret_cast<unsigned long long*>(&hm[(kk >> shift) & 255u]),
+                                                (unsigned long long)mass_of(z, m));
+        }
+      });
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const int l = threadIdx.x;
+      uint64_t b4[4], sum = 0;
+      for (int q = 0; q < 4; ++q) { b4[q] = hm[255 - 4 * l - q]; sum += b4[q]; }
+      uint64_t incl = sum;
+      incl += dpp_mov64<DPP_ROW_SHR + 1>(incl);
+      incl += dpp_mov64<DPP_ROW_SHR + 2>(incl);
+      incl += dpp_mov64<DPP_ROW_SHR + 4>(incl);
+      incl += dpp_mov64<DPP_ROW_SHR + 8>(incl);
+      incl += dpp_mov64<DPP_ROW_BCAST15, 0xa>(incl);
+      incl += dpp_mov64<DPP_ROW_BCAST31, 0xc>(incl);
+      const uint64_t excl = incl - sum;
+      const uint64_t hit = __ballot(above + (double)incl >= target);
+      if (hit == 0) {
+        if (l == 0) s.bc_i[0] = -1;
+      } else if (l == __builtin_ctzll(hit)) {
+        uint64_t cum = excl;
+        int q = 0;
+        while (q < 3 && above + (double)(cum + b4[q]) < target) { cum += b4[q]; ++q; }
+        s.bc_i[0] = 255 - 4 * l - q;
+        s.bc_q[0] = cum;
+      }
+    }
+    __syncthreads();
+    const int b = s.bc_i[0];
+    if (b < 0) return 0u;
+    above += (double)s.bc_q[0];
+    prefix |= (uint32_t)b << shift;
+    pmask |= 255u << shift;
+    __syncthreads();
+  }
+  return prefix;
+}
+
+// General path: kept set S = {finite z >= tau}; draws the token with target u * Z_S in ascending id.
+// Returns the id (z in *zid).
+__device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, int vec, float tau, float m, float u, float* zid) {
+  const int P = R.P;
+  uint64_t* cm = s.m.key;  // per chunk mass
+  for (int c = threadIdx.x; c < P; c += CT) cm[c] = 0;
+  __syncthreads();
+  int last = -1;
+  for (int c = 0; c < P; ++c) {
+    uint64_t acc = 0;
+    for_view(a, R, s, c, vec, [&](float z, int pos) {
+      if (z > -INFINITY && z >= tau) {
+        const uint64_t w = mass_of(z, m);
+        acc += w;
+        if (w > 0) last = max(last, pos);
+      }
+    });
+    atomicAdd(reinterpret_cast<unsigned long long*>(&cm[c]), (unsigned long long)acc);
+  }
+  last = blk_max_i(last, s);
+  uint64_t zs = 0;
+  for (int c = 0; c < P; ++c) zs += cm[c];
+  const double target = (double)u * (double)zs;
+  // the chunk holding the first prefix above the target
+  int cs = -1;
+  uint64_t before = 0;
+  for (int c = 0; c < P; ++c) {
+    if ((double)(before + cm[c]) > target) { cs = c; break; }
+    before += cm[c];
+  }
+  __syncthreads();
+  int id = -1;
+  if (cs >= 0) {
+    const ChunkPub& pc = s.m.pub[cs];
+    if (pc.flags & PUB_DENSE) {
+      // thread-contiguous ranges of the chunk, one exclusive scan, then the crossing thread walks
+      const float* drow = a.dense + R.row * a.V;
+      const int lo = chunk_lo(a, R, cs, vec), hi = chunk_hi(a, R, cs, vec);
+      const int per = (hi - lo + CT - 1) / CT;
+      const int p0 = lo + (int)threadIdx.x * per, p1 = min(p0 + per, hi);
+      uint64_t mine = 0;
+      for (int p = p0; p < p1; ++p) {
+        const float z = ld_agent(drow + p);
+        if (z > -INFINITY && z >= tau) mine += mass_of(z, m);
+      }
+      uint64_t tot;
+      uint64_t cum = before + blk_excl_scan_u64(mine, s, &tot);
+      int found = 0x7fffffff;
+      if ((double)(cum + mine) > target) {
+        for (int p = p0; p < p1; ++p) {
+          const float z = ld_agent(drow + p);
+          if (z > -INFINITY && z >= tau) {
+            cum += mass_of(z, m);
+            if ((double)cum > target) { found = p; break; }
+          }
+        }
+      }
+      id = blk_min_i(found, s);
+      if (id == 0x7fffffff) id = -1;
+    } else {
+      // list view (at most LCAPC entries): staged in LDS, then the prefix of every kept entry in id
+      // order by counting
+      const uint64_t* lst = a.lists + (R.row * P + cs) * (int64_t)LCAPC;
+      const int n = pc.n_list;
+      uint64_t* lk = s.m.key + MAXPC;
+      for (int i = threadIdx.x; i < n; i += CT) lk[i] = ld_agent(lst + i);
+      __syncthreads();
+      int found = 0x7fffffff;
+      for (int i = threadIdx.x; i < n; i += CT) {
+        const uint64_t ki = lk[i];
+        const float zi = cand_z(ki);
+        if (!(zi > -INFINITY && zi >= tau)) continue;
+        const int pi = cand_pos(ki);
+        uint64_t pre = before;
+        for (int j = 0; j < n; ++j) {
+          const uint64_t kj = lk[j];
+          const float zj = cand_z(kj);
+          if (zj > -INFINITY && zj >= tau && cand_pos(kj) <= pi) pre += mass_of(zj, m);
+        }
+        if ((double)pre > target) found = min(found, pi);
+      }
+      id = blk_min_i(found, s);
+      if (id == 0x7fffffff) id = -1;
+    }
+  }
+  if (id < 0) id = last;
+  // its value
+  if (threadIdx.x == 0) s.bc_f[0] = -INFINITY;
+  __syncthreads();
+  for (int c = 0; c < P; ++c) {
+    if (id < chunk_lo(a, R, c, vec) || id >= chunk_hi(a, R, c, vec)) continue;
+    for_view(a, R, s, c, vec, [&](float z, int pos) {
+      if (pos == id) s.bc_f[0] = z;
+    });
+  }
+  __syncthreads();
+  *zid = s.bc_f[0];
+  __syncthreads();
+  return id;
+}
+
+template <class DT, bool SEG>
+__device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& s) {
+  const int t = threadIdx.x, P = R.P, VEC = DT::VEC;
+  const int64_t row = R.row;
+  const int nt = a.n_top;
+  // ---- one round trip: the chunk records, the row's uniform and the heads of the chunk lists ----
+  Spec sp;
+  sp.E = nt;
+  if (R.kon) sp.E = max(sp.E, min(R.k, LCAPC));
+  sp.on = sp.E > 0 && P * sp.E <= SPQ * CT;
+  if (sp.on) {
+    const uint64_t* base = a.lists + (row * P) * (int64_t)LCAPC;
+#pragma unroll
+    for (int q = 0; q < SPQ; ++q) {
+      const int f = t + q * CT;
+      sp.v[q] = 0;
+      if (f < P * sp.E) {
+        const int c = f / sp.E;
+        sp.v[q] = ld_agent(base + (int64_t)c * LCAPC + (f - c * sp.E));
+      }
+    }
+  }
+  if (t < P) {
+    const ChunkPub* g = a.pub + row * P + t;
+    ChunkPub& q = s.m.pub[t];
+    q.zmax = ld_agent(&g->zmax);
+    q.mref = ld_agent(&g->mref);
+    q.s = ld_agent(&g->s);
+    q.flags = ld_agent(&g->flags);
+    q.argpos = ld_agent(&g->argpos);
+    q.n_list = ld_agent(&g->n_list);
+    q.qk = ld_agent(&g->qk);
+    q.qn = ld_agent(&g->qn);
+  }
+  float u = 0.0f;
+  if (a.rng_on) {
+    const uint64_t seq = a.seq_ids ? (uint64_t)a.seq_ids[row] : (uint64_t)row;
+    u = philox_uniform(a.rng_seed, a.rng_step, seq);
+  } else {
+    u = a.uniforms[row];
+  }
+  __syncthreads();
+  // row totals, in chunk order (every thread computes the same)
+  float m = -INFINITY, mref = MREF0, S = 0.0f;
+  uint32_t flags = R.flags;
+  bool fin = false, dense_any = false;
+  int argpos = -1;
+  for (int c = 0; c < P; ++c) {
+    const ChunkPub& q = s.m.pub[c];
+    m = fmaxf(m, q.zmax);
+    lse_add(mref, S, q.mref, q.s);
+    flags |= q.flags & (FLAG_BAD_INPUT | FLAG_LIMIT);
+    fin = fin || (q.flags & PUB_FINITE);
+    dense_any = dense_any || (q.flags & PUB_DENSE);
+  }
+  for (int c = 0; c < P; ++c)
+    if (s.m.pub[c].zmax == m) { argpos = s.m.pub[c].argpos; break; }
+  const bool empty = !fin;
+  if (empty) flags |= FLAG_EMPTY;
+  const double L = log((double)S) - ((double)m * (double)L2E - (double)mref) * LN2;
+
+  // ---- top-n: the n largest keys of the lists (each list holds its chunk's top n), by counted rank ----
+  if (nt > 0) {
+    if (t < nt) {
+      s.top_id[t] = -1;
+      s.top_lp[t] = -INFINITY;
+    }
+    if (!empty) {
+      float lo = INFINITY;
+      for (int c = 0; c < P; ++c) lo = fminf(lo, s.m.pub[c].qn);
+      const int ns = stage_entries(a, R, s, sp, lo, nt, MSTAGE);
+      for (int f = t; f < ns; f += CT) {
+        const uint64_t key = s.m.key[f];
+        const int rk = count_above(s.m.key, ns, key);
+        if (rk < nt) {
+          s.top_id[rk] = cand_pos(key);
+          s.top_lp[rk] = (float)((double)cand_z(key) - (double)m - L);
+        }
+      }
+    }
+    __syncthreads();
+    if (t < nt) {
+      a.out_top_ids[row * nt + t] = s.top_id[t];
+      a.out_top_logprobs[row * nt + t] = s.top_lp[t];
+    }
+  }
+
+  int id = -1;
+  float zid = -INFINITY;
+  if (empty) {
+    id = -1;
+  } else if (R.greedy) {
+    id = argpos;
+    zid = m;
+  } else {
+    // ---- the kept set from the lists when it is small; otherwise the general path ----
+    const bool s2b = R.kon || R.minp_on;
+    const float tau_m = R.minp_on ? __fadd_rn(m, (float)log((double)R.minp)) : -INFINITY;
+    bool general = !s2b || dense_any;
+    // kept set S2: A[i] = (order key of z << 32) | mass, Bk[i] = (position << 32) | mass kept by the
+    // nucleus; masses 2^((z - m) L2E) in units of 2^-31
+    uint64_t* A = s.m.key + (MSTAGE - 2 * MCAP);
+    uint64_t* Bk = s.m.key + (MSTAGE - MCAP);
+    int n2 = 0;
+    if (!general) {
+      float tau2 = tau_m;
+      const int imax = R.kon ? min(R.k, LCAPC) : LCAPC;
+      float zthr = tau_m;
+      if (R.kon) {
+        float lo = INFINITY;
+        for (int c = 0; c < P; ++c) lo = fminf(lo, s.m.pub[c].qk);
+        zthr = fmaxf(zthr, lo);
+      }
+      const int ns = stage_entries(a, R, s, sp, zthr, imax, MSTAGE - 2 * MCAP);
+      if (ns < 0) {
+        general = true;
+      } else {
+        if (R.kon) {
+          if (t == 0) s.bc_f[1] = -INFINITY;
+          __syncthreads();
+          for (int f = t; f < ns; f += CT)
+            if (count_above(s.m.key, ns, s.m.key[f]) == R.k - 1) s.bc_f[1] = cand_z(s.m.key[f]);
+          __syncthreads();
+          tau2 = fmaxf(tau2, s.bc_f[1]);
+        }
+        // a list cut off at imax whose last taken entry is kept may hold more of a tie at tau_k
+        bool cutkept = false;
+        for (int c = 0; c < P; ++c)
+          if (s.m.cut[c] && __int_as_float(s.m.cnt[c]) >= tau2) cutkept = true;
+        if (t == 0) s.bc_i[2] = 0;
+        __syncthreads();
+        for (int f = t; f < ns; f += CT) {
+          const uint64_t key = s.m.key[f];
+          const float z = cand_z(key);
+          if (z >= tau2) {
+            const int idx = atomicAdd(&s.bc_i[2], 1);
+            if (idx < MCAP) {
+              const uint32_t w = (uint32_t)(__builtin_amdgcn_exp2f(__fmul_rn(__fsub_rn(z, m), L2E)) * 2147483648.0f);
+              A[idx] = ((uint64_t)f2key(z) << 32) | w;
+              Bk[idx] = ((uint64_t)(uint32_t)cand_pos(key) << 32) | w;
+            }
+          }
+        }
+        __syncthreads();
+        n2 = s.bc_i[2];
+        if (n2 > MCAP || n2 == 0 || cutkept) general = true;
+      }
+    }
+    if (!general) {
+      // nucleus: keep every entry whose strictly larger values carry less than p of the S2 mass
+      uint64_t z2 = 0;
+      for (int i = t; i < n2; i += CT) z2 += (uint32_t)A[i];
+      z2 = blk_sum_u64(z2, s);
+      const double T = (double)R.p * (double)z2;
+      uint64_t zsum = 0;
+      for (int i = t; i < n2; i += CT) {
+        const uint64_t ai = A[i];
+        bool keep = true;
+        if (R.topp_on) {
+          const uint32_t zk = (uint32_t)(ai >> 32);
+          uint64_t above = 0;
+#pragma unroll 8
+          for (int j = 0; j < n2; ++j) {
+            const uint64_t aj = A[j];
+            above += ((uint32_t)(aj >> 32) > zk) ? (uint32_t)aj : 0u;
+          }
+          keep = above == 0 || (double)above < T;
+        }
+        if (!keep) Bk[i] &= 0xffffffff00000000ull;
+        zsum += keep ? (uint32_t)ai : 0u;
+      }
+      zsum = blk_sum_u64(zsum, s);
+      // inverse CDF in ascending token id: the first kept position whose prefix mass exceeds u Z_S
+      const double target = (double)u * (double)zsum;
+      int found = 0x7fffffff, lastp = -1;
+      for (int i = t; i < n2; i += CT) {
+        const uint64_t bi = Bk[i];
+        if ((uint32_t)bi == 0) continue;
+        const uint32_t pi = (uint32_t)(bi >> 32);
+        lastp = max(lastp, (int)pi);
+        uint64_t pre = 0;
+#pragma unroll 8
+        for (int j = 0; j < n2; ++j) {
+          const uint64_t bj = Bk[j];
+          pre += ((uint32_t)(bj >> 32) <= pi) ? (uint32_t)bj : 0u;
+        }
+        if ((double)pre > target) found = min(found, (int)pi);
+      }
+      found = blk_min_i(found, s);
+      lastp = blk_max_i(lastp, s);
+      id = found != 0x7fffffff ? found : lastp;
+      if (t == 0) s.bc_f[2] = -INFINITY;
+      __syncthreads();
+      for (int i = t; i < n2; i += CT)
+        if ((int)(uint32_t)(Bk[i] >> 32) == id) s.bc_f[2] = key2f((uint32_t)(A[i] >> 32));
+      __syncthreads();
+      zid = s.bc_f[2];
+    } else {
+      // ---- general path over the chunk views ----
+      float tau_k = -INFINITY;
+      if (R.kon) {
+        const uint32_t kk = gp_kth_key(a, R, s, VEC, R.k);
+        tau_k = kk ? key2f(kk) : -INFINITY;
+      }
+      const float tau2 = fmaxf(tau_k, tau_m);
+      float tau = tau2;
+      if (R.topp_on) {
+        uint64_t z2 = 0;
+        for (int c = 0; c < P; ++c)
+          for_view(a, R, s, c, VEC, [&](float z, int) {
+            if (z > -INFINITY && z >= tau2) z2 += mass_of(z, m);
+          });
+        z2 = blk_sum_u64(z2, s);
+        const double target = (double)R.p * (double)z2;
+        if (!(target > 0.0)) {
+          tau = m;  // p <= 0: the top group only
+        } else {
+          const uint32_t kk = gp_topp_key(a, R, s, VEC, tau2, m, target);
+          if (kk) tau = fmaxf(tau2, key2f(kk));
+        }
+      }
+      id = gp_draw(a, R, s, VEC, tau, m, u, &zid);
+    }
+  }
+  // leave the workspace as it was found: zero the row's chunk records, lists and dense values
+  {
+    uint64_t* lbase = a.lists + (row * P) * (int64_t)LCAPC;
+    for (int c = 0; c < P; ++c) {
+      const int n = s.m.pub[c].n_list;
+      for (int i = t; i < n; i += CT) st_agent(lbase + (int64_t)c * LCAPC + i, (uint64_t)0);
+      if (s.m.pub[c].flags & PUB_DENSE) {
+        float* drow = a.dense + row * a.V;
+        const int lo = chunk_lo(a, R, c, VEC), hi = chunk_hi(a, R, c, VEC);
+        for (int p = lo + t; p < hi; p += CT) st_agent(drow + p, 0.0f);
+      }
+    }
+    uint32_t* pw = reinterpret_cast<uint32_t*>(a.pub + row * P);
+    for (int i = t; i < P * (int)(sizeof(ChunkPub) / 4); i += CT) st_agent(pw + i, 0u);
+  }
+  if (t == 0) {
+    float lp = -INFINITY;
+    if (!empty) lp = (float)((double)zid - (double)m - L);
+    a.out_ids[row] = id;
+    a.out_logprobs[row] = lp;
+    if (a.out_flags) a.out_flags[row] = flags;
+    if (a.next_tokens) {
+      const int32_t dst = a.backfill_dest[row];
+      if (dst >= 0 && (int64_t)dst < a.next_len) a.next_tokens[dst] = id;
+    }
+    st_agent(&a.ctr[row], 0u);  // the workspace is left zeroed
+  }
+}
+
+// ----------------------------------------------------------------------------------------------
+// The kernel: one workgroup per (row, chunk)
+// ----------------------------------------------------------------------------------------------
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT) void k_split(SArgs a) {
+  __shared__ SSm s;
+  const int t = threadIdx.x;
+  constexpr int VEC = DT::VEC;
+  int64_t L = blockIdx.x;
+  if (a.xcd_map) L = (L & 7) * (a.grid >> 3) + (L >> 3);
+  const int64_t row = L / a.P;
+  const int c = (int)(L - row * a.P);
+  SRow R;
+  row_setup<DT, SEG>(a, row, c, R);
+
+  // ---- the row's history first (HPT ids per thread, in registers): waiting for these loads then
+  //      never waits for the row data issued after them (the vector memory counter is in order) ----
+  constexpr int HPT = 8;
+  const int32_t* hid = a.prm.hist_ids;
+  int32_t hreg[HPT];
+  static_for<HPT>([&](auto Q) {
+    constexpr int q = decltype(Q)::value;
+    const int64_t h = R.h_lo + t + (int64_t)q * CT;
+    hreg[q] = (R.pen_on && h < R.h_hi) ? hid[h] : 0;
+  });
+  asm volatile("" ::: "memory");  // the row loads stay behind the history loads
+
+  // ---- every slot of the chunk: one 16-byte load each, all in flight before any use ----
+  uint4 d[CJ];
+  static_for<CJ>([&](auto J) {
+    constexpr int j = decltype(J)::value;
+    const int64_t slot = R.s0 + (int64_t)j * CT + t;
+    if (slot < R.s1) d[j] = *slot_ptr<DT, SEG>(a, R, slot);
+    else d[j] = make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG);
+  });
+
+  if (t < HXN) s.hx_pos[t] = -1;
+  if (t == 0) {
+    s.n_list = 0;
+    s.flags = 0;
+  }
+
+  // ---- penalty overlay: presence bitmap, numbering by word prefix counts, counts by number ----
+  const int64_t e_base = (int64_t)R.head + (R.s0 - 1) * VEC;  // row position of bitmap bit 0
+  const int nwords = (int)(((R.s1 - R.s0 + 2) * VEC + 31) >> 5);
+  int n_x = 0;  // penalised extras
+  if (R.pen_on) {
+    for (int w = t; w < nwords; w += CT) s.c.bitmap[w] = 0;
+    for (int i = t; i < XCAP; i += CT) s.c.xval[i] = 0;
+    __syncthreads();
+    const int64_t e_lo = c == 0 ? 0 : (int64_t)R.head + R.s0 * VEC;
+    const int64_t e_hi = c == R.P - 1 ? (int64_t)R.V : (int64_t)R.head + R.s1 * VEC;
+    uint32_t bad = 0;
+    auto mark = [&](int32_t id) {
+      if (id < 0 || id >= R.V) {
+        bad = 1;
+      } else if (id >= e_lo && id < e_hi) {
+        const int b = (int)(id - e_base);
+        atomicOr(&s.c.bitmap[b >> 5], 1u << (b & 31));
+      }
+    };
+    static_for<HPT>([&](auto Q) {
+      constexpr int q = decltype(Q)::value;
+      if (R.h_lo + t + (int64_t)q * CT < R.h_hi) mark(hreg[q]);
+    });
+    for (int64_t h = R.h_lo + t + (int64_t)HPT * CT; h < R.h_hi; h += CT) mark(hid[h]);
+    if (bad) atomicOr(&s.flags, FLAG_BAD_INPUT);
+    __syncthreads();
+    const int wpt = (nwords + CT - 1) / CT;
+    const int w0 = t * wpt;
+    int loc = 0;
+    for (int q = 0; q < wpt; ++q)
+      if (w0 + q < nwords) loc += __popc(s.c.bitmap[w0 + q]);
+    int tot;
+    int ex = blk_excl_scan_i(loc, s, &tot);
+    for (int q = 0; q < wpt; ++q)
+      if (w0 + q < nwords) {
+        s.c.wpref[w0 + q] = (uint16_t)ex;
+        ex += __popc(s.c.bitmap[w0 + q]);
+      }
+    n_x = tot < XCAP ? tot : XCAP;
+    if (tot > XCAP && t == 0) atomicOr(&s.flags, FLAG_LIMIT);
+    __syncthreads();
+    auto count = [&](int32_t id) {
+      if (id >= e_lo && id < e_hi) {
+        const int b = (int)(id - e_base);
+        const int w = b >> 5;
+        const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
+        if (rank < XCAP) atomicAdd(&s.c.xval[rank], 1u);
+      }
+    };
+    static_for<HPT>([&](auto Q) {
+      constexpr int q = decltype(Q)::value;
+      if (R.h_lo + t + (int64_t)q * CT < R.h_hi) count(hreg[q]);
+    });
+    for (int64_t h = R.h_lo + t + (int64_t)HPT * CT; h < R.h_hi; h += CT) count(hid[h]);
+    __syncthreads();
+  }
+
+  // ---- one pass over the slots in arrival order: the penalised elements leave the registers for
+  //      the extras, then the slot's maximum and its exponentials against a running reference
+  //      (moved to each new thread maximum, with the sum rescaled), so the pass keeps pace with the
+  //      loads instead of waiting for the whole chunk ----
+  const float r = R.r;
+  float smax[CJ];
+  float xref = -INFINITY;       // running maximum of x
+  float mref_t = MREF0;         // fl32(fl32(xref r) L2E), the exponent reference
+  float acc0 = 0.0f, acc1 = 0.0f;
+  static_for<CJ>([&](auto J) {
+    constexpr int j = decltype(J)::value;
+    {  // slot j is processed here and not earlier: no slot's values are hoisted into registers
+      uint32_t x0 = d[j].x, x1 = d[j].y, x2 = d[j].z, x3 = d[j].w;
+      asm volatile("" : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3));
+      d[j] = make_uint4(x0, x1, x2, x3);
+    }
+    if (R.pen_on) {
+      const int64_t slot = R.s0 + (int64_t)j * CT + t;
+      if (slot < R.s1) {
+        const int b0 = (int)(slot - R.s0 + 1) * VEC;
+        const uint32_t bits = (s.c.bitmap[b0 >> 5] >> (b0 & 31)) & ((1u << VEC) - 1u);
+        if (bits) {
+          uint32_t applied = 0;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            if ((bits >> e) & 1u) {
+              const int b = b0 + e, w = b >> 5;
+              const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
+              if (rank < XCAP) {
+                const float x = elem<DT>(d[j], e);
+                s.c.xval[rank] = __float_as_uint(penalise(x, s.c.xval[rank], R.rep, R.freq, R.pres));
+                applied |= 1u << e;
+              }
+            }
+          }
+          const uint4 mk = DT::mask_of(applied);
+          d[j].x = (d[j].x & ~mk.x) | (DT::NEG & mk.x);
+          d[j].y = (d[j].y & ~mk.y) | (DT::NEG & mk.y);
+          d[j].z = (d[j].z & ~mk.z) | (DT::NEG & mk.z);
+          d[j].w = (d[j].w & ~mk.w) | (DT::NEG & mk.w);
+        }
+      }
+    }
+    float v = elem<DT>(d[j], 0);
+#pragma unroll
+    for (int e = 1; e < VEC; ++e) v = fmaxf(v, elem<DT>(d[j], e));
+    smax[j] = v;
+    if (v > xref) {
+      xref = v;
+      const float mnew = __fmul_rn(__fmul_rn(v, r), L2E);
+      const float sc = rel2(mref_t, mnew);
+      acc0 *= sc;
+      acc1 *= sc;
+      mref_t = mnew;
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; e += 2) {
+      acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(__fmul_rn(elem<DT>(d[j], e), r), L2E, -mref_t));
+      acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(__fmul_rn(elem<DT>(d[j], e + 1), r), L2E, -mref_t));
+    }
+  });
+  // the unaligned head (chunk 0) and tail (last chunk) positions
+  {
+    int pos = -1;
+    if (c == 0 && t < R.head) pos = t;
+    else if (c == R.P - 1 && t >= 8 && t < 8 + (R.V - R.tail_lo)) pos = R.tail_lo + (t - 8);
+    if (pos >= 0) {
+      const float x = load_elem<DT, SEG>(a, R, pos);
+      bool pen = false;
+      if (R.pen_on) {
+        const int b = (int)(pos - e_base), w = b >> 5;
+        if ((s.c.bitmap[w] >> (b & 31)) & 1u) {
+          const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
+          if (rank < XCAP) {
+            s.c.xval[rank] = __float_as_uint(penalise(x, s.c.xval[rank], R.rep, R.freq, R.pres));
+            pen = true;
+          }
+        }
+      }
+      if (!pen) {
+        s.hx_pos[t] = pos;
+        s.hx_val[t] = x;
+      }
+    }
+  }
+  __syncthreads();
+  // the extras this thread owns join its maximum and its sum
+  const bool own_hx = t < HXN && s.hx_pos[t] >= 0;
+  {
+    float xe = -INFINITY;
+    for (int i = t; i < n_x; i += CT) xe = fmaxf(xe, __uint_as_float(s.c.xval[i]));
+    if (own_hx) xe = fmaxf(xe, s.hx_val[t]);
+    if (xe > xref) {
+      xref = xe;
+      const float mnew = __fmul_rn(__fmul_rn(xe, r), L2E);
+      const float sc = rel2(mref_t, mnew);
+      acc0 *= sc;
+      acc1 *= sc;
+      mref_t = mnew;
+    }
+    for (int i = t; i < n_x; i += CT)
+      acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(__fmul_rn(__uint_as_float(s.c.xval[i]), r), L2E, -mref_t));
+    if (own_hx) acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(__fmul_rn(s.hx_val[t], r), L2E, -mref_t));
+  }
+  const float zt = canon(xref, r);
+  const float st = acc0 + acc1;
+
+  // ---- chunk totals: waves on DPP, then the four waves in order ----
+  {
+    const float Mw = wave_max(mref_t);
+    const float Sw = wave_sum(st * rel2(mref_t, Mw));
+    const float Zw = wave_max(zt);
+    if (lane_id() == 0) {
+      s.wred[0][wave_id()] = Mw;
+      s.wred[1][wave_id()] = Sw;
+      s.wred[2][wave_id()] = Zw;
+    }
+  }
+  __syncthreads();
+  float cm = s.wred[0][0], cs = s.wred[1][0], zmax = s.wred[2][0];
+  for (int w = 1; w < CW; ++w) {
+    lse_add(cm, cs, s.wred[0][w], s.wred[1][w]);
+    zmax = fmaxf(zmax, s.wred[2][w]);
+  }
+  uint32_t cflags = s.flags;
+  bool has_fin = zmax > -INFINITY;
+  if (!(zmax < INFINITY) || cs != cs) {
+    // a NaN or +inf processed value: flag the row; whether any value is finite needs a look at each
+    cflags |= FLAG_BAD_INPUT;
+    uint32_t f = 0;
+    reload_barrier(d);
+    static_for<CJ>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) f |= isfinite(canon(elem<DT>(d[j], e), r)) ? 1u : 0u;
+    });
+    for (int i = t; i < n_x; i += CT) f |= isfinite(canon(__uint_as_float(s.c.xval[i]), r)) ? 1u : 0u;
+    if (own_hx) f |= isfinite(canon(s.hx_val[t], r)) ? 1u : 0u;
+    has_fin = blk_or(f, s) != 0;
+  }
+
+  reload_barrier(d);
+  // ---- greedy rows: lowest position of the maximum ----
+  int argpos = -1;
+  if (R.greedy) {
+    int best = 0x7fffffff;
+    static_for<CJ>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      const int64_t slot = R.s0 + (int64_t)j * CT + t;
+      if (best == 0x7fffffff && smax[j] == zmax && slot < R.s1) {
+        #pragma unroll
+        for (int e = VEC - 1; e >= 0; --e)
+          if (canon(elem<DT>(d[j], e), 1.0f) == zmax) best = R.head + (int)slot * VEC + e;
+      }
+    });
+    for (int i = t; i < n_x; i += CT)
+      if (canon(__uint_as_float(s.c.xval[i]), 1.0f) == zmax) best = min(best, pos_of_rank(s, nwords, e_base, i));
+    if (own_hx && canon(s.hx_val[t], 1.0f) == zmax) best = min(best, s.hx_pos[t]);
+    argpos = blk_min_i(best, s);
+  }
+
+  // ---- candidate bounds from the per-thread maxima ----
+  const int Kk = R.kon ? R.k : 0, Kn = a.n_top;
+  const bool s2b = !R.greedy && (R.kon || R.minp_on);
+  const bool want_list = s2b || Kn > 0;
+  const bool want_dense = !R.greedy && !s2b;
+  float bound = INFINITY;
+  if (want_list) {
+    float bk = -INFINITY, bn = -INFINITY;
+    const int Rk = (Kk + CW - 1) / CW, Rn = (Kn + CW - 1) / CW;
+    if (Kk > 0 || Kn > 0) {
+      // bitonic sort of the 64 thread maxima of the wave, descending in lane order
+      float v = zt;
+      const int l = lane_id();
+#pragma unroll
+      for (int kk = 2; kk <= 64; kk <<= 1) {
+#pragma unroll
+        for (int jj = kk >> 1; jj > 0; jj >>= 1) {
+          const float o = __shfl_xor(v, jj);
+          const bool take_max = ((l & kk) == 0) == ((l & jj) == 0);
+          v = take_max ? fmaxf(v, o) : fminf(v, o);
+        }
+      }
+      const float wk = (Kk > 0 && Rk <= 64) ? lane_f32(v, Rk - 1) : -INFINITY;
+      const float wn = (Kn > 0 && Rn <= 64) ? lane_f32(v, Rn - 1) : -INFINITY;
+      __syncthreads();
+      if (l == 0) {
+        s.wred[0][wave_id()] = wk;
+        s.wred[1][wave_id()] = wn;
+      }
+      __syncthreads();
+      bk = fminf(fminf(s.wred[0][0], s.wred[0][1]), fminf(s.wred[0][2], s.wred[0][3]));
+      bn = fminf(fminf(s.wred[1][0], s.wred[1][1]), fminf(s.wred[1][2], s.wred[1][3]));
+    }
+    if (s2b) {
+      const float bm = R.minp_on ? __fadd_rn(zmax, (float)log((double)R.minp)) : -INFINITY;
+      const float b2 = fmaxf(Kk > 0 ? bk : -INFINITY, bm);
+      bound = Kn > 0 ? fminf(b2, bn) : b2;
+    } else {
+      bound = bn;
+    }
+  }
+
+  reload_barrier(d);
+  // ---- gather the candidates z >= bound ----
+  uint64_t* glist = a.lists + L * (int64_t)LCAPC;
+  int n_list = 0;
+  bool overflow = false;
+  if (want_list) {
+    uint32_t pm = 0;
+    static_for<CJ>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      if (smax[j] > -INFINITY && canon(smax[j], r) >= bound) pm |= 1u << j;
+    });
+    reload_barrier(d);
+    while (pm) {
+      const int j = __builtin_ctz(pm);
+      pm &= pm - 1u;
+      const int64_t slot = R.s0 + (int64_t)j * CT + t;
+      // slot j through a select chain written in the kernel body, so that the register slots stay
+      // registers (a helper taking the slots by reference would index them as memory)
+      uint4 dd = d[0];
+      static_for<CJ>([&](auto J) {
+        constexpr int jj = decltype(J)::value;
+        if (jj > 0 && j == jj) dd = d[jj];
+      });
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float z = canon(elem<DT>(dd, e), r);
+        if (z > -INFINITY && z >= bound) {
+          const int idx = atomicAdd(&s.n_list, 1);
+          if (idx < LCAPC) s.c.list[idx] = cand_key(z, R.head + (int)slot * VEC + e);
+        }
+      }
+    }
+    for (int i = t; i < n_x; i += CT) {
+      const float z = canon(__uint_as_float(s.c.xval[i]), r);
+      if (z > -INFINITY && z >= bound) {
+        const int idx = atomicAdd(&s.n_list, 1);
+        if (idx < LCAPC) s.c.list[idx] = cand_key(z, pos_of_rank(s, nwords, e_base, i));
+      }
+    }
+    if (own_hx) {
+      const float z = canon(s.hx_val[t], r);
+      if (z > -INFINITY && z >= bound) {
+        const int idx = atomicAdd(&s.n_list, 1);
+        if (idx < LCAPC) s.c.list[idx] = cand_key(z, s.hx_pos[t]);
+      }
+    }
+    __syncthreads();
+    n_list = s.n_list;
+    overflow = n_list > LCAPC;
+  }
+
+  reload_barrier(d);
+  // ---- publish the list, sorted in descending key order (rank by counting) ----
+  float qk = -INFINITY, qn = -INFINITY;
+  if (want_list && !overflow) {
+    const int P = R.P;
+    const int qki = Kk > 0 ? (Kk + P - 1) / P - 1 : -1;
+    const int qni = Kn > 0 ? (Kn + P - 1) / P - 1 : -1;
+    if (t == 0) {
+      s.bc_f[0] = -INFINITY;
+      s.bc_f[1] = -INFINITY;
+    }
+    __syncthreads();
+    for (int i = t; i < n_list; i += CT) {
+      const uint64_t key = s.c.list[i];
+      const int rank = count_above(s.c.list, n_list, key);
+      st_agent(glist + rank, key);
+      if (rank == qki) s.bc_f[0] = cand_z(key);
+      if (rank == qni) s.bc_f[1] = cand_z(key);
+    }
+    __syncthreads();
+    qk = s.bc_f[0];
+    qn = s.bc_f[1];
+  } else if (want_list) {
+    // too many candidates (ties): the dense row stands for the kept set; the top n exactly, slowly
+    n_list = 0;
+    if (Kn > 0) {
+      uint64_t prev = ~0ull;
+      for (int it = 0; it < Kn; ++it) {
+        uint64_t best = 0;
+        reload_barrier(d);
+#pragma unroll 1
+        for (int j = 0; j < CJ; ++j) {
+          const int64_t slot = R.s0 + (int64_t)j * CT + t;
+          if (slot >= R.s1) continue;
+          uint4 dd = d[0];
+          static_for<CJ>([&](auto J) {
+            constexpr int jj = decltype(J)::value;
+            if (jj > 0 && j == jj) dd = d[jj];
+          });
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            const float z = canon(elem<DT>(dd, e), r);
+            if (z > -INFINITY && z == z) {
+              const uint64_t key = cand_key(z, R.head + (int)slot * VEC + e);
+              if (key < prev && key > best) best = key;
+            }
+          }
+        }
+        for (int i = t; i < n_x; i += CT) {
+          const float z = canon(__uint_as_float(s.c.xval[i]), r);
+          if (z > -INFINITY && z == z) {
+            const uint64_t key = cand_key(z, pos_of_rank(s, nwords, e_base, i));
+            if (key < prev && key > best) best = key;
+          }
+        }
+        if (own_hx) {
+          const float z = canon(s.hx_val[t], r);
+          if (z > -INFINITY && z == z) {
+            const uint64_t key = cand_key(z, s.hx_pos[t]);
+            if (key < prev && key > best) best = key;
+          }
+        }
+        best = blk_max_u64(best, s);
+        if (best == 0) break;
+        if (t == 0) st_agent(glist + it, best);
+        prev = best;
+        n_list = it + 1;
+      }
+      qn = -INFINITY;  // the top-n staging then takes the whole short list
+    }
+  }
+
+  reload_barrier(d);
+  // ---- rows without a small kept set: the processed values of the whole chunk ----
+  const bool dense = want_dense || (s2b && overflow);
+  if (dense) {
+    float* drow = a.dense + row * a.V;
+    static_for<CJ>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      const int64_t slot = R.s0 + (int64_t)j * CT + t;
+      if (slot < R.s1) {
+        uint32_t skip = 0;
+        if (R.pen_on) {
+          const int b0 = (int)(slot - R.s0 + 1) * VEC;
+          const uint32_t bits = (s.c.bitmap[b0 >> 5] >> (b0 & 31)) & ((1u << VEC) - 1u);
+          #pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            if (!((bits >> e) & 1u)) continue;
+            const int b = b0 + e, w = b >> 5;
+            if ((int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u)) < XCAP) skip |= 1u << e;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+          if (!((skip >> e) & 1u)) st_agent(drow + R.head + (int)slot * VEC + e, canon(elem<DT>(d[j], e), r));
+      }
+    });
+    for (int i = t; i < n_x; i += CT)
+      st_agent(drow + pos_of_rank(s, nwords, e_base, i), canon(__uint_as_float(s.c.xval[i]), r));
+    if (own_hx) st_agent(drow + s.hx_pos[t], canon(s.hx_val[t], r));
+  }
+
+  // ---- publish the chunk record, then arrive ----
+  if (t == 0) {
+    ChunkPub* g = a.pub + L;
+    st_agent(&g->zmax, zmax);
+    st_agent(&g->mref, cm);
+    st_agent(&g->s, cs);
+    st_agent(&g->flags, cflags | (dense ? PUB_DENSE : 0u) | (has_fin ? PUB_FINITE : 0u));
+    st_agent(&g->argpos, (int32_t)argpos);
+    st_agent(&g->n_list, (int32_t)n_list);
+    st_agent(&g->qk, qk);
+    st_agent(&g->qn, qn);
+  }
+  // Every value another workgroup reads (record, list, dense row) was written with an agent-scope
+  // store, which writes through this XCD's L2; once the stores have completed they are visible to
+  // every XCD, and the resolving workgroup reads them with agent-scope loads.  So completing the
+  // stores is all the publication needs -- a device-scope fence would also write back and invalidate
+  // the whole L2 of the XCD, once per chunk.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (t == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(&a.ctr[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s.bc_i[3] = (old == (uint32_t)(R.P - 1)) ? 1 : 0;
+  }
+  __syncthreads();
+  if (!s.bc_i[3]) return;
+  resolve_row<DT, SEG>(a, R, s);
+}
+
+// ----------------------------------------------------------------------------------------------
+// Host side
+// ----------------------------------------------------------------------------------------------
+struct SGeo {
+  int P;
+  int64_t chunk_slots;
+  bool ok;
+};
+
+SGeo geometry(int64_t B, int64_t V, albireo_dtype_t dtype) {
+  SGeo g{0, 0, false};
+  const int vec = dtype == ALBIREO_BF16 ? BF16T::VEC : F32T::VEC;
+  const int64_t body = V / vec;
+  int64_t P = (body + CSLOTS - 1) / CSLOTS;
+  if (P < 1) P = 1;
+  if (P > MAXPC || B <= 0 || B * P >= ((int64_t)1 << 31)) return g;
+  g.P = (int)P;
+  g.chunk_slots = (body + P - 1) / P;
+  g.ok = true;
+  return g;
+}
+
+struct WsParts {
+  int64_t ctr, pub, lists, dense, total;
+};
+WsParts ws_parts(int64_t B, int64_t V, int P) {
+  WsParts w;
+  w.ctr = 0;
+  w.pub = align256(w.ctr + B * 4);
+  w.lists = align256(w.pub + B * P * (int64_t)sizeof(ChunkPub));
+  w.dense = align256(w.lists + B * P * (int64_t)LCAPC * 8);
+  w.total = align256(w.dense + B * V * 4);
+  return w;
+}
+
+}  // namespace
+
+namespace albireo_split {
+
+bool supported(int64_t B, int64_t V, albireo_dtype_t dtype) { return geometry(B, V, dtype).ok; }
+
+size_t workspace_bytes(int64_t B, int64_t V, albireo_dtype_t dtype) {
+  const SGeo g = geometry(B, V, dtype);
+  if (!g.ok) return 0;
+  return (size_t)ws_parts(B, V, g.P).total;
+}
+
+albireo_status_t launch(const Request& q) {
+  const SGeo g = geometry(q.B, q.V, q.dtype);
+  if (!g.ok) return ALBIREO_E_UNSUPPORTED;
+  SArgs a;
+  memset(&a, 0, sizeof a);
+  a.logits = static_cast<const unsigned char*>(q.logits);
+  a.B = q.B;
+  a.V = q.V;
+  a.ld = q.ld;
+  if (q.params) {
+    const albireo_params_t* p = q.params;
+    a.prm.temperature = p->temperature;
+    a.prm.top_k = p->top_k;
+    a.prm.top_p = p->top_p;
+    a.prm.min_p = p->min_p;
+    a.prm.rep = p->repetition_penalty;
+    a.prm.freq = p->frequency_penalty;
+    a.prm.pres = p->presence_penalty;
+    a.prm.hist_offsets = p->hist_offsets;
+    a.prm.hist_ids = p->hist_ids;
+    a.prm.hist_len = p->hist_len;
+  }
+  a.uniforms = q.uniforms;
+  a.out_ids = q.out_ids;
+  a.out_logprobs = q.out_logprobs;
+  a.n_top = q.n_top;
+  a.out_top_ids = q.out_top_ids;
+  a.out_top_logprobs = q.out_top_logprobs;
+  a.out_flags = q.out_flags;
+  if (q.step) {
+    a.rng_on = 1;
+    a.rng_seed = q.step->seed;
+    a.rng_step = q.step->step;
+    a.seq_ids = q.step->seq_ids;
+    a.next_tokens = q.step->next_tokens;
+    a.backfill_dest = q.step->backfill_dest;
+    a.next_len = q.step->next_len;
+  }
+  const int es = q.dtype == ALBIREO_BF16 ? 2 : 4;
+  if (q.shards) {
+    const int64_t Ls = q.shards->shard_len, Ss = q.shards->shard_stride;
+    const int64_t t = (q.V + Ls - 1) / Ls;
+    const int64_t sps = Ls * es / 16;
+    a.seg_sps = (uint32_t)sps;
+    a.seg_magic = (uint32_t)(0xffffffffull / (uint64_t)sps);
+    a.seg_gap = t > 1 ? (Ss - Ls) * es : 0;
+  }
+  a.P = g.P;
+  a.chunk_slots = g.chunk_slots;
+  a.grid = q.B * g.P;
+  a.xcd_map = (a.grid % 8 == 0) ? 1 : 0;
+  const WsParts w = ws_parts(q.B, q.V, g.P);
+  a.ctr = reinterpret_cast<uint32_t*>(q.ws + w.ctr);
+  a.pub = reinterpret_cast<ChunkPub*>(q.ws + w.pub);
+  a.lists = reinterpret_cast<uint64_t*>(q.ws + w.lists);
+  a.dense = reinterpret_cast<float*>(q.ws + w.dense);
+  void* args[] = {&a};
+  const void* fn;
+  if (q.dtype == ALBIREO_BF16)
+    fn = q.shards ? reinterpret_cast<const void*>(&k_split<BF16T, true>) : reinterpret_cast<const void*>(&k_split<BF16T, false>);
+  else
+    fn = q.shards ? reinterpret_cast<const void*>(&k_split<F32T, true>) : reinterpret_cast<const void*>(&k_split<F32T, false>);
+  const hipError_t e = hipLaunchKernel(fn, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
+  return e == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
+}
+
+}  // namespace albireo_split
