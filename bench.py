@@ -39,13 +39,18 @@ def algorithmic_bytes(w) -> int:
     return int(b)
 
 
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_01927_amd", "csrc", "albireo.hip")
+# the sources the headline workload's kernel (k_sample) is compiled from
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_01927_amd", "csrc", n) for n in ("albireo.hip", "common.h")] + [
+    os.path.join(ROOT, "include", "albireo.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sample_C3_B256_V152064_bf16_traffic.txt")
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for p in KERNEL_SRCS:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic():
