@@ -90,7 +90,58 @@ typedef struct {
   const int64_t* hist_offsets;     /* [B+1] CSR row pointers into hist_ids; NULL => no penalties   */
   const int32_t* hist_ids;         /* [hist_len] token ids; ids outside [0, V) are skipped+flagged */
   int64_t hist_len;                /* [host value] number of entries in hist_ids                   */
+  /* Optional prompt history.  When given, hist_* holds each row's generated (output) tokens only and
+   * the penalties split as the OpenAI definition the paper cites for frequency and presence does:
+   * the repetition penalty covers every id of the prompt or the output, the frequency and presence
+   * penalties count the output only.  Without it hist_* feeds all three penalties. */
+  const int64_t* prompt_offsets;   /* [B+1] CSR row pointers into prompt_ids, or NULL              */
+  const int32_t* prompt_ids;       /* [prompt_len] token ids; ids outside [0, V) are skipped+flagged */
+  int64_t prompt_len;              /* [host value] number of entries in prompt_ids                 */
+  /* Optional per-sequence penalty state (below) in place of the histories: the rows' distinct ids
+   * with their output counts and prompt marks, kept on the device from step to step.  When given,
+   * hist_* and prompt_* must be NULL. */
+  const struct albireo_penalty_state_s* state; /* [host] or NULL                                  */
 } albireo_params_t;
+
+/*
+ * Per-sequence penalty state (host struct of device arrays, read during a call only).  Row i holds
+ * the distinct token ids of its prompt and output in ids[i * cap + e], e < len[i], in ascending
+ * order, with counts[i * cap + e] = the id's number of occurrences in the output (bits 0-30) and bit 31
+ * set when the id occurs in the prompt.  Sampling from the state gives the same penalties as sampling
+ * from the prompt and output histories it was built from, without re-counting H ids per call; the
+ * state follows the sequence by albireo_penalty_state_append after every step.  Ids that find no free
+ * entry are left out and set ALBIREO_FLAG_LIMIT in flags[i]; ids outside [0, V) are skipped and set
+ * ALBIREO_FLAG_BAD_INPUT; malformed history offsets set ALBIREO_FLAG_BAD_PARAM.  The sampling entry
+ * points copy flags[i] into out_flags[i].
+ */
+typedef struct albireo_penalty_state_s {
+  int32_t cap;       /* [host value] entries per row, 1 .. ALBIREO_MAX_STATE_ENTRIES              */
+  int32_t* ids;      /* [B, cap] device                                                          */
+  uint32_t* counts;  /* [B, cap] device                                                          */
+  int32_t* len;      /* [B] device                                                               */
+  uint32_t* flags;   /* [B] device                                                               */
+} albireo_penalty_state_t;
+
+#define ALBIREO_MAX_STATE_ENTRIES 8192
+
+/*
+ * Build the state of B rows from their prompt and output histories (CSR as in albireo_params_t; either
+ * may be NULL).  Overwrites ids, counts, len and flags of every row.  A row whose two histories hold
+ * more than ALBIREO_MAX_STATE_ENTRIES ids in all keeps the state of their first that many (prompt
+ * first) and sets ALBIREO_FLAG_LIMIT.
+ */
+albireo_status_t albireo_penalty_state_init(const albireo_penalty_state_t* state, int64_t B, int64_t V,
+                                            const int64_t* prompt_offsets, const int32_t* prompt_ids,
+                                            int64_t prompt_len, const int64_t* out_offsets,
+                                            const int32_t* out_ids, int64_t out_len, hipStream_t stream);
+
+/*
+ * Fold one sampled token per row into the state (the step's output): ids[i] gains one output
+ * occurrence; an id not yet in the row takes a new entry in order.  ids[i] outside [0, V) (an EMPTY
+ * row's -1, padding rows) changes nothing.  Stream-ordered after the sampling call that produced ids.
+ */
+albireo_status_t albireo_penalty_state_append(const albireo_penalty_state_t* state, int64_t B, int64_t V,
+                                              const int32_t* ids, hipStream_t stream);
 
 /*
  * Bytes of device workspace needed by any entry point for this shape on the current device.

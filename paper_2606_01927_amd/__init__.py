@@ -29,12 +29,19 @@ FLAG_GREEDY, FLAG_EMPTY, FLAG_BAD_INPUT, FLAG_BAD_PARAM, FLAG_LIMIT = 1, 2, 4, 8
 MAX_TOP_N = 32
 
 
+class _State(ctypes.Structure):
+    _fields_ = [("cap", ctypes.c_int32), ("ids", ctypes.c_void_p), ("counts", ctypes.c_void_p),
+                ("len", ctypes.c_void_p), ("flags", ctypes.c_void_p)]
+
+
 class _Params(ctypes.Structure):
     _fields_ = [
         ("temperature", ctypes.c_void_p), ("top_k", ctypes.c_void_p), ("top_p", ctypes.c_void_p),
         ("min_p", ctypes.c_void_p), ("repetition_penalty", ctypes.c_void_p),
         ("frequency_penalty", ctypes.c_void_p), ("presence_penalty", ctypes.c_void_p),
         ("hist_offsets", ctypes.c_void_p), ("hist_ids", ctypes.c_void_p), ("hist_len", ctypes.c_int64),
+        ("prompt_offsets", ctypes.c_void_p), ("prompt_ids", ctypes.c_void_p), ("prompt_len", ctypes.c_int64),
+        ("state", ctypes.POINTER(_State)),
     ]
 
 
@@ -72,12 +79,17 @@ _lib.albireo_philox_uniforms.argtypes = [ctypes.c_uint64, ctypes.c_uint64, _vp, 
 _lib.albireo_philox_uniforms.restype = ctypes.c_int
 _lib.albireo_backfill.argtypes = [_vp, _vp, _i64, _vp, _i64, _vp]
 _lib.albireo_backfill.restype = ctypes.c_int
+_lib.albireo_penalty_state_init.argtypes = [ctypes.POINTER(_State), _i64, _i64, _vp, _vp, _i64, _vp, _vp, _i64, _vp]
+_lib.albireo_penalty_state_init.restype = ctypes.c_int
+_lib.albireo_penalty_state_append.argtypes = [ctypes.POINTER(_State), _i64, _i64, _vp, _vp]
+_lib.albireo_penalty_state_append.restype = ctypes.c_int
 _lib.albireo_status_string.argtypes = [ctypes.c_int]
 _lib.albireo_status_string.restype = ctypes.c_char_p
 
 EXPORTED = ("albireo_workspace_size", "albireo_sample", "albireo_sample_step", "albireo_sample_sharded",
             "albireo_philox_uniforms",
-            "albireo_backfill", "albireo_apply_penalties", "albireo_topk_topp", "albireo_status_string")
+            "albireo_backfill", "albireo_apply_penalties", "albireo_topk_topp", "albireo_status_string",
+            "albireo_penalty_state_init", "albireo_penalty_state_append")
 
 
 class AlbireoError(RuntimeError):
@@ -102,11 +114,15 @@ class SamplingParams:
     presence_penalty: Optional[torch.Tensor] = None    # float32
     hist_offsets: Optional[torch.Tensor] = None        # int64 [B + 1]
     hist_ids: Optional[torch.Tensor] = None            # int32
+    prompt_offsets: Optional[torch.Tensor] = None      # int64 [B + 1]: with it, hist_* is the output only
+    prompt_ids: Optional[torch.Tensor] = None          # int32
+    state: Optional["PenaltyState"] = None             # in place of hist_* and prompt_*
 
 
 _DT = {"temperature": torch.float32, "top_k": torch.int32, "top_p": torch.float32, "min_p": torch.float32,
        "repetition_penalty": torch.float32, "frequency_penalty": torch.float32,
-       "presence_penalty": torch.float32, "hist_offsets": torch.int64, "hist_ids": torch.int32}
+       "presence_penalty": torch.float32, "hist_offsets": torch.int64, "hist_ids": torch.int32,
+       "prompt_offsets": torch.int64, "prompt_ids": torch.int32}
 
 
 def _ptr(t: Optional[torch.Tensor], name: str, device) -> Optional[int]:
@@ -122,10 +138,57 @@ def _params(p: Optional[SamplingParams], device) -> Optional[_Params]:
         return None
     s = _Params()
     for f in ("temperature", "top_k", "top_p", "min_p", "repetition_penalty", "frequency_penalty",
-              "presence_penalty", "hist_offsets", "hist_ids"):
+              "presence_penalty", "hist_offsets", "hist_ids", "prompt_offsets", "prompt_ids"):
         setattr(s, f, _ptr(getattr(p, f), f, device))
     s.hist_len = 0 if p.hist_ids is None else int(p.hist_ids.numel())
+    s.prompt_len = 0 if p.prompt_ids is None else int(p.prompt_ids.numel())
+    if p.state is not None:
+        s._state = p.state._struct(device)  # kept alive with the struct
+        s.state = ctypes.pointer(s._state)
     return s
+
+
+class PenaltyState:
+    """Per-sequence penalty state of B rows on the device (the distinct ids of each row's prompt and
+    output with their output counts and prompt marks), built from histories by init() and advanced by
+    one sampled token per row with append()."""
+
+    def __init__(self, B: int, cap: int, device=None):
+        self.device = torch.device("cuda") if device is None else torch.device(device)
+        self.B, self.cap = B, cap
+        self.ids = torch.zeros((B, cap), dtype=torch.int32, device=self.device)
+        self.counts = torch.zeros((B, cap), dtype=torch.int32, device=self.device)  # uint32 bit patterns
+        self.len = torch.zeros(B, dtype=torch.int32, device=self.device)
+        self.flags = torch.zeros(B, dtype=torch.int32, device=self.device)
+        self.device = self.ids.device  # with its index
+
+    def _struct(self, device) -> _State:
+        if self.ids.device != device:
+            raise ValueError("penalty state lives on %s, not %s" % (self.ids.device, device))
+        return _State(cap=self.cap, ids=self.ids.data_ptr(), counts=self.counts.data_ptr(),
+                      len=self.len.data_ptr(), flags=self.flags.data_ptr())
+
+    def init(self, V: int, prompt_offsets=None, prompt_ids=None, out_offsets=None, out_ids=None, stream=None):
+        st = self._struct(self.device)
+        po = _ptr(prompt_offsets, "prompt_offsets", self.device)
+        pi = _ptr(prompt_ids, "prompt_ids", self.device)
+        oo = _ptr(out_offsets, "hist_offsets", self.device)
+        oi = _ptr(out_ids, "hist_ids", self.device)
+        rc = _lib.albireo_penalty_state_init(ctypes.byref(st), self.B, V, po, pi,
+                                             0 if prompt_ids is None else int(prompt_ids.numel()), oo, oi,
+                                             0 if out_ids is None else int(out_ids.numel()), _stream(stream))
+        if rc != OK:
+            raise AlbireoError(rc, "albireo_penalty_state_init")
+        return self
+
+    def append(self, ids: torch.Tensor, V: int, stream=None):
+        if ids.device != self.device or ids.dtype != torch.int32 or not ids.is_contiguous():
+            raise ValueError("ids must be a contiguous int32 tensor on %s" % self.device)
+        st = self._struct(self.device)
+        rc = _lib.albireo_penalty_state_append(ctypes.byref(st), self.B, V, ids.data_ptr(), _stream(stream))
+        if rc != OK:
+            raise AlbireoError(rc, "albireo_penalty_state_append")
+        return self
 
 
 def _dtype_code(t: torch.Tensor) -> int:

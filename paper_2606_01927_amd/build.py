@@ -7,7 +7,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", "albireo.hip"), os.path.join(HERE, "csrc", "split.hip")]
+SRCS = [os.path.join(HERE, "csrc", n) for n in ("albireo.hip", "split.hip", "state.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libalbireo.so")
 

@@ -2689,7 +2689,22 @@ albireo_status_t check_common(const void* logits, albireo_dtype_t dtype, int64_t
     if (params->hist_len < 0) return ALBIREO_E_INVALID;
     if (params->hist_len > 0 && !params->hist_ids) return ALBIREO_E_INVALID;
   }
+  if (params && params->prompt_offsets) {
+    if (params->prompt_len < 0) return ALBIREO_E_INVALID;
+    if (params->prompt_len > 0 && !params->prompt_ids) return ALBIREO_E_INVALID;
+  }
+  if (params && params->state) {
+    const albireo_penalty_state_t* st = params->state;
+    if (params->hist_offsets || params->prompt_offsets) return ALBIREO_E_INVALID;
+    if (st->cap < 1 || st->cap > ALBIREO_MAX_STATE_ENTRIES) return ALBIREO_E_INVALID;
+    if (B > 0 && (!st->ids || !st->counts || !st->len || !st->flags)) return ALBIREO_E_INVALID;
+  }
   return ALBIREO_OK;
+}
+
+// A prompt history or a penalty state is read by the split-row kernel only.
+bool needs_split(const albireo_params_t* params) {
+  return params && (params->prompt_offsets || params->state);
 }
 
 albireo_status_t check_ws(void* ws, size_t bytes, size_t need) {
@@ -2753,7 +2768,8 @@ albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t 
     st = check_shards(logits, dtype, V, ld, *shards);
     if (st != ALBIREO_OK) return st;
   }
-  if (use_split(B, V, dtype)) {
+  if (needs_split(params) && !albireo_split::supported(B, V, dtype)) return ALBIREO_E_UNSUPPORTED;
+  if (use_split(B, V, dtype) || needs_split(params)) {
     // the split-row kernel; its part of the workspace follows the other kernels' part
     const size_t off = (size_t)align256((int64_t)legacy_ws(B, V, dtype));
     st = check_ws(workspace, workspace_bytes, off + albireo_split::workspace_bytes(B, V, dtype));
@@ -2825,7 +2841,9 @@ size_t albireo_workspace_size(int64_t B, int64_t V, albireo_dtype_t dtype, int32
   if (V >= ((int64_t)1 << 31) - 16) return 0;
   // the split-row kernel's part follows the other kernels' part (both may serve one workspace)
   const size_t legacy = legacy_ws(B, V, dtype);
-  const size_t split = use_split(B, V, dtype) ? albireo_split::workspace_bytes(B, V, dtype) : 0;
+  // the split-row kernel's part whenever it can serve the shape: rows with a prompt history or a
+  // penalty state go to it whatever their width
+  const size_t split = albireo_split::workspace_bytes(B, V, dtype);
   if (split == 0) {
     Geometry G;
     if (make_geometry(B, V, dtype, G) != hipSuccess || !G.ok) return 0;
@@ -2927,6 +2945,7 @@ albireo_status_t albireo_apply_penalties(const void* logits, albireo_dtype_t dty
   (void)workspace_bytes;
   albireo_status_t st = check_common(logits, dtype, B, V, ld, params);
   if (st != ALBIREO_OK) return st;
+  if (needs_split(params)) return ALBIREO_E_UNSUPPORTED;
   if (B == 0) return ALBIREO_OK;
   if (!out_logits) return ALBIREO_E_INVALID;
   // aliasing is only defined for an fp32 input with ld == V (element-wise in place)

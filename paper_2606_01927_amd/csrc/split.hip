@@ -84,6 +84,15 @@ struct SArgs {
   int64_t next_len;
   uint32_t seg_sps, seg_magic;  // blocked layout: slots per block, floor((2^32 - 1) / seg_sps)
   int64_t seg_gap;              // bytes between the end of a block and the start of the next
+  // prompt history (repetition only) and per-sequence penalty state, in place of or beside hist_*
+  const int64_t* prompt_offsets;
+  const int32_t* prompt_ids;
+  int64_t prompt_len;
+  const int32_t* st_ids;
+  const uint32_t* st_counts;
+  const int32_t* st_len;
+  const uint32_t* st_flags;
+  int32_t st_cap;
   int32_t P;
   int32_t xcd_map;
   int64_t chunk_slots;
@@ -102,7 +111,9 @@ struct SRow {
   bool greedy, kon, minp_on, topp_on, pen_on;
   float r, p, minp, rep, freq, pres;
   int k;
-  int64_t h_lo, h_hi;
+  int64_t h_lo, h_hi;  // output history [h_lo, h_hi)
+  int64_t p_lo, p_hi;  // prompt history
+  int st_n;            // penalty state entries
   uint32_t flags;
 };
 
@@ -252,6 +263,18 @@ __device__ __forceinline__ uint64_t blk_excl_scan_u64(uint64_t v, SSm& s, uint64
   return off + incl - v;
 }
 
+// The penalty overlay of one logit whose history record is cv: bits 0-30 its count in the output, bit 31
+// set when it occurs in the prompt.  Repetition covers both; frequency and presence count the output.
+__device__ __forceinline__ float penalise_cv(float x, uint32_t cv, float rep, float freq, float pres) {
+  const uint32_t c = cv & 0x7fffffffu;
+  float v = (x > 0.0f) ? __fdiv_rn(x, rep) : __fmul_rn(x, rep);
+  if (c > 0) {
+    v = __fsub_rn(v, __fmul_rn(freq, (float)c));
+    v = __fsub_rn(v, pres);
+  }
+  return v;
+}
+
 // (mref, s) pairs: s is relative to 2^mref
 __device__ __forceinline__ void lse_add(float& m, float& s, float m2, float s2) {
   const float M = fmaxf(m, m2);
@@ -338,6 +361,8 @@ __device__ __forceinline__ void row_setup(const SArgs& a, int64_t row, int c, SR
   R.pres = pres;
   R.pen_on = false;
   R.h_lo = R.h_hi = 0;
+  R.p_lo = R.p_hi = 0;
+  R.st_n = 0;
   if (q.hist_offsets) {
     if (lo < 0 || hi < lo || hi > q.hist_len) {
       flags |= FLAG_BAD_PARAM;
@@ -346,6 +371,21 @@ __device__ __forceinline__ void row_setup(const SArgs& a, int64_t row, int c, SR
       R.h_lo = lo;
       R.h_hi = hi;
     }
+  }
+  if (a.prompt_offsets) {
+    const int64_t plo = sload(a.prompt_offsets + row), phi = sload(a.prompt_offsets + row + 1);
+    if (plo < 0 || phi < plo || phi > a.prompt_len) {
+      flags |= FLAG_BAD_PARAM;
+    } else if (phi > plo) {
+      R.pen_on = true;
+      R.p_lo = plo;
+      R.p_hi = phi;
+    }
+  }
+  if (a.st_len) {
+    const int n = sload(a.st_len + row);
+    R.st_n = n < 0 ? 0 : (n > a.st_cap ? a.st_cap : n);
+    if (R.st_n > 0) R.pen_on = true;
   }
   R.flags = flags;
 }
@@ -723,6 +763,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
   }
   for (int c = 0; c < P; ++c)
     if (s.m.pub[c].zmax == m) { argpos = s.m.pub[c].argpos; break; }
+  if (a.st_flags) flags |= a.st_flags[row] & (FLAG_BAD_INPUT | FLAG_BAD_PARAM | FLAG_LIMIT);
   const bool empty = !fin;
   if (empty) flags |= FLAG_EMPTY;
   const double L = log((double)S) - ((double)m * (double)L2E - (double)mref) * LN2;
@@ -985,6 +1026,8 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
       if (R.h_lo + t + (int64_t)q * CT < R.h_hi) mark(hreg[q]);
     });
     for (int64_t h = R.h_lo + t + (int64_t)HPT * CT; h < R.h_hi; h += CT) mark(hid[h]);
+    for (int64_t h = R.p_lo + t; h < R.p_hi; h += CT) mark(a.prompt_ids[h]);
+    for (int e = t; e < R.st_n; e += CT) mark(a.st_ids[row * a.st_cap + e]);
     if (bad) atomicOr(&s.flags, FLAG_BAD_INPUT);
     __syncthreads();
     const int wpt = (nwords + CT - 1) / CT;
@@ -1002,19 +1045,28 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     n_x = tot < XCAP ? tot : XCAP;
     if (tot > XCAP && t == 0) atomicOr(&s.flags, FLAG_LIMIT);
     __syncthreads();
-    auto count = [&](int32_t id) {
+    // per numbered position: the output count in bits 0-30, the prompt mark in bit 31
+    auto count = [&](int32_t id, uint32_t add, uint32_t mark_bits) {
       if (id >= e_lo && id < e_hi) {
         const int b = (int)(id - e_base);
         const int w = b >> 5;
         const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
-        if (rank < XCAP) atomicAdd(&s.c.xval[rank], 1u);
+        if (rank < XCAP) {
+          if (add) atomicAdd(&s.c.xval[rank], add);
+          if (mark_bits) atomicOr(&s.c.xval[rank], mark_bits);
+        }
       }
     };
     static_for<HPT>([&](auto Q) {
       constexpr int q = decltype(Q)::value;
-      if (R.h_lo + t + (int64_t)q * CT < R.h_hi) count(hreg[q]);
+      if (R.h_lo + t + (int64_t)q * CT < R.h_hi) count(hreg[q], 1u, 0u);
     });
-    for (int64_t h = R.h_lo + t + (int64_t)HPT * CT; h < R.h_hi; h += CT) count(hid[h]);
+    for (int64_t h = R.h_lo + t + (int64_t)HPT * CT; h < R.h_hi; h += CT) count(hid[h], 1u, 0u);
+    for (int64_t h = R.p_lo + t; h < R.p_hi; h += CT) count(a.prompt_ids[h], 0u, 0x80000000u);
+    for (int e = t; e < R.st_n; e += CT) {
+      const uint32_t cv = a.st_counts[row * a.st_cap + e];
+      count(a.st_ids[row * a.st_cap + e], cv & 0x7fffffffu, cv & 0x80000000u);
+    }
     __syncthreads();
   }
 
@@ -1048,7 +1100,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
               const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
               if (rank < XCAP) {
                 const float x = elem<DT>(d[j], e);
-                s.c.xval[rank] = __float_as_uint(penalise(x, s.c.xval[rank], R.rep, R.freq, R.pres));
+                s.c.xval[rank] = __float_as_uint(penalise_cv(x, s.c.xval[rank], R.rep, R.freq, R.pres));
                 applied |= 1u << e;
               }
             }
@@ -1092,7 +1144,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
         if ((s.c.bitmap[w] >> (b & 31)) & 1u) {
           const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
           if (rank < XCAP) {
-            s.c.xval[rank] = __float_as_uint(penalise(x, s.c.xval[rank], R.rep, R.freq, R.pres));
+            s.c.xval[rank] = __float_as_uint(penalise_cv(x, s.c.xval[rank], R.rep, R.freq, R.pres));
             pen = true;
           }
         }
@@ -1470,6 +1522,19 @@ albireo_status_t launch(const Request& q) {
     a.prm.hist_offsets = p->hist_offsets;
     a.prm.hist_ids = p->hist_ids;
     a.prm.hist_len = p->hist_len;
+  }
+  if (q.params) {
+    const albireo_params_t* p = q.params;
+    a.prompt_offsets = p->prompt_offsets;
+    a.prompt_ids = p->prompt_ids;
+    a.prompt_len = p->prompt_len;
+    if (p->state) {
+      a.st_ids = p->state->ids;
+      a.st_counts = p->state->counts;
+      a.st_len = p->state->len;
+      a.st_flags = p->state->flags;
+      a.st_cap = p->state->cap;
+    }
   }
   a.uniforms = q.uniforms;
   a.out_ids = q.out_ids;

@@ -29,6 +29,7 @@ def alb():
 
 def test_header_declares_the_entry_points():
     assert _declared() == sorted(["albireo_apply_penalties", "albireo_backfill", "albireo_philox_uniforms",
+                                  "albireo_penalty_state_append", "albireo_penalty_state_init",
                                   "albireo_sample", "albireo_sample_sharded", "albireo_sample_step",
                                   "albireo_status_string",
                                   "albireo_topk_topp", "albireo_workspace_size"])

@@ -5,6 +5,7 @@ oracle (``oracle/``) and the GPU path (``paper_2606_01927_amd``) can consume the
 sharing any code of the method itself.
 """
 from .configs import (  # noqa: F401
+    add_prompt,
     CONFIGS,
     Workload,
     generate,

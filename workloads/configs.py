@@ -201,3 +201,15 @@ def generate(cfg: int, B: Optional[int] = None, V: Optional[int] = None, variant
         full[:, :V] = data
         data = full
     return Workload(name=c["name"], B=B, V=V, dtype=dtype, ld=ld, logits=data, uniforms=u, n_top=n_top, **kw)
+
+
+def add_prompt(w: Workload, P: int, seed: int = 0, s: float = 1.2) -> Workload:
+    """Give every row of ``w`` a prompt history of ``P`` ids, ranks drawn with probability proportional
+    to ``r**-s`` over a seeded permutation of the vocabulary; ``w``'s own history becomes the output
+    history (the split of the repetition penalty from the frequency and presence penalties)."""
+    rng = np.random.default_rng(np.random.SeedSequence(20269000 + seed))
+    perm = rng.permutation(w.V)
+    offs, ids = _zipf_hist(rng, perm, w.B, P, w.V, s)
+    w.prompt_offsets, w.prompt_ids = offs, ids
+    return w
+

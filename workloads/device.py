@@ -36,6 +36,8 @@ def to_device(w, device="cuda", row_offset_bytes: int = 0):
         repetition_penalty=t(w.repetition_penalty, torch.float32),
         frequency_penalty=t(w.frequency_penalty, torch.float32),
         presence_penalty=t(w.presence_penalty, torch.float32),
-        hist_offsets=t(w.hist_offsets, torch.int64), hist_ids=t(w.hist_ids, torch.int32))
+        hist_offsets=t(w.hist_offsets, torch.int64), hist_ids=t(w.hist_ids, torch.int32),
+        prompt_offsets=t(getattr(w, "prompt_offsets", None), torch.int64),
+        prompt_ids=t(getattr(w, "prompt_ids", None), torch.int32))
     u = t(w.uniforms, torch.float32)
     return logits, u, p
