@@ -100,7 +100,8 @@ struct SArgs {
   uint32_t* ctr;     // [B] arrival counters (zero between calls)
   ChunkPub* pub;     // [B * P]
   uint64_t* lists;   // [B * P * LCAPC]
-  float* dense;      // [B * V]
+  float* dense;      // [B * Vp]
+  int64_t Vp;        // dense row stride: V rounded up to 4 (16-byte rows)
 };
 
 struct SRow {
@@ -489,22 +490,49 @@ __device__ __forceinline__ int count_above(const uint64_t* arr, int n, uint64_t 
   return r;
 }
 
-// Iterate over the values of chunk c's view: its dense processed row, or its candidate list.
+// Iterate over the values of chunk c's view: its dense processed row, or its candidate list.  Plain
+// loads: the general path reads the views only after an agent-scope acquire (see gp_acquire), and
+// every view was written with agent-scope stores completed before the writer's arrival.  The dense row
+// (16-byte aligned, stride Vp) goes in 16-byte loads, eight per thread in flight.
 template <class F>
 __device__ __forceinline__ void for_view(const SArgs& a, const SRow& R, const SSm& s, int c, int vec, F&& f) {
   const ChunkPub& pc = s.m.pub[c];
   if (pc.flags & PUB_DENSE) {
-    const float* drow = a.dense + R.row * a.V;
+    const float* drow = a.dense + R.row * a.Vp;
     const int lo = chunk_lo(a, R, c, vec), hi = chunk_hi(a, R, c, vec);
-    for (int p = lo + (int)threadIdx.x; p < hi; p += CT) f(ld_agent(drow + p), p);
+    const int g0 = lo >> 2, g1 = (hi + 3) >> 2;
+    const float4* d4 = reinterpret_cast<const float4*>(drow);
+    constexpr int U = 8;  // 16-byte loads in flight per thread
+    for (int g = g0 + (int)threadIdx.x; g < g1; g += U * CT) {
+      float4 v[U];
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+        const int gq = g + q * CT;
+        v[q] = gq < g1 ? d4[gq] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+        const int p0 = (g + q * CT) * 4;
+        if (g + q * CT < g1) {
+          if (p0 >= lo && p0 < hi) f(v[q].x, p0);
+          if (p0 + 1 >= lo && p0 + 1 < hi) f(v[q].y, p0 + 1);
+          if (p0 + 2 >= lo && p0 + 2 < hi) f(v[q].z, p0 + 2);
+          if (p0 + 3 >= lo && p0 + 3 < hi) f(v[q].w, p0 + 3);
+        }
+      }
+    }
   } else {
     const uint64_t* lst = a.lists + (R.row * R.P + c) * (int64_t)LCAPC;
     for (int i = (int)threadIdx.x; i < pc.n_list; i += CT) {
-      const uint64_t key = ld_agent(lst + i);
+      const uint64_t key = lst[i];
       f(cand_z(key), cand_pos(key));
     }
   }
 }
+
+// Before the general path reads the chunks' views with plain loads: no line of this XCD's caches may
+// hold an older copy of them.
+__device__ __forceinline__ void gp_acquire() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
 
 // General path, radix selection by count: the order key of the K-th largest finite value (counting
 // duplicates), or 0 when there are fewer than K.
@@ -552,10 +580,12 @@ __device__ __forceinline__ uint32_t gp_kth_key(const SArgs& a, const SRow& R, SS
 }
 
 // General path, radix selection by mass: the order key of the nucleus' closing group among the values
-// z >= tau2 (the first group, in descending order, at which the cumulative mass reaches target), or 0
-// when the cumulative mass never reaches it.
+// z >= tau2 (the first group, in descending order, at which the cumulative mass reaches p times the
+// mass of all of them), or 0 when the cumulative mass never reaches it.  The first level's histogram
+// also gives that total.
 __device__ __forceinline__ uint32_t gp_topp_key(const SArgs& a, const SRow& R, SSm& s, int vec, float tau2, float m,
-                                double target) {
+                                                double p) {
+  double target = 0.0;
   uint64_t* hm = s.m.key;  // 256 masses
   uint32_t prefix = 0, pmask = 0;
   double above = 0.0;
@@ -583,6 +613,7 @@ __device__ __forceinline__ uint32_t gp_topp_key(const SArgs& a, const SRow& R, S
       incl += dpp_mov64<DPP_ROW_BCAST15, 0xa>(incl);
       incl += dpp_mov64<DPP_ROW_BCAST31, 0xc>(incl);
       const uint64_t excl = incl - sum;
+      if (shift == 24) target = p * (double)lane_u64(incl, 63);  // p times the mass of every z >= tau2
       const uint64_t hit = __ballot(above + (double)incl >= target);
       if (hit == 0) {
         if (l == 0) s.bc_i[0] = -1;
@@ -641,13 +672,13 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
     const ChunkPub& pc = s.m.pub[cs];
     if (pc.flags & PUB_DENSE) {
       // thread-contiguous ranges of the chunk, one exclusive scan, then the crossing thread walks
-      const float* drow = a.dense + R.row * a.V;
+      const float* drow = a.dense + R.row * a.Vp;
       const int lo = chunk_lo(a, R, cs, vec), hi = chunk_hi(a, R, cs, vec);
       const int per = (hi - lo + CT - 1) / CT;
       const int p0 = lo + (int)threadIdx.x * per, p1 = min(p0 + per, hi);
       uint64_t mine = 0;
       for (int p = p0; p < p1; ++p) {
-        const float z = ld_agent(drow + p);
+        const float z = drow[p];
         if (z > -INFINITY && z >= tau) mine += mass_of(z, m);
       }
       uint64_t tot;
@@ -655,7 +686,7 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
       int found = 0x7fffffff;
       if ((double)(cum + mine) > target) {
         for (int p = p0; p < p1; ++p) {
-          const float z = ld_agent(drow + p);
+          const float z = drow[p];
           if (z > -INFINITY && z >= tau) {
             cum += mass_of(z, m);
             if ((double)cum > target) { found = p; break; }
@@ -670,7 +701,7 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
       const uint64_t* lst = a.lists + (R.row * P + cs) * (int64_t)LCAPC;
       const int n = pc.n_list;
       uint64_t* lk = s.m.key + MAXPC;
-      for (int i = threadIdx.x; i < n; i += CT) lk[i] = ld_agent(lst + i);
+      for (int i = threadIdx.x; i < n; i += CT) lk[i] = lst[i];
       __syncthreads();
       int found = 0x7fffffff;
       for (int i = threadIdx.x; i < n; i += CT) {
@@ -906,6 +937,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       zid = s.bc_f[2];
     } else {
       // ---- general path over the chunk views ----
+      gp_acquire();
       float tau_k = -INFINITY;
       if (R.kon) {
         const uint32_t kk = gp_kth_key(a, R, s, VEC, R.k);
@@ -914,17 +946,10 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       const float tau2 = fmaxf(tau_k, tau_m);
       float tau = tau2;
       if (R.topp_on) {
-        uint64_t z2 = 0;
-        for (int c = 0; c < P; ++c)
-          for_view(a, R, s, c, VEC, [&](float z, int) {
-            if (z > -INFINITY && z >= tau2) z2 += mass_of(z, m);
-          });
-        z2 = blk_sum_u64(z2, s);
-        const double target = (double)R.p * (double)z2;
-        if (!(target > 0.0)) {
+        if (!(R.p > 0.0f)) {
           tau = m;  // p <= 0: the top group only
         } else {
-          const uint32_t kk = gp_topp_key(a, R, s, VEC, tau2, m, target);
+          const uint32_t kk = gp_topp_key(a, R, s, VEC, tau2, m, (double)R.p);
           if (kk) tau = fmaxf(tau2, key2f(kk));
         }
       }
@@ -938,7 +963,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       const int n = s.m.pub[c].n_list;
       for (int i = t; i < n; i += CT) st_agent(lbase + (int64_t)c * LCAPC + i, (uint64_t)0);
       if (s.m.pub[c].flags & PUB_DENSE) {
-        float* drow = a.dense + row * a.V;
+        float* drow = a.dense + row * a.Vp;
         const int lo = chunk_lo(a, R, c, VEC), hi = chunk_hi(a, R, c, VEC);
         for (int p = lo + t; p < hi; p += CT) st_agent(drow + p, 0.0f);
       }
@@ -1400,7 +1425,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
   // ---- rows without a small kept set: the processed values of the whole chunk ----
   const bool dense = want_dense || (s2b && overflow);
   if (dense) {
-    float* drow = a.dense + row * a.V;
+    float* drow = a.dense + row * a.Vp;
     static_for<CJ>([&](auto J) {
       constexpr int j = decltype(J)::value;
       const int64_t slot = R.s0 + (int64_t)j * CT + t;
@@ -1485,7 +1510,7 @@ WsParts ws_parts(int64_t B, int64_t V, int P) {
   w.pub = align256(w.ctr + B * 4);
   w.lists = align256(w.pub + B * P * (int64_t)sizeof(ChunkPub));
   w.dense = align256(w.lists + B * P * (int64_t)LCAPC * 8);
-  w.total = align256(w.dense + B * V * 4);
+  w.total = align256(w.dense + B * ((V + 3) & ~int64_t(3)) * 4);
   return w;
 }
 
@@ -1570,6 +1595,7 @@ albireo_status_t launch(const Request& q) {
   a.pub = reinterpret_cast<ChunkPub*>(q.ws + w.pub);
   a.lists = reinterpret_cast<uint64_t*>(q.ws + w.lists);
   a.dense = reinterpret_cast<float*>(q.ws + w.dense);
+  a.Vp = (q.V + 3) & ~int64_t(3);
   void* args[] = {&a};
   const void* fn;
   if (q.dtype == ALBIREO_BF16)
