@@ -101,7 +101,7 @@ struct SArgs {
   ChunkPub* pub;     // [B * P]
   uint64_t* lists;   // [B * P * LCAPC]
   float* dense;      // [B * Vp]
-  int64_t Vp;        // dense row stride: V rounded up to 4 (16-byte rows)
+  int64_t Vp;        // dense row stride: V rounded up to 16 (64-byte rows)
 };
 
 struct SRow {
@@ -443,7 +443,7 @@ struct Spec {
 // registers (sp.on) or from the lists themselves.  The order is arbitrary (ranks are counted).  For the
 // check of ties cut off at imax, s.m.cut[c] gets 1 (and s.m.cnt[c] the value's bits) when chunk c's
 // list goes on past imax and its entry imax - 1 passes.  Returns the count, or -1 above cap.
-__device__ int stage_entries(const SArgs& a, const SRow& R, SSm& s, const Spec& sp, float zthr, int imax, int cap) {
+__device__ __forceinline__ int stage_entries(const SArgs& a, const SRow& R, SSm& s, const Spec& sp, float zthr, int imax, int cap) {
   const int P = R.P, t = threadIdx.x;
   if (t == 0) s.bc_i[2] = 0;
   if (t < P) s.m.cut[t] = 0;
@@ -493,7 +493,7 @@ __device__ __forceinline__ int count_above(const uint64_t* arr, int n, uint64_t 
 // Iterate over the values of chunk c's view: its dense processed row, or its candidate list.  Plain
 // loads: the general path reads the views only after an agent-scope acquire (see gp_acquire), and
 // every view was written with agent-scope stores completed before the writer's arrival.  The dense row
-// (16-byte aligned, stride Vp) goes in 16-byte loads, eight per thread in flight.
+// (64-byte aligned, stride Vp) goes in 16-byte loads, eight per thread in flight.
 template <class F>
 __device__ __forceinline__ void for_view(const SArgs& a, const SRow& R, const SSm& s, int c, int vec, F&& f) {
   const ChunkPub& pc = s.m.pub[c];
@@ -534,22 +534,42 @@ __device__ __forceinline__ void for_view(const SArgs& a, const SRow& R, const SS
 // hold an older copy of them.
 __device__ __forceinline__ void gp_acquire() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
 
-// General path, radix selection by count: the order key of the K-th largest finite value (counting
-// duplicates), or 0 when there are fewer than K.
-__device__ __forceinline__ uint32_t gp_kth_key(const SArgs& a, const SRow& R, SSm& s, int vec, int K) {
-  uint32_t* hc = reinterpret_cast<uint32_t*>(s.m.key);
+// The general path visits the kept values of the row in one of two ways: every chunk view (a pass over
+// the row), or the order keys staged in LDS by gp_gather.  Either way the visitor calls f(z) once per
+// value.
+struct ViewSrc {
+  const SArgs& a;
+  const SRow& R;
+  const SSm& s;
+  int vec;
+  template <class F>
+  __device__ __forceinline__ void operator()(F&& f) const {
+    for (int c = 0; c < R.P; ++c) for_view(a, R, s, c, vec, [&](float z, int) __attribute__((always_inline)) { f(z); });
+  }
+};
+struct StagedSrc {
+  const uint32_t* keys;
+  int n;
+  template <class F>
+  __device__ __forceinline__ void operator()(F&& f) const {
+    for (int i = (int)threadIdx.x; i < n; i += CT) f(key2f(keys[i]));
+  }
+};
+
+// General path, radix selection by count: the order key of the remaining-th largest finite value
+// (counting duplicates) among those the source visits, or 0 when there are fewer.  hc: 256 LDS words.
+template <class Src>
+__device__ __forceinline__ uint32_t gp_kth_key(const Src& src, SSm& s, uint32_t* hc, int remaining) {
   uint32_t prefix = 0, pmask = 0;
-  int remaining = K;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = threadIdx.x; b < 256; b += CT) hc[b] = 0;
     __syncthreads();
-    for (int c = 0; c < R.P; ++c)
-      for_view(a, R, s, c, vec, [&](float z, int) {
-        if (z > -INFINITY && z == z) {
-          const uint32_t kk = f2key(z);
-          if ((kk & pmask) == prefix) atomicAdd(&hc[(kk >> shift) & 255u], 1u);
-        }
-      });
+    src([&](float z) __attribute__((always_inline)) {
+      if (z > -INFINITY && z == z) {
+        const uint32_t kk = f2key(z);
+        if ((kk & pmask) == prefix) atomicAdd(&hc[(kk >> shift) & 255u], 1u);
+      }
+    });
     __syncthreads();
     if (threadIdx.x < 64) {
       const int l = threadIdx.x;  // lane l holds buckets 255 - 4l .. 252 - 4l (descending)
@@ -579,27 +599,25 @@ __device__ __forceinline__ uint32_t gp_kth_key(const SArgs& a, const SRow& R, SS
   return prefix;
 }
 
-// General path, radix selection by mass: the order key of the nucleus' closing group among the values
-// z >= tau2 (the first group, in descending order, at which the cumulative mass reaches p times the
-// mass of all of them), or 0 when the cumulative mass never reaches it.  The first level's histogram
-// also gives that total.
-__device__ __forceinline__ uint32_t gp_topp_key(const SArgs& a, const SRow& R, SSm& s, int vec, float tau2, float m,
-                                                double p) {
-  double target = 0.0;
-  uint64_t* hm = s.m.key;  // 256 masses
+// General path, radix selection by mass: the order key of the closing group among the values
+// z >= tau2 that the source visits, walking them in descending order from a cumulative mass of
+// `above` (the mass of every kept value above them): the first group at which the cumulative
+// reaches `target`, or 0 when it never does.  hm: 256 LDS words of 64 bits.
+template <class Src>
+__device__ __forceinline__ uint32_t gp_topp_key(const Src& src, SSm& s, uint64_t* hm, float tau2, float m,
+                                                double target, double above) {
   uint32_t prefix = 0, pmask = 0;
-  double above = 0.0;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = threadIdx.x; b < 256; b += CT) hm[b] = 0;
     __syncthreads();
-    for (int c = 0; c < R.P; ++c)
-      for_view(a, R, s, c, vec, [&](float z, int) {
-        if (z > -INFINITY && z >= tau2) {
-          const uint32_t kk = f2key(z);
-          if ((kk & pmask) == prefix) atomicAdd(reinterpret_cast<unsigned long long*>(&hm[(kk >> shift) & 255u]),
-                                                (unsigned long long)mass_of(z, m));
-        }
-      });
+    src([&](float z) __attribute__((always_inline)) {
+      if (z > -INFINITY && z >= tau2) {
+        const uint32_t kk = f2key(z);
+        if ((kk & pmask) == prefix)
+          atomicAdd(reinterpret_cast<unsigned long long*>(&hm[(kk >> shift) & 255u]),
+                    (unsigned long long)mass_of(z, m));
+      }
+    });
     __syncthreads();
     if (threadIdx.x < 64) {
       const int l = threadIdx.x;
@@ -613,7 +631,6 @@ __device__ __forceinline__ uint32_t gp_topp_key(const SArgs& a, const SRow& R, S
       incl += dpp_mov64<DPP_ROW_BCAST15, 0xa>(incl);
       incl += dpp_mov64<DPP_ROW_BCAST31, 0xc>(incl);
       const uint64_t excl = incl - sum;
-      if (shift == 24) target = p * (double)lane_u64(incl, 63);  // p times the mass of every z >= tau2
       const uint64_t hit = __ballot(above + (double)incl >= target);
       if (hit == 0) {
         if (l == 0) s.bc_i[0] = -1;
@@ -634,6 +651,115 @@ __device__ __forceinline__ uint32_t gp_topp_key(const SArgs& a, const SRow& R, S
     __syncthreads();
   }
   return prefix;
+}
+
+// First level of the general path's selections: buckets of the distance d = m - z from the row
+// maximum, GD_SCALE per unit.  fl(m - z) and its product with GD_SCALE are monotone in z, so a value
+// in a lower bucket is larger than every value in a higher one, and equal values share a bucket;
+// masses (2^32 units) vanish from d = 32 ln 2 on, inside the last bucket.
+constexpr int GDB = 2048;
+constexpr float GD_SCALE = 64.0f;
+constexpr int GKCAP = 3072;  // boundary-bucket keys staged in LDS (u32), then a 256-entry histogram
+static_assert(GDB <= MSTAGE && GKCAP / 2 + 256 <= MSTAGE, "general-path staging exceeds the merge area");
+
+__device__ __forceinline__ int gp_dbucket(float z, float m) {
+  const float d = __fmul_rn(__fsub_rn(m, z), GD_SCALE);
+  return d < (float)(GDB - 1) ? (int)d : GDB - 1;
+}
+
+// One pass over the views: per distance bucket, the number (MASS false) or the fixed-point mass (MASS
+// true) of the finite values z >= lo.  Then the first bucket, from the top, at which the cumulative
+// reaches the target -- K for the count, p times the total for the mass -- with the cumulative of the
+// buckets before it.  Returns false when the target is never reached.
+template <bool MASS>
+__device__ __forceinline__ bool gp_level1(const SArgs& a, const SRow& R, SSm& s, int vec, float lo, float m,
+                                          double tgt, int& bb, uint64_t& before, uint64_t& total) {
+  uint64_t* h64 = s.m.key;
+  uint32_t* h32 = reinterpret_cast<uint32_t*>(s.m.key);
+  for (int b = threadIdx.x; b < GDB; b += CT) {
+    if (MASS) h64[b] = 0;
+    else h32[b] = 0;
+  }
+  __syncthreads();
+  ViewSrc{a, R, s, vec}([&](float z) __attribute__((always_inline)) {
+    if (z > -INFINITY && z >= lo) {
+      const int b = gp_dbucket(z, m);
+      if (MASS) atomicAdd(reinterpret_cast<unsigned long long*>(&h64[b]), (unsigned long long)mass_of(z, m));
+      else atomicAdd(&h32[b], 1u);
+    }
+  });
+  __syncthreads();
+  constexpr int BPT = GDB / CT;  // consecutive buckets per thread
+  auto hv = [&](int b) __attribute__((always_inline)) -> uint64_t { return MASS ? h64[b] : (uint64_t)h32[b]; };
+  const int b0 = (int)threadIdx.x * BPT;
+  uint64_t sum = 0;
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) sum += hv(b0 + q);
+  uint64_t tot;
+  const uint64_t excl = blk_excl_scan_u64(sum, s, &tot);
+  total = tot;
+  const double target = MASS ? tgt * (double)tot : tgt;
+  int mine = 0x7fffffff;
+  if ((double)excl < target && (double)(excl + sum) >= target) {  // at most one thread
+    uint64_t cum = excl;
+    int b = b0;
+    while (b < b0 + BPT - 1 && (double)(cum + hv(b)) < target) cum += hv(b++);
+    mine = b;
+    s.bc_q[1] = cum;
+  }
+  bb = blk_min_i(mine, s);
+  before = s.bc_q[1];
+  __syncthreads();
+  return bb != 0x7fffffff;
+}
+
+// Pass two: the order keys of the finite values z >= lo of distance bucket bb, staged in LDS.  Returns
+// their number, or -1 when they do not fit.
+__device__ __forceinline__ int gp_gather(const SArgs& a, const SRow& R, SSm& s, int vec, float lo, float m, int bb) {
+  uint32_t* keys = reinterpret_cast<uint32_t*>(s.m.key);
+  if (threadIdx.x == 0) s.bc_i[2] = 0;
+  __syncthreads();
+  ViewSrc{a, R, s, vec}([&](float z) __attribute__((always_inline)) {
+    if (z > -INFINITY && z >= lo && gp_dbucket(z, m) == bb) {
+      const int i = atomicAdd(&s.bc_i[2], 1);
+      if (i < GKCAP) keys[i] = f2key(z);
+    }
+  });
+  __syncthreads();
+  const int n = s.bc_i[2];
+  __syncthreads();
+  return n <= GKCAP ? n : -1;
+}
+
+// General path: the order key of the K-th largest finite value (counting duplicates), or 0 when there
+// are fewer than K: a count over the distance buckets, then the exact selection among the values of
+// the bucket holding it (over every view only when that bucket does not fit in LDS).
+__device__ __forceinline__ uint32_t gp_kth(const SArgs& a, const SRow& R, SSm& s, int vec, float m, int K) {
+  int bb;
+  uint64_t before, total;
+  if (!gp_level1<false>(a, R, s, vec, -INFINITY, m, (double)K, bb, before, total)) return 0u;
+  const int n = gp_gather(a, R, s, vec, -INFINITY, m, bb);
+  if (n >= 0)
+    return gp_kth_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.m.key), n}, s,
+                      reinterpret_cast<uint32_t*>(s.m.key + GKCAP / 2), K - (int)before);
+  return gp_kth_key(ViewSrc{a, R, s, vec}, s, reinterpret_cast<uint32_t*>(s.m.key), K);
+}
+
+// General path: the order key of the nucleus' closing group among the values z >= tau2 (the first
+// group, in descending order, at which the cumulative mass reaches p times the mass of all of them),
+// or 0 when the cumulative never reaches it: a mass over the distance buckets, then the exact
+// selection inside the bucket where the cumulative crosses.
+__device__ __forceinline__ uint32_t gp_topp(const SArgs& a, const SRow& R, SSm& s, int vec, float tau2, float m,
+                                            double p) {
+  int bb;
+  uint64_t before, total;
+  if (!gp_level1<true>(a, R, s, vec, tau2, m, p, bb, before, total)) return 0u;
+  const double target = p * (double)total;
+  const int n = gp_gather(a, R, s, vec, tau2, m, bb);
+  if (n >= 0)
+    return gp_topp_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.m.key), n}, s, s.m.key + GKCAP / 2, tau2, m,
+                       target, (double)before);
+  return gp_topp_key(ViewSrc{a, R, s, vec}, s, s.m.key, tau2, m, target, 0.0);
 }
 
 // General path: kept set S = {finite z >= tau}; draws the token with target u * Z_S in ascending id.
@@ -671,25 +797,50 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
   if (cs >= 0) {
     const ChunkPub& pc = s.m.pub[cs];
     if (pc.flags & PUB_DENSE) {
-      // thread-contiguous ranges of the chunk, one exclusive scan, then the crossing thread walks
+      // the chunk in groups of 16 positions (aligned in the row): each group's kept mass from four
+      // 16-byte loads, an exclusive scan over the groups in position order, then the crossing group
+      // walked by the thread that holds it
       const float* drow = a.dense + R.row * a.Vp;
       const int lo = chunk_lo(a, R, cs, vec), hi = chunk_hi(a, R, cs, vec);
-      const int per = (hi - lo + CT - 1) / CT;
-      const int p0 = lo + (int)threadIdx.x * per, p1 = min(p0 + per, hi);
-      uint64_t mine = 0;
-      for (int p = p0; p < p1; ++p) {
-        const float z = drow[p];
-        if (z > -INFINITY && z >= tau) mine += mass_of(z, m);
+      const int gf = lo >> 4, ng = ((hi - 1) >> 4) - gf + 1;
+      uint64_t* gm = s.m.key + MAXPC;  // per-group mass
+      const float4* d4 = reinterpret_cast<const float4*>(drow);
+      auto kept_mass = [&](float z, int p) __attribute__((always_inline)) -> uint64_t {
+        return (p >= lo && p < hi && z > -INFINITY && z >= tau) ? mass_of(z, m) : 0ull;
+      };
+      for (int g = (int)threadIdx.x; g < ng; g += CT) {
+        const int p0 = (gf + g) << 4;
+        float4 v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = d4[(p0 >> 2) + q];
+        uint64_t w = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          w += kept_mass(v[q].x, p0 + 4 * q);
+          w += kept_mass(v[q].y, p0 + 4 * q + 1);
+          w += kept_mass(v[q].z, p0 + 4 * q + 2);
+          w += kept_mass(v[q].w, p0 + 4 * q + 3);
+        }
+        gm[g] = w;
       }
+      __syncthreads();
+      const int per = (ng + CT - 1) / CT;  // consecutive groups per thread in the scan
+      const int g0 = (int)threadIdx.x * per, g1 = min(g0 + per, ng);
+      uint64_t mine = 0;
+      for (int g = g0; g < g1; ++g) mine += gm[g];
       uint64_t tot;
       uint64_t cum = before + blk_excl_scan_u64(mine, s, &tot);
       int found = 0x7fffffff;
       if ((double)(cum + mine) > target) {
-        for (int p = p0; p < p1; ++p) {
-          const float z = drow[p];
-          if (z > -INFINITY && z >= tau) {
-            cum += mass_of(z, m);
-            if ((double)cum > target) { found = p; break; }
+        int g = g0;
+        while (g < g1 - 1 && (double)(cum + gm[g]) <= target) cum += gm[g++];
+        const int p0 = (gf + g) << 4;
+        for (int q = 0; q < 16; ++q) {
+          const float z = drow[p0 + q];
+          cum += kept_mass(z, p0 + q);
+          if ((double)cum > target) {
+            found = p0 + q;
+            break;
           }
         }
       }
@@ -727,9 +878,13 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
   __syncthreads();
   for (int c = 0; c < P; ++c) {
     if (id < chunk_lo(a, R, c, vec) || id >= chunk_hi(a, R, c, vec)) continue;
-    for_view(a, R, s, c, vec, [&](float z, int pos) {
-      if (pos == id) s.bc_f[0] = z;
-    });
+    if (s.m.pub[c].flags & PUB_DENSE) {
+      if (threadIdx.x == 0) s.bc_f[0] = a.dense[R.row * a.Vp + id];
+    } else {
+      for_view(a, R, s, c, vec, [&](float z, int pos) {
+        if (pos == id) s.bc_f[0] = z;
+      });
+    }
   }
   __syncthreads();
   *zid = s.bc_f[0];
@@ -940,7 +1095,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       gp_acquire();
       float tau_k = -INFINITY;
       if (R.kon) {
-        const uint32_t kk = gp_kth_key(a, R, s, VEC, R.k);
+        const uint32_t kk = gp_kth(a, R, s, VEC, m, R.k);
         tau_k = kk ? key2f(kk) : -INFINITY;
       }
       const float tau2 = fmaxf(tau_k, tau_m);
@@ -949,7 +1104,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
         if (!(R.p > 0.0f)) {
           tau = m;  // p <= 0: the top group only
         } else {
-          const uint32_t kk = gp_topp_key(a, R, s, VEC, tau2, m, (double)R.p);
+          const uint32_t kk = gp_topp(a, R, s, VEC, tau2, m, (double)R.p);
           if (kk) tau = fmaxf(tau2, key2f(kk));
         }
       }
@@ -1504,13 +1659,16 @@ SGeo geometry(int64_t B, int64_t V, albireo_dtype_t dtype) {
 struct WsParts {
   int64_t ctr, pub, lists, dense, total;
 };
+// Dense view row stride: V rounded up to 16 floats, so that the draw's aligned 16-position groups stay
+// inside the row.
+int64_t dense_stride(int64_t V) { return (V + 15) & ~int64_t(15); }
 WsParts ws_parts(int64_t B, int64_t V, int P) {
   WsParts w;
   w.ctr = 0;
   w.pub = align256(w.ctr + B * 4);
   w.lists = align256(w.pub + B * P * (int64_t)sizeof(ChunkPub));
   w.dense = align256(w.lists + B * P * (int64_t)LCAPC * 8);
-  w.total = align256(w.dense + B * ((V + 3) & ~int64_t(3)) * 4);
+  w.total = align256(w.dense + B * dense_stride(V) * 4);
   return w;
 }
 
@@ -1595,7 +1753,7 @@ albireo_status_t launch(const Request& q) {
   a.pub = reinterpret_cast<ChunkPub*>(q.ws + w.pub);
   a.lists = reinterpret_cast<uint64_t*>(q.ws + w.lists);
   a.dense = reinterpret_cast<float*>(q.ws + w.dense);
-  a.Vp = (q.V + 3) & ~int64_t(3);
+  a.Vp = dense_stride(q.V);
   void* args[] = {&a};
   const void* fn;
   if (q.dtype == ALBIREO_BF16)

@@ -170,6 +170,43 @@ def test_edge_cases(lib, oracle_mod):
     compare_sample(ref, out, n_top=7)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_general_path_wide_rows(dtype, lib, oracle_mod):
+    """Wide rows whose kept sets are too large for candidate lists: the selections over the whole row
+    (top-k above the list capacity, top-p without top-k), including rows whose boundary values are so
+    often tied that they do not fit in the on-chip staging and take the whole-row selection."""
+    rng = np.random.default_rng(11)
+    V = 100003
+    rows, K, Pp, MP = [], [], [], []
+
+    def add(x, k=0, p=1.0, mp=0.0):
+        rows.append(np.asarray(x, np.float32)); K.append(k); Pp.append(p); MP.append(mp)
+
+    base = rng.normal(0, 2, size=V).astype(np.float32)
+    add(base, k=2000, p=0.9)                      # count selection, then the nucleus
+    add(base, p=0.6)                              # nucleus alone
+    add(base, k=600)                              # top-k just above the list capacity
+    tied = base.copy(); tied[rng.random(V) < 0.5] = 1.5
+    add(tied, p=0.95)                             # ~50000 equal values around the boundary
+    add(tied, k=30000, p=0.99)                    # the K-th value among them
+    q = np.round(base * 16) / 16
+    add(q, p=0.8)                                 # coarse values: many ties in every bucket
+    add(rng.standard_t(3, size=V) * 2, p=0.98, mp=0.02)  # heavy tail with min-p
+    half = base.copy(); half[rng.random(V) < 0.5] = -np.inf
+    add(half, p=0.7, k=5000)                      # masked entries
+    x = np.stack(rows)
+    w = workloads.Workload(name="wide", B=len(rows), V=V, dtype=dtype, ld=V,
+                           logits=workloads.to_bf16_bits(x) if dtype == "bf16" else x,
+                           uniforms=np.linspace(0.07, 0.93, len(rows)).astype(np.float32),
+                           temperature=np.full(len(rows), 0.9, np.float32), top_k=np.array(K, np.int32),
+                           top_p=np.array(Pp, np.float32), min_p=np.array(MP, np.float32))
+    _say("wide rows", dtype)
+    out = _run(lib, w)
+    rep = compare_sample(oracle_mod.sample(w), out)
+    _say("  ", rep)
+    assert rep["band"] <= 1
+
+
 def test_penalty_edge_cases(lib, oracle_mod):
     rng = np.random.default_rng(6)
     V = 3001
