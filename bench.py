@@ -161,6 +161,50 @@ def step_extras(alb, w, copies, p, ws, stream, reps: int = 50) -> dict:
     return res
 
 
+def other_configs(alb, dev, reps: int = 20) -> dict:
+    """Per-call time of the sampling step on the four other workloads at their full sizes (HIP events
+    over back-to-back calls, logits rotated over copies of at least 512 MiB so that they come from
+    HBM), with the algorithmic bytes per call against the 8 TB/s peak."""
+    import torch
+
+    import workloads
+    from workloads.device import to_device
+
+    res = {}
+    stream = torch.cuda.current_stream()
+    for cfg in (1, 2, 4, 5):
+        w = workloads.generate(cfg)
+        logits0, u, p = to_device(w, device=dev)
+        nbytes = logits0.numel() * logits0.element_size()
+        ncopy = max(2, -(-(1 << 29) // nbytes))
+        copies = [logits0] + [logits0.clone() for _ in range(ncopy - 1)]
+        ws = alb.Workspace(dev)
+        outs = [torch.empty(w.B, dtype=torch.int32, device=dev), torch.empty(w.B, dtype=torch.float32, device=dev),
+                torch.empty((w.B, max(w.n_top, 1)), dtype=torch.int32, device=dev),
+                torch.empty((w.B, max(w.n_top, 1)), dtype=torch.float32, device=dev),
+                torch.empty(w.B, dtype=torch.int32, device=dev)]
+        call = alb.PreparedSample(logits0, u, p, w.n_top, w.V, outs, workspace=ws, stream=stream)
+        ptrs = [c.data_ptr() for c in copies]
+        for i in range(3):
+            call(ptrs[i % ncopy])
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(reps):
+            call(ptrs[i % ncopy])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        alg = algorithmic_bytes(w)
+        res[w.name] = {"us_per_call": us, "rows_per_s": w.B / (us * 1e-6), "algorithmic_bytes": alg,
+                       "hbm_gbs": alg / (us * 1e-6) / 1e9, "frac_of_peak": alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
+        print("config %d: %.1f us per call" % (cfg, us), file=sys.stderr, flush=True)
+        del copies, logits0, ws, call
+        torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -168,6 +212,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--config", type=int, default=3, help="workload index (3 is the headline one)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-call times of the other four workloads after the main loop")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the timing of the step extras (device uniforms, backfill) after the main loop")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -251,12 +297,15 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic() if args.config == 3 else None,
-                     "kernel": "k_sample (one launch per step)", "algorithmic_bytes": alg,
+                     "kernel": "%s (one launch per step)" % ("k_split" if args.config in (4, 5) else "k_sample"),
+                     "algorithmic_bytes": alg,
                      "launch_us_avg": launch_us, "host_wall_us_per_step": wall * 1e6 / args.steps},
         "wall_s": wall,
     }
     if not args.no_extras:
         res["step_extras"] = step_extras(alb, w, copies, p, ws, stream)
+    if not args.no_configs and args.config == 3:
+        res["other_configs"] = other_configs(alb, dev)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res))
