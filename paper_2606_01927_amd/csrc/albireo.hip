@@ -610,8 +610,12 @@ struct Resolution {
 // Re-read one body slot of the chunk from memory with the penalised entries masked to -inf (their
 // values are in the extras).  Used by the stages that run after the registers are released.
 template <class DT>
-__device__ __forceinline__ uint4 load_masked(const RowState& R, const Smem& s, int64_t slot) {
-  uint4 d = *reinterpret_cast<const uint4*>(R.rowp + slot_off<DT>(R, slot));
+__device__ __forceinline__ uint4 load_slot(const RowState& R, int64_t slot) {
+  return *reinterpret_cast<const uint4*>(R.rowp + slot_off<DT>(R, slot));
+}
+// The penalised elements of a body slot read from memory set to -inf (their values are extras).
+template <class DT>
+__device__ __forceinline__ uint4 mask_slot(const RowState& R, const Smem& s, int64_t slot, uint4 d) {
   if (R.pen_on) {
     const int sl = (int)(slot - R.s0);
     const uint32_t byte = (s.bitmap[sl >> 2] >> ((sl & 3) * 8)) & 255u;
@@ -623,15 +627,32 @@ __device__ __forceinline__ uint4 load_masked(const RowState& R, const Smem& s, i
   }
   return d;
 }
+template <class DT>
+__device__ __forceinline__ uint4 load_masked(const RowState& R, const Smem& s, int64_t slot) {
+  return mask_slot<DT>(R, s, slot, load_slot<DT>(R, slot));
+}
 
-// Iterate over the chunk's body elements re-read from memory.  BODY sees x and pos.
+// Iterate over the chunk's body elements re-read from memory.  BODY sees x and pos.  MEM_U slots per
+// thread are loaded before any is used (unconditional loads: a slot past the chunk reloads the first
+// of the group), so that one pass keeps MEM_U round trips in flight.
+constexpr int MEM_U = 4;
 #define FOR_MEM_ELEMS(R, S, BODY)                                                               \
-  for (int64_t slot_ = (R).s0 + threadIdx.x; slot_ < (R).s1; slot_ += NT) {                    \
-    const uint4 d_ = load_masked<DT>((R), (S), slot_);                                          \
-    _Pragma("unroll") for (int e_ = 0; e_ < DT::VEC; ++e_) {                                    \
-      const float x = DT::get(d_, e_);                                                          \
-      const int pos = (R).head + (int)slot_ * DT::VEC + e_;                                     \
-      BODY                                                                                      \
+  for (int64_t sb_ = (R).s0 + threadIdx.x; sb_ < (R).s1; sb_ += (int64_t)MEM_U * NT) {          \
+    uint4 dd_[MEM_U];                                                                           \
+    _Pragma("unroll") for (int u_ = 0; u_ < MEM_U; ++u_) {                                      \
+      const int64_t sl_ = sb_ + (int64_t)u_ * NT;                                               \
+      dd_[u_] = load_slot<DT>((R), sl_ < (R).s1 ? sl_ : sb_);                                   \
+    }                                                                                           \
+    _Pragma("unroll") for (int u_ = 0; u_ < MEM_U; ++u_) {                                      \
+      const int64_t slot_ = sb_ + (int64_t)u_ * NT;                                             \
+      if (slot_ < (R).s1) {                                                                     \
+        const uint4 d_ = mask_slot<DT>((R), (S), slot_, dd_[u_]);                               \
+        _Pragma("unroll") for (int e_ = 0; e_ < DT::VEC; ++e_) {                                \
+          const float x = DT::get(d_, e_);                                                      \
+          const int pos = (R).head + (int)slot_ * DT::VEC + e_;                                 \
+          BODY                                                                                  \
+        }                                                                                       \
+      }                                                                                         \
     }                                                                                           \
   }
 
@@ -813,6 +834,142 @@ __device__ bool radix_select(Smem& s, const RowState& R, const RowCtx& X, float 
     if (d < 0) return false;
     prefix |= (uint32_t)d << shift;
   }
+  out_key = prefix;
+  return true;
+}
+
+// Single-chunk rows: the selection radix_select makes (the key of the first group, in descending z,
+// at which the cumulative count or fixed-point mass of the finite z >= zlo reaches the target; a
+// negative target is that fraction of the total), with a first level over the distance from the row
+// maximum instead of the top byte of the order key, whose few buckets collect most values and
+// serialise the LDS atomics.  fl(m - z) scaled by SD_SCALE is monotone in z, so a lower bucket holds
+// only larger values and equal values share a bucket.  The bucket where the cumulative crosses is
+// staged in LDS and finished by the byte radix there, from the cumulative of the buckets above it; a
+// bucket too large to stage (or a target of 0) goes to radix_select.
+constexpr int SD_B = 2048;
+constexpr float SD_SCALE = 64.0f;
+constexpr int SD_CAP = 2 * LCAP;  // 32-bit keys in the 64-bit candidate list area
+static_assert(sizeof(Smem::scode) >= SD_B * sizeof(uint64_t) && SD_B % NT == 0, "distance histogram does not fit");
+
+__device__ __forceinline__ int dist_bucket(float z, float m) {
+  const float d = __fmul_rn(__fsub_rn(m, z), SD_SCALE);
+  return d < (float)(SD_B - 1) ? (int)d : SD_B - 1;
+}
+
+template <class DT>
+__device__ bool select_dist(Smem& s, const RowState& R, const RowCtx& X, float zlo, int wmode, double target,
+                            uint32_t& out_key) {
+  const float r = R.r, m = X.m;
+  uint64_t* h = reinterpret_cast<uint64_t*>(s.scode);
+  uint32_t* keys = reinterpret_cast<uint32_t*>(s.sk);
+  __syncthreads();
+  for (int b = threadIdx.x; b < SD_B; b += NT) h[b] = 0;
+  if (threadIdx.x == 0) {
+    s.bc_i[0] = -1;
+    s.bc_i[1] = 0;
+  }
+  __syncthreads();
+  auto weight = [&](float z) __attribute__((always_inline)) -> uint64_t {
+    return wmode ? fixmass(__expf(z - m)) : 1ull;
+  };
+  auto add = [&](float x) __attribute__((always_inline)) {
+    const float z = canon(x, r);
+    if (z > -INFINITY && z >= zlo)
+      atomicAdd((unsigned long long*)&h[dist_bucket(z, m)], (unsigned long long)weight(z));
+  };
+  FOR_MEM_ELEMS(R, s, { add(x); })
+  FOR_EXTRAS(s, X.n_ext, { add(x); })
+  __syncthreads();
+  // consecutive buckets per thread, an exclusive scan over the threads, the crossing bucket
+  constexpr int BPT = SD_B / NT;
+  const int b0 = (int)threadIdx.x * BPT;
+  uint64_t mine = 0;
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) mine += h[b0 + q];
+  uint64_t incl = mine;
+  incl += dpp_mov64<DPP_ROW_SHR + 1>(incl);
+  incl += dpp_mov64<DPP_ROW_SHR + 2>(incl);
+  incl += dpp_mov64<DPP_ROW_SHR + 4>(incl);
+  incl += dpp_mov64<DPP_ROW_SHR + 8>(incl);
+  incl += dpp_mov64<DPP_ROW_BCAST15, 0xa>(incl);
+  incl += dpp_mov64<DPP_ROW_BCAST31, 0xc>(incl);
+  if (lane_id() == 63) s.red_q[wave_id()] = incl;
+  __syncthreads();
+  uint64_t off = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const uint64_t tw = s.red_q[w];
+    off += w < wave_id() ? tw : 0ull;
+    total += tw;
+  }
+  const double tgt = target < 0 ? (double)total * (-target) : target;
+  if (!(tgt > 0.0)) return radix_select<DT>(s, R, X, zlo, wmode, target, out_key);  // uniform
+  const uint64_t excl = off + incl - mine;
+  if ((double)excl < tgt && (double)(excl + mine) >= tgt) {  // at most one thread
+    uint64_t cum = excl;
+    int b = b0;
+    while (b < b0 + BPT - 1 && (double)(cum + h[b]) < tgt) cum += h[b++];
+    s.bc_i[0] = b;
+    s.bc_q[0] = cum;
+  }
+  __syncthreads();
+  const int bb = s.bc_i[0];
+  uint64_t above = s.bc_q[0];
+  if (bb < 0) return false;  // the cumulative never reaches the target (uniform)
+  // the crossing bucket's keys into LDS
+  auto put = [&](float x) __attribute__((always_inline)) {
+    const float z = canon(x, r);
+    if (z > -INFINITY && z >= zlo && dist_bucket(z, m) == bb) {
+      const int i = atomicAdd(&s.bc_i[1], 1);
+      if (i < SD_CAP) keys[i] = f2key(z);
+    }
+  };
+  FOR_MEM_ELEMS(R, s, { put(x); })
+  FOR_EXTRAS(s, X.n_ext, { put(x); })
+  __syncthreads();
+  const int n = s.bc_i[1];
+  if (n > SD_CAP) return radix_select<DT>(s, R, X, zlo, wmode, target, out_key);  // uniform
+  // byte radix over the staged keys; a thread merges its equal buckets before the atomic
+  uint32_t prefix = 0;
+#pragma unroll 1
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    __syncthreads();
+    if (threadIdx.x < 256) s.hist[threadIdx.x] = 0;
+    __syncthreads();
+    const uint32_t hi_mask = (shift == 24) ? 0u : (0xffffffffu << (shift + 8));
+    uint32_t cb = 0xffffffffu;
+    uint64_t cw = 0;
+    for (int i = threadIdx.x; i < n; i += NT) {
+      const uint32_t kz = keys[i];
+      if ((kz & hi_mask) == (prefix & hi_mask)) {
+        const uint32_t b = (kz >> shift) & 255u;
+        if (b != cb) {
+          if (cw) atomicAdd((unsigned long long*)&s.hist[cb], (unsigned long long)cw);
+          cb = b;
+          cw = 0;
+        }
+        cw += weight(key2f(kz));
+      }
+    }
+    if (cw) atomicAdd((unsigned long long*)&s.hist[cb], (unsigned long long)cw);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint64_t cum = above;
+      int d = 255;
+      for (; d >= 0; --d) {
+        if ((double)(cum + s.hist[d]) >= tgt) break;
+        cum += s.hist[d];
+      }
+      s.bc_i[0] = d;
+      s.bc_q[0] = cum;
+    }
+    __syncthreads();
+    const int d = s.bc_i[0];
+    above = s.bc_q[0];
+    if (d < 0) return false;  // not reached: the bucket holds the crossing
+    prefix |= (uint32_t)d << shift;
+  }
+  __syncthreads();
   out_key = prefix;
   return true;
 }
@@ -1198,9 +1355,13 @@ __device__ __noinline__ Resolution resolve_general(const OutArgs a, Smem& s, con
   } else {
     float tau2 = X.tau_m;
     uint32_t kk = 0;
-    if (R.k_on && radix_select<DT>(s, R, X, -INFINITY, 0, (double)R.k, kk)) tau2 = fmaxf(tau2, key2f(kk));
+    auto select = [&](float zlo, int wmode, double target, uint32_t& key) -> bool {
+      return P == 1 ? select_dist<DT>(s, R, X, zlo, wmode, target, key)
+                    : radix_select<DT>(s, R, X, zlo, wmode, target, key);
+    };
+    if (R.k_on && select(-INFINITY, 0, (double)R.k, kk)) tau2 = fmaxf(tau2, key2f(kk));
     tau_star = tau2;
-    if (R.topp_on && radix_select<DT>(s, R, X, tau2, 1, -(double)R.p, kk)) tau_star = fmaxf(tau_star, key2f(kk));
+    if (R.topp_on && select(tau2, 1, -(double)R.p, kk)) tau_star = fmaxf(tau_star, key2f(kk));
   }
   // kept count, min z and fixed-point mass of S = {finite z >= tau_star}; greedy argmax position
   int kept = 0, best = INT32_MAX;
@@ -1232,51 +1393,74 @@ __device__ __noinline__ Resolution resolve_general(const OutArgs a, Smem& s, con
   const int64_t lo = R.owns_head ? 0 : (int64_t)R.head + R.s0 * DT::VEC;
   const int64_t hi = R.owns_tail ? (int64_t)R.V : (int64_t)R.head + R.s1 * DT::VEC;
   const bool draw = (a.mode == 0) && !R.greedy;
-  // 4 consecutive entries per thread per block.  An element's cumulative is
-  // run + (exclusive thread prefix + serial sum within the thread); the block total is the last
-  // thread's value of that expression, so a block whose total exceeds the target contains an element
-  // that does too.
+  // The region in groups of GS consecutive positions (GS = 16, doubled until the group weights fit
+  // the slot-code area, which is free once the candidates are gathered): every group's weight summed
+  // in position order, the group weights summed in order per thread over a contiguous run of groups,
+  // an exclusive scan over the threads, then the crossing thread walks its run and the crossing group.
+  // An element's cumulative is thus (thread prefix + earlier groups of its run + earlier elements of
+  // its group), the same expression for the search and for the totals.  Each element is loaded
+  // unconditionally (its extras value replaces it where it has one), so a group's loads are in
+  // flight together.
   float ctot = 0.f;
   int clast = -1;
-  auto scan_find = [&](float target) -> int {
-    float run = 0.f;
-    int found = -1;
-    int lastp = -1;
-    for (int64_t b0 = lo; b0 < hi; b0 += 4 * NT) {
-      float w4[4];
-      float ts = 0.f;
-      int lp = -1;
+  float* gw = reinterpret_cast<float*>(s.scode);
+  constexpr int GMAX = (int)(sizeof(s.scode) / sizeof(float));
+  int gsz = 16;
+  while ((hi - lo + gsz - 1) / gsz > GMAX) gsz *= 2;
+  const int ng = (int)((hi - lo + gsz - 1) / gsz);
+  auto elem_w = [&](int64_t i) __attribute__((always_inline)) -> float {
+    const int pos = (int)(i < hi ? i : lo);
+    const int u = n_ext > 0 ? extras_index<DT>(s, R, pos) : -1;
+    const float raw = load_pos<DT>(R, pos);
+    const float z = canon(u >= 0 ? s.x_val[u] : raw, r);
+    return (i < hi && z > -INFINITY && z >= tau_star) ? __expf(z - m) : 0.f;
+  };
+  auto group_w = [&](int g, int* lp) __attribute__((always_inline)) -> float {
+    const int64_t p0 = lo + (int64_t)g * gsz;
+    float w = 0.f;
+    for (int q0 = 0; q0 < gsz; q0 += 16) {
+      float wq[16];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t i = b0 + 4 * (int64_t)threadIdx.x + q;
-        float w = 0.f;
-        if (i < hi) {
-          const float z = canon(x_at<DT>(s, R, n_ext, (int)i), r);
-          w = (z > -INFINITY && z >= tau_star) ? __expf(z - m) : 0.f;
-        }
-        w4[q] = w;
-        ts += w;
-        if (w > 0.f) lp = (int)i;
-      }
-      float btot;
-      const float ex = block_excl_scan(ts, s, &btot);
-      lastp = max(lastp, block_max_i(lp, s));
-      if (found < 0 && run + btot > target) {
-        float cum = ex;
-        int f = INT32_MAX;
+      for (int q = 0; q < 16; ++q) wq[q] = elem_w(p0 + q0 + q);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          cum += w4[q];
-          if (f == INT32_MAX && run + cum > target) f = (int)(b0 + 4 * (int64_t)threadIdx.x + q);
-        }
-        f = block_min_i(f, s);
-        found = (f == INT32_MAX) ? -1 : f;
+      for (int q = 0; q < 16; ++q) {
+        w += wq[q];
+        if (wq[q] > 0.f) *lp = (int)(p0 + q0 + q);
       }
-      run += btot;
     }
-    ctot = run;
-    clast = lastp;
-    return found;
+    return w;
+  };
+  bool weights_done = false;
+  auto scan_find = [&](float target) -> int {
+    if (!weights_done) {
+      int lp = -1;
+      for (int g = threadIdx.x; g < ng; g += NT) gw[g] = group_w(g, &lp);
+      clast = block_max_i(lp, s);  // its barriers also publish gw
+      weights_done = true;
+    }
+    const int per = (ng + NT - 1) / NT;
+    const int g0 = (int)threadIdx.x * per, g1 = min(g0 + per, ng);
+    float mine = 0.f;
+    for (int g = g0; g < g1; ++g) mine += gw[g];
+    float btot;
+    float cum = block_excl_scan(mine, s, &btot);
+    ctot = btot;
+    int f = INT32_MAX;
+    if (cum + mine > target) {
+      int g = g0;
+      while (g < g1 - 1 && cum + gw[g] <= target) cum += gw[g++];
+      const int64_t p0 = lo + (int64_t)g * gsz;
+      for (int q = 0; q < gsz && p0 + q < hi; ++q) {
+        const float w = elem_w(p0 + q);
+        cum += w;
+        if (w > 0.f && cum > target) {  // a later thread that starts above the target takes its
+          f = (int)(p0 + q);            // first kept element: the minimum over threads decides
+          break;
+        }
+      }
+    }
+    f = block_min_i(f, s);
+    return f == INT32_MAX ? -1 : f;
   };
   if (draw) (void)scan_find(INFINITY);
   // per-chunk results, combined in chunk order (identical arithmetic in every chunk)
