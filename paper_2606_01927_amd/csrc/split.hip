@@ -490,25 +490,49 @@ __device__ __forceinline__ int count_above(const uint64_t* arr, int n, uint64_t 
   return r;
 }
 
-// Iterate over the values of chunk c's view: its dense processed row, or its candidate list.  Plain
-// loads: the general path reads the views only after an agent-scope acquire (see gp_acquire), and
-// every view was written with agent-scope stores completed before the writer's arrival.  The dense row
-// (64-byte aligned, stride Vp) goes in 16-byte loads, eight per thread in flight.
+// A row's dense view as a buffer resource (wave-uniform base, Vp floats), read with the agent-scope
+// load's cache policy (sc1): the views were written through other XCDs' L2 by agent-scope stores, and
+// these loads see them without any fence.
+constexpr int CPOL_SC1 = 16;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t dense_rsrc(const SArgs& a, int64_t row) {
+  const uint64_t b = reinterpret_cast<uint64_t>(a.dense + row * a.Vp);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(((uint64_t)hi << 32) | lo), (short)0,
+                                           __builtin_amdgcn_readfirstlane((int)(a.Vp * 4)), 0x00020000);
+}
+// floats 4 g .. 4 g + 3 of the view
+__device__ __forceinline__ float4 ld_dense4(__amdgpu_buffer_rsrc_t rs, int g) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, g * 16, 0, CPOL_SC1);
+  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+}
+__device__ __forceinline__ float ld_dense1(__amdgpu_buffer_rsrc_t rs, int p) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, p * 4, 0, CPOL_SC1));
+}
+// floats p .. p + 3 of the view (p a multiple of 4), with the agent-scope store's cache policy
+__device__ __forceinline__ void st_dense4(__amdgpu_buffer_rsrc_t rs, int p, float x, float y, float z, float w) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = {__float_as_uint(x), __float_as_uint(y), __float_as_uint(z), __float_as_uint(w)};
+  __builtin_amdgcn_raw_buffer_store_b128(v, rs, p * 4, 0, CPOL_SC1);
+}
+
+// Iterate over the values of chunk c's view: its dense processed row, or its candidate list.  Every view
+// was written with agent-scope stores completed before the writer's arrival; the dense row (64-byte
+// aligned, stride Vp) is read with 16-byte agent-scope loads, eight per thread in flight.
 template <class F>
 __device__ __forceinline__ void for_view(const SArgs& a, const SRow& R, const SSm& s, int c, int vec, F&& f) {
   const ChunkPub& pc = s.m.pub[c];
   if (pc.flags & PUB_DENSE) {
-    const float* drow = a.dense + R.row * a.Vp;
+    const __amdgpu_buffer_rsrc_t rs = dense_rsrc(a, R.row);
     const int lo = chunk_lo(a, R, c, vec), hi = chunk_hi(a, R, c, vec);
     const int g0 = lo >> 2, g1 = (hi + 3) >> 2;
-    const float4* d4 = reinterpret_cast<const float4*>(drow);
     constexpr int U = 8;  // 16-byte loads in flight per thread
     for (int g = g0 + (int)threadIdx.x; g < g1; g += U * CT) {
       float4 v[U];
 #pragma unroll
       for (int q = 0; q < U; ++q) {
         const int gq = g + q * CT;
-        v[q] = gq < g1 ? d4[gq] : make_float4(0.f, 0.f, 0.f, 0.f);
+        v[q] = ld_dense4(rs, gq < g1 ? gq : g);  // unconditional: past the chunk, a repeat ignored below
       }
 #pragma unroll
       for (int q = 0; q < U; ++q) {
@@ -524,15 +548,13 @@ __device__ __forceinline__ void for_view(const SArgs& a, const SRow& R, const SS
   } else {
     const uint64_t* lst = a.lists + (R.row * R.P + c) * (int64_t)LCAPC;
     for (int i = (int)threadIdx.x; i < pc.n_list; i += CT) {
-      const uint64_t key = lst[i];
+      const uint64_t key = ld_agent(lst + i);
       f(cand_z(key), cand_pos(key));
     }
   }
 }
 
-// Before the general path reads the chunks' views with plain loads: no line of this XCD's caches may
-// hold an older copy of them.
-__device__ __forceinline__ void gp_acquire() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+
 
 // The general path visits the kept values of the row in one of two ways: every chunk view (a pass over
 // the row), or the order keys staged in LDS by gp_gather.  Either way the visitor calls f(z) once per
@@ -800,11 +822,10 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
       // the chunk in groups of 16 positions (aligned in the row): each group's kept mass from four
       // 16-byte loads, an exclusive scan over the groups in position order, then the crossing group
       // walked by the thread that holds it
-      const float* drow = a.dense + R.row * a.Vp;
+      const __amdgpu_buffer_rsrc_t rs = dense_rsrc(a, R.row);
       const int lo = chunk_lo(a, R, cs, vec), hi = chunk_hi(a, R, cs, vec);
       const int gf = lo >> 4, ng = ((hi - 1) >> 4) - gf + 1;
       uint64_t* gm = s.m.key + MAXPC;  // per-group mass
-      const float4* d4 = reinterpret_cast<const float4*>(drow);
       auto kept_mass = [&](float z, int p) __attribute__((always_inline)) -> uint64_t {
         return (p >= lo && p < hi && z > -INFINITY && z >= tau) ? mass_of(z, m) : 0ull;
       };
@@ -812,7 +833,7 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
         const int p0 = (gf + g) << 4;
         float4 v[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = d4[(p0 >> 2) + q];
+        for (int q = 0; q < 4; ++q) v[q] = ld_dense4(rs, (p0 >> 2) + q);
         uint64_t w = 0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -836,7 +857,7 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
         while (g < g1 - 1 && (double)(cum + gm[g]) <= target) cum += gm[g++];
         const int p0 = (gf + g) << 4;
         for (int q = 0; q < 16; ++q) {
-          const float z = drow[p0 + q];
+          const float z = ld_dense1(rs, p0 + q);
           cum += kept_mass(z, p0 + q);
           if ((double)cum > target) {
             found = p0 + q;
@@ -852,7 +873,7 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
       const uint64_t* lst = a.lists + (R.row * P + cs) * (int64_t)LCAPC;
       const int n = pc.n_list;
       uint64_t* lk = s.m.key + MAXPC;
-      for (int i = threadIdx.x; i < n; i += CT) lk[i] = lst[i];
+      for (int i = threadIdx.x; i < n; i += CT) lk[i] = ld_agent(lst + i);
       __syncthreads();
       int found = 0x7fffffff;
       for (int i = threadIdx.x; i < n; i += CT) {
@@ -879,7 +900,7 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
   for (int c = 0; c < P; ++c) {
     if (id < chunk_lo(a, R, c, vec) || id >= chunk_hi(a, R, c, vec)) continue;
     if (s.m.pub[c].flags & PUB_DENSE) {
-      if (threadIdx.x == 0) s.bc_f[0] = a.dense[R.row * a.Vp + id];
+      if (threadIdx.x == 0) s.bc_f[0] = ld_agent(a.dense + R.row * a.Vp + id);
     } else {
       for_view(a, R, s, c, vec, [&](float z, int pos) {
         if (pos == id) s.bc_f[0] = z;
@@ -1092,7 +1113,6 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       zid = s.bc_f[2];
     } else {
       // ---- general path over the chunk views ----
-      gp_acquire();
       float tau_k = -INFINITY;
       if (R.kon) {
         const uint32_t kk = gp_kth(a, R, s, VEC, m, R.k);
@@ -1119,8 +1139,13 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       for (int i = t; i < n; i += CT) st_agent(lbase + (int64_t)c * LCAPC + i, (uint64_t)0);
       if (s.m.pub[c].flags & PUB_DENSE) {
         float* drow = a.dense + row * a.Vp;
+        const __amdgpu_buffer_rsrc_t drs = dense_rsrc(a, row);
         const int lo = chunk_lo(a, R, c, VEC), hi = chunk_hi(a, R, c, VEC);
-        for (int p = lo + t; p < hi; p += CT) st_agent(drow + p, 0.0f);
+        // the unaligned ends one by one, the 16-byte aligned middle four at a time
+        const int a0 = min((lo + 3) & ~3, hi), a1 = max(hi & ~3, a0);
+        for (int p = lo + t; p < a0; p += CT) st_agent(drow + p, 0.0f);
+        for (int p = a1 + t; p < hi; p += CT) st_agent(drow + p, 0.0f);
+        for (int p = a0 + 4 * t; p < a1; p += 4 * CT) st_dense4(drs, p, 0.f, 0.f, 0.f, 0.f);
       }
     }
     uint32_t* pw = reinterpret_cast<uint32_t*>(a.pub + row * P);
@@ -1581,6 +1606,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
   const bool dense = want_dense || (s2b && overflow);
   if (dense) {
     float* drow = a.dense + row * a.Vp;
+    const __amdgpu_buffer_rsrc_t drs = dense_rsrc(a, row);
     static_for<CJ>([&](auto J) {
       constexpr int j = decltype(J)::value;
       const int64_t slot = R.s0 + (int64_t)j * CT + t;
@@ -1596,9 +1622,17 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
             if ((int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u)) < XCAP) skip |= 1u << e;
           }
         }
+        const int p0 = R.head + (int)slot * VEC;
+        if (skip == 0 && (p0 & 3) == 0) {  // whole slot, 16-byte aligned: VEC / 4 wide stores
 #pragma unroll
-        for (int e = 0; e < VEC; ++e)
-          if (!((skip >> e) & 1u)) st_agent(drow + R.head + (int)slot * VEC + e, canon(elem<DT>(d[j], e), r));
+          for (int e = 0; e < VEC; e += 4)
+            st_dense4(drs, p0 + e, canon(elem<DT>(d[j], e), r), canon(elem<DT>(d[j], e + 1), r),
+                      canon(elem<DT>(d[j], e + 2), r), canon(elem<DT>(d[j], e + 3), r));
+        } else {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e)
+            if (!((skip >> e) & 1u)) st_agent(drow + p0 + e, canon(elem<DT>(d[j], e), r));
+        }
       }
     });
     for (int i = t; i < n_x; i += CT)
