@@ -784,26 +784,109 @@ __device__ __forceinline__ uint32_t gp_topp(const SArgs& a, const SRow& R, SSm& 
   return gp_topp_key(ViewSrc{a, R, s, vec}, s, s.m.key, tau2, m, target, 0.0);
 }
 
-// General path: kept set S = {finite z >= tau}; draws the token with target u * Z_S in ascending id.
-// Returns the id (z in *zid).
-__device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, int vec, float tau, float m, float u, float* zid) {
-  const int P = R.P;
-  uint64_t* cm = s.m.key;  // per chunk mass
-  for (int c = threadIdx.x; c < P; c += CT) cm[c] = 0;
+// LDS of the merge area (64-bit words) in the general path: per-chunk kept masses of the draw at
+// GD_CM; the fused nucleus stages (key, position) pairs below GKCAP2 and its radix histogram after.
+constexpr int GD_CM = MSTAGE - MAXPC;
+constexpr int GKCAP2 = 1536;
+static_assert(GKCAP2 + 256 <= GD_CM && MAXPC + (CSLOTS * 8) / 16 + 1 <= GD_CM, "general-path LDS areas overlap");
+
+struct StagedPairs {  // (order key << 32 | position) pairs
+  const uint64_t* ent;
+  int n;
+  template <class F>
+  __device__ __forceinline__ void operator()(F&& f) const {
+    for (int i = (int)threadIdx.x; i < n; i += CT) f(key2f((uint32_t)(ent[i] >> 32)));
+  }
+};
+
+__device__ __forceinline__ int chunk_of(const SArgs& a, const SRow& R, int vec, int pos) {
+  int c = 0;
+  while (c < R.P - 1 && pos >= chunk_hi(a, R, c, vec)) ++c;
+  return c;
+}
+
+// The nucleus cut among the values z >= tau2 (as gp_topp), with the draw's per-chunk kept masses taken
+// in the same passes: a value in a distance bucket above the crossing one is kept whatever the cut
+// inside that bucket, so its mass goes to its chunk during the gather; the crossing bucket's values are
+// staged with their positions and, once the cut is known, the kept ones join their chunks.  The sums are
+// integers, so the masses equal those of a separate pass.  Returns false (nothing decided) when the
+// cumulative never reaches the target or the bucket does not fit in LDS; the caller then selects and
+// draws the separate way.
+__device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm& s, int vec, float tau2, float m,
+                                              double p, float& tau, int& last) {
+  int bb;
+  uint64_t before, total;
+  if (!gp_level1<true>(a, R, s, vec, tau2, m, p, bb, before, total)) return false;
+  const double target = p * (double)total;
+  uint64_t* ent = s.m.key;
+  uint64_t* cm = s.m.key + GD_CM;
+  for (int c = threadIdx.x; c < R.P; c += CT) cm[c] = 0;
+  if (threadIdx.x == 0) s.bc_i[2] = 0;
   __syncthreads();
-  int last = -1;
-  for (int c = 0; c < P; ++c) {
+  int lastp = -1;
+  for (int c = 0; c < R.P; ++c) {
     uint64_t acc = 0;
-    for_view(a, R, s, c, vec, [&](float z, int pos) {
-      if (z > -INFINITY && z >= tau) {
-        const uint64_t w = mass_of(z, m);
-        acc += w;
-        if (w > 0) last = max(last, pos);
+    for_view(a, R, s, c, vec, [&](float z, int pos) __attribute__((always_inline)) {
+      if (z > -INFINITY && z >= tau2) {
+        const int b = gp_dbucket(z, m);
+        if (b < bb) {
+          const uint64_t w = mass_of(z, m);
+          acc += w;
+          if (w > 0) lastp = max(lastp, pos);
+        } else if (b == bb) {
+          const int i = atomicAdd(&s.bc_i[2], 1);
+          if (i < GKCAP2) ent[i] = ((uint64_t)f2key(z) << 32) | (uint32_t)pos;
+        }
       }
     });
-    atomicAdd(reinterpret_cast<unsigned long long*>(&cm[c]), (unsigned long long)acc);
+    if (acc) atomicAdd(reinterpret_cast<unsigned long long*>(&cm[c]), (unsigned long long)acc);
   }
-  last = blk_max_i(last, s);
+  __syncthreads();
+  const int n = s.bc_i[2];
+  __syncthreads();
+  if (n > GKCAP2) return false;
+  const uint32_t kk = gp_topp_key(StagedPairs{ent, n}, s, s.m.key + GKCAP2, tau2, m, target, (double)before);
+  if (!kk) return false;  // not reached inside the crossing bucket: cannot happen, decided the separate way
+  tau = fmaxf(tau2, key2f(kk));
+  for (int i = threadIdx.x; i < n; i += CT) {
+    const uint64_t e = ent[i];
+    const float z = key2f((uint32_t)(e >> 32));
+    if (z >= tau) {
+      const int pos = (int)(uint32_t)e;
+      const uint64_t w = mass_of(z, m);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&cm[chunk_of(a, R, vec, pos)]), (unsigned long long)w);
+      if (w > 0) lastp = max(lastp, pos);
+    }
+  }
+  last = blk_max_i(lastp, s);  // its barriers also publish cm
+  return true;
+}
+
+// General path: kept set S = {finite z >= tau}; draws the token with target u * Z_S in ascending id.
+// Returns the id (z in *zid).
+// masses_known: the per-chunk kept masses are already at GD_CM and `last` is the last position of
+// positive kept mass (the nucleus selection took them in its own pass).
+__device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, int vec, float tau, float m, float u,
+                                       float* zid, bool masses_known = false, int last = -1) {
+  const int P = R.P;
+  uint64_t* cm = s.m.key + GD_CM;  // per chunk mass
+  if (!masses_known) {
+    for (int c = threadIdx.x; c < P; c += CT) cm[c] = 0;
+    __syncthreads();
+    last = -1;
+    for (int c = 0; c < P; ++c) {
+      uint64_t acc = 0;
+      for_view(a, R, s, c, vec, [&](float z, int pos) {
+        if (z > -INFINITY && z >= tau) {
+          const uint64_t w = mass_of(z, m);
+          acc += w;
+          if (w > 0) last = max(last, pos);
+        }
+      });
+      atomicAdd(reinterpret_cast<unsigned long long*>(&cm[c]), (unsigned long long)acc);
+    }
+    last = blk_max_i(last, s);
+  }
   uint64_t zs = 0;
   for (int c = 0; c < P; ++c) zs += cm[c];
   const double target = (double)u * (double)zs;
@@ -1120,15 +1203,20 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       }
       const float tau2 = fmaxf(tau_k, tau_m);
       float tau = tau2;
+      bool fused = false;
+      int last = -1;
       if (R.topp_on) {
         if (!(R.p > 0.0f)) {
           tau = m;  // p <= 0: the top group only
         } else {
-          const uint32_t kk = gp_topp(a, R, s, VEC, tau2, m, (double)R.p);
-          if (kk) tau = fmaxf(tau2, key2f(kk));
+          fused = gp_topp_fused(a, R, s, VEC, tau2, m, (double)R.p, tau, last);
+          if (!fused) {
+            const uint32_t kk = gp_topp(a, R, s, VEC, tau2, m, (double)R.p);
+            tau = kk ? fmaxf(tau2, key2f(kk)) : tau2;
+          }
         }
       }
-      id = gp_draw(a, R, s, VEC, tau, m, u, &zid);
+      id = gp_draw(a, R, s, VEC, tau, m, u, &zid, fused, last);
     }
   }
   // leave the workspace as it was found: zero the row's chunk records, lists and dense values
