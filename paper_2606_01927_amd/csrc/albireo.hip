@@ -1363,10 +1363,12 @@ __device__ __noinline__ Resolution resolve_general(const OutArgs a, Smem& s, con
     tau_star = tau2;
     if (R.topp_on && select(tau2, 1, -(double)R.p, kk)) tau_star = fmaxf(tau_star, key2f(kk));
   }
-  // kept count, min z and fixed-point mass of S = {finite z >= tau_star}; greedy argmax position
+  // kept count, min z and fixed-point mass of S = {finite z >= tau_star}; greedy argmax position.  A
+  // sampled (mode 0) row that is not greedy reports none of them, so it skips this pass.
   int kept = 0, best = INT32_MAX;
   float zmin = INFINITY;
   uint64_t zsx = 0;
+  if (a.mode == 1 || R.greedy) {  // uniform over the workgroup
   FOR_MEM_ELEMS(R, s, {
     const float z = canon(x, r);
     if (z > -INFINITY && z >= tau_star) {
@@ -1389,6 +1391,7 @@ __device__ __noinline__ Resolution resolve_general(const OutArgs a, Smem& s, con
   zmin = block_min(zmin, s);
   zsx = block_sum_u64(zsx, s);
   best = block_min_i(best, s);
+  }
   // draw: blocked scans in ascending id over this chunk's region [lo, hi), reading the logits back
   const int64_t lo = R.owns_head ? 0 : (int64_t)R.head + R.s0 * DT::VEC;
   const int64_t hi = R.owns_tail ? (int64_t)R.V : (int64_t)R.head + R.s1 * DT::VEC;
