@@ -1306,6 +1306,24 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     const int64_t e_lo = c == 0 ? 0 : (int64_t)R.head + R.s0 * VEC;
     const int64_t e_hi = c == R.P - 1 ? (int64_t)R.V : (int64_t)R.head + R.s1 * VEC;
     uint32_t bad = 0;
+    // ids [lo, hi) of an array, IDU loads per thread in flight before any is used (unconditional:
+    // an index past the range reloads the first of the group); f(id, index)
+    constexpr int IDU = 4;
+    auto for_ids = [&](const int32_t* ids, int64_t lo, int64_t hi, auto&& f) __attribute__((always_inline)) {
+      for (int64_t h0 = lo + t; h0 < hi; h0 += IDU * (int64_t)CT) {
+        int32_t v[IDU];
+#pragma unroll
+        for (int q = 0; q < IDU; ++q) {
+          const int64_t h = h0 + (int64_t)q * CT;
+          v[q] = ids[h < hi ? h : h0];
+        }
+#pragma unroll
+        for (int q = 0; q < IDU; ++q) {
+          const int64_t h = h0 + (int64_t)q * CT;
+          if (h < hi) f(v[q], h);
+        }
+      }
+    };
     auto mark = [&](int32_t id) {
       if (id < 0 || id >= R.V) {
         bad = 1;
@@ -1318,9 +1336,11 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
       constexpr int q = decltype(Q)::value;
       if (R.h_lo + t + (int64_t)q * CT < R.h_hi) mark(hreg[q]);
     });
-    for (int64_t h = R.h_lo + t + (int64_t)HPT * CT; h < R.h_hi; h += CT) mark(hid[h]);
-    for (int64_t h = R.p_lo + t; h < R.p_hi; h += CT) mark(a.prompt_ids[h]);
-    for (int e = t; e < R.st_n; e += CT) mark(a.st_ids[row * a.st_cap + e]);
+    const int64_t h_tail = R.h_lo + (int64_t)HPT * CT;  // history ids past the register copy
+    for_ids(hid, h_tail, R.h_hi, [&](int32_t id, int64_t) { mark(id); });
+    for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { mark(id); });
+    const int32_t* st_row = a.st_ids + row * a.st_cap;
+    for_ids(st_row, 0, R.st_n, [&](int32_t id, int64_t) { mark(id); });
     if (bad) atomicOr(&s.flags, FLAG_BAD_INPUT);
     __syncthreads();
     const int wpt = (nwords + CT - 1) / CT;
@@ -1354,12 +1374,13 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
       constexpr int q = decltype(Q)::value;
       if (R.h_lo + t + (int64_t)q * CT < R.h_hi) count(hreg[q], 1u, 0u);
     });
-    for (int64_t h = R.h_lo + t + (int64_t)HPT * CT; h < R.h_hi; h += CT) count(hid[h], 1u, 0u);
-    for (int64_t h = R.p_lo + t; h < R.p_hi; h += CT) count(a.prompt_ids[h], 0u, 0x80000000u);
-    for (int e = t; e < R.st_n; e += CT) {
-      const uint32_t cv = a.st_counts[row * a.st_cap + e];
-      count(a.st_ids[row * a.st_cap + e], cv & 0x7fffffffu, cv & 0x80000000u);
-    }
+    for_ids(hid, h_tail, R.h_hi, [&](int32_t id, int64_t) { count(id, 1u, 0u); });
+    for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { count(id, 0u, 0x80000000u); });
+    const int32_t* st_cnt = reinterpret_cast<const int32_t*>(a.st_counts + row * a.st_cap);
+    for_ids(st_cnt, 0, R.st_n, [&](int32_t cvi, int64_t e) {
+      const uint32_t cv = (uint32_t)cvi;
+      count(st_row[e], cv & 0x7fffffffu, cv & 0x80000000u);
+    });
     __syncthreads();
   }
 
