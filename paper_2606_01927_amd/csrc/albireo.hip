@@ -180,15 +180,6 @@ __device__ __forceinline__ float block_max(float v, Smem& s) {
   return r;
 }
 __device__ __forceinline__ float block_min(float v, Smem& s) { return -block_max(-v, s); }
-__device__ __forceinline__ uint32_t block_or(uint32_t v, Smem& s) {
-  v = wave_or(v);
-  __syncthreads();
-  if (lane_id() == 0) s.red_u[wave_id()] = v;
-  __syncthreads();
-  uint32_t r = 0;
-  for (int w = 0; w < NW; ++w) r |= s.red_u[w];
-  return r;
-}
 __device__ __forceinline__ int block_min_i(int v, Smem& s) {
   v = wave_min_i(v);
   __syncthreads();
@@ -1763,13 +1754,6 @@ __device__ __forceinline__ uint32_t finish_presence(Smem& s, const RowState& R, 
   return flags;
 }
 
-// Extras index of a penalised body element from its body code (see extras_index).
-__device__ __forceinline__ int rank_of_code(const Smem& s, int code) {
-  const uint32_t word = s.bitmap[code >> 5];
-  const int b = code & 31;
-  if (!((word >> b) & 1u)) return -1;
-  return (int)s.wpref[code >> 5] + __popc(word & ((1u << b) - 1u));
-}
 
 // Wave 0, second: number the extras entries (penalised body elements by position, through the word
 // prefixes of the bitmap, then the unaligned head / tail positions the chunk owns), clear their

@@ -184,13 +184,6 @@ __device__ __forceinline__ float elem(uint4 d, int e) {
 // ----------------------------------------------------------------------------------------------
 // Workgroup reductions (4 waves; fixed combination order)
 // ----------------------------------------------------------------------------------------------
-__device__ __forceinline__ int blk_sum_i(int v, SSm& s) {
-  v = wave_sum_i(v);
-  __syncthreads();
-  if (lane_id() == 0) s.bc_i[wave_id()] = v;
-  __syncthreads();
-  return s.bc_i[0] + s.bc_i[1] + s.bc_i[2] + s.bc_i[3];
-}
 __device__ __forceinline__ int blk_min_i(int v, SSm& s) {
   v = wave_min_i(v);
   __syncthreads();
