@@ -8,7 +8,7 @@
  * sec. 8 "Workload" lists top-p, top-k, min-p, temperature and repetition, presence and frequency
  * penalties; sec. 6 keeps the per-row sampling computation unchanged while rows are split across
  * GPUs, Eq. (opt_sample)).  The paper fixes none of the formulas, so the oracle follows the plain
- * definitions below, in this order, with every reading listed in the design doc:
+ * definitions below, in this order, each reading of the paper stated with its step:
  *
  *   O-0  x_v = logit as fp32 (bf16 widened exactly).
  *   O-1  penalties from the row's token history (repetition: the divide-positive / multiply-negative
