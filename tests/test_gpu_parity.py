@@ -170,8 +170,9 @@ def test_edge_cases(lib, oracle_mod):
     compare_sample(ref, out, n_top=7)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_general_path_wide_rows(dtype, lib, oracle_mod):
+@pytest.mark.parametrize("dtype,extras", [("f32", False), ("bf16", False), ("bf16", True)],
+                         ids=["f32", "bf16", "bf16_topn_penalties"])
+def test_general_path_wide_rows(dtype, extras, lib, oracle_mod):
     """Wide rows whose kept sets are too large for candidate lists: the selections over the whole row
     (top-k above the list capacity, top-p without top-k), including rows whose boundary values are so
     often tied that they do not fit in the on-chip staging and take the whole-row selection."""
@@ -200,9 +201,19 @@ def test_general_path_wide_rows(dtype, lib, oracle_mod):
                            uniforms=np.linspace(0.07, 0.93, len(rows)).astype(np.float32),
                            temperature=np.full(len(rows), 0.9, np.float32), top_k=np.array(K, np.int32),
                            top_p=np.array(Pp, np.float32), min_p=np.array(MP, np.float32))
-    _say("wide rows", dtype)
+    if extras:  # top-5 logprobs and penalties from 1500-id histories over the same rows
+        hr = np.random.default_rng(12)
+        B = len(rows)
+        lens = hr.integers(200, 1500, size=B)
+        w.hist_offsets = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        w.hist_ids = hr.integers(0, V, size=int(lens.sum())).astype(np.int32)
+        w.repetition_penalty = hr.uniform(1.05, 1.4, size=B).astype(np.float32)
+        w.frequency_penalty = hr.uniform(0.0, 0.4, size=B).astype(np.float32)
+        w.presence_penalty = hr.uniform(-0.1, 0.3, size=B).astype(np.float32)
+        w.n_top = 5
+    _say("wide rows", dtype, extras)
     out = _run(lib, w)
-    rep = compare_sample(oracle_mod.sample(w), out)
+    rep = compare_sample(oracle_mod.sample(w), out, n_top=w.n_top)
     _say("  ", rep)
     assert rep["band"] <= 1
 
