@@ -53,6 +53,13 @@ MUTANTS = [
      "const uint32_t ctr[4] = {(uint32_t)step, 0u,"),
     ("backfill skips slot 0", "if (d >= 0 && d < n_next) next_tokens[d] = ids[i];",
      "if (d > 0 && d < n_next) next_tokens[d] = ids[i];"),
+    ("nucleus margin forced to zero", "double a = c - (double)p, b = (double)p - c_prev;\n      out->topp_margin[i] = a < b ? a : b;",
+     "double a = c - (double)p, b = (double)p - c_prev;\n      out->topp_margin[i] = 0.0 * (a < b ? a : b);"),
+    ("CDF margin forced to zero", "double a = u - Cb, b = C - u;\n        out->cdf_margin[i] = a < b ? a : b;",
+     "double a = u - Cb, b = C - u;\n        out->cdf_margin[i] = 0.0 * (a < b ? a : b);"),
+    ("log-normaliser drops the max", "out->log_norm[i] = (double)m + log(ZS);", "out->log_norm[i] = log(ZS);"),
+    ("top-n logprobs drop the max", "out->top_logprobs[i * nt + t] = (double)ord[t].z - (double)m - L;",
+     "out->top_logprobs[i * nt + t] = (double)ord[t].z - L;"),
     ("block stride taken as the row stride", "const int64_t at = (v / L) * S + i * ld + v % L;",
      "const int64_t at = (v / L) * ld + i * ld + v % L;"),
     ("row stride taken as the block length", "const int64_t at = (v / L) * S + i * ld + v % L;",

@@ -75,13 +75,23 @@ def test_worked_example(case, oracle_mod):
     if "expect_id" in case:
         assert r["ids"][0] == case["expect_id"]
     if "expect_cdf_margin" in case:
-        assert abs(r["cdf_margin"][0] - case["expect_cdf_margin"]) < 1e-12
+        assert abs(r["cdf_margin"][0] - case["expect_cdf_margin"]) <= max(tol, 1e-12)
+    if "expect_topp_margin" in case:
+        assert abs(r["topp_margin"][0] - case["expect_topp_margin"]) <= max(tol, 1e-12)
+    if "expect_log_norm" in case:
+        assert abs(r["log_norm"][0] - case["expect_log_norm"]) <= max(tol, 1e-12)
     if "expect_flags" in case:
         assert r["flags"][0] == case["expect_flags"]
     if "expect_logprob" in case:
         assert abs(r["logprobs"][0] - case["expect_logprob"]) <= tol
     if "expect_top_ids" in case:
         assert r["top_ids"][0].tolist() == case["expect_top_ids"]
+    if "expect_top_logprobs" in case:
+        want = np.array([_f(v) for v in case["expect_top_logprobs"]])
+        got = r["top_logprobs"][0]
+        assert (np.isinf(got) == np.isinf(want)).all()
+        fin = np.isfinite(want)
+        np.testing.assert_allclose(got[fin], want[fin], rtol=0, atol=max(tol, 1e-12))
 
 
 # ---------------------------------------------------------------- numpy special cases
