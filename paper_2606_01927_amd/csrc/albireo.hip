@@ -26,7 +26,7 @@
 #include <utility>
 
 #include "albireo.h"
-#include "split.h"
+#include "stream.h"
 
 namespace {
 
@@ -246,6 +246,8 @@ __device__ __forceinline__ float block_excl_scan(float v, Smem& s, float* total)
 // ----------------------------------------------------------------------------------------------
 // Row-group synchronisation through the workspace (P > 1).  The wait is bounded: after SPIN_LIMIT
 // polls it records an error in the group's sync block and continues, so a bug cannot hang the GPU.
+// The leader ORs FLAG_TIMEOUT into the flags of every row it writes once the error is set, and the
+// group's last workgroup to exit clears it with the counters.
 // ----------------------------------------------------------------------------------------------
 __device__ __forceinline__ void group_barrier(GroupSync* gs, int P) {
   __threadfence();
@@ -1627,11 +1629,13 @@ __device__ __noinline__ void dense_probs(const OutArgs a, Smem& s, const RowStat
 // Wait (bounded) until the row's penalty state has reached the given level of the LDS counter: one
 // count per wave that has marked its share of the history, then one for wave 0's finished presence
 // bitmap, then one for its extras numbering and cleared counts.
+// A wait that gives up sets FLAG_TIMEOUT in the row's LDS flags.
 __device__ __forceinline__ void wait_ready(Smem& s, uint32_t level) {
   for (uint32_t n = 0; n < SPIN_LIMIT; ++n) {
     if (__hip_atomic_load(&s.ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= level) return;
     __builtin_amdgcn_s_sleep(1);
   }
+  atomicOr(&s.flags, FLAG_TIMEOUT);
 }
 
 // Whether a history id lies in this chunk (the chunk's body slots, or the head / tail it owns).
@@ -2490,6 +2494,8 @@ __device__ __forceinline__ void process_row(const KArgs& a, Smem& s, RowCtx& X, 
       }
     }
     if (leader && threadIdx.x == 0) {
+      if (MULTI && __hip_atomic_load(&X.gsync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+        row_flags |= FLAG_TIMEOUT;
       if (a.out_flags) a.out_flags[row] = row_flags;
       if (a.mode == 1) {
         if (a.out_threshold) a.out_threshold[row] = skip ? -INFINITY : res.zmin;
@@ -2550,6 +2556,7 @@ __global__ __launch_bounds__(NT) void k_sample_multi(KArgs a) {
     const uint32_t old = __hip_atomic_fetch_add(&X.gsync->exit, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (old == (uint32_t)a.P - 1) {
       __hip_atomic_store(&X.gsync->arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&X.gsync->error, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&X.gsync->exit, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
@@ -2678,28 +2685,20 @@ struct KernelInfo {
   int J;
 };
 
-template <class DT, int J, bool SEG>
-KernelInfo kinfo1(bool multi) {
-  return {multi ? reinterpret_cast<const void*>(&k_sample_multi<DT, J, SEG>)
-                : reinterpret_cast<const void*>(&k_sample<DT, J, SEG>),
+// The one-workgroup-per-row kernel and the row-group kernel serve albireo_topk_topp only: fp32 rows,
+// row-major.
+template <int J>
+KernelInfo kinfo(bool multi) {
+  return {multi ? reinterpret_cast<const void*>(&k_sample_multi<F32T, J, false>)
+                : reinterpret_cast<const void*>(&k_sample<F32T, J, false>),
           J};
 }
-template <class DT, int J>
-KernelInfo kinfo(bool multi, bool seg) {
-  return seg ? kinfo1<DT, J, true>(multi) : kinfo1<DT, J, false>(multi);
-}
 
-template <class DT>
-KernelInfo pick_kernel(int64_t chunk_slots, bool multi, bool seg) {
-#ifdef ALBIREO_DEV_ONE_J  // development builds: a single instantiation for quick compiles
-  (void)chunk_slots;
-  return kinfo<DT, ALBIREO_DEV_ONE_J>(multi, seg);
-#else
-  if (chunk_slots <= (int64_t)JSIZES[0] * NT) return kinfo<DT, JSIZES[0]>(multi, seg);
-  if (chunk_slots <= (int64_t)JSIZES[1] * NT) return kinfo<DT, JSIZES[1]>(multi, seg);
-  if (chunk_slots <= (int64_t)JSIZES[2] * NT) return kinfo<DT, JSIZES[2]>(multi, seg);
-  return kinfo<DT, JSIZES[3]>(multi, seg);
-#endif
+KernelInfo pick_kernel(int64_t chunk_slots, bool multi) {
+  if (chunk_slots <= (int64_t)JSIZES[0] * NT) return kinfo<JSIZES[0]>(multi);
+  if (chunk_slots <= (int64_t)JSIZES[1] * NT) return kinfo<JSIZES[1]>(multi);
+  if (chunk_slots <= (int64_t)JSIZES[2] * NT) return kinfo<JSIZES[2]>(multi);
+  return kinfo<JSIZES[3]>(multi);
 }
 
 struct Geometry {
@@ -2756,8 +2755,8 @@ hipError_t device_caps(int dev, const void* fn, size_t smem, DeviceCaps& out) {
   return hipErrorUnknown;
 }
 
-hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& G, bool seg = false) {
-  const int VEC = dtype == ALBIREO_BF16 ? BF16T::VEC : F32T::VEC;
+hipError_t make_geometry(int64_t B, int64_t V, Geometry& G) {
+  const int VEC = F32T::VEC;
   const int64_t max_body = V / VEC;
   int64_t P = (max_body + (int64_t)JMAX * NT - 1) / ((int64_t)JMAX * NT);
   if (P < 1) P = 1;
@@ -2765,8 +2764,7 @@ hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& 
   if (!G.ok) return hipSuccess;
   G.P = (int)P;
   G.chunk_slots = (max_body + P - 1) / P;
-  G.k = dtype == ALBIREO_BF16 ? pick_kernel<BF16T>(G.chunk_slots, G.P > 1, seg)
-                              : pick_kernel<F32T>(G.chunk_slots, G.P > 1, seg);
+  G.k = pick_kernel(G.chunk_slots, G.P > 1);
   // the single-chunk kernel skips the dead-slot test below live_slots_min(J) (always true for the
   // size pick_kernel chose; a build restricted to one size can miss it for small rows)
   if (G.P == 1 && max_body - 1 < (int64_t)live_slots_min(G.k.J) * NT) {
@@ -2795,22 +2793,11 @@ hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& 
 
 size_t required_ws(const Geometry& G) { return (size_t)G.group_bytes * (size_t)G.n_groups; }
 
-// Workspace of the single-workgroup / multi-chunk kernels for (B, V, dtype), 0 when they do not apply.
-size_t legacy_ws(int64_t B, int64_t V, albireo_dtype_t dtype) {
+// Workspace of the filtered-distribution kernels for B fp32 rows of V, 0 when they do not apply.
+size_t legacy_ws(int64_t B, int64_t V) {
   Geometry G;
-  if (make_geometry(B, V, dtype, G) != hipSuccess || !G.ok) return 0;
+  if (make_geometry(B, V, G) != hipSuccess || !G.ok) return 0;
   return required_ws(G);
-}
-
-// Kernel choice by shape alone (so a row gets the same arithmetic in every layout and batch): a row
-// that fits one workgroup's registers is sampled by that one workgroup, with no global round trip
-// between its phases; wider rows go to the split-row kernel, whose chunk workgroups need no
-// co-residency and whose last chunk resolves the row.
-bool use_split(int64_t B, int64_t V, albireo_dtype_t dtype) {
-  if (!albireo_split::supported(B, V, dtype)) return false;
-  Geometry G;
-  if (make_geometry(B, V, dtype, G) != hipSuccess) return false;
-  return !G.ok || G.P > 1;
 }
 
 albireo_status_t launch_sample(const KArgs& a0, const Geometry& G, hipStream_t stream) {
@@ -2873,11 +2860,6 @@ albireo_status_t check_common(const void* logits, albireo_dtype_t dtype, int64_t
   return ALBIREO_OK;
 }
 
-// A prompt history or a penalty state is read by the split-row kernel only.
-bool needs_split(const albireo_params_t* params) {
-  return params && (params->prompt_offsets || params->state);
-}
-
 albireo_status_t check_ws(void* ws, size_t bytes, size_t need) {
   if (need == 0) return ALBIREO_OK;
   if (!ws || reinterpret_cast<uintptr_t>(ws) % 256) return ALBIREO_E_WORKSPACE;
@@ -2901,25 +2883,6 @@ albireo_status_t check_shards(const void* logits, albireo_dtype_t dtype, int64_t
   return ALBIREO_OK;
 }
 
-// The blocked layout's kernel arguments (after check_shards), once the kernel size is known.
-albireo_status_t shard_args(albireo_dtype_t dtype, int64_t V, const albireo_shards_t& sh, const Geometry& G,
-                            KArgs& a) {
-  const int64_t es = dtype == ALBIREO_BF16 ? 2 : 4;
-  const int64_t L = sh.shard_len, S = sh.shard_stride;
-  const int64_t t = (V + L - 1) / L;
-  const int64_t sps = L * es / 16;
-  const int64_t gap = t > 1 ? (S - L) * es : 0;
-  // the lane offsets of all J slots a workgroup issues stay below 2^31
-  const int64_t issued = (int64_t)G.k.J * NT;
-  if (issued * 16 + (issued / sps + 1) * gap >= ((int64_t)1 << 31)) return ALBIREO_E_UNSUPPORTED;
-  a.seg_sps = (uint32_t)sps;
-  a.seg_magic = (uint32_t)(0xffffffffull / (uint64_t)sps);
-  a.seg_ntq = (uint32_t)(NT / sps);
-  a.seg_ntr = (uint32_t)(NT % sps);
-  a.seg_gap = gap;
-  return ALBIREO_OK;
-}
-
 // albireo_sample / albireo_sample_step / albireo_sample_sharded: shards NULL is the row-major layout;
 // exactly one of uniforms and step is given.
 albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
@@ -2939,67 +2902,28 @@ albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t 
     st = check_shards(logits, dtype, V, ld, *shards);
     if (st != ALBIREO_OK) return st;
   }
-  if (needs_split(params) && !albireo_split::supported(B, V, dtype)) return ALBIREO_E_UNSUPPORTED;
-  if (use_split(B, V, dtype) || needs_split(params)) {
-    // the split-row kernel; its part of the workspace follows the other kernels' part
-    const size_t off = (size_t)align256((int64_t)legacy_ws(B, V, dtype));
-    st = check_ws(workspace, workspace_bytes, off + albireo_split::workspace_bytes(B, V, dtype));
-    if (st != ALBIREO_OK) return st;
-    albireo_split::Request r;
-    r.logits = logits;
-    r.dtype = dtype;
-    r.B = B;
-    r.V = V;
-    r.ld = ld;
-    r.params = params;
-    r.uniforms = uniforms;
-    r.step = step;
-    r.shards = shards;
-    r.out_ids = out_ids;
-    r.out_logprobs = out_logprobs;
-    r.n_top = n_top;
-    r.out_top_ids = out_top_ids;
-    r.out_top_logprobs = out_top_logprobs;
-    r.out_flags = out_flags;
-    r.ws = static_cast<unsigned char*>(workspace) + off;
-    r.stream = stream;
-    return albireo_split::launch(r);
-  }
-  Geometry G;
-  if (make_geometry(B, V, dtype, G, shards != nullptr) != hipSuccess) return ALBIREO_E_LAUNCH;
-  if (!G.ok) return ALBIREO_E_UNSUPPORTED;
-  KArgs a;
-  memset(&a, 0, sizeof a);
-  if (shards) {
-    st = shard_args(dtype, V, *shards, G, a);
-    if (st != ALBIREO_OK) return st;
-  }
-  st = check_ws(workspace, workspace_bytes, required_ws(G));
+  if (!albireo_stream::supported(B, V, dtype)) return ALBIREO_E_UNSUPPORTED;
+  st = check_ws(workspace, workspace_bytes, albireo_stream::workspace_bytes(B, V, dtype));
   if (st != ALBIREO_OK) return st;
-  a.logits = static_cast<const unsigned char*>(logits);
-  a.B = B;
-  a.V = V;
-  a.ld = ld;
-  a.prm = dev_params(params);
-  a.uniforms = uniforms;
-  if (step) {
-    a.rng_on = 1;
-    a.rng_seed = step->seed;
-    a.rng_step = step->step;
-    a.seq_ids = step->seq_ids;
-    a.next_tokens = step->next_tokens;
-    a.backfill_dest = step->backfill_dest;
-    a.next_len = step->next_len;
-  }
-  a.out_ids = out_ids;
-  a.out_logprobs = out_logprobs;
-  a.n_top = n_top;
-  a.out_top_ids = out_top_ids;
-  a.out_top_logprobs = out_top_logprobs;
-  a.out_flags = out_flags;
-  a.mode = 0;
-  a.ws = static_cast<unsigned char*>(workspace);
-  return launch_sample(a, G, stream);
+  albireo_stream::Request r;
+  r.logits = logits;
+  r.dtype = dtype;
+  r.B = B;
+  r.V = V;
+  r.ld = ld;
+  r.params = params;
+  r.uniforms = uniforms;
+  r.step = step;
+  r.shards = shards;
+  r.out_ids = out_ids;
+  r.out_logprobs = out_logprobs;
+  r.n_top = n_top;
+  r.out_top_ids = out_top_ids;
+  r.out_top_logprobs = out_top_logprobs;
+  r.out_flags = out_flags;
+  r.ws = static_cast<unsigned char*>(workspace);
+  r.stream = stream;
+  return albireo_stream::launch(r);
 }
 
 }  // namespace
@@ -3010,16 +2934,12 @@ size_t albireo_workspace_size(int64_t B, int64_t V, albireo_dtype_t dtype, int32
   (void)n_top;
   if (B <= 0 || V <= 0 || (dtype != ALBIREO_F32 && dtype != ALBIREO_BF16)) return 256;
   if (V >= ((int64_t)1 << 31) - 16) return 0;
-  // the split-row kernel's part follows the other kernels' part (both may serve one workspace)
-  const size_t legacy = legacy_ws(B, V, dtype);
-  // the split-row kernel's part whenever it can serve the shape: rows with a prompt history or a
-  // penalty state go to it whatever their width
-  const size_t split = albireo_split::workspace_bytes(B, V, dtype);
-  if (split == 0) {
-    Geometry G;
-    if (make_geometry(B, V, dtype, G) != hipSuccess || !G.ok) return 0;
-  }
-  return (size_t)align256((int64_t)legacy) + split;
+  // the sampling kernel's part and the filtered-distribution kernel's part share the bytes: every call
+  // leaves what it used zeroed
+  const size_t stream = albireo_stream::workspace_bytes(B, V, dtype);
+  const size_t legacy = dtype == ALBIREO_F32 ? legacy_ws(B, V) : 0;
+  const size_t need = stream > legacy ? stream : legacy;
+  return need < 256 ? 256 : need;
 }
 
 albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
@@ -3083,7 +3003,7 @@ albireo_status_t albireo_topk_topp(const float* logits, int64_t B, int64_t V, in
   if (st != ALBIREO_OK) return st;
   if (B == 0) return ALBIREO_OK;
   Geometry G;
-  if (make_geometry(B, V, ALBIREO_F32, G) != hipSuccess) return ALBIREO_E_LAUNCH;
+  if (make_geometry(B, V, G) != hipSuccess) return ALBIREO_E_LAUNCH;
   if (!G.ok) return ALBIREO_E_UNSUPPORTED;
   st = check_ws(workspace, workspace_bytes, required_ws(G));
   if (st != ALBIREO_OK) return st;
@@ -3116,7 +3036,7 @@ albireo_status_t albireo_apply_penalties(const void* logits, albireo_dtype_t dty
   (void)workspace_bytes;
   albireo_status_t st = check_common(logits, dtype, B, V, ld, params);
   if (st != ALBIREO_OK) return st;
-  if (needs_split(params)) return ALBIREO_E_UNSUPPORTED;
+  if (params && (params->prompt_offsets || params->state)) return ALBIREO_E_UNSUPPORTED;
   if (B == 0) return ALBIREO_OK;
   if (!out_logits) return ALBIREO_E_INVALID;
   // aliasing is only defined for an fp32 input with ld == V (element-wise in place)

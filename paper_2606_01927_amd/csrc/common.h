@@ -1,7 +1,7 @@
 // common.h -- device helpers shared by the sampling kernels of this library (one copy per
 // translation unit; everything here has internal linkage through the enclosing anonymous namespace).
 //
-// Included by albireo.hip and split.hip inside `namespace {`.
+// Included by albireo.hip and stream.hip inside `namespace {`.
 #pragma once
 constexpr uint32_t SPIN_LIMIT = 1u << 24;
 constexpr double FIX_SCALE = 4294967296.0;  // fixed-point scale of the general path's masses
@@ -13,6 +13,7 @@ constexpr uint32_t FLAG_EMPTY = ALBIREO_FLAG_EMPTY;
 constexpr uint32_t FLAG_BAD_INPUT = ALBIREO_FLAG_BAD_INPUT;
 constexpr uint32_t FLAG_BAD_PARAM = ALBIREO_FLAG_BAD_PARAM;
 constexpr uint32_t FLAG_LIMIT = ALBIREO_FLAG_LIMIT;
+constexpr uint32_t FLAG_TIMEOUT = ALBIREO_FLAG_TIMEOUT;
 
 struct DevParams {
   const float* temperature;

@@ -1,5 +1,5 @@
-// split.h -- internal interface between the C ABI (albireo.hip) and the split-row sampling kernel
-// (split.hip).  Not part of the public header: the public entry points route here.
+// stream.h -- internal interface between the C ABI (albireo.hip) and the streaming sampling kernel
+// (stream.hip).  Not part of the public header: the public sampling entry points route here.
 #pragma once
 
 #include <stddef.h>
@@ -9,7 +9,7 @@
 
 #include "albireo.h"
 
-namespace albireo_split {
+namespace albireo_stream {
 
 // Everything one sampling launch needs (device pointers unless noted).
 struct Request {
@@ -26,19 +26,19 @@ struct Request {
   int32_t* out_top_ids;
   float* out_top_logprobs;
   uint32_t* out_flags;
-  unsigned char* ws;  // the split kernel's part of the caller's workspace (256-byte aligned)
+  unsigned char* ws;  // the caller's workspace (256-byte aligned), workspace_bytes(B, V, dtype) long
   hipStream_t stream;
 };
 
-// Whether the split kernel handles rows of this shape (V, dtype, batch size).
+// Whether the kernel handles rows of this shape (V, dtype, batch size).
 bool supported(int64_t B, int64_t V, albireo_dtype_t dtype);
 
-// Workspace bytes the split kernel needs for B rows (0 when not supported).  The bytes must be zero
-// before a call, and the kernel leaves every byte it wrote zero again (the workspace contract of the
-// public header), so one workspace can serve every entry point and shape in turn.
+// Workspace bytes the kernel needs for B rows (0 when not supported).  The bytes must be zero before a
+// call, and the kernel leaves every byte it wrote zero again (the workspace contract of the public
+// header), so one workspace serves every entry point and shape in turn.
 size_t workspace_bytes(int64_t B, int64_t V, albireo_dtype_t dtype);
 
 // Enqueue one launch.  The caller has validated every host-checkable argument.
 albireo_status_t launch(const Request& r);
 
-}  // namespace albireo_split
+}  // namespace albireo_stream

@@ -1,24 +1,33 @@
-// split.hip -- the split-row kernel of the per-sequence sampling step (sec. 6.1, Eq. opt_sample: every
+// stream.hip -- the streaming kernel of the per-sequence sampling step (sec. 6.1, Eq. opt_sample: every
 // worker runs the unchanged per-row sampling computation on its rows; the computation is the one of
 // the workload of sec. 8.1: penalties, temperature, top-k, top-p, min-p, greedy, and the draw).
 //
-// A row of the [B, V] logits is cut into P chunks of at most CSLOTS 16-byte slots (16384 bf16 or
-// 8192 fp32 logits).  One 256-thread workgroup per chunk
-//   * issues one 16-byte load per slot into registers, all up front;
-//   * applies the penalty overlay: the chunk's history ids go into an LDS presence bitmap, a word
-//     prefix count numbers them, their counts are accumulated by number, and every penalised element
-//     leaves the registers (masked to -inf) for a small LDS "extras" list that holds its new value;
-//   * reduces the chunk to its max, a sum of exponentials relative to a reference, and, for rows with
-//     a top-k / min-p / top-n bound, a short candidate list sorted in descending order (the bound is a
-//     provable lower limit of the chunk's K-th largest value, taken from the per-thread maxima).
-// The workgroups of a row never wait for each other.  Each publishes its results in the workspace and
-// bumps the row's arrival counter; the last to arrive resolves the row: log-sum-exp over the chunks
-// in chunk order, top-n and the top-k threshold by ranking the staged list heads, then min-p, the
-// nucleus and the inverse-CDF draw in ascending token id on the (small) kept set.  Rows whose kept set
-// has no small bound (top-p alone, no filter) or whose lists overflow take a slower general path in
-// the same workgroup over the chunks' processed values (radix selection by count and by mass).
+// A row of the [B, V] logits is cut into P chunks of at most CSLOTS 16-byte slots (38912 bf16 or 19456
+// fp32 logits).  Two launches on the caller's stream sample a batch.
 //
-// Many small workgroups per row keep every CU streaming while other chunks run their reductions.
+// The chunk kernel runs one 256-thread workgroup per chunk (four resident per CU).  A chunk workgroup
+//   * issues every 16-byte load of its chunk up front with the non-temporal hint (each logit is read
+//     once; the hint keeps the stream from displacing cached data), after the loads of the row's
+//     token history;
+//   * builds the penalty overlay of its range: the history ids that fall in the chunk go into an LDS
+//     presence bitmap, a word prefix count numbers the marked positions, and their counts are
+//     accumulated by number;
+//   * takes the slots in arrival order: penalised elements are masked out of the registers, the rest
+//     enter a running maximum and a sum of exponentials against a reference that moves with the
+//     thread maximum; the penalised elements then join with their new values (LDS "extras");
+//   * reduces the chunk to its max, its sum and, for rows with a top-k / min-p / top-n bound, a short
+//     candidate list sorted in descending order (the bound is a provable lower limit of the chunk's
+//     K-th largest value: the K-th largest per-thread maximum);
+//   * writes its record and its list to the workspace with plain stores and ends.
+// The resolution kernel runs one workgroup per row once the chunk kernel has finished (the end of a
+// launch makes its stores visible to the next launch on the stream, whichever XCD wrote them): the
+// log-sum-exp over the chunks in chunk order, top-n and the top-k threshold by ranking the list heads,
+// min-p, the nucleus and the inverse-CDF draw in ascending token id on the (small) kept set.  Rows whose
+// kept set has no small bound (top-p alone, no filter, lists over capacity) take the general path:
+// distance histograms, the crossing bucket and the draw over re-reads of the row's logits with the
+// penalty overlay rebuilt per chunk, so nothing of size [B, V] is ever written.  No workgroup ever
+// waits for another.
+//
 // Everything that combines values across threads, waves or chunks does so in a fixed order or in
 // integers, so the results depend only on the row's values, V, the dtype and the row's alignment.
 #include <hip/hip_runtime.h>
@@ -30,29 +39,31 @@
 #include <utility>
 
 #include "albireo.h"
-#include "split.h"
+#include "stream.h"
 
 namespace {
 
 #include "common.h"
 
-constexpr int CT = 256;                          // threads per chunk workgroup
-constexpr int CW = CT / 64;                      // waves per workgroup
-constexpr int CJ = 8;                            // 16-byte register slots per thread
-constexpr int CSLOTS = CT * CJ;                  // body slots per chunk at most
+constexpr int CT = 256;                            // threads per chunk workgroup
+constexpr int CW = CT / 64;                        // waves per workgroup
+constexpr int CJ = 19;                             // 16-byte register slots per thread (chunk kernel)
+constexpr int GJ = 19;                             // slots per thread per re-read batch (resolution kernel)
+constexpr int CSLOTS = CT * CJ;                    // body slots per chunk at most
 constexpr int BMW = ((CSLOTS + 2) * 8 + 31) / 32;  // bitmap words (one bit per element, +1 slot each side)
-constexpr int XCAP = ALBIREO_MAX_UNIQUE_HISTORY;  // distinct penalised positions tracked per chunk
-constexpr int LCAPC = 512;                       // candidate list capacity of a chunk
-constexpr int MSTAGE = 2048;                     // list entries the resolving workgroup stages in LDS
-constexpr int MCAP = 512;                        // kept-set capacity of the list resolution
-constexpr int MAXPC = 64;                        // chunks per row
-constexpr int HXN = 16;                          // plain head (threads 0-7) and tail (8-15) extras
+constexpr int XCAP = ALBIREO_MAX_UNIQUE_HISTORY;   // distinct penalised positions tracked per chunk
+constexpr int LCAPC = 512;                         // candidate list capacity of a chunk
+constexpr int MCAP = 512;                          // kept-set capacity of the list resolution
+constexpr int MAXPC = 64;                          // chunks per row
+constexpr int HXN = 16;                            // plain head (threads 0-7) and tail (8-15) extras
+constexpr int GEN_WORDS = 512;                     // general-path histogram area (64-bit words)
 constexpr double LN2 = 0.6931471805599453;
 
-constexpr uint32_t PUB_DENSE = 1u << 30;   // the chunk wrote its processed values to the dense row
 constexpr uint32_t PUB_FINITE = 1u << 29;  // the chunk holds a finite processed value
+constexpr uint32_t PUB_OVER = 1u << 28;    // the chunk's candidate list did not fit
+constexpr int REC_WORDS = 8;               // 64-bit words per chunk record (5 used)
 
-// What one chunk publishes for the row's resolution (32 bytes).
+// What one chunk publishes for the row's resolution (decoded form).
 struct ChunkPub {
   float zmax;      // max processed value z of the chunk (+inf in rows with a bad input)
   float mref;      // reference of s (log2 units)
@@ -63,7 +74,6 @@ struct ChunkPub {
   float qk;        // z of list entry ceil(k / P) - 1 (-inf if the list is shorter)
   float qn;        // z of list entry ceil(n_top / P) - 1
 };
-static_assert(sizeof(ChunkPub) == 32, "chunk record layout");
 
 struct SArgs {
   const unsigned char* logits;
@@ -97,11 +107,8 @@ struct SArgs {
   int32_t xcd_map;
   int64_t chunk_slots;
   int64_t grid;
-  uint32_t* ctr;     // [B] arrival counters (zero between calls)
-  ChunkPub* pub;     // [B * P]
-  uint64_t* lists;   // [B * P * LCAPC]
-  float* dense;      // [B * Vp]
-  int64_t Vp;        // dense row stride: V rounded up to 16 (64-byte rows)
+  uint64_t* rec;     // [B * P * REC_WORDS] chunk records
+  uint64_t* lists;   // [B * P * LCAPC] candidate keys
 };
 
 struct SRow {
@@ -118,36 +125,45 @@ struct SRow {
   uint32_t flags;
 };
 
-// LDS of one workgroup: the chunk phase and the resolution phase share the same bytes.
+// Penalty overlay of one chunk in LDS.
+struct PenLds {
+  uint32_t bitmap[BMW];      // presence of the chunk's positions in the row's history
+  uint16_t wpref[BMW + 2];   // set bits in the bitmap words before each word
+  uint32_t xval[XCAP];       // per penalised position: its count, then its new value
+};
+
+// LDS of one workgroup: the chunk phase, the general path and the list resolution share the bytes.
 struct SSm {
   union {
     struct {
-      uint32_t bitmap[BMW];        // presence of the chunk's positions in the row's history
-      uint16_t wpref[BMW + 1];     // set bits in the bitmap words before each word
-      uint32_t xval[XCAP];         // per penalised position: its count, then its new value
-      uint64_t list[LCAPC];        // candidate keys
+      PenLds p;
+      uint64_t list[LCAPC];      // candidate keys; the general path's staged crossing bucket
+      uint64_t gen[GEN_WORDS];   // general path: histograms
     } c;
-    struct {
-      uint64_t key[MSTAGE];        // staged list prefixes / kept set keys and weights
-      ChunkPub pub[MAXPC];
-      int32_t off[MAXPC + 1];
-      int32_t cnt[MAXPC];
-      int32_t cut[MAXPC];
-    } m;
+    uint64_t key[(sizeof(PenLds) + 8 * (LCAPC + GEN_WORDS)) / 8];  // list resolution staging
   };
+  ChunkPub pub[MAXPC];
+  uint64_t cm[MAXPC];  // general path: per-chunk kept masses
+  int32_t cnt[MAXPC];
+  int32_t cut[MAXPC];
   int32_t hx_pos[HXN];
   float hx_val[HXN];
   float wred[3][CW];
+  float tmx[CW][64];  // the thread maxima of each wave, sorted in descending order
+  float kb[2];        // the K-th largest thread maximum for top-k and for top-n
   uint64_t qred[CW];
   int32_t n_list;
   uint32_t flags;
+  int32_t ov_red[CW];  // the overlay build's block scan (callers keep counters in bc_i across it)
   int32_t bc_i[4];
   float bc_f[4];
   uint64_t bc_q[2];
   int32_t top_id[ALBIREO_MAX_TOP_N];
   float top_lp[ALBIREO_MAX_TOP_N];
 };
-static_assert(sizeof(SSm) <= 20 * 1024, "LDS of a chunk workgroup exceeds an eighth of a gfx950 CU");
+constexpr int MSTAGE = (int)(sizeof(SSm::key) / 8);
+static_assert(MSTAGE >= 2048, "list staging area below 2048 keys");
+static_assert(sizeof(SSm) <= 40 * 1024, "LDS of a chunk workgroup exceeds a quarter of a gfx950 CU");
 
 // Hide the register slots' contents from the optimiser between passes, so that it unpacks the slots
 // again in every pass instead of keeping all unpacked (or scaled) values of the previous one alive.
@@ -283,6 +299,35 @@ __device__ __forceinline__ uint64_t mass_of(float z, float m) {
 }
 
 // ----------------------------------------------------------------------------------------------
+// Chunk records: five 64-bit words (a 32-bit field and a float each)
+// ----------------------------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t rec_word(uint32_t hi, float lo) {
+  return ((uint64_t)hi << 32) | __float_as_uint(lo);
+}
+__device__ __forceinline__ void rec_store(uint64_t* g, const ChunkPub& p) {
+  g[0] = rec_word(p.flags, p.zmax);
+  g[1] = rec_word((uint32_t)(p.argpos + 1), p.mref);
+  g[2] = rec_word((uint32_t)p.n_list, p.s);
+  g[3] = rec_word(0u, p.qk);
+  g[4] = rec_word(0u, p.qn);
+}
+__device__ __forceinline__ ChunkPub rec_load(const uint64_t* g) {
+  uint64_t w[5];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) w[i] = g[i];
+  ChunkPub p;
+  p.flags = (uint32_t)(w[0] >> 32);
+  p.zmax = __uint_as_float((uint32_t)w[0]);
+  p.argpos = (int32_t)(uint32_t)(w[1] >> 32) - 1;
+  p.mref = __uint_as_float((uint32_t)w[1]);
+  p.n_list = (int32_t)(uint32_t)(w[2] >> 32);
+  p.s = __uint_as_float((uint32_t)w[2]);
+  p.qk = __uint_as_float((uint32_t)w[3]);
+  p.qn = __uint_as_float((uint32_t)w[4]);
+  return p;
+}
+
+// ----------------------------------------------------------------------------------------------
 // Row geometry and parameters
 // ----------------------------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t seg_block(const SArgs& a, uint32_t q) {
@@ -384,6 +429,13 @@ __device__ __forceinline__ void row_setup(const SArgs& a, int64_t row, int c, SR
   R.flags = flags;
 }
 
+// body slots [s0, s1) of chunk c
+__device__ __forceinline__ void chunk_range(const SArgs& a, const SRow& R, int c, int64_t& s0, int64_t& s1) {
+  s0 = (int64_t)c * a.chunk_slots;
+  if (s0 > R.body_slots) s0 = R.body_slots;
+  s1 = s0 + a.chunk_slots;
+  if (s1 > R.body_slots) s1 = R.body_slots;
+}
 // first and one-past-last row position of chunk c
 __device__ __forceinline__ int chunk_lo(const SArgs& a, const SRow& R, int c, int vec) {
   if (c == 0) return 0;
@@ -397,34 +449,203 @@ __device__ __forceinline__ int chunk_hi(const SArgs& a, const SRow& R, int c, in
   if (s > R.body_slots) s = R.body_slots;
   return R.head + (int)s * vec;
 }
+__device__ __forceinline__ int chunk_of(const SArgs& a, const SRow& R, int vec, int pos) {
+  int c = 0;
+  while (c < R.P - 1 && pos >= chunk_hi(a, R, c, vec)) ++c;
+  return c;
+}
 
 // Row position of the penalised extras entry of rank i (the i-th set bit of the bitmap).
 __device__ __forceinline__ int pos_of_rank(const SSm& s, int nwords, int64_t e_base, int i) {
   int lo = 0, hi = nwords - 1;
   while (lo < hi) {  // last word whose prefix count is <= i
     const int mid = (lo + hi + 1) >> 1;
-    if ((int)s.c.wpref[mid] <= i) lo = mid;
+    if ((int)s.c.p.wpref[mid] <= i) lo = mid;
     else hi = mid - 1;
   }
-  uint32_t w = s.c.bitmap[lo];
-  for (int q = i - (int)s.c.wpref[lo]; q > 0; --q) w &= w - 1;
+  uint32_t w = s.c.p.bitmap[lo];
+  for (int q = i - (int)s.c.p.wpref[lo]; q > 0; --q) w &= w - 1;
   return (int)(e_base + lo * 32 + __builtin_ctz(w));
+}
+
+// ----------------------------------------------------------------------------------------------
+// The penalty overlay of chunk c (body slots [s0, s1)): bit b of the bitmap stands for row position
+// e_base + b with e_base = head + (s0 - 1) VEC, so the slot before and the slot after the chunk (the
+// unaligned head of chunk 0, the tail of the last chunk) have bits too.  Every history id in the
+// chunk's positions marks its bit; word prefix counts number the marked positions; per number, the
+// output count (bits 0-30) and the prompt mark (bit 31).  The first HPT * CT history ids come from the
+// caller's registers (hreg, this thread's share), the rest from memory.  Returns the number of tracked
+// positions (at most XCAP; past that the highest positions are left out and FLAG_LIMIT is set) and ORs
+// FLAG_BAD_INPUT / FLAG_LIMIT into *fl.
+// ----------------------------------------------------------------------------------------------
+template <int HPT>
+__device__ __forceinline__ int build_overlay(const SArgs& a, const SRow& R, SSm& s, int c, int64_t s0, int64_t s1,
+                                             int vec, const int32_t (&hreg)[HPT > 0 ? HPT : 1], uint32_t* fl) {
+  const int t = threadIdx.x;
+  const int64_t e_base = (int64_t)R.head + (s0 - 1) * vec;
+  const int nwords = (int)(((s1 - s0 + 2) * vec + 31) >> 5);
+  for (int w = t; w < nwords; w += CT) s.c.p.bitmap[w] = 0;
+  __syncthreads();
+  const int64_t e_lo = c == 0 ? 0 : (int64_t)R.head + s0 * vec;
+  const int64_t e_hi = c == R.P - 1 ? (int64_t)R.V : (int64_t)R.head + s1 * vec;
+  uint32_t bad = 0;
+  const int32_t* hid = a.prm.hist_ids;
+  // ids [lo, hi) of an array, IDU loads per thread in flight before any is used (unconditional: an
+  // index past the range reloads the first of the group); f(id, index)
+  constexpr int IDU = 4;
+  auto for_ids = [&](const int32_t* ids, int64_t lo, int64_t hi, auto&& f) __attribute__((always_inline)) {
+    for (int64_t h0 = lo + t; h0 < hi; h0 += IDU * (int64_t)CT) {
+      int32_t v[IDU];
+#pragma unroll
+      for (int q = 0; q < IDU; ++q) {
+        const int64_t h = h0 + (int64_t)q * CT;
+        v[q] = ids[h < hi ? h : h0];
+      }
+#pragma unroll
+      for (int q = 0; q < IDU; ++q) {
+        const int64_t h = h0 + (int64_t)q * CT;
+        if (h < hi) f(v[q], h);
+      }
+    }
+  };
+  auto mark = [&](int32_t id) {
+    if (id < 0 || id >= R.V) {
+      bad = 1;
+    } else if (id >= e_lo && id < e_hi) {
+      const int b = (int)(id - e_base);
+      atomicOr(&s.c.p.bitmap[b >> 5], 1u << (b & 31));
+    }
+  };
+  const int64_t h_reg_end = min(R.h_hi, R.h_lo + (int64_t)HPT * CT);  // history ids held in hreg
+  static_for<HPT>([&](auto Q) {
+    constexpr int q = decltype(Q)::value;
+    if (R.h_lo + t + (int64_t)q * CT < h_reg_end) mark(hreg[q]);
+  });
+  for_ids(hid, h_reg_end, R.h_hi, [&](int32_t id, int64_t) { mark(id); });
+  for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { mark(id); });
+  const int32_t* st_row = a.st_ids + R.row * a.st_cap;
+  for_ids(st_row, 0, R.st_n, [&](int32_t id, int64_t) { mark(id); });
+  if (bad) *fl |= FLAG_BAD_INPUT;
+  __syncthreads();
+  const int wpt = (nwords + CT - 1) / CT;
+  const int w0 = t * wpt;
+  int loc = 0;
+  for (int q = 0; q < wpt; ++q)
+    if (w0 + q < nwords) loc += __popc(s.c.p.bitmap[w0 + q]);
+  int tot;
+  int ex;
+  {  // exclusive scan of loc in thread order through ov_red (bc_i belongs to the callers)
+    const int incl = wave_incl_scan_i(loc);
+    if (lane_id() == 63) s.ov_red[wave_id()] = incl;
+    __syncthreads();
+    int off = 0;
+    for (int w = 0; w < wave_id(); ++w) off += s.ov_red[w];
+    tot = s.ov_red[0] + s.ov_red[1] + s.ov_red[2] + s.ov_red[3];
+    ex = off + incl - loc;
+  }
+  for (int q = 0; q < wpt; ++q)
+    if (w0 + q < nwords) {
+      s.c.p.wpref[w0 + q] = (uint16_t)min(ex, 0xffff);
+      ex += __popc(s.c.p.bitmap[w0 + q]);
+    }
+  const int n_x = tot < XCAP ? tot : XCAP;
+  if (tot > XCAP) *fl |= FLAG_LIMIT;
+  for (int i = t; i < n_x; i += CT) s.c.p.xval[i] = 0;
+  __syncthreads();
+  // per numbered position: the output count in bits 0-30, the prompt mark in bit 31
+  auto count = [&](int32_t id, uint32_t add, uint32_t mark_bits) {
+    if (id >= e_lo && id < e_hi) {
+      const int b = (int)(id - e_base);
+      const int w = b >> 5;
+      const int rank = (int)s.c.p.wpref[w] + __popc(s.c.p.bitmap[w] & ((1u << (b & 31)) - 1u));
+      if (rank < XCAP) {
+        if (add) atomicAdd(&s.c.p.xval[rank], add);
+        if (mark_bits) atomicOr(&s.c.p.xval[rank], mark_bits);
+      }
+    }
+  };
+  static_for<HPT>([&](auto Q) {
+    constexpr int q = decltype(Q)::value;
+    if (R.h_lo + t + (int64_t)q * CT < h_reg_end) count(hreg[q], 1u, 0u);
+  });
+  for_ids(hid, h_reg_end, R.h_hi, [&](int32_t id, int64_t) { count(id, 1u, 0u); });
+  for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { count(id, 0u, 0x80000000u); });
+  const int32_t* st_cnt = reinterpret_cast<const int32_t*>(a.st_counts + R.row * a.st_cap);
+  for_ids(st_cnt, 0, R.st_n, [&](int32_t cvi, int64_t e) {
+    const uint32_t cv = (uint32_t)cvi;
+    count(st_row[e], cv & 0x7fffffffu, cv & 0x80000000u);
+  });
+  __syncthreads();
+  return n_x;
+}
+
+// rank of the marked bit b of the overlay, or -1 when b is not marked or not tracked
+__device__ __forceinline__ int overlay_rank(const SSm& s, int b) {
+  const int w = b >> 5;
+  const uint32_t bw = s.c.p.bitmap[w];
+  if (!((bw >> (b & 31)) & 1u)) return -1;
+  const int rank = (int)s.c.p.wpref[w] + __popc(bw & ((1u << (b & 31)) - 1u));
+  return rank < XCAP ? rank : -1;
+}
+
+// ----------------------------------------------------------------------------------------------
+// Re-reading a chunk (general path of the resolving workgroup): f(z, pos) for every processed value of
+// chunk c -- penalties from a rebuilt overlay, canonical z -- in the order thread t, slot j.  Every
+// thread of the workgroup must call it (it synchronises).
+// ----------------------------------------------------------------------------------------------
+template <class DT, bool SEG, class F>
+__device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s, int c, F&& f) {
+  constexpr int VEC = DT::VEC;
+  const int t = threadIdx.x;
+  int64_t s0, s1;
+  chunk_range(a, R, c, s0, s1);
+  const int ns = (int)(s1 - s0);
+  int hpos = -1;
+  if (c == 0 && t < R.head) hpos = t;
+  else if (c == R.P - 1 && t >= 8 && t < 8 + (R.V - R.tail_lo)) hpos = R.tail_lo + (t - 8);
+  const float hx = hpos >= 0 ? load_elem<DT, SEG>(a, R, hpos) : 0.0f;
+  const int64_t e_base = (int64_t)R.head + (s0 - 1) * VEC;
+  if (R.pen_on) {
+    uint32_t fl = 0;
+    const int32_t none[1] = {0};
+    build_overlay<0>(a, R, s, c, s0, s1, VEC, none, &fl);
+  }
+  const float r = R.r;
+  auto value = [&](float x, int pos) __attribute__((always_inline)) -> float {
+    if (R.pen_on) {
+      const int rk = overlay_rank(s, (int)(pos - e_base));
+      if (rk >= 0) x = penalise_cv(x, s.c.p.xval[rk], R.rep, R.freq, R.pres);
+    }
+    return canon(x, r);
+  };
+  // batches of CT * GJ slots, slot j * CT + t of a batch to thread t; every load of a batch is issued
+  // before any is used (indices clamped into the batch)
+  for (int b0 = 0; b0 < ns; b0 += CT * GJ) {
+    const int nb = min(ns - b0, CT * GJ);
+    uint4 d[GJ];
+    static_for<GJ>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      d[j] = *slot_ptr<DT, SEG>(a, R, s0 + b0 + min(j * CT + t, nb - 1));
+    });
+    static_for<GJ>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      if (j * CT + t < nb) {
+        const int p0 = R.head + (int)(s0 + b0 + j * CT + t) * VEC;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) f(value(elem<DT>(d[j], e), p0 + e), p0 + e);
+      }
+    });
+  }
+  if (hpos >= 0) f(value(hx, hpos), hpos);
+  __syncthreads();  // the overlay is rebuilt for the next chunk
 }
 
 // ----------------------------------------------------------------------------------------------
 // Resolution of a row by its last chunk workgroup
 // ----------------------------------------------------------------------------------------------
-struct RowTot {
-  float m;       // max z of the row
-  double L;      // log sum_v exp(z_v - m)
-  uint32_t flags;
-  bool empty, dense_any;
-  int argpos;
-};
-
 // Entries of the chunk lists that the resolving workgroup loads together with the chunk records (one
-// round trip): entries [0, E) of every chunk's list, SPQ per thread.  Entries past a list's end read 0
-// (the workspace is zero there), and no valid key is 0.
+// round trip): entries [0, E) of every chunk's list, SPQ per thread.  Entries past a list's end (its
+// length comes with the records) are ignored.
 constexpr int SPQ = 8;
 struct Spec {
   uint64_t v[SPQ];
@@ -432,22 +653,26 @@ struct Spec {
   bool on;
 };
 
-// Stage into s.m.key the list entries i < imax of every chunk with z >= zthr, from the speculative
+// Stage into s.key the list entries i < imax of every chunk with z >= zthr, from the speculative
 // registers (sp.on) or from the lists themselves.  The order is arbitrary (ranks are counted).  For the
-// check of ties cut off at imax, s.m.cut[c] gets 1 (and s.m.cnt[c] the value's bits) when chunk c's
-// list goes on past imax and its entry imax - 1 passes.  Returns the count, or -1 above cap.
-__device__ __forceinline__ int stage_entries(const SArgs& a, const SRow& R, SSm& s, const Spec& sp, float zthr, int imax, int cap) {
+// check of ties cut off at imax, s.cut[c] gets 1 (and s.cnt[c] the value's bits) when chunk c's list
+// goes on past imax and its entry imax - 1 passes.  Returns the count, or -1 above cap.
+__device__ __forceinline__ int stage_entries(const SArgs& a, const SRow& R, SSm& s, const Spec& sp, float zthr,
+                                             int imax, int cap) {
   const int P = R.P, t = threadIdx.x;
   if (t == 0) s.bc_i[2] = 0;
-  if (t < P) s.m.cut[t] = 0;
+  if (t < P) s.cut[t] = 0;
   __syncthreads();
+  const uint64_t* base = a.lists + (R.row * P) * (int64_t)LCAPC;
   auto take = [&](uint64_t key, int c, int i) {
-    if (key != 0 && i < imax && cand_z(key) >= zthr) {
-      const int idx = atomicAdd(&s.bc_i[2], 1);
-      if (idx < cap) s.m.key[idx] = key;
-      if (i == imax - 1 && s.m.pub[c].n_list > imax) {
-        s.m.cut[c] = 1;
-        s.m.cnt[c] = __float_as_int(cand_z(key));  // its value, for the tie test
+    if (i < imax && i < s.pub[c].n_list) {
+      if (cand_z(key) >= zthr) {
+        const int idx = atomicAdd(&s.bc_i[2], 1);
+        if (idx < cap) s.key[idx] = key;
+        if (i == imax - 1 && s.pub[c].n_list > imax) {
+          s.cut[c] = 1;
+          s.cnt[c] = __float_as_int(cand_z(key));  // its value, for the tie test
+        }
       }
     }
   };
@@ -461,12 +686,11 @@ __device__ __forceinline__ int stage_entries(const SArgs& a, const SRow& R, SSm&
       }
     }
   } else {
-    const uint64_t* base = a.lists + (R.row * P) * (int64_t)LCAPC;
     int emax = 0;
-    for (int c = 0; c < P; ++c) emax = max(emax, min(s.m.pub[c].n_list, imax));
+    for (int c = 0; c < P; ++c) emax = max(emax, min(s.pub[c].n_list, imax));
     for (int f = t; f < P * emax; f += CT) {
       const int c = f / emax, i = f - c * emax;
-      if (i < s.m.pub[c].n_list) take(ld_agent(base + (int64_t)c * LCAPC + i), c, i);
+      if (i < s.pub[c].n_list) take(base[(int64_t)c * LCAPC + i], c, i);
     }
   }
   __syncthreads();
@@ -483,83 +707,17 @@ __device__ __forceinline__ int count_above(const uint64_t* arr, int n, uint64_t 
   return r;
 }
 
-// A row's dense view as a buffer resource (wave-uniform base, Vp floats), read with the agent-scope
-// load's cache policy (sc1): the views were written through other XCDs' L2 by agent-scope stores, and
-// these loads see them without any fence.
-constexpr int CPOL_SC1 = 16;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t dense_rsrc(const SArgs& a, int64_t row) {
-  const uint64_t b = reinterpret_cast<uint64_t>(a.dense + row * a.Vp);
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
-  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(((uint64_t)hi << 32) | lo), (short)0,
-                                           __builtin_amdgcn_readfirstlane((int)(a.Vp * 4)), 0x00020000);
-}
-// floats 4 g .. 4 g + 3 of the view
-__device__ __forceinline__ float4 ld_dense4(__amdgpu_buffer_rsrc_t rs, int g) {
-  const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, g * 16, 0, CPOL_SC1);
-  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
-}
-__device__ __forceinline__ float ld_dense1(__amdgpu_buffer_rsrc_t rs, int p) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, p * 4, 0, CPOL_SC1));
-}
-// floats p .. p + 3 of the view (p a multiple of 4), with the agent-scope store's cache policy
-__device__ __forceinline__ void st_dense4(__amdgpu_buffer_rsrc_t rs, int p, float x, float y, float z, float w) {
-  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  const u32x4 v = {__float_as_uint(x), __float_as_uint(y), __float_as_uint(z), __float_as_uint(w)};
-  __builtin_amdgcn_raw_buffer_store_b128(v, rs, p * 4, 0, CPOL_SC1);
-}
-
-// Iterate over the values of chunk c's view: its dense processed row, or its candidate list.  Every view
-// was written with agent-scope stores completed before the writer's arrival; the dense row (64-byte
-// aligned, stride Vp) is read with 16-byte agent-scope loads, eight per thread in flight.
-template <class F>
-__device__ __forceinline__ void for_view(const SArgs& a, const SRow& R, const SSm& s, int c, int vec, F&& f) {
-  const ChunkPub& pc = s.m.pub[c];
-  if (pc.flags & PUB_DENSE) {
-    const __amdgpu_buffer_rsrc_t rs = dense_rsrc(a, R.row);
-    const int lo = chunk_lo(a, R, c, vec), hi = chunk_hi(a, R, c, vec);
-    const int g0 = lo >> 2, g1 = (hi + 3) >> 2;
-    constexpr int U = 8;  // 16-byte loads in flight per thread
-    for (int g = g0 + (int)threadIdx.x; g < g1; g += U * CT) {
-      float4 v[U];
-#pragma unroll
-      for (int q = 0; q < U; ++q) {
-        const int gq = g + q * CT;
-        v[q] = ld_dense4(rs, gq < g1 ? gq : g);  // unconditional: past the chunk, a repeat ignored below
-      }
-#pragma unroll
-      for (int q = 0; q < U; ++q) {
-        const int p0 = (g + q * CT) * 4;
-        if (g + q * CT < g1) {
-          if (p0 >= lo && p0 < hi) f(v[q].x, p0);
-          if (p0 + 1 >= lo && p0 + 1 < hi) f(v[q].y, p0 + 1);
-          if (p0 + 2 >= lo && p0 + 2 < hi) f(v[q].z, p0 + 2);
-          if (p0 + 3 >= lo && p0 + 3 < hi) f(v[q].w, p0 + 3);
-        }
-      }
-    }
-  } else {
-    const uint64_t* lst = a.lists + (R.row * R.P + c) * (int64_t)LCAPC;
-    for (int i = (int)threadIdx.x; i < pc.n_list; i += CT) {
-      const uint64_t key = ld_agent(lst + i);
-      f(cand_z(key), cand_pos(key));
-    }
-  }
-}
-
-
-
-// The general path visits the kept values of the row in one of two ways: every chunk view (a pass over
-// the row), or the order keys staged in LDS by gp_gather.  Either way the visitor calls f(z) once per
-// value.
-struct ViewSrc {
+// The general path visits the row's values in one of two ways: re-reads of every chunk (a pass over
+// the row), or order keys staged in LDS.  Either way the visitor calls f(z) once per value.
+template <class DT, bool SEG>
+struct RowSrc {
   const SArgs& a;
   const SRow& R;
-  const SSm& s;
-  int vec;
+  SSm& s;
   template <class F>
   __device__ __forceinline__ void operator()(F&& f) const {
-    for (int c = 0; c < R.P; ++c) for_view(a, R, s, c, vec, [&](float z, int) __attribute__((always_inline)) { f(z); });
+    for (int c = 0; c < R.P; ++c)
+      for_chunk<DT, SEG>(a, R, s, c, [&](float z, int) __attribute__((always_inline)) { f(z); });
   }
 };
 struct StagedSrc {
@@ -568,6 +726,14 @@ struct StagedSrc {
   template <class F>
   __device__ __forceinline__ void operator()(F&& f) const {
     for (int i = (int)threadIdx.x; i < n; i += CT) f(key2f(keys[i]));
+  }
+};
+struct StagedPairs {  // (order key << 32 | position) pairs
+  const uint64_t* ent;
+  int n;
+  template <class F>
+  __device__ __forceinline__ void operator()(F&& f) const {
+    for (int i = (int)threadIdx.x; i < n; i += CT) f(key2f((uint32_t)(ent[i] >> 32)));
   }
 };
 
@@ -672,31 +838,31 @@ __device__ __forceinline__ uint32_t gp_topp_key(const Src& src, SSm& s, uint64_t
 // maximum, GD_SCALE per unit.  fl(m - z) and its product with GD_SCALE are monotone in z, so a value
 // in a lower bucket is larger than every value in a higher one, and equal values share a bucket;
 // masses (2^32 units) vanish from d = 32 ln 2 on, inside the last bucket.
-constexpr int GDB = 2048;
-constexpr float GD_SCALE = 64.0f;
-constexpr int GKCAP = 3072;  // boundary-bucket keys staged in LDS (u32), then a 256-entry histogram
-static_assert(GDB <= MSTAGE && GKCAP / 2 + 256 <= MSTAGE, "general-path staging exceeds the merge area");
+constexpr int GDB = GEN_WORDS;
+constexpr float GD_SCALE = 16.0f;
+constexpr int GKCAP = 2 * LCAPC - 256;  // crossing-bucket keys staged (u32) before a 256-word histogram
+constexpr int GKCAP2 = LCAPC;           // crossing-bucket (key, position) pairs staged
 
 __device__ __forceinline__ int gp_dbucket(float z, float m) {
   const float d = __fmul_rn(__fsub_rn(m, z), GD_SCALE);
   return d < (float)(GDB - 1) ? (int)d : GDB - 1;
 }
 
-// One pass over the views: per distance bucket, the number (MASS false) or the fixed-point mass (MASS
+// One pass over the row: per distance bucket, the number (MASS false) or the fixed-point mass (MASS
 // true) of the finite values z >= lo.  Then the first bucket, from the top, at which the cumulative
 // reaches the target -- K for the count, p times the total for the mass -- with the cumulative of the
 // buckets before it.  Returns false when the target is never reached.
-template <bool MASS>
-__device__ __forceinline__ bool gp_level1(const SArgs& a, const SRow& R, SSm& s, int vec, float lo, float m,
-                                          double tgt, int& bb, uint64_t& before, uint64_t& total) {
-  uint64_t* h64 = s.m.key;
-  uint32_t* h32 = reinterpret_cast<uint32_t*>(s.m.key);
+template <bool MASS, class DT, bool SEG>
+__device__ __forceinline__ bool gp_level1(const SArgs& a, const SRow& R, SSm& s, float lo, float m, double tgt,
+                                          int& bb, uint64_t& before, uint64_t& total) {
+  uint64_t* h64 = s.c.gen;
+  uint32_t* h32 = reinterpret_cast<uint32_t*>(s.c.gen);
   for (int b = threadIdx.x; b < GDB; b += CT) {
     if (MASS) h64[b] = 0;
     else h32[b] = 0;
   }
   __syncthreads();
-  ViewSrc{a, R, s, vec}([&](float z) __attribute__((always_inline)) {
+  RowSrc<DT, SEG>{a, R, s}([&](float z) __attribute__((always_inline)) {
     if (z > -INFINITY && z >= lo) {
       const int b = gp_dbucket(z, m);
       if (MASS) atomicAdd(reinterpret_cast<unsigned long long*>(&h64[b]), (unsigned long long)mass_of(z, m));
@@ -728,13 +894,14 @@ __device__ __forceinline__ bool gp_level1(const SArgs& a, const SRow& R, SSm& s,
   return bb != 0x7fffffff;
 }
 
-// Pass two: the order keys of the finite values z >= lo of distance bucket bb, staged in LDS.  Returns
-// their number, or -1 when they do not fit.
-__device__ __forceinline__ int gp_gather(const SArgs& a, const SRow& R, SSm& s, int vec, float lo, float m, int bb) {
-  uint32_t* keys = reinterpret_cast<uint32_t*>(s.m.key);
+// Pass two: the order keys of the finite values z >= lo of distance bucket bb, staged in LDS (the list
+// area).  Returns their number, or -1 when they do not fit.
+template <class DT, bool SEG>
+__device__ __forceinline__ int gp_gather(const SArgs& a, const SRow& R, SSm& s, float lo, float m, int bb) {
+  uint32_t* keys = reinterpret_cast<uint32_t*>(s.c.list);
   if (threadIdx.x == 0) s.bc_i[2] = 0;
   __syncthreads();
-  ViewSrc{a, R, s, vec}([&](float z) __attribute__((always_inline)) {
+  RowSrc<DT, SEG>{a, R, s}([&](float z) __attribute__((always_inline)) {
     if (z > -INFINITY && z >= lo && gp_dbucket(z, m) == bb) {
       const int i = atomicAdd(&s.bc_i[2], 1);
       if (i < GKCAP) keys[i] = f2key(z);
@@ -748,54 +915,34 @@ __device__ __forceinline__ int gp_gather(const SArgs& a, const SRow& R, SSm& s, 
 
 // General path: the order key of the K-th largest finite value (counting duplicates), or 0 when there
 // are fewer than K: a count over the distance buckets, then the exact selection among the values of
-// the bucket holding it (over every view only when that bucket does not fit in LDS).
-__device__ __forceinline__ uint32_t gp_kth(const SArgs& a, const SRow& R, SSm& s, int vec, float m, int K) {
+// the bucket holding it (over the whole row only when that bucket does not fit in LDS).
+template <class DT, bool SEG>
+__device__ __forceinline__ uint32_t gp_kth(const SArgs& a, const SRow& R, SSm& s, float m, int K) {
   int bb;
   uint64_t before, total;
-  if (!gp_level1<false>(a, R, s, vec, -INFINITY, m, (double)K, bb, before, total)) return 0u;
-  const int n = gp_gather(a, R, s, vec, -INFINITY, m, bb);
+  if (!gp_level1<false, DT, SEG>(a, R, s, -INFINITY, m, (double)K, bb, before, total)) return 0u;
+  const int n = gp_gather<DT, SEG>(a, R, s, -INFINITY, m, bb);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(s.c.list) + GKCAP;
   if (n >= 0)
-    return gp_kth_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.m.key), n}, s,
-                      reinterpret_cast<uint32_t*>(s.m.key + GKCAP / 2), K - (int)before);
-  return gp_kth_key(ViewSrc{a, R, s, vec}, s, reinterpret_cast<uint32_t*>(s.m.key), K);
+    return gp_kth_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.c.list), n}, s, hist, K - (int)before);
+  return gp_kth_key(RowSrc<DT, SEG>{a, R, s}, s, reinterpret_cast<uint32_t*>(s.c.gen), K);
 }
 
 // General path: the order key of the nucleus' closing group among the values z >= tau2 (the first
 // group, in descending order, at which the cumulative mass reaches p times the mass of all of them),
 // or 0 when the cumulative never reaches it: a mass over the distance buckets, then the exact
 // selection inside the bucket where the cumulative crosses.
-__device__ __forceinline__ uint32_t gp_topp(const SArgs& a, const SRow& R, SSm& s, int vec, float tau2, float m,
-                                            double p) {
+template <class DT, bool SEG>
+__device__ __forceinline__ uint32_t gp_topp(const SArgs& a, const SRow& R, SSm& s, float tau2, float m, double p) {
   int bb;
   uint64_t before, total;
-  if (!gp_level1<true>(a, R, s, vec, tau2, m, p, bb, before, total)) return 0u;
+  if (!gp_level1<true, DT, SEG>(a, R, s, tau2, m, p, bb, before, total)) return 0u;
   const double target = p * (double)total;
-  const int n = gp_gather(a, R, s, vec, tau2, m, bb);
+  const int n = gp_gather<DT, SEG>(a, R, s, tau2, m, bb);
   if (n >= 0)
-    return gp_topp_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.m.key), n}, s, s.m.key + GKCAP / 2, tau2, m,
-                       target, (double)before);
-  return gp_topp_key(ViewSrc{a, R, s, vec}, s, s.m.key, tau2, m, target, 0.0);
-}
-
-// LDS of the merge area (64-bit words) in the general path: per-chunk kept masses of the draw at
-// GD_CM; the fused nucleus stages (key, position) pairs below GKCAP2 and its radix histogram after.
-constexpr int GD_CM = MSTAGE - MAXPC;
-constexpr int GKCAP2 = 1536;
-static_assert(GKCAP2 + 256 <= GD_CM && MAXPC + (CSLOTS * 8) / 16 + 1 <= GD_CM, "general-path LDS areas overlap");
-
-struct StagedPairs {  // (order key << 32 | position) pairs
-  const uint64_t* ent;
-  int n;
-  template <class F>
-  __device__ __forceinline__ void operator()(F&& f) const {
-    for (int i = (int)threadIdx.x; i < n; i += CT) f(key2f((uint32_t)(ent[i] >> 32)));
-  }
-};
-
-__device__ __forceinline__ int chunk_of(const SArgs& a, const SRow& R, int vec, int pos) {
-  int c = 0;
-  while (c < R.P - 1 && pos >= chunk_hi(a, R, c, vec)) ++c;
-  return c;
+    return gp_topp_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.c.list), n}, s, s.c.gen, tau2, m, target,
+                       (double)before);
+  return gp_topp_key(RowSrc<DT, SEG>{a, R, s}, s, s.c.gen, tau2, m, target, 0.0);
 }
 
 // The nucleus cut among the values z >= tau2 (as gp_topp), with the draw's per-chunk kept masses taken
@@ -805,21 +952,22 @@ __device__ __forceinline__ int chunk_of(const SArgs& a, const SRow& R, int vec, 
 // integers, so the masses equal those of a separate pass.  Returns false (nothing decided) when the
 // cumulative never reaches the target or the bucket does not fit in LDS; the caller then selects and
 // draws the separate way.
-__device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm& s, int vec, float tau2, float m,
-                                              double p, float& tau, int& last) {
+template <class DT, bool SEG>
+__device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm& s, float tau2, float m, double p,
+                                              float& tau, int& last) {
   int bb;
   uint64_t before, total;
-  if (!gp_level1<true>(a, R, s, vec, tau2, m, p, bb, before, total)) return false;
+  if (!gp_level1<true, DT, SEG>(a, R, s, tau2, m, p, bb, before, total)) return false;
   const double target = p * (double)total;
-  uint64_t* ent = s.m.key;
-  uint64_t* cm = s.m.key + GD_CM;
+  uint64_t* ent = s.c.list;
+  uint64_t* cm = s.cm;
   for (int c = threadIdx.x; c < R.P; c += CT) cm[c] = 0;
   if (threadIdx.x == 0) s.bc_i[2] = 0;
   __syncthreads();
   int lastp = -1;
   for (int c = 0; c < R.P; ++c) {
     uint64_t acc = 0;
-    for_view(a, R, s, c, vec, [&](float z, int pos) __attribute__((always_inline)) {
+    for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
       if (z > -INFINITY && z >= tau2) {
         const int b = gp_dbucket(z, m);
         if (b < bb) {
@@ -838,7 +986,7 @@ __device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm
   const int n = s.bc_i[2];
   __syncthreads();
   if (n > GKCAP2) return false;
-  const uint32_t kk = gp_topp_key(StagedPairs{ent, n}, s, s.m.key + GKCAP2, tau2, m, target, (double)before);
+  const uint32_t kk = gp_topp_key(StagedPairs{ent, n}, s, s.c.gen, tau2, m, target, (double)before);
   if (!kk) return false;  // not reached inside the crossing bucket: cannot happen, decided the separate way
   tau = fmaxf(tau2, key2f(kk));
   for (int i = threadIdx.x; i < n; i += CT) {
@@ -847,7 +995,7 @@ __device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm
     if (z >= tau) {
       const int pos = (int)(uint32_t)e;
       const uint64_t w = mass_of(z, m);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&cm[chunk_of(a, R, vec, pos)]), (unsigned long long)w);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&cm[chunk_of(a, R, DT::VEC, pos)]), (unsigned long long)w);
       if (w > 0) lastp = max(lastp, pos);
     }
   }
@@ -856,27 +1004,28 @@ __device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm
 }
 
 // General path: kept set S = {finite z >= tau}; draws the token with target u * Z_S in ascending id.
-// Returns the id (z in *zid).
-// masses_known: the per-chunk kept masses are already at GD_CM and `last` is the last position of
-// positive kept mass (the nucleus selection took them in its own pass).
-__device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, int vec, float tau, float m, float u,
-                                       float* zid, bool masses_known = false, int last = -1) {
-  const int P = R.P;
-  uint64_t* cm = s.m.key + GD_CM;  // per chunk mass
+// Returns the id (z in *zid).  masses_known: the per-chunk kept masses are already in s.cm and `last`
+// is the last position of positive kept mass (the nucleus selection took them in its own pass).
+template <class DT, bool SEG>
+__device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, float tau, float m, float u, float* zid,
+                                       bool masses_known, int last) {
+  constexpr int VEC = DT::VEC;
+  const int P = R.P, t = threadIdx.x;
+  uint64_t* cm = s.cm;  // per chunk mass
   if (!masses_known) {
-    for (int c = threadIdx.x; c < P; c += CT) cm[c] = 0;
+    for (int c = t; c < P; c += CT) cm[c] = 0;
     __syncthreads();
     last = -1;
     for (int c = 0; c < P; ++c) {
       uint64_t acc = 0;
-      for_view(a, R, s, c, vec, [&](float z, int pos) {
+      for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
         if (z > -INFINITY && z >= tau) {
           const uint64_t w = mass_of(z, m);
           acc += w;
           if (w > 0) last = max(last, pos);
         }
       });
-      atomicAdd(reinterpret_cast<unsigned long long*>(&cm[c]), (unsigned long long)acc);
+      if (acc) atomicAdd(reinterpret_cast<unsigned long long*>(&cm[c]), (unsigned long long)acc);
     }
     last = blk_max_i(last, s);
   }
@@ -892,106 +1041,150 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, in
   }
   __syncthreads();
   int id = -1;
+  float zf = -INFINITY;
   if (cs >= 0) {
-    const ChunkPub& pc = s.m.pub[cs];
-    if (pc.flags & PUB_DENSE) {
-      // the chunk in groups of 16 positions (aligned in the row): each group's kept mass from four
-      // 16-byte loads, an exclusive scan over the groups in position order, then the crossing group
-      // walked by the thread that holds it
-      const __amdgpu_buffer_rsrc_t rs = dense_rsrc(a, R.row);
-      const int lo = chunk_lo(a, R, cs, vec), hi = chunk_hi(a, R, cs, vec);
-      const int gf = lo >> 4, ng = ((hi - 1) >> 4) - gf + 1;
-      uint64_t* gm = s.m.key + MAXPC;  // per-group mass
-      auto kept_mass = [&](float z, int p) __attribute__((always_inline)) -> uint64_t {
-        return (p >= lo && p < hi && z > -INFINITY && z >= tau) ? mass_of(z, m) : 0ull;
-      };
-      for (int g = (int)threadIdx.x; g < ng; g += CT) {
-        const int p0 = (gf + g) << 4;
-        float4 v[4];
+    // chunk cs in ascending position, in batches of CT * GJ consecutive slots: thread t of a batch takes
+    // GJ consecutive slots (thread 0 of the first batch also the unaligned head before them, the last
+    // thread of the last batch the tail after them); each thread's kept mass, an exclusive scan in
+    // thread order; the batch holding the crossing has its crossing thread walk its positions
+    int64_t s0, s1;
+    chunk_range(a, R, cs, s0, s1);
+    const int ns = (int)(s1 - s0);
+    const int64_t e_base = (int64_t)R.head + (s0 - 1) * VEC;
+    float hx[8];
+    int hn = 0, hp0 = 0;
+    if (t == 0 && cs == 0) { hn = R.head; hp0 = 0; }
+    if (t == CT - 1 && cs == P - 1) { hn = R.V - R.tail_lo; hp0 = R.tail_lo; }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = ld_dense4(rs, (p0 >> 2) + q);
-        uint64_t w = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          w += kept_mass(v[q].x, p0 + 4 * q);
-          w += kept_mass(v[q].y, p0 + 4 * q + 1);
-          w += kept_mass(v[q].z, p0 + 4 * q + 2);
-          w += kept_mass(v[q].w, p0 + 4 * q + 3);
-        }
-        gm[g] = w;
-      }
-      __syncthreads();
-      const int per = (ng + CT - 1) / CT;  // consecutive groups per thread in the scan
-      const int g0 = (int)threadIdx.x * per, g1 = min(g0 + per, ng);
-      uint64_t mine = 0;
-      for (int g = g0; g < g1; ++g) mine += gm[g];
-      uint64_t tot;
-      uint64_t cum = before + blk_excl_scan_u64(mine, s, &tot);
-      int found = 0x7fffffff;
-      if ((double)(cum + mine) > target) {
-        int g = g0;
-        while (g < g1 - 1 && (double)(cum + gm[g]) <= target) cum += gm[g++];
-        const int p0 = (gf + g) << 4;
-        for (int q = 0; q < 16; ++q) {
-          const float z = ld_dense1(rs, p0 + q);
-          cum += kept_mass(z, p0 + q);
-          if ((double)cum > target) {
-            found = p0 + q;
-            break;
-          }
-        }
-      }
-      id = blk_min_i(found, s);
-      if (id == 0x7fffffff) id = -1;
-    } else {
-      // list view (at most LCAPC entries): staged in LDS, then the prefix of every kept entry in id
-      // order by counting
-      const uint64_t* lst = a.lists + (R.row * P + cs) * (int64_t)LCAPC;
-      const int n = pc.n_list;
-      uint64_t* lk = s.m.key + MAXPC;
-      for (int i = threadIdx.x; i < n; i += CT) lk[i] = ld_agent(lst + i);
-      __syncthreads();
-      int found = 0x7fffffff;
-      for (int i = threadIdx.x; i < n; i += CT) {
-        const uint64_t ki = lk[i];
-        const float zi = cand_z(ki);
-        if (!(zi > -INFINITY && zi >= tau)) continue;
-        const int pi = cand_pos(ki);
-        uint64_t pre = before;
-        for (int j = 0; j < n; ++j) {
-          const uint64_t kj = lk[j];
-          const float zj = cand_z(kj);
-          if (zj > -INFINITY && zj >= tau && cand_pos(kj) <= pi) pre += mass_of(zj, m);
-        }
-        if ((double)pre > target) found = min(found, pi);
-      }
-      id = blk_min_i(found, s);
-      if (id == 0x7fffffff) id = -1;
+    for (int q = 0; q < 8; ++q) hx[q] = hn > 0 ? load_elem<DT, SEG>(a, R, hp0 + min(q, hn - 1)) : 0.0f;
+    if (R.pen_on) {
+      uint32_t fl = 0;
+      const int32_t none[1] = {0};
+      build_overlay<0>(a, R, s, cs, s0, s1, VEC, none, &fl);
     }
+    const float r = R.r;
+    auto value = [&](float x, int pos) __attribute__((always_inline)) -> float {
+      if (R.pen_on) {
+        const int rk = overlay_rank(s, (int)(pos - e_base));
+        if (rk >= 0) x = penalise_cv(x, s.c.p.xval[rk], R.rep, R.freq, R.pres);
+      }
+      return canon(x, r);
+    };
+    auto kept = [&](float z) __attribute__((always_inline)) -> uint64_t {
+      return (z > -INFINITY && z >= tau) ? mass_of(z, m) : 0ull;
+    };
+    const int nbat = max(1, (ns + CT * GJ - 1) / (CT * GJ));  // a chunk of head and tail alone: one batch
+    uint64_t cum0 = before;
+    for (int bt = 0; bt < nbat; ++bt) {
+      const int b0 = bt * CT * GJ;
+      const int nb = min(ns - b0, CT * GJ);
+      uint4 d[GJ];
+      static_for<GJ>([&](auto J) {  // unconditional loads (clamped into the batch, or the records' first word)
+        constexpr int j = decltype(J)::value;
+        d[j] = *(nb > 0 ? slot_ptr<DT, SEG>(a, R, s0 + b0 + min(t * GJ + j, nb - 1))
+                        : reinterpret_cast<const uint4*>(a.rec));
+      });
+      const bool head_here = t == 0 && cs == 0 && bt == 0;
+      const bool tail_here = t == CT - 1 && cs == P - 1 && bt == nbat - 1;
+      // walk(f): this thread's positions of the batch in ascending order
+      auto walk = [&](auto&& f) __attribute__((always_inline)) {
+        if (head_here)
+          for (int q = 0; q < hn; ++q) f(value(hx[q], hp0 + q), hp0 + q);
+        static_for<GJ>([&](auto J) {
+          constexpr int j = decltype(J)::value;
+          if (t * GJ + j < nb) {
+            const int p0 = R.head + (int)(s0 + b0 + t * GJ + j) * VEC;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) f(value(elem<DT>(d[j], e), p0 + e), p0 + e);
+          }
+        });
+        if (tail_here)
+          for (int q = 0; q < hn; ++q) f(value(hx[q], hp0 + q), hp0 + q);
+      };
+      uint64_t mine = 0;
+      walk([&](float z, int) __attribute__((always_inline)) { mine += kept(z); });
+      uint64_t tot;
+      uint64_t cum = cum0 + blk_excl_scan_u64(mine, s, &tot);
+      int found = 0x7fffffff;
+      float zfound = -INFINITY;
+      if ((double)cum <= target && (double)(cum + mine) > target) {
+        bool done = false;
+        walk([&](float z, int pos) __attribute__((always_inline)) {
+          if (!done) {
+            cum += kept(z);
+            if ((double)cum > target) {
+              done = true;
+              found = pos;
+              zfound = z;
+            }
+          }
+        });
+      }
+      const int idb = blk_min_i(found, s);
+      if (found == idb && idb != 0x7fffffff) s.bc_f[0] = zfound;
+      __syncthreads();
+      if (idb != 0x7fffffff) {  // the same for every thread
+        id = idb;
+        zf = s.bc_f[0];
+        break;
+      }
+      cum0 += tot;
+    }
+    __syncthreads();  // the overlay and bc_f are free again
   }
-  if (id < 0) id = last;
-  // its value
-  if (threadIdx.x == 0) s.bc_f[0] = -INFINITY;
-  __syncthreads();
-  for (int c = 0; c < P; ++c) {
-    if (id < chunk_lo(a, R, c, vec) || id >= chunk_hi(a, R, c, vec)) continue;
-    if (s.m.pub[c].flags & PUB_DENSE) {
-      if (threadIdx.x == 0) s.bc_f[0] = ld_agent(a.dense + R.row * a.Vp + id);
-    } else {
-      for_view(a, R, s, c, vec, [&](float z, int pos) {
+  if (id < 0) {
+    id = last;
+    // its value: a re-read of its chunk
+    if (threadIdx.x == 0) s.bc_f[0] = -INFINITY;
+    __syncthreads();
+    if (id >= 0) {
+      for_chunk<DT, SEG>(a, R, s, chunk_of(a, R, VEC, id), [&](float z, int pos) __attribute__((always_inline)) {
         if (pos == id) s.bc_f[0] = z;
       });
     }
+    __syncthreads();
+    zf = s.bc_f[0];
+    __syncthreads();
   }
-  __syncthreads();
-  *zid = s.bc_f[0];
-  __syncthreads();
+  *zid = zf;
   return id;
 }
 
+// The general path of a row with no small kept-set bound: the top-k threshold, the nucleus and the draw
+// over re-reads of the row.  Returns (id, bits of its z).
+template <class DT, bool SEG>
+__device__ __forceinline__ int2 resolve_general(const SArgs& a, const SRow& R, SSm& s, float m, float tau_m, float u) {
+  float tau_k = -INFINITY;
+  if (R.kon) {
+    const uint32_t kk = gp_kth<DT, SEG>(a, R, s, m, R.k);
+    tau_k = kk ? key2f(kk) : -INFINITY;
+  }
+  const float tau2 = fmaxf(tau_k, tau_m);
+  float tau = tau2;
+  bool fused = false;
+  int last = -1;
+  if (R.topp_on) {
+    if (!(R.p > 0.0f)) {
+      tau = m;  // p <= 0: the top group only
+    } else {
+      fused = gp_topp_fused<DT, SEG>(a, R, s, tau2, m, (double)R.p, tau, last);
+      if (!fused) {
+        const uint32_t kk = gp_topp<DT, SEG>(a, R, s, tau2, m, (double)R.p);
+        tau = kk ? fmaxf(tau2, key2f(kk)) : tau2;
+      }
+    }
+  }
+  float zid = -INFINITY;
+  const int id = gp_draw<DT, SEG>(a, R, s, tau, m, u, &zid, fused, last);
+  return make_int2(id, __float_as_int(zid));
+}
+
+// ----------------------------------------------------------------------------------------------
+// The row's resolution by its last chunk workgroup
+// ----------------------------------------------------------------------------------------------
 template <class DT, bool SEG>
 __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& s) {
-  const int t = threadIdx.x, P = R.P, VEC = DT::VEC;
+  const int t = threadIdx.x, P = R.P;
   const int64_t row = R.row;
   const int nt = a.n_top;
   // ---- one round trip: the chunk records, the row's uniform and the heads of the chunk lists ----
@@ -1007,22 +1200,11 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       sp.v[q] = 0;
       if (f < P * sp.E) {
         const int c = f / sp.E;
-        sp.v[q] = ld_agent(base + (int64_t)c * LCAPC + (f - c * sp.E));
+        sp.v[q] = base[(int64_t)c * LCAPC + (f - c * sp.E)];
       }
     }
   }
-  if (t < P) {
-    const ChunkPub* g = a.pub + row * P + t;
-    ChunkPub& q = s.m.pub[t];
-    q.zmax = ld_agent(&g->zmax);
-    q.mref = ld_agent(&g->mref);
-    q.s = ld_agent(&g->s);
-    q.flags = ld_agent(&g->flags);
-    q.argpos = ld_agent(&g->argpos);
-    q.n_list = ld_agent(&g->n_list);
-    q.qk = ld_agent(&g->qk);
-    q.qn = ld_agent(&g->qn);
-  }
+  if (t < P) s.pub[t] = rec_load(a.rec + (row * P + t) * REC_WORDS);
   float u = 0.0f;
   if (a.rng_on) {
     const uint64_t seq = a.seq_ids ? (uint64_t)a.seq_ids[row] : (uint64_t)row;
@@ -1034,18 +1216,18 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
   // row totals, in chunk order (every thread computes the same)
   float m = -INFINITY, mref = MREF0, S = 0.0f;
   uint32_t flags = R.flags;
-  bool fin = false, dense_any = false;
+  bool fin = false, over_any = false;
   int argpos = -1;
   for (int c = 0; c < P; ++c) {
-    const ChunkPub& q = s.m.pub[c];
+    const ChunkPub& q = s.pub[c];
     m = fmaxf(m, q.zmax);
     lse_add(mref, S, q.mref, q.s);
     flags |= q.flags & (FLAG_BAD_INPUT | FLAG_LIMIT);
     fin = fin || (q.flags & PUB_FINITE);
-    dense_any = dense_any || (q.flags & PUB_DENSE);
+    over_any = over_any || (q.flags & PUB_OVER);
   }
   for (int c = 0; c < P; ++c)
-    if (s.m.pub[c].zmax == m) { argpos = s.m.pub[c].argpos; break; }
+    if (s.pub[c].zmax == m) { argpos = s.pub[c].argpos; break; }
   if (a.st_flags) flags |= a.st_flags[row] & (FLAG_BAD_INPUT | FLAG_BAD_PARAM | FLAG_LIMIT);
   const bool empty = !fin;
   if (empty) flags |= FLAG_EMPTY;
@@ -1059,11 +1241,11 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
     }
     if (!empty) {
       float lo = INFINITY;
-      for (int c = 0; c < P; ++c) lo = fminf(lo, s.m.pub[c].qn);
+      for (int c = 0; c < P; ++c) lo = fminf(lo, s.pub[c].qn);
       const int ns = stage_entries(a, R, s, sp, lo, nt, MSTAGE);
       for (int f = t; f < ns; f += CT) {
-        const uint64_t key = s.m.key[f];
-        const int rk = count_above(s.m.key, ns, key);
+        const uint64_t key = s.key[f];
+        const int rk = count_above(s.key, ns, key);
         if (rk < nt) {
           s.top_id[rk] = cand_pos(key);
           s.top_lp[rk] = (float)((double)cand_z(key) - (double)m - L);
@@ -1088,11 +1270,11 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
     // ---- the kept set from the lists when it is small; otherwise the general path ----
     const bool s2b = R.kon || R.minp_on;
     const float tau_m = R.minp_on ? __fadd_rn(m, (float)log((double)R.minp)) : -INFINITY;
-    bool general = !s2b || dense_any;
+    bool general = !s2b || over_any;
     // kept set S2: A[i] = (order key of z << 32) | mass, Bk[i] = (position << 32) | mass kept by the
     // nucleus; masses 2^((z - m) L2E) in units of 2^-31
-    uint64_t* A = s.m.key + (MSTAGE - 2 * MCAP);
-    uint64_t* Bk = s.m.key + (MSTAGE - MCAP);
+    uint64_t* A = s.key + (MSTAGE - 2 * MCAP);
+    uint64_t* Bk = s.key + (MSTAGE - MCAP);
     int n2 = 0;
     if (!general) {
       float tau2 = tau_m;
@@ -1100,7 +1282,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       float zthr = tau_m;
       if (R.kon) {
         float lo = INFINITY;
-        for (int c = 0; c < P; ++c) lo = fminf(lo, s.m.pub[c].qk);
+        for (int c = 0; c < P; ++c) lo = fminf(lo, s.pub[c].qk);
         zthr = fmaxf(zthr, lo);
       }
       const int ns = stage_entries(a, R, s, sp, zthr, imax, MSTAGE - 2 * MCAP);
@@ -1111,18 +1293,18 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
           if (t == 0) s.bc_f[1] = -INFINITY;
           __syncthreads();
           for (int f = t; f < ns; f += CT)
-            if (count_above(s.m.key, ns, s.m.key[f]) == R.k - 1) s.bc_f[1] = cand_z(s.m.key[f]);
+            if (count_above(s.key, ns, s.key[f]) == R.k - 1) s.bc_f[1] = cand_z(s.key[f]);
           __syncthreads();
           tau2 = fmaxf(tau2, s.bc_f[1]);
         }
         // a list cut off at imax whose last taken entry is kept may hold more of a tie at tau_k
         bool cutkept = false;
         for (int c = 0; c < P; ++c)
-          if (s.m.cut[c] && __int_as_float(s.m.cnt[c]) >= tau2) cutkept = true;
+          if (s.cut[c] && __int_as_float(s.cnt[c]) >= tau2) cutkept = true;
         if (t == 0) s.bc_i[2] = 0;
         __syncthreads();
         for (int f = t; f < ns; f += CT) {
-          const uint64_t key = s.m.key[f];
+          const uint64_t key = s.key[f];
           const float z = cand_z(key);
           if (z >= tau2) {
             const int idx = atomicAdd(&s.bc_i[2], 1);
@@ -1188,49 +1370,20 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       __syncthreads();
       zid = s.bc_f[2];
     } else {
-      // ---- general path over the chunk views ----
-      float tau_k = -INFINITY;
-      if (R.kon) {
-        const uint32_t kk = gp_kth(a, R, s, VEC, m, R.k);
-        tau_k = kk ? key2f(kk) : -INFINITY;
-      }
-      const float tau2 = fmaxf(tau_k, tau_m);
-      float tau = tau2;
-      bool fused = false;
-      int last = -1;
-      if (R.topp_on) {
-        if (!(R.p > 0.0f)) {
-          tau = m;  // p <= 0: the top group only
-        } else {
-          fused = gp_topp_fused(a, R, s, VEC, tau2, m, (double)R.p, tau, last);
-          if (!fused) {
-            const uint32_t kk = gp_topp(a, R, s, VEC, tau2, m, (double)R.p);
-            tau = kk ? fmaxf(tau2, key2f(kk)) : tau2;
-          }
-        }
-      }
-      id = gp_draw(a, R, s, VEC, tau, m, u, &zid, fused, last);
+      const int2 r2 = resolve_general<DT, SEG>(a, R, s, m, tau_m, u);
+      id = r2.x;
+      zid = __int_as_float(r2.y);
     }
   }
-  // leave the workspace as it was found: zero the row's chunk records, lists and dense values
+  // leave the workspace as it was found: zero the row's chunk records and lists
   {
     uint64_t* lbase = a.lists + (row * P) * (int64_t)LCAPC;
     for (int c = 0; c < P; ++c) {
-      const int n = s.m.pub[c].n_list;
-      for (int i = t; i < n; i += CT) st_agent(lbase + (int64_t)c * LCAPC + i, (uint64_t)0);
-      if (s.m.pub[c].flags & PUB_DENSE) {
-        float* drow = a.dense + row * a.Vp;
-        const __amdgpu_buffer_rsrc_t drs = dense_rsrc(a, row);
-        const int lo = chunk_lo(a, R, c, VEC), hi = chunk_hi(a, R, c, VEC);
-        // the unaligned ends one by one, the 16-byte aligned middle four at a time
-        const int a0 = min((lo + 3) & ~3, hi), a1 = max(hi & ~3, a0);
-        for (int p = lo + t; p < a0; p += CT) st_agent(drow + p, 0.0f);
-        for (int p = a1 + t; p < hi; p += CT) st_agent(drow + p, 0.0f);
-        for (int p = a0 + 4 * t; p < a1; p += 4 * CT) st_dense4(drs, p, 0.f, 0.f, 0.f, 0.f);
-      }
+      const int n = min(s.pub[c].n_list, LCAPC);
+      for (int i = t; i < n; i += CT) lbase[(int64_t)c * LCAPC + i] = 0;
     }
-    uint32_t* pw = reinterpret_cast<uint32_t*>(a.pub + row * P);
-    for (int i = t; i < P * (int)(sizeof(ChunkPub) / 4); i += CT) st_agent(pw + i, 0u);
+    uint64_t* rw = a.rec + row * P * REC_WORDS;
+    for (int i = t; i < P * REC_WORDS; i += CT) rw[i] = 0;
   }
   if (t == 0) {
     float lp = -INFINITY;
@@ -1242,7 +1395,6 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
       const int32_t dst = a.backfill_dest[row];
       if (dst >= 0 && (int64_t)dst < a.next_len) a.next_tokens[dst] = id;
     }
-    st_agent(&a.ctr[row], 0u);  // the workspace is left zeroed
   }
 }
 
@@ -1250,7 +1402,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
 // The kernel: one workgroup per (row, chunk)
 // ----------------------------------------------------------------------------------------------
 template <class DT, bool SEG>
-__global__ __launch_bounds__(CT) void k_split(SArgs a) {
+__global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
   __shared__ SSm s;
   const int t = threadIdx.x;
   constexpr int VEC = DT::VEC;
@@ -1263,23 +1415,33 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
 
   // ---- the row's history first (HPT ids per thread, in registers): waiting for these loads then
   //      never waits for the row data issued after them (the vector memory counter is in order) ----
+  // Loads are unconditional (indices clamped into range) so that none waits for another: a load under
+  // a per-lane branch is followed by a wait for it before the branch closes.
+  // Loads are unconditional (indices clamped into range, or a dummy address when there is nothing to
+  // read: the workspace's first bytes, always valid) so that none waits for another -- a load under a
+  // branch is followed by a wait for it before the branch closes.
+  const void* dummy = a.rec;
   constexpr int HPT = 8;
-  const int32_t* hid = a.prm.hist_ids;
   int32_t hreg[HPT];
-  static_for<HPT>([&](auto Q) {
-    constexpr int q = decltype(Q)::value;
-    const int64_t h = R.h_lo + t + (int64_t)q * CT;
-    hreg[q] = (R.pen_on && h < R.h_hi) ? hid[h] : 0;
-  });
+  const int nh = R.pen_on ? (int)min(R.h_hi - R.h_lo, (int64_t)HPT * CT) : 0;  // ids held in hreg
+  {
+    const int32_t* hrow = nh > 0 ? a.prm.hist_ids + R.h_lo : static_cast<const int32_t*>(dummy);
+    static_for<HPT>([&](auto Q) {
+      constexpr int q = decltype(Q)::value;
+      hreg[q] = hrow[min(t + q * CT, max(nh - 1, 0))];
+    });
+  }
   asm volatile("" ::: "memory");  // the row loads stay behind the history loads
 
-  // ---- every slot of the chunk: one 16-byte load each, all in flight before any use ----
+  // ---- every slot of the chunk: one 16-byte non-temporal load each, all in flight before any use ----
+  const int ns = (int)(R.s1 - R.s0);  // body slots of the chunk; slot j of thread t is j * CT + t
   uint4 d[CJ];
   static_for<CJ>([&](auto J) {
     constexpr int j = decltype(J)::value;
-    const int64_t slot = R.s0 + (int64_t)j * CT + t;
-    if (slot < R.s1) d[j] = *slot_ptr<DT, SEG>(a, R, slot);
-    else d[j] = make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG);
+    const uint4* sp = ns > 0 ? slot_ptr<DT, SEG>(a, R, R.s0 + min(j * CT + t, ns - 1)) : static_cast<const uint4*>(dummy);
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(sp));
+    d[j] = make_uint4(v.x, v.y, v.z, v.w);
   });
 
   if (t < HXN) s.hx_pos[t] = -1;
@@ -1288,101 +1450,19 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     s.flags = 0;
   }
 
-  // ---- penalty overlay: presence bitmap, numbering by word prefix counts, counts by number ----
+  // ---- penalty overlay of the chunk's range ----
   const int64_t e_base = (int64_t)R.head + (R.s0 - 1) * VEC;  // row position of bitmap bit 0
   const int nwords = (int)(((R.s1 - R.s0 + 2) * VEC + 31) >> 5);
   int n_x = 0;  // penalised extras
-  if (R.pen_on) {
-    for (int w = t; w < nwords; w += CT) s.c.bitmap[w] = 0;
-    for (int i = t; i < XCAP; i += CT) s.c.xval[i] = 0;
-    __syncthreads();
-    const int64_t e_lo = c == 0 ? 0 : (int64_t)R.head + R.s0 * VEC;
-    const int64_t e_hi = c == R.P - 1 ? (int64_t)R.V : (int64_t)R.head + R.s1 * VEC;
-    uint32_t bad = 0;
-    // ids [lo, hi) of an array, IDU loads per thread in flight before any is used (unconditional:
-    // an index past the range reloads the first of the group); f(id, index)
-    constexpr int IDU = 4;
-    auto for_ids = [&](const int32_t* ids, int64_t lo, int64_t hi, auto&& f) __attribute__((always_inline)) {
-      for (int64_t h0 = lo + t; h0 < hi; h0 += IDU * (int64_t)CT) {
-        int32_t v[IDU];
-#pragma unroll
-        for (int q = 0; q < IDU; ++q) {
-          const int64_t h = h0 + (int64_t)q * CT;
-          v[q] = ids[h < hi ? h : h0];
-        }
-#pragma unroll
-        for (int q = 0; q < IDU; ++q) {
-          const int64_t h = h0 + (int64_t)q * CT;
-          if (h < hi) f(v[q], h);
-        }
-      }
-    };
-    auto mark = [&](int32_t id) {
-      if (id < 0 || id >= R.V) {
-        bad = 1;
-      } else if (id >= e_lo && id < e_hi) {
-        const int b = (int)(id - e_base);
-        atomicOr(&s.c.bitmap[b >> 5], 1u << (b & 31));
-      }
-    };
-    static_for<HPT>([&](auto Q) {
-      constexpr int q = decltype(Q)::value;
-      if (R.h_lo + t + (int64_t)q * CT < R.h_hi) mark(hreg[q]);
-    });
-    const int64_t h_tail = R.h_lo + (int64_t)HPT * CT;  // history ids past the register copy
-    for_ids(hid, h_tail, R.h_hi, [&](int32_t id, int64_t) { mark(id); });
-    for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { mark(id); });
-    const int32_t* st_row = a.st_ids + row * a.st_cap;
-    for_ids(st_row, 0, R.st_n, [&](int32_t id, int64_t) { mark(id); });
-    if (bad) atomicOr(&s.flags, FLAG_BAD_INPUT);
-    __syncthreads();
-    const int wpt = (nwords + CT - 1) / CT;
-    const int w0 = t * wpt;
-    int loc = 0;
-    for (int q = 0; q < wpt; ++q)
-      if (w0 + q < nwords) loc += __popc(s.c.bitmap[w0 + q]);
-    int tot;
-    int ex = blk_excl_scan_i(loc, s, &tot);
-    for (int q = 0; q < wpt; ++q)
-      if (w0 + q < nwords) {
-        s.c.wpref[w0 + q] = (uint16_t)ex;
-        ex += __popc(s.c.bitmap[w0 + q]);
-      }
-    n_x = tot < XCAP ? tot : XCAP;
-    if (tot > XCAP && t == 0) atomicOr(&s.flags, FLAG_LIMIT);
-    __syncthreads();
-    // per numbered position: the output count in bits 0-30, the prompt mark in bit 31
-    auto count = [&](int32_t id, uint32_t add, uint32_t mark_bits) {
-      if (id >= e_lo && id < e_hi) {
-        const int b = (int)(id - e_base);
-        const int w = b >> 5;
-        const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
-        if (rank < XCAP) {
-          if (add) atomicAdd(&s.c.xval[rank], add);
-          if (mark_bits) atomicOr(&s.c.xval[rank], mark_bits);
-        }
-      }
-    };
-    static_for<HPT>([&](auto Q) {
-      constexpr int q = decltype(Q)::value;
-      if (R.h_lo + t + (int64_t)q * CT < R.h_hi) count(hreg[q], 1u, 0u);
-    });
-    for_ids(hid, h_tail, R.h_hi, [&](int32_t id, int64_t) { count(id, 1u, 0u); });
-    for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { count(id, 0u, 0x80000000u); });
-    const int32_t* st_cnt = reinterpret_cast<const int32_t*>(a.st_counts + row * a.st_cap);
-    for_ids(st_cnt, 0, R.st_n, [&](int32_t cvi, int64_t e) {
-      const uint32_t cv = (uint32_t)cvi;
-      count(st_row[e], cv & 0x7fffffffu, cv & 0x80000000u);
-    });
-    __syncthreads();
-  }
+  uint32_t tfl = 0;
+  if (R.pen_on) n_x = build_overlay<HPT>(a, R, s, c, R.s0, R.s1, VEC, hreg, &tfl);
+  if (tfl) atomicOr(&s.flags, tfl);
 
   // ---- one pass over the slots in arrival order: the penalised elements leave the registers for
   //      the extras, then the slot's maximum and its exponentials against a running reference
   //      (moved to each new thread maximum, with the sum rescaled), so the pass keeps pace with the
   //      loads instead of waiting for the whole chunk ----
   const float r = R.r;
-  float smax[CJ];
   float xref = -INFINITY;       // running maximum of x
   float mref_t = MREF0;         // fl32(fl32(xref r) L2E), the exponent reference
   float acc0 = 0.0f, acc1 = 0.0f;
@@ -1393,21 +1473,21 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
       asm volatile("" : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3));
       d[j] = make_uint4(x0, x1, x2, x3);
     }
+    if ((j + 1) * CT > ns && j * CT + t >= ns) d[j] = make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG);
     if (R.pen_on) {
-      const int64_t slot = R.s0 + (int64_t)j * CT + t;
-      if (slot < R.s1) {
-        const int b0 = (int)(slot - R.s0 + 1) * VEC;
-        const uint32_t bits = (s.c.bitmap[b0 >> 5] >> (b0 & 31)) & ((1u << VEC) - 1u);
+      if (j * CT + t < ns) {
+        const int b0 = (j * CT + t + 1) * VEC;
+        const uint32_t bits = (s.c.p.bitmap[b0 >> 5] >> (b0 & 31)) & ((1u << VEC) - 1u);
         if (bits) {
           uint32_t applied = 0;
 #pragma unroll
           for (int e = 0; e < VEC; ++e) {
             if ((bits >> e) & 1u) {
               const int b = b0 + e, w = b >> 5;
-              const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
+              const int rank = (int)s.c.p.wpref[w] + __popc(s.c.p.bitmap[w] & ((1u << (b & 31)) - 1u));
               if (rank < XCAP) {
                 const float x = elem<DT>(d[j], e);
-                s.c.xval[rank] = __float_as_uint(penalise_cv(x, s.c.xval[rank], R.rep, R.freq, R.pres));
+                s.c.p.xval[rank] = __float_as_uint(penalise_cv(x, s.c.p.xval[rank], R.rep, R.freq, R.pres));
                 applied |= 1u << e;
               }
             }
@@ -1423,7 +1503,6 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     float v = elem<DT>(d[j], 0);
 #pragma unroll
     for (int e = 1; e < VEC; ++e) v = fmaxf(v, elem<DT>(d[j], e));
-    smax[j] = v;
     if (v > xref) {
       xref = v;
       const float mnew = __fmul_rn(__fmul_rn(v, r), L2E);
@@ -1447,13 +1526,10 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
       const float x = load_elem<DT, SEG>(a, R, pos);
       bool pen = false;
       if (R.pen_on) {
-        const int b = (int)(pos - e_base), w = b >> 5;
-        if ((s.c.bitmap[w] >> (b & 31)) & 1u) {
-          const int rank = (int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u));
-          if (rank < XCAP) {
-            s.c.xval[rank] = __float_as_uint(penalise_cv(x, s.c.xval[rank], R.rep, R.freq, R.pres));
-            pen = true;
-          }
+        const int rank = overlay_rank(s, (int)(pos - e_base));
+        if (rank >= 0) {
+          s.c.p.xval[rank] = __float_as_uint(penalise_cv(x, s.c.p.xval[rank], R.rep, R.freq, R.pres));
+          pen = true;
         }
       }
       if (!pen) {
@@ -1467,7 +1543,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
   const bool own_hx = t < HXN && s.hx_pos[t] >= 0;
   {
     float xe = -INFINITY;
-    for (int i = t; i < n_x; i += CT) xe = fmaxf(xe, __uint_as_float(s.c.xval[i]));
+    for (int i = t; i < n_x; i += CT) xe = fmaxf(xe, __uint_as_float(s.c.p.xval[i]));
     if (own_hx) xe = fmaxf(xe, s.hx_val[t]);
     if (xe > xref) {
       xref = xe;
@@ -1478,7 +1554,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
       mref_t = mnew;
     }
     for (int i = t; i < n_x; i += CT)
-      acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(__fmul_rn(__uint_as_float(s.c.xval[i]), r), L2E, -mref_t));
+      acc0 += __builtin_amdgcn_exp2f(__builtin_fmaf(__fmul_rn(__uint_as_float(s.c.p.xval[i]), r), L2E, -mref_t));
     if (own_hx) acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(__fmul_rn(s.hx_val[t], r), L2E, -mref_t));
   }
   const float zt = canon(xref, r);
@@ -1513,11 +1589,10 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
 #pragma unroll
       for (int e = 0; e < VEC; ++e) f |= isfinite(canon(elem<DT>(d[j], e), r)) ? 1u : 0u;
     });
-    for (int i = t; i < n_x; i += CT) f |= isfinite(canon(__uint_as_float(s.c.xval[i]), r)) ? 1u : 0u;
+    for (int i = t; i < n_x; i += CT) f |= isfinite(canon(__uint_as_float(s.c.p.xval[i]), r)) ? 1u : 0u;
     if (own_hx) f |= isfinite(canon(s.hx_val[t], r)) ? 1u : 0u;
     has_fin = blk_or(f, s) != 0;
   }
-
   reload_barrier(d);
   // ---- greedy rows: lowest position of the maximum ----
   int argpos = -1;
@@ -1526,14 +1601,14 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     static_for<CJ>([&](auto J) {
       constexpr int j = decltype(J)::value;
       const int64_t slot = R.s0 + (int64_t)j * CT + t;
-      if (best == 0x7fffffff && smax[j] == zmax && slot < R.s1) {
+      if (best == 0x7fffffff && slot < R.s1) {
         #pragma unroll
         for (int e = VEC - 1; e >= 0; --e)
           if (canon(elem<DT>(d[j], e), 1.0f) == zmax) best = R.head + (int)slot * VEC + e;
       }
     });
     for (int i = t; i < n_x; i += CT)
-      if (canon(__uint_as_float(s.c.xval[i]), 1.0f) == zmax) best = min(best, pos_of_rank(s, nwords, e_base, i));
+      if (canon(__uint_as_float(s.c.p.xval[i]), 1.0f) == zmax) best = min(best, pos_of_rank(s, nwords, e_base, i));
     if (own_hx && canon(s.hx_val[t], 1.0f) == zmax) best = min(best, s.hx_pos[t]);
     argpos = blk_min_i(best, s);
   }
@@ -1542,15 +1617,16 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
   const int Kk = R.kon ? R.k : 0, Kn = a.n_top;
   const bool s2b = !R.greedy && (R.kon || R.minp_on);
   const bool want_list = s2b || Kn > 0;
-  const bool want_dense = !R.greedy && !s2b;
   float bound = INFINITY;
   if (want_list) {
     float bk = -INFINITY, bn = -INFINITY;
-    const int Rk = (Kk + CW - 1) / CW, Rn = (Kn + CW - 1) / CW;
     if (Kk > 0 || Kn > 0) {
-      // bitonic sort of the 64 thread maxima of the wave, descending in lane order
+      // The K-th largest of the CT thread maxima bounds the chunk's K-th largest value from below (K
+      // threads hold a value at least that large).  Each wave sorts its 64 maxima (bitonic, descending
+      // in lane order); every maximum then finds its rank in the workgroup's order (value descending,
+      // then wave, then lane) by binary searches in the other waves' sorted lists.
       float v = zt;
-      const int l = lane_id();
+      const int l = lane_id(), w = wave_id();
 #pragma unroll
       for (int kk = 2; kk <= 64; kk <<= 1) {
 #pragma unroll
@@ -1560,16 +1636,30 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
           v = take_max ? fmaxf(v, o) : fminf(v, o);
         }
       }
-      const float wk = (Kk > 0 && Rk <= 64) ? lane_f32(v, Rk - 1) : -INFINITY;
-      const float wn = (Kn > 0 && Rn <= 64) ? lane_f32(v, Rn - 1) : -INFINITY;
-      __syncthreads();
-      if (l == 0) {
-        s.wred[0][wave_id()] = wk;
-        s.wred[1][wave_id()] = wn;
+      s.tmx[w][l] = v;
+      if (t == 0) {
+        s.kb[0] = -INFINITY;
+        s.kb[1] = -INFINITY;
       }
       __syncthreads();
-      bk = fminf(fminf(s.wred[0][0], s.wred[0][1]), fminf(s.wred[0][2], s.wred[0][3]));
-      bn = fminf(fminf(s.wred[1][0], s.wred[1][1]), fminf(s.wred[1][2], s.wred[1][3]));
+      int rank = l;
+#pragma unroll
+      for (int w2 = 0; w2 < CW; ++w2) {
+        if (w2 == w) continue;
+        int lo = 0, hi = 64;  // entries of wave w2 ordered before v form a prefix of its list
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          const float x = s.tmx[w2][mid];
+          if (x > v || (x == v && w2 < w)) lo = mid + 1;
+          else hi = mid;
+        }
+        rank += lo;
+      }
+      if (Kk > 0 && rank == Kk - 1) s.kb[0] = v;
+      if (Kn > 0 && rank == Kn - 1) s.kb[1] = v;
+      __syncthreads();
+      bk = s.kb[0];  // -inf when K exceeds the thread count
+      bn = s.kb[1];
     }
     if (s2b) {
       const float bm = R.minp_on ? __fadd_rn(zmax, (float)log((double)R.minp)) : -INFINITY;
@@ -1589,7 +1679,10 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     uint32_t pm = 0;
     static_for<CJ>([&](auto J) {
       constexpr int j = decltype(J)::value;
-      if (smax[j] > -INFINITY && canon(smax[j], r) >= bound) pm |= 1u << j;
+      float v = elem<DT>(d[j], 0);
+#pragma unroll
+      for (int e = 1; e < VEC; ++e) v = fmaxf(v, elem<DT>(d[j], e));
+      if (v > -INFINITY && canon(v, r) >= bound) pm |= 1u << j;
     });
     reload_barrier(d);
     while (pm) {
@@ -1613,7 +1706,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
       }
     }
     for (int i = t; i < n_x; i += CT) {
-      const float z = canon(__uint_as_float(s.c.xval[i]), r);
+      const float z = canon(__uint_as_float(s.c.p.xval[i]), r);
       if (z > -INFINITY && z >= bound) {
         const int idx = atomicAdd(&s.n_list, 1);
         if (idx < LCAPC) s.c.list[idx] = cand_key(z, pos_of_rank(s, nwords, e_base, i));
@@ -1646,7 +1739,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     for (int i = t; i < n_list; i += CT) {
       const uint64_t key = s.c.list[i];
       const int rank = count_above(s.c.list, n_list, key);
-      st_agent(glist + rank, key);
+      glist[rank] = key;
       if (rank == qki) s.bc_f[0] = cand_z(key);
       if (rank == qni) s.bc_f[1] = cand_z(key);
     }
@@ -1654,7 +1747,8 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     qk = s.bc_f[0];
     qn = s.bc_f[1];
   } else if (want_list) {
-    // too many candidates (ties): the dense row stands for the kept set; the top n exactly, slowly
+    // too many candidates (ties): the row's kept set comes from the general path; the top n exactly,
+    // slowly
     n_list = 0;
     if (Kn > 0) {
       uint64_t prev = ~0ull;
@@ -1680,7 +1774,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
           }
         }
         for (int i = t; i < n_x; i += CT) {
-          const float z = canon(__uint_as_float(s.c.xval[i]), r);
+          const float z = canon(__uint_as_float(s.c.p.xval[i]), r);
           if (z > -INFINITY && z == z) {
             const uint64_t key = cand_key(z, pos_of_rank(s, nwords, e_base, i));
             if (key < prev && key > best) best = key;
@@ -1695,7 +1789,7 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
         }
         best = blk_max_u64(best, s);
         if (best == 0) break;
-        if (t == 0) st_agent(glist + it, best);
+        if (t == 0) glist[it] = best;
         prev = best;
         n_list = it + 1;
       }
@@ -1703,70 +1797,30 @@ __global__ __launch_bounds__(CT) void k_split(SArgs a) {
     }
   }
 
-  reload_barrier(d);
-  // ---- rows without a small kept set: the processed values of the whole chunk ----
-  const bool dense = want_dense || (s2b && overflow);
-  if (dense) {
-    float* drow = a.dense + row * a.Vp;
-    const __amdgpu_buffer_rsrc_t drs = dense_rsrc(a, row);
-    static_for<CJ>([&](auto J) {
-      constexpr int j = decltype(J)::value;
-      const int64_t slot = R.s0 + (int64_t)j * CT + t;
-      if (slot < R.s1) {
-        uint32_t skip = 0;
-        if (R.pen_on) {
-          const int b0 = (int)(slot - R.s0 + 1) * VEC;
-          const uint32_t bits = (s.c.bitmap[b0 >> 5] >> (b0 & 31)) & ((1u << VEC) - 1u);
-          #pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            if (!((bits >> e) & 1u)) continue;
-            const int b = b0 + e, w = b >> 5;
-            if ((int)s.c.wpref[w] + __popc(s.c.bitmap[w] & ((1u << (b & 31)) - 1u)) < XCAP) skip |= 1u << e;
-          }
-        }
-        const int p0 = R.head + (int)slot * VEC;
-        if (skip == 0 && (p0 & 3) == 0) {  // whole slot, 16-byte aligned: VEC / 4 wide stores
-#pragma unroll
-          for (int e = 0; e < VEC; e += 4)
-            st_dense4(drs, p0 + e, canon(elem<DT>(d[j], e), r), canon(elem<DT>(d[j], e + 1), r),
-                      canon(elem<DT>(d[j], e + 2), r), canon(elem<DT>(d[j], e + 3), r));
-        } else {
-#pragma unroll
-          for (int e = 0; e < VEC; ++e)
-            if (!((skip >> e) & 1u)) st_agent(drow + p0 + e, canon(elem<DT>(d[j], e), r));
-        }
-      }
-    });
-    for (int i = t; i < n_x; i += CT)
-      st_agent(drow + pos_of_rank(s, nwords, e_base, i), canon(__uint_as_float(s.c.xval[i]), r));
-    if (own_hx) st_agent(drow + s.hx_pos[t], canon(s.hx_val[t], r));
+  // ---- publish the chunk record (read by the resolution kernel, which the stream orders after this
+  //      launch: the end of a launch makes its stores visible to the next one on every XCD) ----
+  if (t == 0) {
+    ChunkPub p;
+    p.zmax = zmax;
+    p.mref = cm;
+    p.s = cs;
+    p.flags = cflags | (has_fin ? PUB_FINITE : 0u) | (overflow ? PUB_OVER : 0u);
+    p.argpos = argpos;
+    p.n_list = n_list;
+    p.qk = qk;
+    p.qn = qn;
+    rec_store(a.rec + L * REC_WORDS, p);
   }
+}
 
-  // ---- publish the chunk record, then arrive ----
-  if (t == 0) {
-    ChunkPub* g = a.pub + L;
-    st_agent(&g->zmax, zmax);
-    st_agent(&g->mref, cm);
-    st_agent(&g->s, cs);
-    st_agent(&g->flags, cflags | (dense ? PUB_DENSE : 0u) | (has_fin ? PUB_FINITE : 0u));
-    st_agent(&g->argpos, (int32_t)argpos);
-    st_agent(&g->n_list, (int32_t)n_list);
-    st_agent(&g->qk, qk);
-    st_agent(&g->qn, qn);
-  }
-  // Every value another workgroup reads (record, list, dense row) was written with an agent-scope
-  // store, which writes through this XCD's L2; once the stores have completed they are visible to
-  // every XCD, and the resolving workgroup reads them with agent-scope loads.  So completing the
-  // stores is all the publication needs -- a device-scope fence would also write back and invalidate
-  // the whole L2 of the XCD, once per chunk.
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (t == 0) {
-    const uint32_t old = __hip_atomic_fetch_add(&a.ctr[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s.bc_i[3] = (old == (uint32_t)(R.P - 1)) ? 1 : 0;
-  }
-  __syncthreads();
-  if (!s.bc_i[3]) return;
+// ----------------------------------------------------------------------------------------------
+// The resolution kernel: one workgroup per row, after the chunk kernel
+// ----------------------------------------------------------------------------------------------
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT, 1) void k_resolve(SArgs a) {
+  __shared__ SSm s;
+  SRow R;
+  row_setup<DT, SEG>(a, (int64_t)blockIdx.x, 0, R);
   resolve_row<DT, SEG>(a, R, s);
 }
 
@@ -1793,31 +1847,26 @@ SGeo geometry(int64_t B, int64_t V, albireo_dtype_t dtype) {
 }
 
 struct WsParts {
-  int64_t ctr, pub, lists, dense, total;
+  int64_t rec, lists, total;
 };
-// Dense view row stride: V rounded up to 16 floats, so that the draw's aligned 16-position groups stay
-// inside the row.
-int64_t dense_stride(int64_t V) { return (V + 15) & ~int64_t(15); }
-WsParts ws_parts(int64_t B, int64_t V, int P) {
+WsParts ws_parts(int64_t B, int P) {
   WsParts w;
-  w.ctr = 0;
-  w.pub = align256(w.ctr + B * 4);
-  w.lists = align256(w.pub + B * P * (int64_t)sizeof(ChunkPub));
-  w.dense = align256(w.lists + B * P * (int64_t)LCAPC * 8);
-  w.total = align256(w.dense + B * dense_stride(V) * 4);
+  w.rec = 0;
+  w.lists = align256(w.rec + B * P * (int64_t)REC_WORDS * 8);
+  w.total = align256(w.lists + B * P * (int64_t)LCAPC * 8);
   return w;
 }
 
 }  // namespace
 
-namespace albireo_split {
+namespace albireo_stream {
 
 bool supported(int64_t B, int64_t V, albireo_dtype_t dtype) { return geometry(B, V, dtype).ok; }
 
 size_t workspace_bytes(int64_t B, int64_t V, albireo_dtype_t dtype) {
   const SGeo g = geometry(B, V, dtype);
   if (!g.ok) return 0;
-  return (size_t)ws_parts(B, V, g.P).total;
+  return (size_t)ws_parts(B, g.P).total;
 }
 
 albireo_status_t launch(const Request& q) {
@@ -1841,9 +1890,6 @@ albireo_status_t launch(const Request& q) {
     a.prm.hist_offsets = p->hist_offsets;
     a.prm.hist_ids = p->hist_ids;
     a.prm.hist_len = p->hist_len;
-  }
-  if (q.params) {
-    const albireo_params_t* p = q.params;
     a.prompt_offsets = p->prompt_offsets;
     a.prompt_ids = p->prompt_ids;
     a.prompt_len = p->prompt_len;
@@ -1884,20 +1930,21 @@ albireo_status_t launch(const Request& q) {
   a.chunk_slots = g.chunk_slots;
   a.grid = q.B * g.P;
   a.xcd_map = (a.grid % 8 == 0) ? 1 : 0;
-  const WsParts w = ws_parts(q.B, q.V, g.P);
-  a.ctr = reinterpret_cast<uint32_t*>(q.ws + w.ctr);
-  a.pub = reinterpret_cast<ChunkPub*>(q.ws + w.pub);
+  const WsParts w = ws_parts(q.B, g.P);
+  a.rec = reinterpret_cast<uint64_t*>(q.ws + w.rec);
   a.lists = reinterpret_cast<uint64_t*>(q.ws + w.lists);
-  a.dense = reinterpret_cast<float*>(q.ws + w.dense);
-  a.Vp = dense_stride(q.V);
   void* args[] = {&a};
-  const void* fn;
-  if (q.dtype == ALBIREO_BF16)
-    fn = q.shards ? reinterpret_cast<const void*>(&k_split<BF16T, true>) : reinterpret_cast<const void*>(&k_split<BF16T, false>);
-  else
-    fn = q.shards ? reinterpret_cast<const void*>(&k_split<F32T, true>) : reinterpret_cast<const void*>(&k_split<F32T, false>);
-  const hipError_t e = hipLaunchKernel(fn, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
+  const void *fc, *fr;
+  if (q.dtype == ALBIREO_BF16) {
+    fc = q.shards ? reinterpret_cast<const void*>(&k_stream<BF16T, true>) : reinterpret_cast<const void*>(&k_stream<BF16T, false>);
+    fr = q.shards ? reinterpret_cast<const void*>(&k_resolve<BF16T, true>) : reinterpret_cast<const void*>(&k_resolve<BF16T, false>);
+  } else {
+    fc = q.shards ? reinterpret_cast<const void*>(&k_stream<F32T, true>) : reinterpret_cast<const void*>(&k_stream<F32T, false>);
+    fr = q.shards ? reinterpret_cast<const void*>(&k_resolve<F32T, true>) : reinterpret_cast<const void*>(&k_resolve<F32T, false>);
+  }
+  hipError_t e = hipLaunchKernel(fc, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
+  if (e == hipSuccess) e = hipLaunchKernel(fr, dim3((unsigned)q.B), dim3(CT), args, 0, q.stream);
   return e == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
 }
 
-}  // namespace albireo_split
+}  // namespace albireo_stream
