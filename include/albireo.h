@@ -55,7 +55,9 @@ typedef enum {
   ALBIREO_E_INVALID = 1,     /* bad pointer, size, stride, dtype or n_top                       */
   ALBIREO_E_UNSUPPORTED = 2, /* shape this build does not handle (e.g. V >= 2^31)                */
   ALBIREO_E_WORKSPACE = 3,   /* workspace NULL, misaligned or smaller than albireo_workspace_size */
-  ALBIREO_E_LAUNCH = 4       /* the HIP runtime refused the launch                               */
+  ALBIREO_E_LAUNCH = 4,      /* the HIP runtime refused the launch                               */
+  ALBIREO_E_SCRATCH = 5      /* albireo_sample_noalloc: the shape needs more device scratch than
+                                ALBIREO_NOALLOC_SCRATCH_BYTES                                     */
 } albireo_status_t;
 
 /* Per-row flag bits written to out_flags. */
@@ -175,6 +177,26 @@ albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64
                                 float* out_logprobs, int32_t n_top, int32_t* out_top_ids,
                                 float* out_top_logprobs, uint32_t* out_flags, void* workspace,
                                 size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * albireo_sample for callers that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation.  The same kernels and the same results as
+ * albireo_sample; the workspace is a fixed array in the library's device memory instead of a caller
+ * buffer, so the call allocates nothing (no hipMalloc, no allocating library routine).
+ *   Arguments and outputs as albireo_sample, without workspace / workspace_bytes.
+ *   Limit: a shape whose albireo_sample workspace exceeds ALBIREO_NOALLOC_SCRATCH_BYTES (32 MiB, i.e.
+ *   B * P > 8065 row chunks, P = ceil(floor(V / 8) / 4864) for bf16 and ceil(floor(V / 4) / 4864) for
+ *   fp32) returns ALBIREO_E_SCRATCH before anything is enqueued.
+ *   Every GPU the library runs on holds one such array until the process ends, shared by all calls on
+ *   that GPU: two calls that overlap in time on one GPU (different streams, or threads) race on it and
+ *   must be serialised by the caller.  Nothing in it needs to be zero between calls.
+ */
+#define ALBIREO_NOALLOC_SCRATCH_BYTES (32u << 20)
+albireo_status_t albireo_sample_noalloc(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V,
+                                        int64_t ld, const albireo_params_t* params, const float* uniforms,
+                                        int32_t* out_ids, float* out_logprobs, int32_t n_top,
+                                        int32_t* out_top_ids, float* out_top_logprobs, uint32_t* out_flags,
+                                        hipStream_t stream);
 
 /*
  * Apply steps 1-2 (penalties only) and write the penalised logits as fp32.

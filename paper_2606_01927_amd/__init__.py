@@ -24,7 +24,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 F32, BF16 = 0, 1
-OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_LAUNCH = 0, 1, 2, 3, 4
+OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_LAUNCH, E_SCRATCH = 0, 1, 2, 3, 4, 5
 FLAG_GREEDY, FLAG_EMPTY, FLAG_BAD_INPUT, FLAG_BAD_PARAM, FLAG_LIMIT = 1, 2, 4, 8, 16
 MAX_TOP_N = 32
 
@@ -62,6 +62,9 @@ _lib.albireo_workspace_size.restype = _sz
 _lib.albireo_sample.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Params), _vp, _vp, _vp,
                                 _i32, _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.albireo_sample.restype = ctypes.c_int
+_lib.albireo_sample_noalloc.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Params), _vp, _vp,
+                                        _vp, _i32, _vp, _vp, _vp, _vp]
+_lib.albireo_sample_noalloc.restype = ctypes.c_int
 _lib.albireo_apply_penalties.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Params), _vp,
                                          _vp, _sz, _vp]
 _lib.albireo_apply_penalties.restype = ctypes.c_int
@@ -89,7 +92,7 @@ _lib.albireo_status_string.restype = ctypes.c_char_p
 EXPORTED = ("albireo_workspace_size", "albireo_sample", "albireo_sample_step", "albireo_sample_sharded",
             "albireo_philox_uniforms",
             "albireo_backfill", "albireo_apply_penalties", "albireo_topk_topp", "albireo_status_string",
-            "albireo_penalty_state_init", "albireo_penalty_state_append")
+            "albireo_penalty_state_init", "albireo_penalty_state_append", "albireo_sample_noalloc")
 
 
 class AlbireoError(RuntimeError):
@@ -273,6 +276,25 @@ def sample(logits: torch.Tensor, uniforms: torch.Tensor, params: Optional[Sampli
                              flags.data_ptr(), wptr, wbytes, _stream(stream))
     if st != OK:
         raise AlbireoError(st, "albireo_sample")
+    return ids, lps, tids, tlps, flags
+
+
+def sample_noalloc(logits: torch.Tensor, uniforms: torch.Tensor, params: Optional[SamplingParams] = None,
+                   n_top: int = 0, V: Optional[int] = None, stream=None, out=None):
+    """albireo_sample_noalloc: sample() with the library's fixed device scratch in place of a workspace
+    (nothing is allocated when `out` is given).  Same return value as sample()."""
+    dev = logits.device
+    B, V, ld = _rows(logits, V)
+    if uniforms.dtype != torch.float32 or uniforms.device != dev or uniforms.numel() < B:
+        raise ValueError("uniforms must be a float32 [B] tensor on the logits' device")
+    ids, lps, tids, tlps, flags = _outs(B, n_top, dev, out)
+    prm = _params(params, dev)
+    st = _lib.albireo_sample_noalloc(logits.data_ptr(), _dtype_code(logits), B, V, ld,
+                                     ctypes.byref(prm) if prm else None, uniforms.data_ptr(), ids.data_ptr(),
+                                     lps.data_ptr(), n_top, tids.data_ptr() if n_top else None,
+                                     tlps.data_ptr() if n_top else None, flags.data_ptr(), _stream(stream))
+    if st != OK:
+        raise AlbireoError(st, "albireo_sample_noalloc")
     return ids, lps, tids, tlps, flags
 
 

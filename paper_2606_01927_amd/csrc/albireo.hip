@@ -2928,6 +2928,34 @@ albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t 
 
 }  // namespace
 
+// ----------------------------------------------------------------------------------------------
+// Device scratch of albireo_sample_noalloc: one array in every device's copy of the code object, held
+// until the process ends.  In host code its name is only a host-side stand-in: the device address of
+// each device's copy comes from hipGetSymbolAddress (once per device, with that device current) and
+// only that address is ever passed to a kernel.
+// ----------------------------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[ALBIREO_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int SCRATCH_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[SCRATCH_DEVICES];  // per device: the address of its copy of `scratch`
+
+// The current device's scratch address (looked up on the first call on that device).
+albireo_status_t scratch_for_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SCRATCH_DEVICES) return ALBIREO_E_LAUNCH;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return ALBIREO_E_LAUNCH;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return ALBIREO_OK;
+}
+}  // namespace
+
 extern "C" {
 
 size_t albireo_workspace_size(int64_t B, int64_t V, albireo_dtype_t dtype, int32_t n_top) {
@@ -2949,6 +2977,22 @@ albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64
                                 size_t workspace_bytes, hipStream_t stream) {
   return sample_impl(logits, dtype, B, V, ld, nullptr, params, uniforms, nullptr, out_ids, out_logprobs, n_top,
                      out_top_ids, out_top_logprobs, out_flags, workspace, workspace_bytes, stream);
+}
+
+albireo_status_t albireo_sample_noalloc(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V,
+                                        int64_t ld, const albireo_params_t* params, const float* uniforms,
+                                        int32_t* out_ids, float* out_logprobs, int32_t n_top,
+                                        int32_t* out_top_ids, float* out_top_logprobs, uint32_t* out_flags,
+                                        hipStream_t stream) {
+  // the same checks as albireo_sample decide the shape's validity; here only the scratch bound
+  if (B > 0 && V > 0 && (dtype == ALBIREO_F32 || dtype == ALBIREO_BF16) &&
+      albireo_stream::workspace_bytes(B, V, dtype) > (size_t)ALBIREO_NOALLOC_SCRATCH_BYTES)
+    return ALBIREO_E_SCRATCH;
+  void* ws = nullptr;
+  const albireo_status_t st = scratch_for_current_device(&ws);
+  if (st != ALBIREO_OK) return st;
+  return sample_impl(logits, dtype, B, V, ld, nullptr, params, uniforms, nullptr, out_ids, out_logprobs, n_top,
+                     out_top_ids, out_top_logprobs, out_flags, ws, (size_t)ALBIREO_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 albireo_status_t albireo_sample_step(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
@@ -3060,6 +3104,7 @@ const char* albireo_status_string(albireo_status_t s) {
     case ALBIREO_E_UNSUPPORTED: return "unsupported shape";
     case ALBIREO_E_WORKSPACE: return "workspace missing, misaligned or too small";
     case ALBIREO_E_LAUNCH: return "kernel launch failed";
+    case ALBIREO_E_SCRATCH: return "shape needs more device scratch than albireo_sample_noalloc holds";
   }
   return "unknown status";
 }

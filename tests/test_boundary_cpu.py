@@ -30,7 +30,8 @@ def alb():
 def test_header_declares_the_entry_points():
     assert _declared() == sorted(["albireo_apply_penalties", "albireo_backfill", "albireo_philox_uniforms",
                                   "albireo_penalty_state_append", "albireo_penalty_state_init",
-                                  "albireo_sample", "albireo_sample_sharded", "albireo_sample_step",
+                                  "albireo_sample", "albireo_sample_noalloc", "albireo_sample_sharded",
+                                  "albireo_sample_step",
                                   "albireo_status_string",
                                   "albireo_topk_topp", "albireo_workspace_size"])
 
@@ -43,7 +44,7 @@ def test_library_exports_every_declared_symbol(alb):
 
 
 def test_status_strings(alb):
-    for st in range(5):
+    for st in range(6):
         assert alb.status_string(st)
     assert alb.status_string(99) == "unknown status"
 
