@@ -130,6 +130,7 @@ struct PenLds {
   uint32_t bitmap[BMW];      // presence of the chunk's positions in the row's history
   uint16_t wpref[BMW + 2];   // set bits in the bitmap words before each word
   uint32_t xval[XCAP];       // per penalised position: its count, then its new value
+  uint32_t xorig[XCAP];      // chunk kernel: per penalised position, its logit as loaded
 };
 
 // LDS of one workgroup: the chunk phase, the general path and the list resolution share the bytes.
@@ -149,8 +150,6 @@ struct SSm {
   int32_t hx_pos[HXN];
   float hx_val[HXN];
   float wred[3][CW];
-  float tmx[CW][64];  // the thread maxima of each wave, sorted in descending order
-  float kb[2];        // the K-th largest thread maximum for top-k and for top-n
   uint64_t qred[CW];
   int32_t n_list;
   uint32_t flags;
@@ -1476,21 +1475,22 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
     if ((j + 1) * CT > ns && j * CT + t >= ns) d[j] = make_uint4(DT::NEG, DT::NEG, DT::NEG, DT::NEG);
     if (R.pen_on) {
       if (j * CT + t < ns) {
+        // a slot's marked positions have consecutive numbers: stage their loaded values (their new
+        // values are computed after the pass, one number per thread), mask them out of the registers
         const int b0 = (j * CT + t + 1) * VEC;
-        const uint32_t bits = (s.c.p.bitmap[b0 >> 5] >> (b0 & 31)) & ((1u << VEC) - 1u);
+        const uint32_t word = s.c.p.bitmap[b0 >> 5];
+        const uint32_t bits = (word >> (b0 & 31)) & ((1u << VEC) - 1u);
         if (bits) {
-          uint32_t applied = 0;
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            if ((bits >> e) & 1u) {
-              const int b = b0 + e, w = b >> 5;
-              const int rank = (int)s.c.p.wpref[w] + __popc(s.c.p.bitmap[w] & ((1u << (b & 31)) - 1u));
-              if (rank < XCAP) {
-                const float x = elem<DT>(d[j], e);
-                s.c.p.xval[rank] = __float_as_uint(penalise_cv(x, s.c.p.xval[rank], R.rep, R.freq, R.pres));
-                applied |= 1u << e;
-              }
+          int rk = (int)s.c.p.wpref[b0 >> 5] + __popc(word & ((1u << (b0 & 31)) - 1u));
+          uint32_t rest = bits, applied = 0;
+          while (rest) {
+            const int e = __builtin_ctz(rest);
+            rest &= rest - 1u;
+            if (rk < XCAP) {
+              s.c.p.xorig[rk] = __float_as_uint(elem<DT>(d[j], e));
+              applied |= 1u << e;
             }
+            ++rk;
           }
           const uint4 mk = DT::mask_of(applied);
           d[j].x = (d[j].x & ~mk.x) | (DT::NEG & mk.x);
@@ -1528,7 +1528,7 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
       if (R.pen_on) {
         const int rank = overlay_rank(s, (int)(pos - e_base));
         if (rank >= 0) {
-          s.c.p.xval[rank] = __float_as_uint(penalise_cv(x, s.c.p.xval[rank], R.rep, R.freq, R.pres));
+          s.c.p.xorig[rank] = __float_as_uint(x);
           pen = true;
         }
       }
@@ -1543,7 +1543,11 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
   const bool own_hx = t < HXN && s.hx_pos[t] >= 0;
   {
     float xe = -INFINITY;
-    for (int i = t; i < n_x; i += CT) xe = fmaxf(xe, __uint_as_float(s.c.p.xval[i]));
+    for (int i = t; i < n_x; i += CT) {
+      const float v = penalise_cv(__uint_as_float(s.c.p.xorig[i]), s.c.p.xval[i], R.rep, R.freq, R.pres);
+      s.c.p.xval[i] = __float_as_uint(v);
+      xe = fmaxf(xe, v);
+    }
     if (own_hx) xe = fmaxf(xe, s.hx_val[t]);
     if (xe > xref) {
       xref = xe;
@@ -1621,45 +1625,29 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
   if (want_list) {
     float bk = -INFINITY, bn = -INFINITY;
     if (Kk > 0 || Kn > 0) {
-      // The K-th largest of the CT thread maxima bounds the chunk's K-th largest value from below (K
-      // threads hold a value at least that large).  Each wave sorts its 64 maxima (bitonic, descending
-      // in lane order); every maximum then finds its rank in the workgroup's order (value descending,
-      // then wave, then lane) by binary searches in the other waves' sorted lists.
-      float v = zt;
-      const int l = lane_id(), w = wave_id();
-#pragma unroll
-      for (int kk = 2; kk <= 64; kk <<= 1) {
-#pragma unroll
-        for (int jj = kk >> 1; jj > 0; jj >>= 1) {
-          const float o = __shfl_xor(v, jj);
-          const bool take_max = ((l & kk) == 0) == ((l & jj) == 0);
-          v = take_max ? fmaxf(v, o) : fminf(v, o);
-        }
+      // Per wave, the R-th largest of its 64 thread maxima (R = ceil(K / 4)), by taking the wave's
+      // maximum out R - 1 times (DPP reductions, no LDS); the smallest of the four waves' values
+      // bounds the chunk's K-th largest value from below: each wave holds R values at least that
+      // large, 4 R >= K in all.
+      const int Rk = Kk > 0 ? (Kk + CW - 1) / CW : 0, Rn = Kn > 0 ? (Kn + CW - 1) / CW : 0;
+      const int Rm = min(max(Rk, Rn), 64);
+      const int l = lane_id();
+      float v = zt, wk = -INFINITY, wn = -INFINITY;
+      for (int it = 0; it < Rm; ++it) {
+        const float mx = wave_max(v);
+        if (it == Rk - 1) wk = mx;
+        if (it == Rn - 1) wn = mx;
+        const uint64_t hit = __ballot(v == mx);
+        if (hit != 0 && l == (int)__builtin_ctzll(hit)) v = -INFINITY;
       }
-      s.tmx[w][l] = v;
-      if (t == 0) {
-        s.kb[0] = -INFINITY;
-        s.kb[1] = -INFINITY;
+      __syncthreads();  // every thread has read the chunk totals out of wred
+      if (l == 0) {
+        s.wred[0][wave_id()] = Rk <= 64 ? wk : -INFINITY;
+        s.wred[1][wave_id()] = Rn <= 64 ? wn : -INFINITY;
       }
       __syncthreads();
-      int rank = l;
-#pragma unroll
-      for (int w2 = 0; w2 < CW; ++w2) {
-        if (w2 == w) continue;
-        int lo = 0, hi = 64;  // entries of wave w2 ordered before v form a prefix of its list
-        while (lo < hi) {
-          const int mid = (lo + hi) >> 1;
-          const float x = s.tmx[w2][mid];
-          if (x > v || (x == v && w2 < w)) lo = mid + 1;
-          else hi = mid;
-        }
-        rank += lo;
-      }
-      if (Kk > 0 && rank == Kk - 1) s.kb[0] = v;
-      if (Kn > 0 && rank == Kn - 1) s.kb[1] = v;
-      __syncthreads();
-      bk = s.kb[0];  // -inf when K exceeds the thread count
-      bn = s.kb[1];
+      bk = fminf(fminf(s.wred[0][0], s.wred[0][1]), fminf(s.wred[0][2], s.wred[0][3]));
+      bn = fminf(fminf(s.wred[1][0], s.wred[1][1]), fminf(s.wred[1][2], s.wred[1][3]));
     }
     if (s2b) {
       const float bm = R.minp_on ? __fadd_rn(zmax, (float)log((double)R.minp)) : -INFINITY;
@@ -1685,10 +1673,11 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
       if (v > -INFINITY && canon(v, r) >= bound) pm |= 1u << j;
     });
     reload_barrier(d);
+    // the flagged slots of this thread, one LDS add per slot for the space of its candidates
     while (pm) {
       const int j = __builtin_ctz(pm);
       pm &= pm - 1u;
-      const int64_t slot = R.s0 + (int64_t)j * CT + t;
+      const int p0 = R.head + (int)(R.s0 + j * CT + t) * VEC;
       // slot j through a select chain written in the kernel body, so that the register slots stay
       // registers (a helper taking the slots by reference would index them as memory)
       uint4 dd = d[0];
@@ -1696,12 +1685,18 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
         constexpr int jj = decltype(J)::value;
         if (jj > 0 && j == jj) dd = d[jj];
       });
+      uint32_t cb = 0;
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
         const float z = canon(elem<DT>(dd, e), r);
-        if (z > -INFINITY && z >= bound) {
-          const int idx = atomicAdd(&s.n_list, 1);
-          if (idx < LCAPC) s.c.list[idx] = cand_key(z, R.head + (int)slot * VEC + e);
+        if (z > -INFINITY && z >= bound) cb |= 1u << e;
+      }
+      int idx = atomicAdd(&s.n_list, __popc(cb));
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        if ((cb >> e) & 1u) {
+          if (idx < LCAPC) s.c.list[idx] = cand_key(canon(elem<DT>(dd, e), r), p0 + e);
+          ++idx;
         }
       }
     }
