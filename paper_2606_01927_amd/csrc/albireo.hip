@@ -2685,20 +2685,24 @@ struct KernelInfo {
   int J;
 };
 
-// The one-workgroup-per-row kernel and the row-group kernel serve albireo_topk_topp only: fp32 rows,
-// row-major.
-template <int J>
-KernelInfo kinfo(bool multi) {
-  return {multi ? reinterpret_cast<const void*>(&k_sample_multi<F32T, J, false>)
-                : reinterpret_cast<const void*>(&k_sample<F32T, J, false>),
+template <class DT, int J, bool SEG>
+KernelInfo kinfo1(bool multi) {
+  return {multi ? reinterpret_cast<const void*>(&k_sample_multi<DT, J, SEG>)
+                : reinterpret_cast<const void*>(&k_sample<DT, J, SEG>),
           J};
 }
 
-KernelInfo pick_kernel(int64_t chunk_slots, bool multi) {
-  if (chunk_slots <= (int64_t)JSIZES[0] * NT) return kinfo<JSIZES[0]>(multi);
-  if (chunk_slots <= (int64_t)JSIZES[1] * NT) return kinfo<JSIZES[1]>(multi);
-  if (chunk_slots <= (int64_t)JSIZES[2] * NT) return kinfo<JSIZES[2]>(multi);
-  return kinfo<JSIZES[3]>(multi);
+template <class DT, int J>
+KernelInfo kinfo(bool multi, bool seg) {
+  return seg ? kinfo1<DT, J, true>(multi) : kinfo1<DT, J, false>(multi);
+}
+
+template <class DT>
+KernelInfo pick_kernel(int64_t chunk_slots, bool multi, bool seg) {
+  if (chunk_slots <= (int64_t)JSIZES[0] * NT) return kinfo<DT, JSIZES[0]>(multi, seg);
+  if (chunk_slots <= (int64_t)JSIZES[1] * NT) return kinfo<DT, JSIZES[1]>(multi, seg);
+  if (chunk_slots <= (int64_t)JSIZES[2] * NT) return kinfo<DT, JSIZES[2]>(multi, seg);
+  return kinfo<DT, JSIZES[3]>(multi, seg);
 }
 
 struct Geometry {
@@ -2755,8 +2759,8 @@ hipError_t device_caps(int dev, const void* fn, size_t smem, DeviceCaps& out) {
   return hipErrorUnknown;
 }
 
-hipError_t make_geometry(int64_t B, int64_t V, Geometry& G) {
-  const int VEC = F32T::VEC;
+hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& G, bool seg = false) {
+  const int VEC = dtype == ALBIREO_BF16 ? BF16T::VEC : F32T::VEC;
   const int64_t max_body = V / VEC;
   int64_t P = (max_body + (int64_t)JMAX * NT - 1) / ((int64_t)JMAX * NT);
   if (P < 1) P = 1;
@@ -2764,7 +2768,8 @@ hipError_t make_geometry(int64_t B, int64_t V, Geometry& G) {
   if (!G.ok) return hipSuccess;
   G.P = (int)P;
   G.chunk_slots = (max_body + P - 1) / P;
-  G.k = pick_kernel(G.chunk_slots, G.P > 1);
+  G.k = dtype == ALBIREO_BF16 ? pick_kernel<BF16T>(G.chunk_slots, G.P > 1, seg)
+                              : pick_kernel<F32T>(G.chunk_slots, G.P > 1, seg);
   // the single-chunk kernel skips the dead-slot test below live_slots_min(J) (always true for the
   // size pick_kernel chose; a build restricted to one size can miss it for small rows)
   if (G.P == 1 && max_body - 1 < (int64_t)live_slots_min(G.k.J) * NT) {
@@ -2793,11 +2798,26 @@ hipError_t make_geometry(int64_t B, int64_t V, Geometry& G) {
 
 size_t required_ws(const Geometry& G) { return (size_t)G.group_bytes * (size_t)G.n_groups; }
 
-// Workspace of the filtered-distribution kernels for B fp32 rows of V, 0 when they do not apply.
-size_t legacy_ws(int64_t B, int64_t V) {
+// Workspace of the register-resident kernels for (B, V, dtype), 0 when they do not apply.
+size_t legacy_ws(int64_t B, int64_t V, albireo_dtype_t dtype) {
   Geometry G;
-  if (make_geometry(B, V, G) != hipSuccess || !G.ok) return 0;
+  if (make_geometry(B, V, dtype, G) != hipSuccess || !G.ok) return 0;
   return required_ws(G);
+}
+
+// Kernel choice by shape alone, so that a row gets the same arithmetic in every layout and batch: a
+// row that fits one workgroup's registers is sampled by that one workgroup (no global round trip
+// between its phases); wider rows go to the streaming kernels.
+bool use_stream(int64_t B, int64_t V, albireo_dtype_t dtype) {
+  if (!albireo_stream::supported(B, V, dtype)) return false;
+  Geometry G;
+  if (make_geometry(B, V, dtype, G) != hipSuccess) return false;
+  return !G.ok || G.P > 1;
+}
+
+// A prompt history or a penalty state is read by the streaming kernels only.
+bool needs_stream(const albireo_params_t* params) {
+  return params && (params->prompt_offsets || params->state);
 }
 
 albireo_status_t launch_sample(const KArgs& a0, const Geometry& G, hipStream_t stream) {
@@ -2883,6 +2903,25 @@ albireo_status_t check_shards(const void* logits, albireo_dtype_t dtype, int64_t
   return ALBIREO_OK;
 }
 
+// The blocked layout's kernel arguments (after check_shards), once the kernel size is known.
+albireo_status_t shard_args(albireo_dtype_t dtype, int64_t V, const albireo_shards_t& sh, const Geometry& G,
+                            KArgs& a) {
+  const int64_t es = dtype == ALBIREO_BF16 ? 2 : 4;
+  const int64_t L = sh.shard_len, S = sh.shard_stride;
+  const int64_t t = (V + L - 1) / L;
+  const int64_t sps = L * es / 16;
+  const int64_t gap = t > 1 ? (S - L) * es : 0;
+  // the lane offsets of all J slots a workgroup issues stay below 2^31
+  const int64_t issued = (int64_t)G.k.J * NT;
+  if (issued * 16 + (issued / sps + 1) * gap >= ((int64_t)1 << 31)) return ALBIREO_E_UNSUPPORTED;
+  a.seg_sps = (uint32_t)sps;
+  a.seg_magic = (uint32_t)(0xffffffffull / (uint64_t)sps);
+  a.seg_ntq = (uint32_t)(NT / sps);
+  a.seg_ntr = (uint32_t)(NT % sps);
+  a.seg_gap = gap;
+  return ALBIREO_OK;
+}
+
 // albireo_sample / albireo_sample_step / albireo_sample_sharded: shards NULL is the row-major layout;
 // exactly one of uniforms and step is given.
 albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,
@@ -2902,8 +2941,48 @@ albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t 
     st = check_shards(logits, dtype, V, ld, *shards);
     if (st != ALBIREO_OK) return st;
   }
-  if (!albireo_stream::supported(B, V, dtype)) return ALBIREO_E_UNSUPPORTED;
-  st = check_ws(workspace, workspace_bytes, albireo_stream::workspace_bytes(B, V, dtype));
+  if (needs_stream(params) && !albireo_stream::supported(B, V, dtype)) return ALBIREO_E_UNSUPPORTED;
+  if (!use_stream(B, V, dtype) && !needs_stream(params)) {
+    // a row that fits one workgroup's registers
+    Geometry G;
+    if (make_geometry(B, V, dtype, G, shards != nullptr) != hipSuccess) return ALBIREO_E_LAUNCH;
+    if (!G.ok) return ALBIREO_E_UNSUPPORTED;
+    KArgs a;
+    memset(&a, 0, sizeof a);
+    if (shards) {
+      st = shard_args(dtype, V, *shards, G, a);
+      if (st != ALBIREO_OK) return st;
+    }
+    st = check_ws(workspace, workspace_bytes, required_ws(G));
+    if (st != ALBIREO_OK) return st;
+    a.logits = static_cast<const unsigned char*>(logits);
+    a.B = B;
+    a.V = V;
+    a.ld = ld;
+    a.prm = dev_params(params);
+    a.uniforms = uniforms;
+    if (step) {
+      a.rng_on = 1;
+      a.rng_seed = step->seed;
+      a.rng_step = step->step;
+      a.seq_ids = step->seq_ids;
+      a.next_tokens = step->next_tokens;
+      a.backfill_dest = step->backfill_dest;
+      a.next_len = step->next_len;
+    }
+    a.out_ids = out_ids;
+    a.out_logprobs = out_logprobs;
+    a.n_top = n_top;
+    a.out_top_ids = out_top_ids;
+    a.out_top_logprobs = out_top_logprobs;
+    a.out_flags = out_flags;
+    a.mode = 0;
+    a.ws = static_cast<unsigned char*>(workspace);
+    return launch_sample(a, G, stream);
+  }
+  // the streaming kernels; their part of the workspace follows the register-resident kernels' part
+  const size_t off = (size_t)align256((int64_t)legacy_ws(B, V, dtype));
+  st = check_ws(workspace, workspace_bytes, off + albireo_stream::workspace_bytes(B, V, dtype));
   if (st != ALBIREO_OK) return st;
   albireo_stream::Request r;
   r.logits = logits;
@@ -2921,7 +3000,7 @@ albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t 
   r.out_top_ids = out_top_ids;
   r.out_top_logprobs = out_top_logprobs;
   r.out_flags = out_flags;
-  r.ws = static_cast<unsigned char*>(workspace);
+  r.ws = static_cast<unsigned char*>(workspace) + off;
   r.stream = stream;
   return albireo_stream::launch(r);
 }
@@ -2962,11 +3041,15 @@ size_t albireo_workspace_size(int64_t B, int64_t V, albireo_dtype_t dtype, int32
   (void)n_top;
   if (B <= 0 || V <= 0 || (dtype != ALBIREO_F32 && dtype != ALBIREO_BF16)) return 256;
   if (V >= ((int64_t)1 << 31) - 16) return 0;
-  // the sampling kernel's part and the filtered-distribution kernel's part share the bytes: every call
-  // leaves what it used zeroed
+  // the register-resident kernels' part, then the streaming kernels' part whenever they can serve the
+  // shape (rows with a prompt history or a penalty state go to them whatever their width)
+  const size_t legacy = legacy_ws(B, V, dtype);
   const size_t stream = albireo_stream::workspace_bytes(B, V, dtype);
-  const size_t legacy = dtype == ALBIREO_F32 ? legacy_ws(B, V) : 0;
-  const size_t need = stream > legacy ? stream : legacy;
+  if (stream == 0) {
+    Geometry G;
+    if (make_geometry(B, V, dtype, G) != hipSuccess || !G.ok) return 0;
+  }
+  const size_t need = (size_t)align256((int64_t)legacy) + stream;
   return need < 256 ? 256 : need;
 }
 
@@ -2986,7 +3069,7 @@ albireo_status_t albireo_sample_noalloc(const void* logits, albireo_dtype_t dtyp
                                         hipStream_t stream) {
   // the same checks as albireo_sample decide the shape's validity; here only the scratch bound
   if (B > 0 && V > 0 && (dtype == ALBIREO_F32 || dtype == ALBIREO_BF16) &&
-      albireo_stream::workspace_bytes(B, V, dtype) > (size_t)ALBIREO_NOALLOC_SCRATCH_BYTES)
+      albireo_workspace_size(B, V, dtype, n_top) > (size_t)ALBIREO_NOALLOC_SCRATCH_BYTES)
     return ALBIREO_E_SCRATCH;
   void* ws = nullptr;
   const albireo_status_t st = scratch_for_current_device(&ws);
@@ -3047,7 +3130,7 @@ albireo_status_t albireo_topk_topp(const float* logits, int64_t B, int64_t V, in
   if (st != ALBIREO_OK) return st;
   if (B == 0) return ALBIREO_OK;
   Geometry G;
-  if (make_geometry(B, V, G) != hipSuccess) return ALBIREO_E_LAUNCH;
+  if (make_geometry(B, V, ALBIREO_F32, G) != hipSuccess) return ALBIREO_E_LAUNCH;
   if (!G.ok) return ALBIREO_E_UNSUPPORTED;
   st = check_ws(workspace, workspace_bytes, required_ws(G));
   if (st != ALBIREO_OK) return st;
