@@ -152,6 +152,8 @@ struct SSm {
   float wred[3][CW];
   uint64_t qred[CW];
   int32_t n_list;
+  uint64_t* gst;       // resolution kernel: the general path's staging area (GSTAGE words)
+  const int32_t* hst;  // resolution kernel: the row's output history copied to LDS, or null
   uint32_t flags;
   int32_t ov_red[CW];  // the overlay build's block scan (callers keep counters in bc_i across it)
   int32_t bc_i[4];
@@ -488,7 +490,11 @@ __device__ __forceinline__ int build_overlay(const SArgs& a, const SRow& R, SSm&
   const int64_t e_lo = c == 0 ? 0 : (int64_t)R.head + s0 * vec;
   const int64_t e_hi = c == R.P - 1 ? (int64_t)R.V : (int64_t)R.head + s1 * vec;
   uint32_t bad = 0;
-  const int32_t* hid = a.prm.hist_ids;
+  // the output history: from the caller's registers and memory, or (resolution kernel) all of it from
+  // its LDS copy, indexed from 0
+  const int32_t* hst = s.hst;
+  const int32_t* hid = hst ? hst : a.prm.hist_ids;
+  const int64_t hb = hst ? R.h_lo : 0;  // the history index of hid[0]
   // ids [lo, hi) of an array, IDU loads per thread in flight before any is used (unconditional: an
   // index past the range reloads the first of the group); f(id, index)
   constexpr int IDU = 4;
@@ -515,12 +521,12 @@ __device__ __forceinline__ int build_overlay(const SArgs& a, const SRow& R, SSm&
       atomicOr(&s.c.p.bitmap[b >> 5], 1u << (b & 31));
     }
   };
-  const int64_t h_reg_end = min(R.h_hi, R.h_lo + (int64_t)HPT * CT);  // history ids held in hreg
+  const int64_t h_reg_end = hst ? R.h_lo : min(R.h_hi, R.h_lo + (int64_t)HPT * CT);  // ids held in hreg
   static_for<HPT>([&](auto Q) {
     constexpr int q = decltype(Q)::value;
     if (R.h_lo + t + (int64_t)q * CT < h_reg_end) mark(hreg[q]);
   });
-  for_ids(hid, h_reg_end, R.h_hi, [&](int32_t id, int64_t) { mark(id); });
+  for_ids(hid, h_reg_end - hb, R.h_hi - hb, [&](int32_t id, int64_t) { mark(id); });
   for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { mark(id); });
   const int32_t* st_row = a.st_ids + R.row * a.st_cap;
   for_ids(st_row, 0, R.st_n, [&](int32_t id, int64_t) { mark(id); });
@@ -567,7 +573,7 @@ __device__ __forceinline__ int build_overlay(const SArgs& a, const SRow& R, SSm&
     constexpr int q = decltype(Q)::value;
     if (R.h_lo + t + (int64_t)q * CT < h_reg_end) count(hreg[q], 1u, 0u);
   });
-  for_ids(hid, h_reg_end, R.h_hi, [&](int32_t id, int64_t) { count(id, 1u, 0u); });
+  for_ids(hid, h_reg_end - hb, R.h_hi - hb, [&](int32_t id, int64_t) { count(id, 1u, 0u); });
   for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { count(id, 0u, 0x80000000u); });
   const int32_t* st_cnt = reinterpret_cast<const int32_t*>(a.st_counts + R.row * a.st_cap);
   for_ids(st_cnt, 0, R.st_n, [&](int32_t cvi, int64_t e) {
@@ -629,9 +635,25 @@ __device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s,
     static_for<GJ>([&](auto J) {
       constexpr int j = decltype(J)::value;
       if (j * CT + t < nb) {
-        const int p0 = R.head + (int)(s0 + b0 + j * CT + t) * VEC;
+        const int l = b0 + j * CT + t;  // the slot within the chunk
+        const int p0 = R.head + (int)(s0 + l) * VEC;
+        // the slot's overlay bits, one LDS word per slot (a slot's bits share one word)
+        uint32_t word = 0, bits = 0, wpre = 0;
+        const int ob = (l + 1) * VEC;
+        if (R.pen_on) {
+          word = s.c.p.bitmap[ob >> 5];
+          bits = (word >> (ob & 31)) & ((1u << VEC) - 1u);
+          if (bits) wpre = s.c.p.wpref[ob >> 5];
+        }
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) f(value(elem<DT>(d[j], e), p0 + e), p0 + e);
+        for (int e = 0; e < VEC; ++e) {
+          float x = elem<DT>(d[j], e);
+          if ((bits >> e) & 1u) {
+            const int rk = (int)wpre + __popc(word & ((1u << ((ob & 31) + e)) - 1u));
+            if (rk < XCAP) x = penalise_cv(x, s.c.p.xval[rk], R.rep, R.freq, R.pres);
+          }
+          f(canon(x, r), p0 + e);
+        }
       }
     });
   }
@@ -653,11 +675,12 @@ struct Spec {
 };
 
 // Stage into s.key the list entries i < imax of every chunk with z >= zthr, from the speculative
-// registers (sp.on) or from the lists themselves.  The order is arbitrary (ranks are counted).  For the
-// check of ties cut off at imax, s.cut[c] gets 1 (and s.cnt[c] the value's bits) when chunk c's list
-// goes on past imax and its entry imax - 1 passes.  Returns the count, or -1 above cap.
+// registers (sp.on) or from the lists themselves.  The order is arbitrary (ranks are counted).  With
+// cut_test, for the check of ties cut off at imax, s.cut[c] gets 1 (and s.cnt[c] the value's bits of
+// chunk c's entry imax, the first one left out) when the list goes on past imax.  Returns the count,
+// or -1 above cap.
 __device__ __forceinline__ int stage_entries(const SArgs& a, const SRow& R, SSm& s, const Spec& sp, float zthr,
-                                             int imax, int cap) {
+                                             int imax, int cap, bool cut_test) {
   const int P = R.P, t = threadIdx.x;
   if (t == 0) s.bc_i[2] = 0;
   if (t < P) s.cut[t] = 0;
@@ -668,14 +691,14 @@ __device__ __forceinline__ int stage_entries(const SArgs& a, const SRow& R, SSm&
       if (cand_z(key) >= zthr) {
         const int idx = atomicAdd(&s.bc_i[2], 1);
         if (idx < cap) s.key[idx] = key;
-        if (i == imax - 1 && s.pub[c].n_list > imax) {
-          s.cut[c] = 1;
-          s.cnt[c] = __float_as_int(cand_z(key));  // its value, for the tie test
-        }
       }
+    } else if (i == imax && i < s.pub[c].n_list) {
+      s.cut[c] = 1;
+      s.cnt[c] = __float_as_int(cand_z(key));  // the first entry left out, for the tie test
     }
   };
-  if (sp.on && imax <= sp.E) {
+  const int ilim = cut_test ? imax + 1 : imax;  // entries looked at per chunk
+  if (sp.on && ilim <= sp.E) {
 #pragma unroll
     for (int q = 0; q < SPQ; ++q) {
       const int f = t + q * CT;
@@ -686,7 +709,7 @@ __device__ __forceinline__ int stage_entries(const SArgs& a, const SRow& R, SSm&
     }
   } else {
     int emax = 0;
-    for (int c = 0; c < P; ++c) emax = max(emax, min(s.pub[c].n_list, imax));
+    for (int c = 0; c < P; ++c) emax = max(emax, min(s.pub[c].n_list, ilim));
     for (int f = t; f < P * emax; f += CT) {
       const int c = f / emax, i = f - c * emax;
       if (i < s.pub[c].n_list) take(base[(int64_t)c * LCAPC + i], c, i);
@@ -839,8 +862,9 @@ __device__ __forceinline__ uint32_t gp_topp_key(const Src& src, SSm& s, uint64_t
 // masses (2^32 units) vanish from d = 32 ln 2 on, inside the last bucket.
 constexpr int GDB = GEN_WORDS;
 constexpr float GD_SCALE = 16.0f;
-constexpr int GKCAP = 2 * LCAPC - 256;  // crossing-bucket keys staged (u32) before a 256-word histogram
-constexpr int GKCAP2 = LCAPC;           // crossing-bucket (key, position) pairs staged
+constexpr int GSTAGE = 1024;            // 64-bit words of the resolution kernel's staging area (s.gst)
+constexpr int GKCAP = 2 * GSTAGE - 256;  // crossing-bucket keys staged (u32) before a 256-word histogram
+constexpr int GKCAP2 = GSTAGE;           // crossing-bucket (key, position) pairs staged
 
 __device__ __forceinline__ int gp_dbucket(float z, float m) {
   const float d = __fmul_rn(__fsub_rn(m, z), GD_SCALE);
@@ -897,7 +921,7 @@ __device__ __forceinline__ bool gp_level1(const SArgs& a, const SRow& R, SSm& s,
 // area).  Returns their number, or -1 when they do not fit.
 template <class DT, bool SEG>
 __device__ __forceinline__ int gp_gather(const SArgs& a, const SRow& R, SSm& s, float lo, float m, int bb) {
-  uint32_t* keys = reinterpret_cast<uint32_t*>(s.c.list);
+  uint32_t* keys = reinterpret_cast<uint32_t*>(s.gst);
   if (threadIdx.x == 0) s.bc_i[2] = 0;
   __syncthreads();
   RowSrc<DT, SEG>{a, R, s}([&](float z) __attribute__((always_inline)) {
@@ -921,9 +945,9 @@ __device__ __forceinline__ uint32_t gp_kth(const SArgs& a, const SRow& R, SSm& s
   uint64_t before, total;
   if (!gp_level1<false, DT, SEG>(a, R, s, -INFINITY, m, (double)K, bb, before, total)) return 0u;
   const int n = gp_gather<DT, SEG>(a, R, s, -INFINITY, m, bb);
-  uint32_t* hist = reinterpret_cast<uint32_t*>(s.c.list) + GKCAP;
+  uint32_t* hist = reinterpret_cast<uint32_t*>(s.gst) + GKCAP;
   if (n >= 0)
-    return gp_kth_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.c.list), n}, s, hist, K - (int)before);
+    return gp_kth_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.gst), n}, s, hist, K - (int)before);
   return gp_kth_key(RowSrc<DT, SEG>{a, R, s}, s, reinterpret_cast<uint32_t*>(s.c.gen), K);
 }
 
@@ -939,7 +963,7 @@ __device__ __forceinline__ uint32_t gp_topp(const SArgs& a, const SRow& R, SSm& 
   const double target = p * (double)total;
   const int n = gp_gather<DT, SEG>(a, R, s, tau2, m, bb);
   if (n >= 0)
-    return gp_topp_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.c.list), n}, s, s.c.gen, tau2, m, target,
+    return gp_topp_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.gst), n}, s, s.c.gen, tau2, m, target,
                        (double)before);
   return gp_topp_key(RowSrc<DT, SEG>{a, R, s}, s, s.c.gen, tau2, m, target, 0.0);
 }
@@ -951,6 +975,15 @@ __device__ __forceinline__ uint32_t gp_topp(const SArgs& a, const SRow& R, SSm& 
 // integers, so the masses equal those of a separate pass.  Returns false (nothing decided) when the
 // cumulative never reaches the target or the bucket does not fit in LDS; the caller then selects and
 // draws the separate way.
+// Sub-bucket (0 .. GDB - 1) of a value inside distance bucket bb: the fraction of the bucket, GDB steps.
+// fl(m - z) GD_SCALE is monotone in z and its distance from the integer bb is exact, so the sub-buckets
+// order the bucket's values as the buckets order the row's.
+__device__ __forceinline__ int gp_dsub(float z, float m, int bb) {
+  const float d = __fmul_rn(__fsub_rn(m, z), GD_SCALE);
+  const int sb = (int)__fmul_rn(__fsub_rn(d, (float)bb), (float)GDB);
+  return sb < 0 ? 0 : (sb > GDB - 1 ? GDB - 1 : sb);
+}
+
 template <class DT, bool SEG>
 __device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm& s, float tau2, float m, double p,
                                               float& tau, int& last) {
@@ -958,48 +991,87 @@ __device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm
   uint64_t before, total;
   if (!gp_level1<true, DT, SEG>(a, R, s, tau2, m, p, bb, before, total)) return false;
   const double target = p * (double)total;
-  uint64_t* ent = s.c.list;
+  uint64_t* ent = s.gst;
   uint64_t* cm = s.cm;
-  for (int c = threadIdx.x; c < R.P; c += CT) cm[c] = 0;
-  if (threadIdx.x == 0) s.bc_i[2] = 0;
-  __syncthreads();
-  int lastp = -1;
-  for (int c = 0; c < R.P; ++c) {
-    uint64_t acc = 0;
-    for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
-      if (z > -INFINITY && z >= tau2) {
-        const int b = gp_dbucket(z, m);
-        if (b < bb) {
+  // refine: values of bucket bb with sub-bucket < sbb count as above the crossing, those of sub-bucket
+  // sbb are staged (sbb = GDB: the whole bucket is staged)
+  int sbb = GDB;
+  for (int round = 0; round < 2; ++round) {
+    for (int c = threadIdx.x; c < R.P; c += CT) cm[c] = 0;
+    if (threadIdx.x == 0) s.bc_i[2] = 0;
+    __syncthreads();
+    int lastp = -1;
+    for (int c = 0; c < R.P; ++c) {
+      uint64_t acc = 0;
+      for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
+        if (z > -INFINITY && z >= tau2) {
+          const int b = gp_dbucket(z, m);
+          const int sub = (b == bb && sbb < GDB) ? gp_dsub(z, m, bb) : GDB;
+          if (b < bb || (b == bb && sub < sbb)) {
+            const uint64_t w = mass_of(z, m);
+            acc += w;
+            if (w > 0) lastp = max(lastp, pos);
+          } else if (b == bb && sub == sbb) {
+            const int i = atomicAdd(&s.bc_i[2], 1);
+            if (i < GKCAP2) ent[i] = ((uint64_t)f2key(z) << 32) | (uint32_t)pos;
+          }
+        }
+      });
+      if (acc) atomicAdd(reinterpret_cast<unsigned long long*>(&cm[c]), (unsigned long long)acc);
+    }
+    __syncthreads();
+    const int n = s.bc_i[2];
+    __syncthreads();
+    if (n <= GKCAP2) {
+      const uint32_t kk = gp_topp_key(StagedPairs{ent, n}, s, s.c.gen, tau2, m, target, (double)before);
+      if (!kk) return false;  // not reached inside the staged values: cannot happen, decided the separate way
+      tau = fmaxf(tau2, key2f(kk));
+      for (int i = threadIdx.x; i < n; i += CT) {
+        const uint64_t e = ent[i];
+        const float z = key2f((uint32_t)(e >> 32));
+        if (z >= tau) {
+          const int pos = (int)(uint32_t)e;
           const uint64_t w = mass_of(z, m);
-          acc += w;
+          atomicAdd(reinterpret_cast<unsigned long long*>(&cm[chunk_of(a, R, DT::VEC, pos)]), (unsigned long long)w);
           if (w > 0) lastp = max(lastp, pos);
-        } else if (b == bb) {
-          const int i = atomicAdd(&s.bc_i[2], 1);
-          if (i < GKCAP2) ent[i] = ((uint64_t)f2key(z) << 32) | (uint32_t)pos;
         }
       }
-    });
-    if (acc) atomicAdd(reinterpret_cast<unsigned long long*>(&cm[c]), (unsigned long long)acc);
-  }
-  __syncthreads();
-  const int n = s.bc_i[2];
-  __syncthreads();
-  if (n > GKCAP2) return false;
-  const uint32_t kk = gp_topp_key(StagedPairs{ent, n}, s, s.c.gen, tau2, m, target, (double)before);
-  if (!kk) return false;  // not reached inside the crossing bucket: cannot happen, decided the separate way
-  tau = fmaxf(tau2, key2f(kk));
-  for (int i = threadIdx.x; i < n; i += CT) {
-    const uint64_t e = ent[i];
-    const float z = key2f((uint32_t)(e >> 32));
-    if (z >= tau) {
-      const int pos = (int)(uint32_t)e;
-      const uint64_t w = mass_of(z, m);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&cm[chunk_of(a, R, DT::VEC, pos)]), (unsigned long long)w);
-      if (w > 0) lastp = max(lastp, pos);
+      last = blk_max_i(lastp, s);  // its barriers also publish cm
+      return true;
     }
+    if (round == 1) return false;
+    // the bucket does not fit: one pass for the mass histogram of its sub-buckets, then the crossing
+    // sub-bucket becomes the staged part
+    uint64_t* h64 = s.c.gen;
+    for (int i = threadIdx.x; i < GDB; i += CT) h64[i] = 0;
+    __syncthreads();
+    RowSrc<DT, SEG>{a, R, s}([&](float z) __attribute__((always_inline)) {
+      if (z > -INFINITY && z >= tau2 && gp_dbucket(z, m) == bb)
+        atomicAdd(reinterpret_cast<unsigned long long*>(&h64[gp_dsub(z, m, bb)]), (unsigned long long)mass_of(z, m));
+    });
+    __syncthreads();
+    constexpr int BPT = GDB / CT;
+    const int i0 = (int)threadIdx.x * BPT;
+    uint64_t sum = 0;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q) sum += h64[i0 + q];
+    uint64_t tot;
+    const uint64_t excl = blk_excl_scan_u64(sum, s, &tot);
+    int mine = 0x7fffffff;
+    if ((double)before + (double)excl < target && (double)before + (double)(excl + sum) >= target) {
+      uint64_t cum = excl;
+      int i = i0;
+      while (i < i0 + BPT - 1 && (double)before + (double)(cum + h64[i]) < target) cum += h64[i++];
+      mine = i;
+      s.bc_q[1] = cum;
+    }
+    const int sb = blk_min_i(mine, s);
+    if (sb == 0x7fffffff) return false;
+    before += s.bc_q[1];
+    sbb = sb;
+    __syncthreads();
   }
-  last = blk_max_i(lastp, s);  // its barriers also publish cm
-  return true;
+  return false;
 }
 
 // General path: kept set S = {finite z >= tau}; draws the token with target u * Z_S in ascending id.
@@ -1189,7 +1261,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
   // ---- one round trip: the chunk records, the row's uniform and the heads of the chunk lists ----
   Spec sp;
   sp.E = nt;
-  if (R.kon) sp.E = max(sp.E, min(R.k, LCAPC));
+  if (R.kon) sp.E = max(sp.E, min(R.k + 1, LCAPC));  // the k-th entry too, for the tie test
   sp.on = sp.E > 0 && P * sp.E <= SPQ * CT;
   if (sp.on) {
     const uint64_t* base = a.lists + (row * P) * (int64_t)LCAPC;
@@ -1241,7 +1313,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
     if (!empty) {
       float lo = INFINITY;
       for (int c = 0; c < P; ++c) lo = fminf(lo, s.pub[c].qn);
-      const int ns = stage_entries(a, R, s, sp, lo, nt, MSTAGE);
+      const int ns = stage_entries(a, R, s, sp, lo, nt, MSTAGE, false);
       for (int f = t; f < ns; f += CT) {
         const uint64_t key = s.key[f];
         const int rk = count_above(s.key, ns, key);
@@ -1284,7 +1356,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
         for (int c = 0; c < P; ++c) lo = fminf(lo, s.pub[c].qk);
         zthr = fmaxf(zthr, lo);
       }
-      const int ns = stage_entries(a, R, s, sp, zthr, imax, MSTAGE - 2 * MCAP);
+      const int ns = stage_entries(a, R, s, sp, zthr, imax, MSTAGE - 2 * MCAP, true);
       if (ns < 0) {
         general = true;
       } else {
@@ -1296,7 +1368,8 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
           __syncthreads();
           tau2 = fmaxf(tau2, s.bc_f[1]);
         }
-        // a list cut off at imax whose last taken entry is kept may hold more of a tie at tau_k
+        // a list cut off at imax whose first entry left out would be kept (a tie at tau_k) needs the
+        // general path
         bool cutkept = false;
         for (int c = 0; c < P; ++c)
           if (s.cut[c] && __int_as_float(s.cnt[c]) >= tau2) cutkept = true;
@@ -1414,13 +1487,11 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
 
   // ---- the row's history first (HPT ids per thread, in registers): waiting for these loads then
   //      never waits for the row data issued after them (the vector memory counter is in order) ----
-  // Loads are unconditional (indices clamped into range) so that none waits for another: a load under
-  // a per-lane branch is followed by a wait for it before the branch closes.
   // Loads are unconditional (indices clamped into range, or a dummy address when there is nothing to
   // read: the workspace's first bytes, always valid) so that none waits for another -- a load under a
   // branch is followed by a wait for it before the branch closes.
   const void* dummy = a.rec;
-  constexpr int HPT = 8;
+  constexpr int HPT = 16;
   int32_t hreg[HPT];
   const int nh = R.pen_on ? (int)min(R.h_hi - R.h_lo, (int64_t)HPT * CT) : 0;  // ids held in hreg
   {
@@ -1430,23 +1501,33 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
       hreg[q] = hrow[min(t + q * CT, max(nh - 1, 0))];
     });
   }
+  // A penalised row's history arrives before its row data is requested: with every workgroup's row
+  // loads in flight the history would wait behind them, and the overlay (hence the pass) with it.
+  if (R.pen_on) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   asm volatile("" ::: "memory");  // the row loads stay behind the history loads
 
-  // ---- every slot of the chunk: one 16-byte non-temporal load each, all in flight before any use ----
+  // ---- the chunk's slots: one 16-byte non-temporal load each; the first LA are issued here, slot
+  //      j + LA just before slot j is processed, so a wave whose issue stalls on a full memory queue
+  //      still has arrived slots to work on ----
   const int ns = (int)(R.s1 - R.s0);  // body slots of the chunk; slot j of thread t is j * CT + t
+  constexpr int LA = 8;
   uint4 d[CJ];
-  static_for<CJ>([&](auto J) {
+  auto issue = [&](auto J) __attribute__((always_inline)) {
     constexpr int j = decltype(J)::value;
     const uint4* sp = ns > 0 ? slot_ptr<DT, SEG>(a, R, R.s0 + min(j * CT + t, ns - 1)) : static_cast<const uint4*>(dummy);
     typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
     const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(sp));
     d[j] = make_uint4(v.x, v.y, v.z, v.w);
+  };
+  static_for<CJ>([&](auto J) {
+    if constexpr (decltype(J)::value < LA) issue(J);
   });
 
   if (t < HXN) s.hx_pos[t] = -1;
   if (t == 0) {
     s.n_list = 0;
     s.flags = 0;
+    s.hst = nullptr;
   }
 
   // ---- penalty overlay of the chunk's range ----
@@ -1465,8 +1546,26 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
   float xref = -INFINITY;       // running maximum of x
   float mref_t = MREF0;         // fl32(fl32(xref r) L2E), the exponent reference
   float acc0 = 0.0f, acc1 = 0.0f;
+  int jbest = -1;  // the slot where the thread's body maximum was first reached
+  // the overlay word of a slot (and its word prefix), read one slot ahead so that the LDS latency
+  // hides behind the previous slot's arithmetic
+  const int last_slot = max(ns - 1, 0);
+  auto ov_bit0 = [&](int j) __attribute__((always_inline)) { return (min(j * CT + t, last_slot) + 1) * VEC; };
+  uint32_t ov_word = 0, ov_pref = 0;
+  if (R.pen_on) {
+    ov_word = s.c.p.bitmap[ov_bit0(0) >> 5];
+    ov_pref = s.c.p.wpref[ov_bit0(0) >> 5];
+  }
   static_for<CJ>([&](auto J) {
     constexpr int j = decltype(J)::value;
+    if constexpr (j + LA < CJ) issue(std::integral_constant<int, j + LA>{});
+    const uint32_t word = ov_word, wpre = ov_pref;
+    if constexpr (j + 1 < CJ) {
+      if (R.pen_on) {
+        ov_word = s.c.p.bitmap[ov_bit0(j + 1) >> 5];
+        ov_pref = s.c.p.wpref[ov_bit0(j + 1) >> 5];
+      }
+    }
     {  // slot j is processed here and not earlier: no slot's values are hoisted into registers
       uint32_t x0 = d[j].x, x1 = d[j].y, x2 = d[j].z, x3 = d[j].w;
       asm volatile("" : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3));
@@ -1478,10 +1577,9 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
         // a slot's marked positions have consecutive numbers: stage their loaded values (their new
         // values are computed after the pass, one number per thread), mask them out of the registers
         const int b0 = (j * CT + t + 1) * VEC;
-        const uint32_t word = s.c.p.bitmap[b0 >> 5];
         const uint32_t bits = (word >> (b0 & 31)) & ((1u << VEC) - 1u);
         if (bits) {
-          int rk = (int)s.c.p.wpref[b0 >> 5] + __popc(word & ((1u << (b0 & 31)) - 1u));
+          int rk = (int)wpre + __popc(word & ((1u << (b0 & 31)) - 1u));
           uint32_t rest = bits, applied = 0;
           while (rest) {
             const int e = __builtin_ctz(rest);
@@ -1505,6 +1603,7 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
     for (int e = 1; e < VEC; ++e) v = fmaxf(v, elem<DT>(d[j], e));
     if (v > xref) {
       xref = v;
+      jbest = j;
       const float mnew = __fmul_rn(__fmul_rn(v, r), L2E);
       const float sc = rel2(mref_t, mnew);
       acc0 *= sc;
@@ -1517,6 +1616,7 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
       acc1 += __builtin_amdgcn_exp2f(__builtin_fmaf(__fmul_rn(elem<DT>(d[j], e + 1), r), L2E, -mref_t));
     }
   });
+  const float xbody = xref;  // the thread's maximum over its body slots (first reached in slot jbest)
   // the unaligned head (chunk 0) and tail (last chunk) positions
   {
     int pos = -1;
@@ -1602,15 +1702,19 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
   int argpos = -1;
   if (R.greedy) {
     int best = 0x7fffffff;
-    static_for<CJ>([&](auto J) {
-      constexpr int j = decltype(J)::value;
-      const int64_t slot = R.s0 + (int64_t)j * CT + t;
-      if (best == 0x7fffffff && slot < R.s1) {
-        #pragma unroll
-        for (int e = VEC - 1; e >= 0; --e)
-          if (canon(elem<DT>(d[j], e), 1.0f) == zmax) best = R.head + (int)slot * VEC + e;
-      }
-    });
+    if (jbest >= 0 && canon(xbody, 1.0f) == zmax) {
+      // the lowest body position of the maximum is in slot jbest (slots ascend in position with j)
+      uint4 dd = d[0];
+      static_for<CJ>([&](auto J) {
+        constexpr int jj = decltype(J)::value;
+        if (jj > 0 && jbest == jj) dd = d[jj];
+      });
+      int eb = VEC - 1;
+#pragma unroll
+      for (int e = VEC - 1; e >= 0; --e)
+        if (elem<DT>(dd, e) == xbody) eb = e;
+      best = R.head + (int)(R.s0 + jbest * CT + t) * VEC + eb;
+    }
     for (int i = t; i < n_x; i += CT)
       if (canon(__uint_as_float(s.c.p.xval[i]), 1.0f) == zmax) best = min(best, pos_of_rank(s, nwords, e_base, i));
     if (own_hx && canon(s.hx_val[t], 1.0f) == zmax) best = min(best, s.hx_pos[t]);
@@ -1811,11 +1915,37 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
 // ----------------------------------------------------------------------------------------------
 // The resolution kernel: one workgroup per row, after the chunk kernel
 // ----------------------------------------------------------------------------------------------
+constexpr int HSTAGE = 4096;  // output-history ids the resolution kernel keeps in LDS
+
 template <class DT, bool SEG>
 __global__ __launch_bounds__(CT, 1) void k_resolve(SArgs a) {
   __shared__ SSm s;
+  __shared__ uint64_t gstage[GSTAGE];
+  __shared__ int32_t hstage[HSTAGE];
+  const int t = threadIdx.x;
   SRow R;
   row_setup<DT, SEG>(a, (int64_t)blockIdx.x, 0, R);
+  // the general path rebuilds a chunk's penalty overlay for every re-read: its output history comes
+  // from LDS, loaded once (all of a thread's loads in flight together)
+  if (t == 0) {
+    s.gst = gstage;
+    s.hst = nullptr;
+  }
+  const int64_t nh = R.h_hi - R.h_lo;
+  if (R.pen_on && nh > 0 && nh <= HSTAGE) {
+    constexpr int Q = HSTAGE / CT;
+    int32_t v[Q];
+    static_for<Q>([&](auto I) {
+      constexpr int q = decltype(I)::value;
+      v[q] = a.prm.hist_ids[R.h_lo + min((int64_t)(t + q * CT), nh - 1)];
+    });
+    static_for<Q>([&](auto I) {
+      constexpr int q = decltype(I)::value;
+      if (t + q * CT < nh) hstage[t + q * CT] = v[q];
+    });
+    if (t == 0) s.hst = hstage;
+  }
+  __syncthreads();
   resolve_row<DT, SEG>(a, R, s);
 }
 
