@@ -149,6 +149,27 @@ albireo_status_t albireo_penalty_state_init(const albireo_penalty_state_t* state
 albireo_status_t albireo_penalty_state_append(const albireo_penalty_state_t* state, int64_t B, int64_t V,
                                               const int32_t* ids, hipStream_t stream);
 
+/* Which kernels a sampling call takes (albireo_sample_route). */
+typedef enum {
+  ALBIREO_ROUTE_NONE = 0,          /* no kernel of this build takes the shape (ALBIREO_E_UNSUPPORTED) */
+  ALBIREO_ROUTE_ONE_WORKGROUP = 1, /* one launch, one workgroup per row, the row held in registers    */
+  ALBIREO_ROUTE_STREAM = 2,        /* two launches: a workgroup per row chunk, then one per row       */
+  ALBIREO_ROUTE_COOPERATIVE = 3    /* one cooperative launch of chunk workgroups (B x chunks >= 2^31) */
+} albireo_route_t;
+
+/*
+ * The kernels albireo_sample, albireo_sample_step, albireo_sample_sharded (sharded != 0) and
+ * albireo_sample_noalloc take for B rows of V logits of this dtype with these parameters.  Host only:
+ * reads params (host struct, may be NULL; only whether a prompt history or a penalty state is given)
+ * and makes no HIP call, so it works with no device present.  The choice depends on V, dtype and
+ * whether a prompt history or a penalty state is given, and on B only when B x chunks reaches 2^31:
+ * rows of 16 to 38 x 512 x 16 bytes take one workgroup each, other rows up to 64 x 4864 x 16 bytes
+ * and rows with a prompt or a state take the streaming kernels.  ALBIREO_ROUTE_NONE for an invalid dtype, V <= 0, B < 0 or V at or
+ * above 2^31 - 16.
+ */
+albireo_route_t albireo_sample_route(int64_t B, int64_t V, albireo_dtype_t dtype, const albireo_params_t* params,
+                                    int32_t sharded);
+
 /*
  * Bytes of device workspace needed by any entry point for this shape on the current device.
  * The workspace must be 256-byte aligned and zero-filled before its first use; every call leaves it
@@ -200,7 +221,8 @@ albireo_status_t albireo_sample_noalloc(const void* logits, albireo_dtype_t dtyp
 
 /*
  * Apply steps 1-2 (penalties only) and write the penalised logits as fp32.
- *   params      [host] uses repetition/frequency/presence penalties and the history; other members ignored
+ *   params      [host] uses the repetition/frequency/presence penalties and the output history, the prompt
+ *               history or the penalty state as albireo_sample does; other members ignored
  *   out_logits  [B, V] fp32, row stride V.  It may alias `logits` only when dtype is F32 and ld == V.
  */
 albireo_status_t albireo_apply_penalties(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V,

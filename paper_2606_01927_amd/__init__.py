@@ -25,6 +25,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 F32, BF16 = 0, 1
 OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_LAUNCH, E_SCRATCH = 0, 1, 2, 3, 4, 5
+ROUTE_NONE, ROUTE_ONE_WORKGROUP, ROUTE_STREAM, ROUTE_COOPERATIVE = 0, 1, 2, 3
 FLAG_GREEDY, FLAG_EMPTY, FLAG_BAD_INPUT, FLAG_BAD_PARAM, FLAG_LIMIT = 1, 2, 4, 8, 16
 MAX_TOP_N = 32
 
@@ -59,6 +60,8 @@ class _Shards(ctypes.Structure):
 _vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
 _lib.albireo_workspace_size.argtypes = [_i64, _i64, ctypes.c_int, _i32]
 _lib.albireo_workspace_size.restype = _sz
+_lib.albireo_sample_route.argtypes = [_i64, _i64, ctypes.c_int, ctypes.POINTER(_Params), _i32]
+_lib.albireo_sample_route.restype = ctypes.c_int
 _lib.albireo_sample.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.POINTER(_Params), _vp, _vp, _vp,
                                 _i32, _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.albireo_sample.restype = ctypes.c_int
@@ -92,7 +95,8 @@ _lib.albireo_status_string.restype = ctypes.c_char_p
 EXPORTED = ("albireo_workspace_size", "albireo_sample", "albireo_sample_step", "albireo_sample_sharded",
             "albireo_philox_uniforms",
             "albireo_backfill", "albireo_apply_penalties", "albireo_topk_topp", "albireo_status_string",
-            "albireo_penalty_state_init", "albireo_penalty_state_append", "albireo_sample_noalloc")
+            "albireo_penalty_state_init", "albireo_penalty_state_append", "albireo_sample_noalloc",
+            "albireo_sample_route")
 
 
 class AlbireoError(RuntimeError):
@@ -211,18 +215,37 @@ def workspace_size(B: int, V: int, dtype: torch.dtype, n_top: int = 0) -> int:
     return int(_lib.albireo_workspace_size(B, V, BF16 if dtype == torch.bfloat16 else F32, n_top))
 
 
+def sample_route(B: int, V: int, dtype: torch.dtype, params: Optional[SamplingParams] = None,
+                 sharded: bool = False) -> int:
+    """albireo_sample_route: which kernels a sampling call of this shape takes (ROUTE_*); host only."""
+    cp = None
+    if params is not None and (params.prompt_offsets is not None or params.state is not None):
+        cp = _Params()  # only whether a prompt history or a penalty state is given is read
+        if params.prompt_offsets is not None:
+            cp.prompt_offsets = params.prompt_offsets.data_ptr()
+        if params.state is not None:
+            cp._route_state = _State()
+            cp.state = ctypes.pointer(cp._route_state)
+    return int(_lib.albireo_sample_route(B, V, BF16 if dtype == torch.bfloat16 else F32,
+                                         ctypes.byref(cp) if cp is not None else None, 1 if sharded else 0))
+
+
 class Workspace:
-    """A zero-filled device workspace that grows on demand (the library leaves it zeroed)."""
+    """A zero-filled device workspace for the calls of one stream, grown on demand (the library leaves
+    it zeroed).  A new buffer is allocated and zero-filled on the stream that asks for it, so the fill
+    is ordered before that stream's launches."""
 
     def __init__(self, device=None):
         self.device = torch.device("cuda") if device is None else torch.device(device)
         self.buf = None
 
-    def get(self, nbytes: int):
+    def get(self, nbytes: int, stream=None):
         if nbytes == 0:
             return None, 0
-        if self.buf is None or self.buf.numel() < nbytes:
-            self.buf = torch.zeros(max(nbytes, 256) + 256, dtype=torch.uint8, device=self.device)
+        if self.buf is None or self.buf.numel() < nbytes + 256:
+            s = torch.cuda.current_stream(self.device) if stream is None else stream
+            with torch.cuda.stream(s):
+                self.buf = torch.zeros(max(nbytes, 256) + 256, dtype=torch.uint8, device=self.device)
         base = self.buf.data_ptr()
         off = (-base) % 256
         return base + off, self.buf.numel() - off
@@ -231,10 +254,13 @@ class Workspace:
 _default_ws = {}
 
 
-def _ws_for(device, workspace):
+def _ws_for(device, workspace, stream=None):
+    """The caller's workspace, else the default one of (device, stream): calls on different streams
+    never share a workspace."""
     if workspace is not None:
         return workspace
-    key = (device.type, device.index)
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    key = (device.type, device.index, s.cuda_stream)
     if key not in _default_ws:
         _default_ws[key] = Workspace(device)
     return _default_ws[key]
@@ -267,8 +293,8 @@ def sample(logits: torch.Tensor, uniforms: torch.Tensor, params: Optional[Sampli
     else:
         ids, lps, tids, tlps, flags = out
     dt = _dtype_code(logits)
-    ws = _ws_for(dev, workspace)
-    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)))
+    ws = _ws_for(dev, workspace, stream)
+    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)), stream)
     prm = _params(params, dev)
     st = _lib.albireo_sample(logits.data_ptr(), dt, B, V, ld, ctypes.byref(prm) if prm else None,
                              uniforms.data_ptr(), ids.data_ptr(), lps.data_ptr(), n_top,
@@ -307,12 +333,13 @@ class PreparedSample:
         dev = logits.device
         self.B, self.V, self.ld = _rows(logits, V)
         self.dt = _dtype_code(logits)
-        ws = _ws_for(dev, workspace)
-        self.wptr, self.wbytes = ws.get(int(_lib.albireo_workspace_size(self.B, self.V, self.dt, n_top)))
+        ws = _ws_for(dev, workspace, stream)
+        self.wptr, self.wbytes = ws.get(int(_lib.albireo_workspace_size(self.B, self.V, self.dt, n_top)), stream)
         self.prm = _params(params, dev)
         self.prm_ref = ctypes.byref(self.prm) if self.prm else None
         ids, lps, tids, tlps, flags = out
-        self.keep = (uniforms, params, out)
+        # the workspace buffer too: a later, larger call may give the Workspace a new one
+        self.keep = (uniforms, params, out, ws.buf)
         self.tail = (self.prm_ref, uniforms.data_ptr(), ids.data_ptr(), lps.data_ptr(), n_top,
                      tids.data_ptr() if n_top else None, tlps.data_ptr() if n_top else None, flags.data_ptr(),
                      self.wptr, self.wbytes, _stream(stream))
@@ -359,8 +386,8 @@ def sample_step(logits: torch.Tensor, seed: int, step: int, seq_ids: Optional[to
     stp = _step_arg(dev, B, seed, step, seq_ids, next_tokens, backfill_dest)
     ids, lps, tids, tlps, flags = _outs(B, n_top, dev, out)
     dt = _dtype_code(logits)
-    ws = _ws_for(dev, workspace)
-    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)))
+    ws = _ws_for(dev, workspace, stream)
+    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)), stream)
     prm = _params(params, dev)
     st = _lib.albireo_sample_step(logits.data_ptr(), dt, B, V, ld, ctypes.byref(prm) if prm else None,
                                   ctypes.byref(stp), ids.data_ptr(), lps.data_ptr(), n_top,
@@ -412,8 +439,8 @@ def sample_sharded(recv: torch.Tensor, V: Optional[int] = None, uniforms: Option
         raise ValueError("uniforms must be a float32 [B] tensor on the logits' device")
     ids, lps, tids, tlps, flags = _outs(B, n_top, dev, out)
     dt = _dtype_code(recv)
-    ws = _ws_for(dev, workspace)
-    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)))
+    ws = _ws_for(dev, workspace, stream)
+    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, dt, n_top)), stream)
     prm = _params(params, dev)
     shards = _Shards(shard_len=L, shard_stride=recv.stride(0))
     st = _lib.albireo_sample_sharded(recv.data_ptr(), dt, B, V, recv.stride(1), ctypes.byref(shards),
@@ -489,8 +516,8 @@ def topk_topp(logits: torch.Tensor, params: Optional[SamplingParams] = None, V: 
     kept = torch.empty(B, dtype=torch.int32, device=dev)
     lnorm = torch.empty(B, dtype=torch.float32, device=dev)
     flags = torch.empty(B, dtype=torch.int32, device=dev)
-    ws = _ws_for(dev, workspace)
-    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, F32, 0)))
+    ws = _ws_for(dev, workspace, stream)
+    wptr, wbytes = ws.get(int(_lib.albireo_workspace_size(B, V, F32, 0)), stream)
     prm = _params(params, dev)
     st = _lib.albireo_topk_topp(logits.data_ptr(), B, V, ld, ctypes.byref(prm) if prm else None,
                                 pr.data_ptr() if pr is not None else None, thr.data_ptr(), kept.data_ptr(),

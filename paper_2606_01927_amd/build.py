@@ -18,6 +18,8 @@ HIPCC_FLAGS = [
     "-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC",
     # bit-exact processed logits: no contraction of the canonical fp32 multiplies and adds
     "-ffp-contract=off",
+    # a host function whose every path calls itself fails the build (clang leaves this warning off)
+    "-Werror=infinite-recursion",
     # no packed fp32 instructions (v_pk_*_f32) anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]

@@ -2565,26 +2565,16 @@ __global__ __launch_bounds__(NT) void k_sample_multi(KArgs a) {
 }  // namespace
 
 // ==============================================================================================
-// Standalone penalties: albireo_apply_penalties.  A workgroup handles one tile of one row: the
-// tile's history ids are counted in an LDS hash, a bit per tile element marks the penalised ones,
-// and the tile is streamed to the fp32 output (each element read and written by the same thread,
-// so the output may alias an fp32 input).
+// Standalone penalties: albireo_apply_penalties.  A workgroup handles one tile of one row: every id of
+// the row's output history, prompt history or penalty state that falls in the tile is folded into a
+// 32-bit word per tile element in LDS (bits 0-30 the output count, bit 31 the prompt mark: the penalty
+// state's encoding), and the tile is streamed to the fp32 output (each element read and written by the
+// same thread, so the output may alias an fp32 input).  The words are exact for any history length.
 // ==============================================================================================
 namespace {
 
 constexpr int PEN_NT = 256;
-constexpr int PEN_LOG2_HCAP = 13;
-constexpr int PEN_HCAP = 1 << PEN_LOG2_HCAP;
-constexpr int64_t PEN_TILE = 65536;  // elements per workgroup (8 KB bitmap)
-
-struct PenSmem {
-  int32_t h_key[PEN_HCAP];
-  uint32_t h_cnt[PEN_HCAP];
-  uint32_t bits[PEN_TILE / 32];
-  int32_t n_used;
-};
-
-__device__ __forceinline__ uint32_t pen_hash(int id) { return ((uint32_t)id * 2654435761u) >> (32 - PEN_LOG2_HCAP); }
+constexpr int64_t PEN_TILE = 16384;  // elements per workgroup (64 KB of LDS words)
 
 // The uniforms alone (one thread per row), for callers that sample elsewhere.
 __global__ __launch_bounds__(256) void k_philox_uniforms(uint64_t seed, uint64_t step, const int64_t* seq_ids,
@@ -2603,10 +2593,21 @@ __global__ __launch_bounds__(256) void k_backfill(const int32_t* ids, const int3
   }
 }
 
+// The prompt history (repetition only) and the per-sequence penalty state, beside the output history.
+struct PenExtra {
+  const int64_t* prompt_offsets;
+  const int32_t* prompt_ids;
+  int64_t prompt_len;
+  const int32_t* st_ids;
+  const uint32_t* st_counts;
+  const int32_t* st_len;
+  int32_t st_cap;
+};
+
 template <class DT>
 __global__ __launch_bounds__(PEN_NT) void k_penalties(const unsigned char* logits, int64_t V, int64_t ld,
-                                                      DevParams prm, float* out) {
-  __shared__ PenSmem s;
+                                                      DevParams prm, PenExtra ex, float* out) {
+  __shared__ uint32_t cvs[PEN_TILE];
   const int64_t row = blockIdx.y;
   const int64_t t0 = (int64_t)blockIdx.x * PEN_TILE;
   const int64_t t1 = min(V, t0 + PEN_TILE);
@@ -2623,55 +2624,41 @@ __global__ __launch_bounds__(PEN_NT) void k_penalties(const unsigned char* logit
     hi = prm.hist_offsets[row + 1];
     if (lo < 0 || hi < lo || hi > prm.hist_len) lo = hi = 0;
   }
-  const bool pen = hi > lo;
+  int64_t plo = 0, phi = 0;
+  if (ex.prompt_offsets) {
+    plo = ex.prompt_offsets[row];
+    phi = ex.prompt_offsets[row + 1];
+    if (plo < 0 || phi < plo || phi > ex.prompt_len) plo = phi = 0;
+  }
+  int sn = 0;
+  if (ex.st_len) {
+    sn = ex.st_len[row];
+    sn = sn < 0 ? 0 : (sn > ex.st_cap ? ex.st_cap : sn);
+  }
+  const bool pen = hi > lo || phi > plo || sn > 0;
   if (pen) {
-    for (int i = threadIdx.x; i < PEN_HCAP; i += PEN_NT) {
-      s.h_key[i] = -1;
-      s.h_cnt[i] = 0;
-    }
-    for (int i = threadIdx.x; i < PEN_TILE / 32; i += PEN_NT) s.bits[i] = 0;
-    if (threadIdx.x == 0) s.n_used = 0;
+    for (int i = threadIdx.x; i < PEN_TILE; i += PEN_NT) cvs[i] = 0;
     __syncthreads();
     for (int64_t h = lo + threadIdx.x; h < hi; h += PEN_NT) {
       const int id = prm.hist_ids[h];
-      if (id < t0 || id >= t1) continue;
-      uint32_t k = pen_hash(id);
-      for (int probe = 0; probe < PEN_HCAP; ++probe) {
-        const int prev = atomicCAS(&s.h_key[k], -1, id);
-        if (prev == -1) {
-          if (atomicAdd(&s.n_used, 1) >= (PEN_HCAP * 3) / 4) {  // keep probing chains short
-            s.h_key[k] = -2;                                    // tombstone: slot unusable
-            break;
-          }
-          atomicAdd(&s.h_cnt[k], 1u);
-          atomicOr(&s.bits[(id - t0) >> 5], 1u << ((id - t0) & 31));
-          break;
-        }
-        if (prev == id) {
-          atomicAdd(&s.h_cnt[k], 1u);
-          break;
-        }
-        k = (k + 1) & (PEN_HCAP - 1);
-      }
+      if (id >= t0 && id < t1) atomicAdd(&cvs[id - t0], 1u);
+    }
+    for (int64_t h = plo + threadIdx.x; h < phi; h += PEN_NT) {
+      const int id = ex.prompt_ids[h];
+      if (id >= t0 && id < t1) atomicOr(&cvs[id - t0], 0x80000000u);
+    }
+    for (int e = threadIdx.x; e < sn; e += PEN_NT) {
+      const int id = ex.st_ids[row * ex.st_cap + e];
+      if (id >= t0 && id < t1) cvs[id - t0] = ex.st_counts[row * ex.st_cap + e];  // distinct ids
     }
     __syncthreads();
   }
   float* orow = out + row * V;
   for (int64_t i = t0 + threadIdx.x; i < t1; i += PEN_NT) {
     float x = DT::load1(rowp, i);
-    if (pen && ((s.bits[(i - t0) >> 5] >> ((i - t0) & 31)) & 1u)) {
-      uint32_t k = pen_hash((int)i);
-      uint32_t cnt = 0;
-      for (int probe = 0; probe < PEN_HCAP; ++probe) {
-        const int key = s.h_key[k];
-        if (key == (int)i) {
-          cnt = s.h_cnt[k];
-          break;
-        }
-        if (key == -1) break;
-        k = (k + 1) & (PEN_HCAP - 1);
-      }
-      if (cnt > 0) x = penalise(x, cnt, rep, freq, pres);
+    if (pen) {
+      const uint32_t cv = cvs[i - t0];
+      if (cv != 0) x = penalise_cv(x, cv, rep, freq, pres);
     }
     orow[i] = x;
   }
@@ -2759,23 +2746,27 @@ hipError_t device_caps(int dev, const void* fn, size_t smem, DeviceCaps& out) {
   return hipErrorUnknown;
 }
 
-hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& G, bool seg = false) {
+// The shape part of the geometry (chunks per row, register slots, kernel, whether the kernels apply),
+// from V and dtype alone, with no runtime call.
+void shape_geometry(int64_t V, albireo_dtype_t dtype, bool seg, Geometry& G) {
+  memset(&G, 0, sizeof G);
   const int VEC = dtype == ALBIREO_BF16 ? BF16T::VEC : F32T::VEC;
   const int64_t max_body = V / VEC;
   int64_t P = (max_body + (int64_t)JMAX * NT - 1) / ((int64_t)JMAX * NT);
   if (P < 1) P = 1;
-  G.ok = P <= MAXP;
-  if (!G.ok) return hipSuccess;
+  if (P > MAXP) return;
   G.P = (int)P;
   G.chunk_slots = (max_body + P - 1) / P;
   G.k = dtype == ALBIREO_BF16 ? pick_kernel<BF16T>(G.chunk_slots, G.P > 1, seg)
                               : pick_kernel<F32T>(G.chunk_slots, G.P > 1, seg);
   // the single-chunk kernel skips the dead-slot test below live_slots_min(J) (always true for the
   // size pick_kernel chose; a build restricted to one size can miss it for small rows)
-  if (G.P == 1 && max_body - 1 < (int64_t)live_slots_min(G.k.J) * NT) {
-    G.ok = false;
-    return hipSuccess;
-  }
+  G.ok = !(G.P == 1 && max_body - 1 < (int64_t)live_slots_min(G.k.J) * NT);
+}
+
+hipError_t make_geometry(int64_t B, int64_t V, albireo_dtype_t dtype, Geometry& G, bool seg = false) {
+  shape_geometry(V, dtype, seg, G);
+  if (!G.ok) return hipSuccess;
   G.smem = sizeof(Smem);
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -2805,19 +2796,26 @@ size_t legacy_ws(int64_t B, int64_t V, albireo_dtype_t dtype) {
   return required_ws(G);
 }
 
-// Kernel choice by shape alone, so that a row gets the same arithmetic in every layout and batch: a
-// row that fits one workgroup's registers is sampled by that one workgroup (no global round trip
-// between its phases); wider rows go to the streaming kernels.
-bool use_stream(int64_t B, int64_t V, albireo_dtype_t dtype) {
-  if (!albireo_stream::supported(B, V, dtype)) return false;
-  Geometry G;
-  if (make_geometry(B, V, dtype, G) != hipSuccess) return false;
-  return !G.ok || G.P > 1;
-}
-
 // A prompt history or a penalty state is read by the streaming kernels only.
 bool needs_stream(const albireo_params_t* params) {
   return params && (params->prompt_offsets || params->state);
+}
+
+// Kernel choice by shape alone (host only, no runtime call), so that a row gets the same arithmetic in
+// every layout and batch: a row that fits one workgroup's registers is sampled by that one workgroup
+// (no global round trip between its phases); wider rows, and rows with a prompt history or a penalty
+// state, go to the streaming kernels; the cooperative chunked kernel takes what the streaming kernels
+// cannot index (B x chunks >= 2^31).  Every sampling entry point routes through this one decision.
+albireo_route_t route_of(int64_t B, int64_t V, albireo_dtype_t dtype, const albireo_params_t* params, bool seg) {
+  if (B < 0 || V <= 0 || V >= ((int64_t)1 << 31) - 16 || (dtype != ALBIREO_F32 && dtype != ALBIREO_BF16))
+    return ALBIREO_ROUTE_NONE;
+  const bool st = albireo_stream::supported(B > 0 ? B : 1, V, dtype);
+  if (needs_stream(params)) return st ? ALBIREO_ROUTE_STREAM : ALBIREO_ROUTE_NONE;
+  Geometry G;
+  shape_geometry(V, dtype, seg, G);
+  if (G.ok && G.P == 1) return ALBIREO_ROUTE_ONE_WORKGROUP;
+  if (st) return ALBIREO_ROUTE_STREAM;
+  return G.ok ? ALBIREO_ROUTE_COOPERATIVE : ALBIREO_ROUTE_NONE;
 }
 
 albireo_status_t launch_sample(const KArgs& a0, const Geometry& G, hipStream_t stream) {
@@ -2941,9 +2939,10 @@ albireo_status_t sample_impl(const void* logits, albireo_dtype_t dtype, int64_t 
     st = check_shards(logits, dtype, V, ld, *shards);
     if (st != ALBIREO_OK) return st;
   }
-  if (needs_stream(params) && !albireo_stream::supported(B, V, dtype)) return ALBIREO_E_UNSUPPORTED;
-  if (!use_stream(B, V, dtype) && !needs_stream(params)) {
-    // a row that fits one workgroup's registers
+  const albireo_route_t route = route_of(B, V, dtype, params, shards != nullptr);
+  if (route == ALBIREO_ROUTE_NONE) return ALBIREO_E_UNSUPPORTED;
+  if (route != ALBIREO_ROUTE_STREAM) {
+    // the register-resident kernels
     Geometry G;
     if (make_geometry(B, V, dtype, G, shards != nullptr) != hipSuccess) return ALBIREO_E_LAUNCH;
     if (!G.ok) return ALBIREO_E_UNSUPPORTED;
@@ -3036,6 +3035,11 @@ albireo_status_t scratch_for_current_device(void** out) {
 }  // namespace
 
 extern "C" {
+
+albireo_route_t albireo_sample_route(int64_t B, int64_t V, albireo_dtype_t dtype, const albireo_params_t* params,
+                                    int32_t sharded) {
+  return route_of(B, V, dtype, params, sharded != 0);
+}
 
 size_t albireo_workspace_size(int64_t B, int64_t V, albireo_dtype_t dtype, int32_t n_top) {
   (void)n_top;
@@ -3163,20 +3167,32 @@ albireo_status_t albireo_apply_penalties(const void* logits, albireo_dtype_t dty
   (void)workspace_bytes;
   albireo_status_t st = check_common(logits, dtype, B, V, ld, params);
   if (st != ALBIREO_OK) return st;
-  if (params && (params->prompt_offsets || params->state)) return ALBIREO_E_UNSUPPORTED;
   if (B == 0) return ALBIREO_OK;
   if (!out_logits) return ALBIREO_E_INVALID;
   // aliasing is only defined for an fp32 input with ld == V (element-wise in place)
   if (static_cast<const void*>(out_logits) == logits && !(dtype == ALBIREO_F32 && ld == V)) return ALBIREO_E_INVALID;
   if (B > 65535) return ALBIREO_E_UNSUPPORTED;
   const DevParams d = dev_params(params);
+  PenExtra ex;
+  memset(&ex, 0, sizeof ex);
+  if (params) {
+    ex.prompt_offsets = params->prompt_offsets;
+    ex.prompt_ids = params->prompt_ids;
+    ex.prompt_len = params->prompt_len;
+    if (params->state) {
+      ex.st_ids = params->state->ids;
+      ex.st_counts = params->state->counts;
+      ex.st_len = params->state->len;
+      ex.st_cap = params->state->cap;
+    }
+  }
   const dim3 grid((unsigned)((V + PEN_TILE - 1) / PEN_TILE), (unsigned)B);
   if (dtype == ALBIREO_BF16)
     hipLaunchKernelGGL(k_penalties<BF16T>, grid, dim3(PEN_NT), 0, stream,
-                       static_cast<const unsigned char*>(logits), V, ld, d, out_logits);
+                       static_cast<const unsigned char*>(logits), V, ld, d, ex, out_logits);
   else
     hipLaunchKernelGGL(k_penalties<F32T>, grid, dim3(PEN_NT), 0, stream,
-                       static_cast<const unsigned char*>(logits), V, ld, d, out_logits);
+                       static_cast<const unsigned char*>(logits), V, ld, d, ex, out_logits);
   return hipGetLastError() == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
 }
 

@@ -54,6 +54,18 @@ __device__ __forceinline__ float penalise(float x, uint32_t c, float rep, float 
   v = __fsub_rn(v, pres);
   return v;
 }
+// The penalty overlay of one logit whose history record is cv: bits 0-30 its count in the output, bit 31
+// set when it occurs in the prompt.  Repetition covers both; frequency and presence count the output.
+__device__ __forceinline__ float penalise_cv(float x, uint32_t cv, float rep, float freq, float pres) {
+  const uint32_t c = cv & 0x7fffffffu;
+  float v = (x > 0.0f) ? __fdiv_rn(x, rep) : __fmul_rn(x, rep);
+  if (c > 0) {
+    v = __fsub_rn(v, __fmul_rn(freq, (float)c));
+    v = __fsub_rn(v, pres);
+  }
+  return v;
+}
+
 // 2^(a - b) for a <= b; a == b (including both -inf) -> 1
 __device__ __forceinline__ float rel2(float a, float b) { return (a == b) ? 1.0f : __builtin_amdgcn_exp2f(a - b); }
 // candidate sort key: z descending, then position ascending

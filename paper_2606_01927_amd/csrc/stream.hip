@@ -274,18 +274,6 @@ __device__ __forceinline__ uint64_t blk_excl_scan_u64(uint64_t v, SSm& s, uint64
   return off + incl - v;
 }
 
-// The penalty overlay of one logit whose history record is cv: bits 0-30 its count in the output, bit 31
-// set when it occurs in the prompt.  Repetition covers both; frequency and presence count the output.
-__device__ __forceinline__ float penalise_cv(float x, uint32_t cv, float rep, float freq, float pres) {
-  const uint32_t c = cv & 0x7fffffffu;
-  float v = (x > 0.0f) ? __fdiv_rn(x, rep) : __fmul_rn(x, rep);
-  if (c > 0) {
-    v = __fsub_rn(v, __fmul_rn(freq, (float)c));
-    v = __fsub_rn(v, pres);
-  }
-  return v;
-}
-
 // (mref, s) pairs: s is relative to 2^mref
 __device__ __forceinline__ void lse_add(float& m, float& s, float m2, float s2) {
   const float M = fmaxf(m, m2);

@@ -14,7 +14,7 @@ HEADER = os.path.join(ROOT, "include", "albireo.h")
 
 def _declared():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:albireo_status_t|size_t|const char\*)\s+(albireo_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:albireo_status_t|albireo_route_t|size_t|const char\*)\s+(albireo_\w+)\s*\(", text, re.M)))
 
 
 @pytest.fixture(scope="module")
@@ -30,7 +30,8 @@ def alb():
 def test_header_declares_the_entry_points():
     assert _declared() == sorted(["albireo_apply_penalties", "albireo_backfill", "albireo_philox_uniforms",
                                   "albireo_penalty_state_append", "albireo_penalty_state_init",
-                                  "albireo_sample", "albireo_sample_noalloc", "albireo_sample_sharded",
+                                  "albireo_sample", "albireo_sample_noalloc", "albireo_sample_route",
+                                  "albireo_sample_sharded",
                                   "albireo_sample_step",
                                   "albireo_status_string",
                                   "albireo_topk_topp", "albireo_workspace_size"])

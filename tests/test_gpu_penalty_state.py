@@ -203,3 +203,34 @@ def test_sample_with_state_equals_histories(cfg, B, V, lib, oracle_mod):
         p.hist_offsets, p.hist_ids = _dev(w.hist_offsets, torch.int64), _dev(w.hist_ids, torch.int32)
         outs.append(ids)
     assert len(outs) == 4
+
+
+@pytest.mark.parametrize("cfg,B,V,H,P", [(3, 8, 20011, 1000, 600), (5, 4, 170011, 1024, 6000),
+                                         (4, 6, 60013, 0, 300)],
+                         ids=["c3_B8_V20011", "c5_B4_V170011_long_prompt", "c4_B6_V60013_prompt_only"])
+def test_apply_penalties_prompt_and_state_bit_exact(cfg, B, V, H, P, lib, oracle_mod):
+    """albireo_apply_penalties with a prompt history, then with the penalty state built from the same
+    two histories: both bit-identical to the oracle's penalised logits (the long prompt gives each row
+    thousands of distinct ids, within the state's 8192 entries)."""
+    import torch
+
+    from workloads.device import to_device
+
+    w = _with_penalties(workloads.generate(cfg, B=B, V=V, H=H if H else None, variant=8), seed=cfg)
+    if not H:
+        w.hist_offsets, w.hist_ids = _csr([[] for _ in range(B)])
+    workloads.add_prompt(w, P, seed=20 + cfg, s=0.6)
+    ref = oracle_mod.sample(w, penalised=True)["penalised"]
+    logits, u, p = to_device(w)
+    _say("apply_penalties prompt", cfg, B, V, H, P)
+    got = lib.apply_penalties(logits, p, V=V)
+    torch.cuda.synchronize()
+    assert np.array_equal(np_(got).view(np.uint32), ref.view(np.uint32))
+    st = lib.PenaltyState(B, cap=8192).init(V, p.prompt_offsets, p.prompt_ids, p.hist_offsets, p.hist_ids)
+    assert not (np_(st.flags) & lib.FLAG_LIMIT).any()
+    ps = lib.SamplingParams(repetition_penalty=p.repetition_penalty, frequency_penalty=p.frequency_penalty,
+                            presence_penalty=p.presence_penalty, state=st)
+    _say("apply_penalties state", cfg, B, V, H, P)
+    got_s = lib.apply_penalties(logits, ps, V=V)
+    torch.cuda.synchronize()
+    assert np.array_equal(np_(got_s).view(np.uint32), ref.view(np.uint32))
