@@ -6,9 +6,14 @@ top_k 40, top_p 0.95 -- the configuration the headline metric is quoted on.  Inp
 (workloads.generate(3)) and resident in HBM before the timed region; the call rotates over enough
 copies (>= 1 GiB) that every step reads its logits from HBM rather than from the 256 MB MALL.
 
-Prints one JSON line: rows/s (whole job), ms per step, the roofline entry of the sampling kernel
+Timing protocol: REPS (5) repetitions of --steps steps each; before each repetition a spin kernel
+holds the stream while the host enqueues the steps, so the HIP events around the steps time the GPU,
+not the host's enqueue rate.  The reported step time is the median repetition, with the spread.
+
+Prints one JSON line: rows/s (whole job), ms per step, the roofline entry of the dominant kernel
 (algorithmic bytes per launch / its average launch time from HIP events on its stream, against the
-8 TB/s HBM peak) and the CPU oracle timed on a bounded sample of the same workload.
+8 TB/s HBM peak), the device's clock and memory figures as the runtime reports them, and the CPU
+oracle timed on a bounded sample of the same workload (all host threads, and one thread).
 """
 from __future__ import annotations
 
@@ -39,10 +44,44 @@ def algorithmic_bytes(w) -> int:
     return int(b)
 
 
-# the sources the headline workload's kernel (k_sample) is compiled from
+# the sources the headline workload's kernel (k_sample: its rows fit one workgroup) is compiled from
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_01927_amd", "csrc", n) for n in ("albireo.hip", "common.h")] + [
     os.path.join(ROOT, "include", "albireo.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sample_C3_B256_V152064_bf16_traffic.txt")
+REPS = 5
+# hipDeviceAttribute_t values of this ROCm (hip_runtime_api.h)
+HIP_ATTR = {"clock_khz": 5, "memory_bus_bits": 59, "memory_clock_khz": 60, "l2_bytes": 19, "cus": 63}
+
+
+def device_figures(dev: int = 0) -> dict:
+    """What the HIP runtime reports for the device: its name, CU count, peak shader clock, memory clock
+    and bus width (and the DRAM bandwidth they imply at two transfers per clock), L2 size."""
+    import ctypes
+
+    import torch
+
+    props = torch.cuda.get_device_properties(dev)
+    out = {"name": props.name, "gcn_arch": props.gcnArchName, "total_memory_bytes": props.total_memory}
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+        for k, attr in HIP_ATTR.items():
+            v = ctypes.c_int(0)
+            if hip.hipDeviceGetAttribute(ctypes.byref(v), attr, dev) == 0:
+                out[k] = v.value
+    except OSError:
+        pass
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def kernel_source_hash() -> str:
@@ -85,14 +124,16 @@ def copy_calibration(mib: int):
     del src, dst
 
 
-def cpu_baseline(w, seconds_target: float = 15.0) -> dict:
-    """The oracle as it stands, on a bounded sample of rows of the same workload, all host threads."""
+def cpu_baseline(w, seconds_target: float = 15.0, nthreads: int = 0) -> dict:
+    """The oracle as it stands, on a bounded sample of rows of the same workload, on nthreads host
+    threads (0: all of them)."""
     import numpy as np
 
     import oracle
 
     oracle.build(force=False)
-    nthreads = oracle.max_threads()
+    if nthreads <= 0:
+        nthreads = oracle.max_threads()
     rows_done = 0
     t0 = time.perf_counter()
     n = max(nthreads, 8)
@@ -190,6 +231,7 @@ def other_configs(alb, dev, reps: int = 20) -> dict:
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
+        torch.cuda._sleep(int(4e-3 * 2.4e9))  # holds the stream while the calls are enqueued
         e0.record(stream)
         for i in range(reps):
             call(ptrs[i % ncopy])
@@ -258,24 +300,43 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # HIP events on the launch stream bracket the timed region: one kernel launch per step, so the
-    # average launch time of the sampling kernel is the elapsed time over the steps
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
+    # host enqueue rate, to size the spin that keeps the launch queue ahead of the GPU
     t0 = time.perf_counter()
-    e0.record(stream)
     for i in range(args.steps):
         step(i)
-    e1.record(stream)
+    host_enqueue_s = time.perf_counter() - t0
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    total_ms = e0.elapsed_time(e1)
-    ms_per_step = total_ms / args.steps
+    spin_cycles = int(max(2e-3, 3.0 * host_enqueue_s) * 2.4e9)
+
+    # REPS repetitions; HIP events on the launch stream bracket the steps of each (the spin kernel ahead
+    # of the first event holds the stream while the host enqueues them all)
+    reps_ms = []
+    wall = 0.0
+    for rep in range(REPS):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(spin_cycles)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for i in range(args.steps):
+            step(i)
+        e1.record(stream)
+        enq = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        wall += enq
+        reps_ms.append(e0.elapsed_time(e1) / args.steps)
+    order = sorted(reps_ms)
+    ms_per_step = order[len(order) // 2]
     launch_us = ms_per_step * 1e3
     alg = algorithmic_bytes(w)
     achieved = alg / (launch_us * 1e-6) / 1e9
-    rows_per_s = B * args.steps / (total_ms * 1e-3)
+    rows_per_s = B / (ms_per_step * 1e-3)
+    # the kernels the library routes this shape to (the same host decision the call takes)
+    kernel = {alb.ROUTE_ONE_WORKGROUP: "k_sample (one launch per step)",
+              alb.ROUTE_STREAM: "k_stream + k_resolve (two launches per step; the time is both)",
+              alb.ROUTE_COOPERATIVE: "k_sample_multi (one cooperative launch per step)"}[
+                  alb.sample_route(B, V, logits0.dtype, p)]
 
     res = {
         "metric": METRIC,
@@ -284,6 +345,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "reps": REPS,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
@@ -297,9 +359,13 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic() if args.config == 3 else None,
-                     "kernel": "%s (one launch per step)" % ("k_split" if args.config in (4, 5) else "k_sample"),
+                     "kernel": kernel,
                      "algorithmic_bytes": alg,
-                     "launch_us_avg": launch_us, "host_wall_us_per_step": wall * 1e6 / args.steps},
+                     "launch_us_avg": launch_us},
+        "timing": {"ms_per_step_reps": reps_ms, "spread_ms": [order[0], order[-1]],
+                   "host_enqueue_us_per_step": wall * 1e6 / (REPS * args.steps),
+                   "spin_cycles_ahead": spin_cycles},
+        "device": device_figures(0),
         "wall_s": wall,
     }
     if not args.no_extras:
@@ -308,6 +374,9 @@ def main():
         res["other_configs"] = other_configs(alb, dev)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(w)
+        res["cpu_baseline"]["cpu_model"] = cpu_model()
+        one = cpu_baseline(w, seconds_target=10.0, nthreads=1)
+        res["cpu_baseline"]["one_thread"] = {"value": one["value"], "unit": one["unit"], "sample": one["sample"]}
     print(json.dumps(res))
 
 
