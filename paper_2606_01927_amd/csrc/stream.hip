@@ -48,7 +48,7 @@ namespace {
 constexpr int CT = 256;                            // threads per chunk workgroup
 constexpr int CW = CT / 64;                        // waves per workgroup
 constexpr int CJ = 19;                             // 16-byte register slots per thread (chunk kernel)
-constexpr int GJ = 19;                             // slots per thread per re-read batch (resolution kernel)
+constexpr int GJ = 4;                              // slots per thread per re-read batch (resolution kernel)
 constexpr int CSLOTS = CT * CJ;                    // body slots per chunk at most
 constexpr int BMW = ((CSLOTS + 2) * 8 + 31) / 32;  // bitmap words (one bit per element, +1 slot each side)
 constexpr int XCAP = ALBIREO_MAX_UNIQUE_HISTORY;   // distinct penalised positions tracked per chunk
@@ -876,8 +876,12 @@ __device__ __forceinline__ bool gp_level1(const SArgs& a, const SRow& R, SSm& s,
   RowSrc<DT, SEG>{a, R, s}([&](float z) __attribute__((always_inline)) {
     if (z > -INFINITY && z >= lo) {
       const int b = gp_dbucket(z, m);
-      if (MASS) atomicAdd(reinterpret_cast<unsigned long long*>(&h64[b]), (unsigned long long)mass_of(z, m));
-      else atomicAdd(&h32[b], 1u);
+      if (MASS) {
+        const uint64_t w = mass_of(z, m);
+        if (w) atomicAdd(reinterpret_cast<unsigned long long*>(&h64[b]), (unsigned long long)w);  // zero adds nothing
+      } else {
+        atomicAdd(&h32[b], 1u);
+      }
     }
   });
   __syncthreads();
@@ -1034,8 +1038,10 @@ __device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm
     for (int i = threadIdx.x; i < GDB; i += CT) h64[i] = 0;
     __syncthreads();
     RowSrc<DT, SEG>{a, R, s}([&](float z) __attribute__((always_inline)) {
-      if (z > -INFINITY && z >= tau2 && gp_dbucket(z, m) == bb)
-        atomicAdd(reinterpret_cast<unsigned long long*>(&h64[gp_dsub(z, m, bb)]), (unsigned long long)mass_of(z, m));
+      if (z > -INFINITY && z >= tau2 && gp_dbucket(z, m) == bb) {
+        const uint64_t w = mass_of(z, m);
+        if (w) atomicAdd(reinterpret_cast<unsigned long long*>(&h64[gp_dsub(z, m, bb)]), (unsigned long long)w);
+      }
     });
     __syncthreads();
     constexpr int BPT = GDB / CT;
