@@ -44,10 +44,17 @@ def algorithmic_bytes(w) -> int:
     return int(b)
 
 
-# the sources the headline workload's kernel (k_sample: its rows fit one workgroup) is compiled from
-KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_01927_amd", "csrc", n) for n in ("albireo.hip", "common.h")] + [
-    os.path.join(ROOT, "include", "albireo.h")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sample_C3_B256_V152064_bf16_traffic.txt")
+# per workload, the file tag of its profile summaries; per route, the kernels timed and the sources
+# they are compiled from (a summary taken on other sources gives no traffic figure)
+PROFILE_TAGS = {1: "C1_B4_V32000_f32", 2: "C2_B64_V128256_bf16", 3: "C3_B256_V152064_bf16",
+                4: "C4_B512_V152064_f32", 5: "C5_B1024_V256000_bf16"}
+_CSRC = os.path.join(ROOT, "paper_2606_01927_amd", "csrc")
+_HDR = os.path.join(ROOT, "include", "albireo.h")
+ROUTE_KERNELS = {
+    1: ("k_sample", [os.path.join(_CSRC, "albireo.hip"), os.path.join(_CSRC, "common.h"), _HDR]),
+    2: ("k_stream_k_resolve", [os.path.join(_CSRC, "stream.hip"), os.path.join(_CSRC, "stream.h"),
+                               os.path.join(_CSRC, "common.h"), _HDR]),
+}
 REPS = 5
 # hipDeviceAttribute_t values of this ROCm (hip_runtime_api.h)
 HIP_ATTR = {"clock_khz": 5, "memory_bus_bits": 59, "memory_clock_khz": 60, "l2_bytes": 19, "cus": 63}
@@ -84,28 +91,34 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(route: int) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SRCS:
+    for p in ROUTE_KERNELS[route][1]:
         with open(p, "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per launch of the sampling kernel from the committed rocprofv3 --pmc summary
+def traffic_file(cfg: int, route: int) -> str:
+    return os.path.join(ROOT, "profiles", "%s_%s_traffic.txt" % (ROUTE_KERNELS[route][0], PROFILE_TAGS[cfg]))
+
+
+def measured_traffic(cfg: int, route: int):
+    """HBM bytes per step (every launch of the route) from the committed rocprofv3 --pmc summary
     (FETCH_SIZE + WRITE_SIZE, each scaled by what the counter reads for a copy of known size), or
-    None when the summary is missing or was taken on a different kernel source."""
+    None when the summary is missing or was taken on different kernel sources."""
+    if route not in ROUTE_KERNELS:
+        return None
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(cfg, route)) as f:
             kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
     except OSError:
         return None
     kv = {k.strip(): v.strip() for k, v in kv.items()}
-    if kv.get("kernel_source_sha256") != kernel_source_hash():
+    if kv.get("kernel_source_sha256") != kernel_source_hash(route):
         return None
     try:
-        return float(kv["traffic_bytes_per_launch"])
+        return float(kv["traffic_bytes_per_step"])
     except (KeyError, ValueError):
         return None
 
@@ -333,10 +346,10 @@ def main():
     achieved = alg / (launch_us * 1e-6) / 1e9
     rows_per_s = B / (ms_per_step * 1e-3)
     # the kernels the library routes this shape to (the same host decision the call takes)
+    route = alb.sample_route(B, V, logits0.dtype, p)
     kernel = {alb.ROUTE_ONE_WORKGROUP: "k_sample (one launch per step)",
               alb.ROUTE_STREAM: "k_stream + k_resolve (two launches per step; the time is both)",
-              alb.ROUTE_COOPERATIVE: "k_sample_multi (one cooperative launch per step)"}[
-                  alb.sample_route(B, V, logits0.dtype, p)]
+              alb.ROUTE_COOPERATIVE: "k_sample_multi (one cooperative launch per step)"}[route]
 
     res = {
         "metric": METRIC,
@@ -358,7 +371,7 @@ def main():
         "hbm_frac_of_peak": alg / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": measured_traffic() if args.config == 3 else None,
+                     "traffic": measured_traffic(args.config, route),
                      "kernel": kernel,
                      "algorithmic_bytes": alg,
                      "launch_us_avg": launch_us},
