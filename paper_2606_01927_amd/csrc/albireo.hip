@@ -1,21 +1,25 @@
-// albireo.hip -- gfx950 kernels and the C ABI of the per-sequence sampling library.
+// albireo.hip -- the register-resident sampling kernels, the standalone helpers and the C ABI of the
+// per-sequence sampling library.
 //
-// One launch samples B rows.  A row (or, for rows wider than one CU can hold, one of P contiguous
-// chunks of it) is owned by one 1024-thread workgroup that keeps the whole chunk in VGPRs: every
-// logit is read from HBM exactly once with 16-byte loads, all issued up front.  On that resident data
-// the workgroup runs
-//   * the penalty overlay (feature list of sec. 8.1): history counts in an LDS hash; a per-slot LDS
-//     bitmap masks the penalised entries in the registers; their new values live in a small LDS
-//     "extras" list together with the few unaligned head/tail entries of the row;
+// k_sample: one 512-thread workgroup per row keeps the whole row in VGPRs (up to 38 16-byte slots per
+// thread: bf16 rows up to 155655 logits, fp32 up to 77827).  Every logit is read from HBM once with
+// 16-byte loads issued up front.  On that resident data the workgroup runs
+//   * the penalty overlay (the feature list of sec. 8.1): the row's history ids mark a per-slot LDS
+//     presence bitmap, the marked entries are masked in the registers and their new values live in a
+//     small LDS "extras" list together with the few unaligned head/tail entries of the row;
 //   * an online max / sum-exp pass overlapped with the loads, giving the full-vocabulary log-sum-exp
-//     the logprobs need (sec. 2.1 T4; App. A appends the sampled id with its probability);
+//     the logprobs need (sec. 2.1; App. A returns the sampled id with its probability);
 //   * a candidate gather above a provable lower bound of the kept set (the K-th largest per-thread
-//     maximum for top-k / top-n, m + ln(min_p) for min-p, a mass bound for top-p);
-//   * exact resolution of top-k / min-p / top-p and the inverse-CDF draw on that small LDS list, or,
-//     when the kept set is too large for the list, radix histogram selection over the registers and a
-//     draw through an id-ordered scan buffer in the workspace.
+//     maximum for top-k / top-n, m + ln(min_p) for min-p);
+//   * exact resolution of top-k / min-p / top-p and the inverse-CDF draw on that small LDS list or,
+//     when the kept set has no small bound, selections over distance buckets and a draw over re-reads
+//     of the row.
+// k_sample_multi: the same on P <= 8 chunk workgroups of a row in one cooperative launch (bounded waits
+// through the caller's workspace); used by albireo_topk_topp on wide rows, and by sampling only for
+// batches the streaming kernels cannot index.  Wider rows, and rows with a prompt history or a penalty
+// state, go to the streaming kernels (stream.hip).  The choice is made by route_of, on the shape alone.
 // Rows never interact, which is what lets the paper split sampling across ranks by rows (sec. 6.1,
-// Eq. opt_sample); the P > 1 chunks of one row synchronise through the caller's workspace.
+// Eq. opt_sample).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
