@@ -1350,7 +1350,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
         for (int c = 0; c < P; ++c) lo = fminf(lo, s.pub[c].qk);
         zthr = fmaxf(zthr, lo);
       }
-      const int ns = stage_entries(a, R, s, sp, zthr, imax, MSTAGE - 2 * MCAP, true);
+      int ns = stage_entries(a, R, s, sp, zthr, imax, MSTAGE - 2 * MCAP, true);
       if (ns < 0) {
         general = true;
       } else {
@@ -1362,11 +1362,18 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
           __syncthreads();
           tau2 = fmaxf(tau2, s.bc_f[1]);
         }
-        // a list cut off at imax whose first entry left out would be kept (a tie at tau_k) needs the
-        // general path
+        // a list cut off at imax whose first entry left out would be kept (a tie at tau_k): the kept
+        // set is then every list entry z >= tau2 -- no list is over capacity here, and each holds all
+        // of its chunk's values above the chunk's bound, which is at most the chunk's K-th largest
+        // and so at most tau2
         bool cutkept = false;
         for (int c = 0; c < P; ++c)
           if (s.cut[c] && __int_as_float(s.cnt[c]) >= tau2) cutkept = true;
+        if (cutkept) {
+          ns = stage_entries(a, R, s, sp, tau2, LCAPC, MSTAGE - 2 * MCAP, false);
+          cutkept = ns < 0;
+          if (ns < 0) ns = 0;
+        }
         if (t == 0) s.bc_i[2] = 0;
         __syncthreads();
         for (int f = t; f < ns; f += CT) {

@@ -185,6 +185,39 @@ def test_edge_cases(lib, oracle_mod):
     compare_sample(ref, out, n_top=7)
 
 
+@pytest.mark.parametrize("n_top", [0, 4])
+def test_topk_ties_on_streamed_rows(n_top, lib, oracle_mod):
+    """Rows of the streaming route (many chunks per row) whose top-k boundary value is tied, inside one
+    chunk's list beyond its first k entries and across chunks: every tied value is kept (ties kept at
+    the k-th value), with and without top-n."""
+    rng = np.random.default_rng(21)
+    V = 200003  # fp32: 11 chunks per row
+    base = rng.normal(0, 1, size=V).astype(np.float32)
+    rows, K, Pp = [], [], []
+
+    def add(pos, vals, k, p=1.0):
+        x = base.copy()
+        x[pos] = vals
+        rows.append(x); K.append(k); Pp.append(p)
+
+    add([10, 20], 9.0, 1)                          # tied maximum, one chunk
+    add([10, 150000], 9.0, 1)                      # tied maximum, two chunks
+    add([10, 20, 30], 9.0, 2)                      # three-way tie at the top, k = 2
+    add([5, 6, 7, 8], [9.0, 8.5, 8.0, 8.0], 3)     # tie at the k-th value, one chunk
+    add([5, 6, 90000, 190000], [9.0, 8.5, 8.0, 8.0], 3)  # tie at the k-th value, across chunks
+    add([10, 20, 30, 40], 9.0, 1, p=0.5)           # tied maximum with a nucleus
+    add(list(range(100, 140)), 9.0, 7)             # 40 tied values above k = 7
+    w = _rowset(rows, temperature=np.full(len(rows), 0.9, np.float32), top_k=np.array(K, np.int32),
+                top_p=np.array(Pp, np.float32))
+    w.n_top = n_top
+    import torch
+
+    assert lib.sample_route(w.B, V, torch.float32) == lib.ROUTE_STREAM
+    out = _run(lib, w)
+    ref = oracle_mod.sample(w)
+    compare_sample(ref, out, n_top=n_top)
+
+
 @pytest.mark.parametrize("dtype,extras", [("f32", False), ("bf16", False), ("bf16", True)],
                          ids=["f32", "bf16", "bf16_topn_penalties"])
 def test_general_path_wide_rows(dtype, extras, lib, oracle_mod):
