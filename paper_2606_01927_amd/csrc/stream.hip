@@ -583,8 +583,10 @@ __device__ __forceinline__ int overlay_rank(const SSm& s, int b) {
 
 // ----------------------------------------------------------------------------------------------
 // Re-reading a chunk (general path of the resolving workgroup): f(z, pos) for every processed value of
-// chunk c -- penalties from a rebuilt overlay, canonical z -- in the order thread t, slot j.  Every
-// thread of the workgroup must call it (it synchronises).
+// chunk c -- penalties from a rebuilt overlay, canonical z -- in no particular order.  A penalised
+// position is visited twice, first as -inf (masked in the slot loop, which then needs no per-element
+// branch) and then with its new value, so every f must ignore -inf.  Every thread of the workgroup must
+// call it (it synchronises).
 // ----------------------------------------------------------------------------------------------
 template <class DT, bool SEG, class F>
 __device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s, int c, F&& f) {
@@ -598,10 +600,13 @@ __device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s,
   else if (c == R.P - 1 && t >= 8 && t < 8 + (R.V - R.tail_lo)) hpos = R.tail_lo + (t - 8);
   const float hx = hpos >= 0 ? load_elem<DT, SEG>(a, R, hpos) : 0.0f;
   const int64_t e_base = (int64_t)R.head + (s0 - 1) * VEC;
+  int n_x = 0;
+  bool x_all = true;  // every marked position is tracked: the element loop masks them all
   if (R.pen_on) {
     uint32_t fl = 0;
     const int32_t none[1] = {0};
-    build_overlay<0>(a, R, s, c, s0, s1, VEC, none, &fl);
+    n_x = build_overlay<0>(a, R, s, c, s0, s1, VEC, none, &fl);
+    x_all = !(fl & FLAG_LIMIT);
   }
   const float r = R.r;
   auto value = [&](float x, int pos) __attribute__((always_inline)) -> float {
@@ -631,19 +636,38 @@ __device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s,
         if (R.pen_on) {
           word = s.c.p.bitmap[ob >> 5];
           bits = (word >> (ob & 31)) & ((1u << VEC) - 1u);
-          if (bits) wpre = s.c.p.wpref[ob >> 5];
         }
+        if (x_all) {
+          // marked values are visited below with their new values; here they are -inf (ignored)
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          float x = elem<DT>(d[j], e);
-          if ((bits >> e) & 1u) {
-            const int rk = (int)wpre + __popc(word & ((1u << ((ob & 31) + e)) - 1u));
-            if (rk < XCAP) x = penalise_cv(x, s.c.p.xval[rk], R.rep, R.freq, R.pres);
+          for (int e = 0; e < VEC; ++e) {
+            const float x = ((bits >> e) & 1u) ? -INFINITY : elem<DT>(d[j], e);
+            f(canon(x, r), p0 + e);
           }
-          f(canon(x, r), p0 + e);
+        } else {
+          if (bits) wpre = s.c.p.wpref[ob >> 5];
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            float x = elem<DT>(d[j], e);
+            if ((bits >> e) & 1u) {
+              const int rk = (int)wpre + __popc(word & ((1u << ((ob & 31) + e)) - 1u));
+              if (rk < XCAP) x = penalise_cv(x, s.c.p.xval[rk], R.rep, R.freq, R.pres);
+            }
+            f(canon(x, r), p0 + e);
+          }
         }
       }
     });
+  }
+  if (x_all && n_x > 0) {
+    // the marked body positions with their new values (head and tail positions are visited above)
+    const int nwords = (int)(((s1 - s0 + 2) * VEC + 31) >> 5);
+    for (int i = t; i < n_x; i += CT) {
+      const int pos = pos_of_rank(s, nwords, e_base, i);
+      const int b = (int)(pos - e_base);
+      if (b >= VEC && b < (int)(s1 - s0 + 1) * VEC)
+        f(canon(penalise_cv(load_elem<DT, SEG>(a, R, pos), s.c.p.xval[i], R.rep, R.freq, R.pres), r), pos);
+    }
   }
   if (hpos >= 0) f(value(hx, hpos), hpos);
   __syncthreads();  // the overlay is rebuilt for the next chunk
@@ -1204,7 +1228,7 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, fl
     __syncthreads();
     if (id >= 0) {
       for_chunk<DT, SEG>(a, R, s, chunk_of(a, R, VEC, id), [&](float z, int pos) __attribute__((always_inline)) {
-        if (pos == id) s.bc_f[0] = z;
+        if (pos == id && z > -INFINITY) s.bc_f[0] = z;  // a penalised id is also visited as -inf
       });
     }
     __syncthreads();
