@@ -57,6 +57,8 @@ constexpr int MCAP = 512;                          // kept-set capacity of the l
 constexpr int MAXPC = 64;                          // chunks per row
 constexpr int HXN = 16;                            // plain head (threads 0-7) and tail (8-15) extras
 constexpr int GEN_WORDS = 512;                     // general-path histogram area (64-bit words)
+constexpr int GSTAGE = 1024;                       // 64-bit words of the resolution kernel's staging area
+constexpr int HSTAGE = 4096;                       // output-history ids the resolution kernel keeps in LDS
 constexpr double LN2 = 0.6931471805599453;
 
 constexpr uint32_t PUB_FINITE = 1u << 29;  // the chunk holds a finite processed value
@@ -152,8 +154,7 @@ struct SSm {
   float wred[3][CW];
   uint64_t qred[CW];
   int32_t n_list;
-  uint64_t* gst;       // resolution kernel: the general path's staging area (GSTAGE words)
-  const int32_t* hst;  // resolution kernel: the row's output history copied to LDS, or null
+  int32_t hst_on;      // resolution kernel: the row's output history is in r_hstage
   uint32_t flags;
   int32_t ov_red[CW];  // the overlay build's block scan (callers keep counters in bc_i across it)
   int32_t bc_i[4];
@@ -165,6 +166,13 @@ struct SSm {
 constexpr int MSTAGE = (int)(sizeof(SSm::key) / 8);
 static_assert(MSTAGE >= 2048, "list staging area below 2048 keys");
 static_assert(sizeof(SSm) <= 40 * 1024, "LDS of a chunk workgroup exceeds a quarter of a gfx950 CU");
+
+// The resolution kernel's LDS beside SSm, at namespace scope so that every access to it compiles to an
+// LDS instruction (a pointer kept in SSm is generic, and generic accesses wait on the memory counters
+// too): the general path's staging area and the row's output history.  Only the resolution kernel
+// refers to them, so only it allocates them.
+__shared__ uint64_t r_gstage[GSTAGE];
+__shared__ int32_t r_hstage[HSTAGE];
 
 // Hide the register slots' contents from the optimiser between passes, so that it unpacks the slots
 // again in every pass instead of keeping all unpacked (or scaled) values of the previous one alive.
@@ -478,11 +486,6 @@ __device__ __forceinline__ int build_overlay(const SArgs& a, const SRow& R, SSm&
   const int64_t e_lo = c == 0 ? 0 : (int64_t)R.head + s0 * vec;
   const int64_t e_hi = c == R.P - 1 ? (int64_t)R.V : (int64_t)R.head + s1 * vec;
   uint32_t bad = 0;
-  // the output history: from the caller's registers and memory, or (resolution kernel) all of it from
-  // its LDS copy, indexed from 0
-  const int32_t* hst = s.hst;
-  const int32_t* hid = hst ? hst : a.prm.hist_ids;
-  const int64_t hb = hst ? R.h_lo : 0;  // the history index of hid[0]
   // ids [lo, hi) of an array, IDU loads per thread in flight before any is used (unconditional: an
   // index past the range reloads the first of the group); f(id, index)
   constexpr int IDU = 4;
@@ -509,12 +512,23 @@ __device__ __forceinline__ int build_overlay(const SArgs& a, const SRow& R, SSm&
       atomicOr(&s.c.p.bitmap[b >> 5], 1u << (b & 31));
     }
   };
-  const int64_t h_reg_end = hst ? R.h_lo : min(R.h_hi, R.h_lo + (int64_t)HPT * CT);  // ids held in hreg
+  // the output history: the first HPT * CT ids from the caller's registers and the rest from memory,
+  // or (resolution kernel, HPT = 0) all of it from its LDS copy, indexed from 0
+  const int64_t h_reg_end = min(R.h_hi, R.h_lo + (int64_t)HPT * CT);  // ids held in hreg
+  auto for_hist = [&](auto&& f) __attribute__((always_inline)) {
+    if constexpr (HPT == 0) {
+      if (s.hst_on) {
+        for_ids(r_hstage, 0, R.h_hi - R.h_lo, f);
+        return;
+      }
+    }
+    for_ids(a.prm.hist_ids, h_reg_end, R.h_hi, f);
+  };
   static_for<HPT>([&](auto Q) {
     constexpr int q = decltype(Q)::value;
     if (R.h_lo + t + (int64_t)q * CT < h_reg_end) mark(hreg[q]);
   });
-  for_ids(hid, h_reg_end - hb, R.h_hi - hb, [&](int32_t id, int64_t) { mark(id); });
+  for_hist([&](int32_t id, int64_t) { mark(id); });
   for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { mark(id); });
   const int32_t* st_row = a.st_ids + R.row * a.st_cap;
   for_ids(st_row, 0, R.st_n, [&](int32_t id, int64_t) { mark(id); });
@@ -561,7 +575,7 @@ __device__ __forceinline__ int build_overlay(const SArgs& a, const SRow& R, SSm&
     constexpr int q = decltype(Q)::value;
     if (R.h_lo + t + (int64_t)q * CT < h_reg_end) count(hreg[q], 1u, 0u);
   });
-  for_ids(hid, h_reg_end - hb, R.h_hi - hb, [&](int32_t id, int64_t) { count(id, 1u, 0u); });
+  for_hist([&](int32_t id, int64_t) { count(id, 1u, 0u); });
   for_ids(a.prompt_ids, R.p_lo, R.p_hi, [&](int32_t id, int64_t) { count(id, 0u, 0x80000000u); });
   const int32_t* st_cnt = reinterpret_cast<const int32_t*>(a.st_counts + R.row * a.st_cap);
   for_ids(st_cnt, 0, R.st_n, [&](int32_t cvi, int64_t e) {
@@ -874,7 +888,6 @@ __device__ __forceinline__ uint32_t gp_topp_key(const Src& src, SSm& s, uint64_t
 // masses (2^32 units) vanish from d = 32 ln 2 on, inside the last bucket.
 constexpr int GDB = GEN_WORDS;
 constexpr float GD_SCALE = 16.0f;
-constexpr int GSTAGE = 1024;            // 64-bit words of the resolution kernel's staging area (s.gst)
 constexpr int GKCAP = 2 * GSTAGE - 256;  // crossing-bucket keys staged (u32) before a 256-word histogram
 constexpr int GKCAP2 = GSTAGE;           // crossing-bucket (key, position) pairs staged
 
@@ -937,7 +950,7 @@ __device__ __forceinline__ bool gp_level1(const SArgs& a, const SRow& R, SSm& s,
 // area).  Returns their number, or -1 when they do not fit.
 template <class DT, bool SEG>
 __device__ __forceinline__ int gp_gather(const SArgs& a, const SRow& R, SSm& s, float lo, float m, int bb) {
-  uint32_t* keys = reinterpret_cast<uint32_t*>(s.gst);
+  uint32_t* keys = reinterpret_cast<uint32_t*>(r_gstage);
   if (threadIdx.x == 0) s.bc_i[2] = 0;
   __syncthreads();
   RowSrc<DT, SEG>{a, R, s}([&](float z) __attribute__((always_inline)) {
@@ -961,9 +974,9 @@ __device__ __forceinline__ uint32_t gp_kth(const SArgs& a, const SRow& R, SSm& s
   uint64_t before, total;
   if (!gp_level1<false, DT, SEG>(a, R, s, -INFINITY, m, (double)K, bb, before, total)) return 0u;
   const int n = gp_gather<DT, SEG>(a, R, s, -INFINITY, m, bb);
-  uint32_t* hist = reinterpret_cast<uint32_t*>(s.gst) + GKCAP;
+  uint32_t* hist = reinterpret_cast<uint32_t*>(r_gstage) + GKCAP;
   if (n >= 0)
-    return gp_kth_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.gst), n}, s, hist, K - (int)before);
+    return gp_kth_key(StagedSrc{reinterpret_cast<const uint32_t*>(r_gstage), n}, s, hist, K - (int)before);
   return gp_kth_key(RowSrc<DT, SEG>{a, R, s}, s, reinterpret_cast<uint32_t*>(s.c.gen), K);
 }
 
@@ -979,7 +992,7 @@ __device__ __forceinline__ uint32_t gp_topp(const SArgs& a, const SRow& R, SSm& 
   const double target = p * (double)total;
   const int n = gp_gather<DT, SEG>(a, R, s, tau2, m, bb);
   if (n >= 0)
-    return gp_topp_key(StagedSrc{reinterpret_cast<const uint32_t*>(s.gst), n}, s, s.c.gen, tau2, m, target,
+    return gp_topp_key(StagedSrc{reinterpret_cast<const uint32_t*>(r_gstage), n}, s, s.c.gen, tau2, m, target,
                        (double)before);
   return gp_topp_key(RowSrc<DT, SEG>{a, R, s}, s, s.c.gen, tau2, m, target, 0.0);
 }
@@ -1007,7 +1020,7 @@ __device__ __forceinline__ bool gp_topp_fused(const SArgs& a, const SRow& R, SSm
   uint64_t before, total;
   if (!gp_level1<true, DT, SEG>(a, R, s, tau2, m, p, bb, before, total)) return false;
   const double target = p * (double)total;
-  uint64_t* ent = s.gst;
+  uint64_t* ent = r_gstage;
   uint64_t* cm = s.cm;
   // refine: values of bucket bb with sub-bucket < sbb count as above the crossing, those of sub-bucket
   // sbb are staged (sbb = GDB: the whole bucket is staged)
@@ -1552,7 +1565,7 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
   if (t == 0) {
     s.n_list = 0;
     s.flags = 0;
-    s.hst = nullptr;
+    s.hst_on = 0;
   }
 
   // ---- penalty overlay of the chunk's range ----
@@ -1940,22 +1953,16 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
 // ----------------------------------------------------------------------------------------------
 // The resolution kernel: one workgroup per row, after the chunk kernel
 // ----------------------------------------------------------------------------------------------
-constexpr int HSTAGE = 4096;  // output-history ids the resolution kernel keeps in LDS
 
 template <class DT, bool SEG>
 __global__ __launch_bounds__(CT, 1) void k_resolve(SArgs a) {
   __shared__ SSm s;
-  __shared__ uint64_t gstage[GSTAGE];
-  __shared__ int32_t hstage[HSTAGE];
   const int t = threadIdx.x;
   SRow R;
   row_setup<DT, SEG>(a, (int64_t)blockIdx.x, 0, R);
   // the general path rebuilds a chunk's penalty overlay for every re-read: its output history comes
   // from LDS, loaded once (all of a thread's loads in flight together)
-  if (t == 0) {
-    s.gst = gstage;
-    s.hst = nullptr;
-  }
+  if (t == 0) s.hst_on = 0;
   const int64_t nh = R.h_hi - R.h_lo;
   if (R.pen_on && nh > 0 && nh <= HSTAGE) {
     constexpr int Q = HSTAGE / CT;
@@ -1966,9 +1973,9 @@ __global__ __launch_bounds__(CT, 1) void k_resolve(SArgs a) {
     });
     static_for<Q>([&](auto I) {
       constexpr int q = decltype(I)::value;
-      if (t + q * CT < nh) hstage[t + q * CT] = v[q];
+      if (t + q * CT < nh) r_hstage[t + q * CT] = v[q];
     });
-    if (t == 0) s.hst = hstage;
+    if (t == 0) s.hst_on = 1;
   }
   __syncthreads();
   resolve_row<DT, SEG>(a, R, s);
