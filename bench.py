@@ -271,6 +271,9 @@ def main():
                     help="skip the per-call times of the other four workloads after the main loop")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the timing of the step extras (device uniforms, backfill) after the main loop")
+    ap.add_argument("--rows", choices=("as-drawn", "top-p-only", "plain"), default="as-drawn",
+                    help="per-row filters: as the workload draws them, top-k and min-p off (the nucleus "
+                         "alone), or every filter off (a draw over the whole kept row)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="launch one elementwise copy of this many MiB before the timed region (for "
                          "scaling hardware byte counters)")
@@ -291,6 +294,12 @@ def main():
     if args.calib_copy_mib > 0:
         copy_calibration(args.calib_copy_mib)
     w = workloads.generate(args.config)
+    if args.rows != "as-drawn":
+        w.top_k = None
+        w.min_p = None
+        if args.rows == "plain":
+            w.top_p = None
+        w.name += " [rows: %s]" % args.rows
     logits0, u, p = to_device(w, device=dev)
     nbytes = logits0.numel() * logits0.element_size()
     ncopy = max(2, -(-(1 << 30) // nbytes))
@@ -371,7 +380,7 @@ def main():
         "hbm_frac_of_peak": alg / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": measured_traffic(args.config, route),
+                     "traffic": measured_traffic(args.config, route) if args.rows == "as-drawn" else None,
                      "kernel": kernel,
                      "algorithmic_bytes": alg,
                      "launch_us_avg": launch_us},
