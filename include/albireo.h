@@ -72,12 +72,13 @@ typedef enum {
 #define ALBIREO_FLAG_LIMIT 16u    /* a row's history has more distinct ids in one row chunk than
                                      this build handles on chip (ALBIREO_MAX_UNIQUE_HISTORY); the
                                      extra ids are ignored                                        */
-#define ALBIREO_FLAG_TIMEOUT 32u  /* a bounded wait between the workgroups of a wide row gave up (a
-                                     value another workgroup publishes never became visible within
-                                     the spin limit); the row's other outputs are unspecified.  Only
-                                     albireo_topk_topp on rows wider than one workgroup and the
-                                     cooperative sampling route (ALBIREO_ROUTE_COOPERATIVE) wait;
-                                     the other sampling routes never do.                          */
+#define ALBIREO_FLAG_TIMEOUT 32u  /* a bounded wait gave up (a value another workgroup or wave
+                                     publishes never became visible within the spin limit); the
+                                     row's other outputs are unspecified.  The waits: between the
+                                     workgroups of a wide row (albireo_topk_topp, and the cooperative
+                                     sampling route ALBIREO_ROUTE_COOPERATIVE), and, in the
+                                     one-workgroup kernel, between the waves of a penalised row for
+                                     its presence bitmap.  The streaming route never waits.       */
 
 #define ALBIREO_MAX_TOP_N 32
 #define ALBIREO_MAX_UNIQUE_HISTORY 2048
