@@ -1764,8 +1764,8 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
   const bool s2b = !R.greedy && (R.kon || R.minp_on);
   const bool want_list = s2b || Kn > 0;
   float bound = INFINITY;
+  float bk = -INFINITY, bn = -INFINITY;  // bounds of the chunk's K-th and n-th largest values
   if (want_list) {
-    float bk = -INFINITY, bn = -INFINITY;
     if (Kk > 0 || Kn > 0) {
       // Per wave, the R-th largest of its 64 thread maxima (R = ceil(K / 4)), by taking the wave's
       // maximum out R - 1 times (DPP reductions, no LDS); the smallest of the four waves' values
@@ -1804,15 +1804,18 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
   // ---- gather the candidates z >= bound ----
   uint64_t* glist = a.lists + L * (int64_t)LCAPC;
   int n_list = 0;
-  bool overflow = false;
-  if (want_list) {
+  bool overflow = false;  // the kept-set bound's candidates do not fit: the general path decides the kept set
+  // when they do not, a second round gathers the candidates above the top-n bound alone, so that the
+  // list still carries the chunk's top n
+  float gb = bound;
+  for (int round = 0; want_list && round < 2; ++round) {
     uint32_t pm = 0;
     static_for<CJ>([&](auto J) {
       constexpr int j = decltype(J)::value;
       float v = elem<DT>(d[j], 0);
 #pragma unroll
       for (int e = 1; e < VEC; ++e) v = fmaxf(v, elem<DT>(d[j], e));
-      if (v > -INFINITY && canon(v, r) >= bound) pm |= 1u << j;
+      if (v > -INFINITY && canon(v, r) >= gb) pm |= 1u << j;
     });
     reload_barrier(d);
     // the flagged slots of this thread, one LDS add per slot for the space of its candidates
@@ -1831,7 +1834,7 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
         const float z = canon(elem<DT>(dd, e), r);
-        if (z > -INFINITY && z >= bound) cb |= 1u << e;
+        if (z > -INFINITY && z >= gb) cb |= 1u << e;
       }
       int idx = atomicAdd(&s.n_list, __popc(cb));
 #pragma unroll
@@ -1844,27 +1847,35 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
     }
     for (int i = t; i < n_x; i += CT) {
       const float z = canon(__uint_as_float(s.c.p.xval[i]), r);
-      if (z > -INFINITY && z >= bound) {
+      if (z > -INFINITY && z >= gb) {
         const int idx = atomicAdd(&s.n_list, 1);
         if (idx < LCAPC) s.c.list[idx] = cand_key(z, pos_of_rank(s, nwords, e_base, i));
       }
     }
     if (own_hx) {
       const float z = canon(s.hx_val[t], r);
-      if (z > -INFINITY && z >= bound) {
+      if (z > -INFINITY && z >= gb) {
         const int idx = atomicAdd(&s.n_list, 1);
         if (idx < LCAPC) s.c.list[idx] = cand_key(z, s.hx_pos[t]);
       }
     }
     __syncthreads();
     n_list = s.n_list;
+    if (round == 1) break;
     overflow = n_list > LCAPC;
+    if (!(overflow && Kn > 0 && bn > bound)) break;
+    __syncthreads();  // every thread has read the count
+    if (t == 0) s.n_list = 0;
+    __syncthreads();
+    gb = bn;
+    reload_barrier(d);
   }
+  const bool list_fits = want_list && n_list <= LCAPC;
 
   reload_barrier(d);
   // ---- publish the list, sorted in descending key order (rank by counting) ----
   float qk = -INFINITY, qn = -INFINITY;
-  if (want_list && !overflow) {
+  if (list_fits) {
     const int P = R.P;
     const int qki = Kk > 0 ? (Kk + P - 1) / P - 1 : -1;
     const int qni = Kn > 0 ? (Kn + P - 1) / P - 1 : -1;
@@ -1884,8 +1895,7 @@ __global__ __launch_bounds__(CT, 4) void k_stream(SArgs a) {
     qk = s.bc_f[0];
     qn = s.bc_f[1];
   } else if (want_list) {
-    // too many candidates (ties): the row's kept set comes from the general path; the top n exactly,
-    // slowly
+    // too many candidates even above the top-n bound (ties): the top n exactly, slowly
     n_list = 0;
     if (Kn > 0) {
       uint64_t prev = ~0ull;
