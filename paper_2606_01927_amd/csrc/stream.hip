@@ -154,7 +154,9 @@ struct SSm {
   float wred[3][CW];
   uint64_t qred[CW];
   int32_t n_list;
-  int32_t hst_on;      // resolution kernel: the row's output history is in r_hstage
+  int32_t hst_on;      // resolution kernel: the row's output history is in r_hstage, grouped by chunk
+  int32_t hoff[MAXPC + 1];  // resolution kernel: chunk c's history ids are r_hstage[hoff[c], hoff[c + 1])
+  int32_t hcur[MAXPC];      // resolution kernel: scatter cursors of that grouping
   uint32_t flags;
   int32_t ov_red[CW];  // the overlay build's block scan (callers keep counters in bc_i across it)
   int32_t bc_i[4];
@@ -517,8 +519,8 @@ __device__ __forceinline__ int build_overlay(const SArgs& a, const SRow& R, SSm&
   const int64_t h_reg_end = min(R.h_hi, R.h_lo + (int64_t)HPT * CT);  // ids held in hreg
   auto for_hist = [&](auto&& f) __attribute__((always_inline)) {
     if constexpr (HPT == 0) {
-      if (s.hst_on) {
-        for_ids(r_hstage, 0, R.h_hi - R.h_lo, f);
+      if (s.hst_on) {  // only this chunk's ids (the others could not mark or count anything here)
+        for_ids(r_hstage, s.hoff[c], s.hoff[c + 1], f);
         return;
       }
     }
@@ -1252,10 +1254,53 @@ __device__ __forceinline__ int gp_draw(const SArgs& a, const SRow& R, SSm& s, fl
   return id;
 }
 
+// The general path rebuilds a chunk's penalty overlay for every re-read: the row's output history,
+// copied to LDS when the kernel starts, is grouped by the chunk its ids fall in, so that a rebuild
+// reads only its chunk's ids.  Every thread of the workgroup calls it.
+template <class DT>
+__device__ __forceinline__ void stage_history(const SArgs& a, const SRow& R, SSm& s) {
+  const int t = threadIdx.x;
+  const int64_t nh = R.h_hi - R.h_lo;
+  if (s.hst_on) {
+    // the ids grouped by the chunk they fall in (a counting sort; the order inside a group does not
+    // matter, its ids are counted by atomics); ids outside [0, V) are left out (the chunk kernel has
+    // flagged them already)
+    constexpr int Q = HSTAGE / CT;
+    int32_t v[Q];
+    static_for<Q>([&](auto I) {
+      constexpr int q = decltype(I)::value;
+      v[q] = r_hstage[min(t + q * CT, (int)nh - 1)];
+    });
+    if (t <= R.P) s.hoff[t] = 0;
+    __syncthreads();
+    int cq[Q];
+    static_for<Q>([&](auto I) {
+      constexpr int q = decltype(I)::value;
+      const int id = v[q];
+      cq[q] = (t + q * CT < nh && id >= 0 && id < R.V) ? chunk_of(a, R, DT::VEC, id) : -1;
+      if (cq[q] >= 0) atomicAdd(&s.hoff[cq[q] + 1], 1);
+    });
+    __syncthreads();
+    if (t == 0) {
+      for (int c = 0; c < R.P; ++c) {
+        s.hcur[c] = s.hoff[c];
+        s.hoff[c + 1] += s.hoff[c];
+      }
+    }
+    __syncthreads();
+    static_for<Q>([&](auto I) {
+      constexpr int q = decltype(I)::value;
+      if (cq[q] >= 0) r_hstage[atomicAdd(&s.hcur[cq[q]], 1)] = v[q];
+    });
+  }
+  __syncthreads();
+}
+
 // The general path of a row with no small kept-set bound: the top-k threshold, the nucleus and the draw
 // over re-reads of the row.  Returns (id, bits of its z).
 template <class DT, bool SEG>
 __device__ __forceinline__ int2 resolve_general(const SArgs& a, const SRow& R, SSm& s, float m, float tau_m, float u) {
+  stage_history<DT>(a, R, s);
   float tau_k = -INFINITY;
   if (R.kon) {
     const uint32_t kk = gp_kth<DT, SEG>(a, R, s, m, R.k);
@@ -1970,8 +2015,8 @@ __global__ __launch_bounds__(CT, 1) void k_resolve(SArgs a) {
   const int t = threadIdx.x;
   SRow R;
   row_setup<DT, SEG>(a, (int64_t)blockIdx.x, 0, R);
-  // the general path rebuilds a chunk's penalty overlay for every re-read: its output history comes
-  // from LDS, loaded once (all of a thread's loads in flight together)
+  // the output history to LDS (all of a thread's loads in flight together) for the general path, which
+  // groups it by chunk if the row needs it
   if (t == 0) s.hst_on = 0;
   const int64_t nh = R.h_hi - R.h_lo;
   if (R.pen_on && nh > 0 && nh <= HSTAGE) {
