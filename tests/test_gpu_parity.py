@@ -218,6 +218,34 @@ def test_topk_ties_on_streamed_rows(n_top, lib, oracle_mod):
     compare_sample(ref, out, n_top=n_top)
 
 
+def test_overflowing_kept_set_lists_keep_top_n(lib, oracle_mod):
+    """Streamed rows whose min-p or top-k bound lets far more candidates into a chunk than its list
+    holds: the kept set goes to the general path, while the chunk lists fall back to the top-n bound
+    and still give the top-n logprobs (ties at the n-th value included)."""
+    import torch
+
+    rng = np.random.default_rng(31)
+    V = 200003  # fp32: 11 chunks per row
+    base = rng.normal(0, 0.5, size=V).astype(np.float32)  # flat: thousands within ln(1/min_p) of the max
+    rows, K, MP, Pp = [], [], [], []
+
+    def add(x, k=0, mp=0.0, p=1.0):
+        rows.append(x); K.append(k); MP.append(mp); Pp.append(p)
+
+    add(base.copy(), mp=0.001)                     # min-p keeps most of every chunk
+    add(base.copy(), mp=0.01, p=0.9)               # min-p and a nucleus
+    add(base.copy(), k=5000)                       # top-k beyond the list capacity
+    t = base.copy(); t[[3, 40000, 90000, 150000, 199999]] = 4.0; t[[7, 8]] = 3.5
+    add(t, mp=0.001)                               # distinct top values, then a tie inside one chunk
+    w = _rowset(rows, temperature=np.full(len(rows), 1.0, np.float32), top_k=np.array(K, np.int32),
+                min_p=np.array(MP, np.float32), top_p=np.array(Pp, np.float32))
+    w.n_top = 6
+    assert lib.sample_route(w.B, V, torch.float32) == lib.ROUTE_STREAM
+    out = _run(lib, w)
+    ref = oracle_mod.sample(w)
+    compare_sample(ref, out, n_top=6)
+
+
 @pytest.mark.parametrize("dtype,extras", [("f32", False), ("bf16", False), ("bf16", True)],
                          ids=["f32", "bf16", "bf16_topn_penalties"])
 def test_general_path_wide_rows(dtype, extras, lib, oracle_mod):
