@@ -208,14 +208,14 @@ albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64
  * albireo_sample; the workspace is a fixed array in the library's device memory instead of a caller
  * buffer, so the call allocates nothing (no hipMalloc, no allocating library routine).
  *   Arguments and outputs as albireo_sample, without workspace / workspace_bytes.
- *   Limit: a shape whose albireo_sample workspace exceeds ALBIREO_NOALLOC_SCRATCH_BYTES (32 MiB, i.e.
- *   B * P > 8065 row chunks, P = ceil(floor(V / 8) / 4864) for bf16 and ceil(floor(V / 4) / 4864) for
- *   fp32) returns ALBIREO_E_SCRATCH before anything is enqueued.
+ *   Limit: a shape whose albireo_sample workspace exceeds ALBIREO_NOALLOC_SCRATCH_BYTES (96 MiB: about
+ *   10.1 KB per row chunk, so B * P up to about 9700 row chunks, P = ceil(floor(V / 8) / 4864) for bf16
+ *   and ceil(floor(V / 4) / 4864) for fp32) returns ALBIREO_E_SCRATCH before anything is enqueued.
  *   Every GPU the library runs on holds one such array until the process ends, shared by all calls on
  *   that GPU: two calls that overlap in time on one GPU (different streams, or threads) race on it and
  *   must be serialised by the caller.  Nothing in it needs to be zero between calls.
  */
-#define ALBIREO_NOALLOC_SCRATCH_BYTES (32u << 20)
+#define ALBIREO_NOALLOC_SCRATCH_BYTES (96u << 20)
 albireo_status_t albireo_sample_noalloc(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V,
                                         int64_t ld, const albireo_params_t* params, const float* uniforms,
                                         int32_t* out_ids, float* out_logprobs, int32_t n_top,

@@ -64,6 +64,14 @@ constexpr double LN2 = 0.6931471805599453;
 constexpr uint32_t PUB_FINITE = 1u << 29;  // the chunk holds a finite processed value
 constexpr uint32_t PUB_OVER = 1u << 28;    // the chunk's candidate list did not fit
 constexpr int REC_WORDS = 8;               // 64-bit words per chunk record (5 used)
+// A row whose kept set has no small bound and no top-k is resolved chunk-parallel by three launches
+// after the resolution kernel; its state between them (RS_WORDS words per row):
+constexpr int RS_WORDS = 8;
+constexpr uint64_t RS_DEFER = 1;  // word 0: the row is deferred
+constexpr uint64_t RS_TOPP = 2;   // word 0: its kept set is a nucleus (else all values >= lo)
+constexpr int SCAP = 256;         // crossing-bucket values staged per chunk
+constexpr int SSTRIDE = SCAP + GEN_WORDS;  // per chunk: the staged values, then the crossing bucket's
+                                           // mass per sub-bucket
 
 // What one chunk publishes for the row's resolution (decoded form).
 struct ChunkPub {
@@ -111,6 +119,8 @@ struct SArgs {
   int64_t grid;
   uint64_t* rec;     // [B * P * REC_WORDS] chunk records
   uint64_t* lists;   // [B * P * LCAPC] candidate keys
+  uint64_t* rstate;  // [B * RS_WORDS] deferred rows' state
+  uint64_t* stg;     // [B * P * SSTRIDE] deferred rows' staged crossing-bucket values and sub-buckets
 };
 
 struct SRow {
@@ -1408,6 +1418,8 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
 
   int id = -1;
   float zid = -INFINITY;
+  bool defer = false;
+  uint64_t defer_w[4] = {0, 0, 0, 0};
   if (empty) {
     id = -1;
   } else if (R.greedy) {
@@ -1524,6 +1536,17 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
         if ((int)(uint32_t)(Bk[i] >> 32) == id) s.bc_f[2] = key2f((uint32_t)(A[i] >> 32));
       __syncthreads();
       zid = s.bc_f[2];
+    } else if (!R.kon) {
+      // no top-k threshold to select: the chunk-parallel launches take the row from here
+      defer = true;
+      if (t == 0) {
+        const bool topp = R.topp_on && R.p > 0.0f;
+        const float lo = (R.topp_on && !(R.p > 0.0f)) ? m : tau_m;  // p <= 0: the top group only
+        defer_w[0] = RS_DEFER | (topp ? RS_TOPP : 0);
+        defer_w[1] = (uint64_t)__float_as_uint(m) | ((uint64_t)__float_as_uint(lo) << 32);
+        defer_w[2] = (uint64_t)__float_as_uint(u) | ((uint64_t)__float_as_uint(R.p) << 32);
+        defer_w[3] = (uint64_t)__double_as_longlong(L);
+      }
     } else {
       const int2 r2 = resolve_general<DT, SEG>(a, R, s, m, tau_m, u);
       id = r2.x;
@@ -1541,11 +1564,394 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
     for (int i = t; i < P * REC_WORDS; i += CT) rw[i] = 0;
   }
   if (t == 0) {
-    float lp = -INFINITY;
-    if (!empty) lp = (float)((double)zid - (double)m - L);
-    a.out_ids[row] = id;
-    a.out_logprobs[row] = lp;
     if (a.out_flags) a.out_flags[row] = flags;
+    if (defer) {
+      uint64_t* rs = a.rstate + row * RS_WORDS;
+      for (int i = 0; i < 4; ++i) rs[i] = defer_w[i];
+    } else {
+      float lp = -INFINITY;
+      if (!empty) lp = (float)((double)zid - (double)m - L);
+      a.out_ids[row] = id;
+      a.out_logprobs[row] = lp;
+      if (a.next_tokens) {
+        const int32_t dst = a.backfill_dest[row];
+        if (dst >= 0 && (int64_t)dst < a.next_len) a.next_tokens[dst] = id;
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------------------------
+// Deferred rows: the general path of a row with no top-k, spread over its chunks.  The resolution
+// kernel leaves such a row's maximum m, the lower cut lo (min-p, or m for p <= 0), its uniform, p and
+// log-normaliser in the row's state.  Then
+//   k_gen_a (one workgroup per chunk): the chunk's kept mass (values >= lo, fixed-point masses against
+//     m) and, for a nucleus, its mass per distance bucket, into the chunk's list slot;
+//   k_gen_b (one workgroup per chunk, nucleus rows): every chunk of the row merges the histograms to the
+//     bucket where the cumulative reaches p times the total; the chunk sums its mass above that bucket
+//     and stages the bucket's values;
+//   k_gen_c (one workgroup per row): the cut inside the staged bucket, the per-chunk kept masses and
+//     the draw over the crossing chunk; it writes the row's id and logprob and zeroes what the row used.
+// Every sum is an integer sum of the same masses the single-workgroup general path takes, so the result
+// is the same; a row whose crossing bucket does not fit the staging takes that path in k_gen_c.
+// ----------------------------------------------------------------------------------------------
+struct Deferred {
+  bool on, topp;
+  float m, lo, u, p;
+  double L;
+};
+__device__ __forceinline__ Deferred deferred_of(const SArgs& a, int64_t row) {
+  const uint64_t* rs = a.rstate + row * RS_WORDS;
+  Deferred d;
+  const uint64_t w0 = rs[0];
+  d.on = (w0 & RS_DEFER) != 0;
+  d.topp = (w0 & RS_TOPP) != 0;
+  d.m = d.lo = d.u = d.p = 0.0f;
+  d.L = 0.0;
+  if (d.on) {
+    const uint64_t w1 = rs[1], w2 = rs[2];
+    d.m = __uint_as_float((uint32_t)w1);
+    d.lo = __uint_as_float((uint32_t)(w1 >> 32));
+    d.u = __uint_as_float((uint32_t)w2);
+    d.p = __uint_as_float((uint32_t)(w2 >> 32));
+    d.L = __longlong_as_double((long long)rs[3]);
+  }
+  return d;
+}
+
+// The row's distance-bucket masses summed over its chunks' histograms (in their list slots), and the
+// bucket where the cumulative, from the top, reaches p times the total (as the single-workgroup first
+// level finds it).  Returns false when it is never reached.
+__device__ __forceinline__ bool merge_hists(const SArgs& a, const SRow& R, SSm& s, double p, int& bb,
+                                            uint64_t& before, uint64_t& total) {
+  constexpr int BPT = GDB / CT;
+  const uint64_t* base = a.lists + (R.row * R.P) * (int64_t)LCAPC;
+  const int b0 = (int)threadIdx.x * BPT;
+  uint64_t hv[BPT];
+  uint64_t sum = 0;
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    uint64_t v = 0;
+    for (int c = 0; c < R.P; ++c) v += base[(int64_t)c * LCAPC + b0 + q];
+    hv[q] = v;
+    sum += v;
+  }
+  uint64_t tot;
+  const uint64_t excl = blk_excl_scan_u64(sum, s, &tot);
+  total = tot;
+  const double target = p * (double)tot;
+  int mine = 0x7fffffff;
+  if ((double)excl < target && (double)(excl + sum) >= target) {  // at most one thread
+    uint64_t cum = excl;
+    int q = 0;
+    while (q < BPT - 1 && (double)(cum + hv[q]) < target) cum += hv[q++];
+    mine = b0 + q;
+    s.bc_q[1] = cum;
+  }
+  bb = blk_min_i(mine, s);
+  before = s.bc_q[1];
+  __syncthreads();
+  return bb != 0x7fffffff;
+}
+
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT) void k_gen_a(SArgs a) {
+  __shared__ SSm s;
+  const int t = threadIdx.x;
+  int64_t L = blockIdx.x;
+  if (a.xcd_map) L = (L & 7) * (a.grid >> 3) + (L >> 3);
+  const int64_t row = L / a.P;
+  const int c = (int)(L - row * a.P);
+  const Deferred d = deferred_of(a, row);
+  if (!d.on) return;
+  SRow R;
+  row_setup<DT, SEG>(a, row, c, R);
+  if (t == 0) s.hst_on = 0;
+  uint64_t* h64 = s.c.gen;
+  for (int b = t; b < GDB; b += CT) h64[b] = 0;
+  __syncthreads();
+  uint64_t acc = 0;
+  int last = -1;
+  const float m = d.m, lo = d.lo;
+  const bool topp = d.topp;
+  for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
+    if (z > -INFINITY && z >= lo) {
+      const uint64_t w = mass_of(z, m);
+      if (w) {
+        acc += w;
+        last = max(last, pos);
+        if (topp) atomicAdd(reinterpret_cast<unsigned long long*>(&h64[gp_dbucket(z, m)]), (unsigned long long)w);
+      }
+    }
+  });
+  acc = blk_sum_u64(acc, s);
+  last = blk_max_i(last, s);
+  if (topp) {
+    uint64_t* lst = a.lists + L * (int64_t)LCAPC;
+    for (int b = t; b < GDB; b += CT) lst[b] = h64[b];
+  }
+  if (t == 0) {
+    a.rec[L * REC_WORDS + 0] = acc;
+    a.rec[L * REC_WORDS + 1] = (uint64_t)(uint32_t)last;
+  }
+}
+
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT) void k_gen_b(SArgs a) {
+  __shared__ SSm s;
+  const int t = threadIdx.x;
+  int64_t L = blockIdx.x;
+  if (a.xcd_map) L = (L & 7) * (a.grid >> 3) + (L >> 3);
+  const int64_t row = L / a.P;
+  const int c = (int)(L - row * a.P);
+  const Deferred d = deferred_of(a, row);
+  if (!d.on || !d.topp) return;
+  SRow R;
+  row_setup<DT, SEG>(a, row, c, R);
+  if (t == 0) {
+    s.hst_on = 0;
+    s.n_list = 0;
+  }
+  int bb;
+  uint64_t before, total;
+  if (!merge_hists(a, R, s, (double)d.p, bb, before, total)) return;  // the same in every chunk
+  uint64_t acc = 0;
+  int last = -1;
+  const float m = d.m, lo = d.lo;
+  uint64_t* stg = a.stg + L * (int64_t)SSTRIDE;
+  uint64_t* sub = s.c.list;  // the crossing bucket's mass per sub-bucket
+  for (int i = t; i < GDB; i += CT) sub[i] = 0;
+  __syncthreads();
+  for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
+    if (z > -INFINITY && z >= lo) {
+      const int b = gp_dbucket(z, m);
+      if (b < bb) {
+        const uint64_t w = mass_of(z, m);
+        if (w) {
+          acc += w;
+          last = max(last, pos);
+        }
+      } else if (b == bb) {
+        const int i = atomicAdd(&s.n_list, 1);
+        if (i < SCAP) stg[i] = ((uint64_t)f2key(z) << 32) | (uint32_t)pos;
+        const uint64_t w = mass_of(z, m);
+        if (w) atomicAdd(reinterpret_cast<unsigned long long*>(&sub[gp_dsub(z, m, bb)]), (unsigned long long)w);
+      }
+    }
+  });
+  acc = blk_sum_u64(acc, s);
+  last = blk_max_i(last, s);  // its barriers also publish n_list and sub
+  for (int i = t; i < GDB; i += CT) stg[SCAP + i] = sub[i];
+  if (t == 0) {
+    a.rec[L * REC_WORDS + 2] = (uint64_t)(uint32_t)s.n_list + 1;  // + 1: written
+    a.rec[L * REC_WORDS + 3] = acc;
+    a.rec[L * REC_WORDS + 4] = (uint64_t)(uint32_t)last;
+  }
+}
+
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
+  __shared__ SSm s;
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const Deferred d = deferred_of(a, row);
+  if (!d.on) return;
+  SRow R;
+  row_setup<DT, SEG>(a, row, 0, R);
+  const int P = R.P;
+  // the output history to LDS, grouped by chunk, for the overlay rebuilds of this row's passes
+  if (t == 0) s.hst_on = 0;
+  const int64_t nh = R.h_hi - R.h_lo;
+  if (R.pen_on && nh > 0 && nh <= HSTAGE) {
+    for (int64_t i = t; i < nh; i += CT) r_hstage[i] = a.prm.hist_ids[R.h_lo + i];
+    if (t == 0) s.hst_on = 1;
+  }
+  __syncthreads();
+  stage_history<DT>(a, R, s);
+  const uint64_t* rec = a.rec + (row * P) * (int64_t)REC_WORDS;
+  const float m = d.m, lo = d.lo;
+  float tau = lo;
+  int last = -1;
+  bool fast = true;
+  if (!d.topp) {
+    if (t < P) {
+      s.cm[t] = rec[t * REC_WORDS + 0];
+      s.cnt[t] = (int32_t)(uint32_t)rec[t * REC_WORDS + 1];
+    }
+    __syncthreads();
+    for (int c = 0; c < P; ++c) last = max(last, s.cnt[c]);
+  } else {
+    int bb;
+    uint64_t before, total;
+    fast = merge_hists(a, R, s, (double)d.p, bb, before, total);
+    bool overfull = false;  // the crossing bucket's values did not fit the staging
+    int n = 0;
+    if (fast) {
+      if (t == 0) {
+        int off = 0;
+        bool ok = true;
+        for (int c = 0; c < P; ++c) {
+          const uint64_t w2 = rec[c * REC_WORDS + 2];
+          const int nc = w2 ? (int)(w2 - 1) : -1;
+          if (nc < 0 || nc > SCAP) ok = false;
+          s.cut[c] = off;  // where chunk c's entries start
+          s.cnt[c] = nc < 0 ? 0 : min(nc, SCAP);
+          off += s.cnt[c];
+        }
+        s.bc_i[0] = ok && off <= GKCAP2 ? off : -1;
+      }
+      __syncthreads();
+      n = s.bc_i[0];
+      __syncthreads();
+      fast = n >= 0;
+      overfull = !fast;
+    }
+    if (fast) {
+      uint64_t* ent = r_gstage;
+      for (int c = 0; c < P; ++c) {
+        const uint64_t* src = a.stg + (row * P + c) * (int64_t)SSTRIDE;
+        for (int i = t; i < s.cnt[c]; i += CT) ent[s.cut[c] + i] = src[i];
+      }
+      __syncthreads();
+      const uint32_t kk = gp_topp_key(StagedPairs{ent, n}, s, s.c.gen, lo, m, (double)d.p * (double)total,
+                                      (double)before);
+      fast = kk != 0;
+      if (fast) {
+        tau = fmaxf(lo, key2f(kk));
+        if (t < P) s.cm[t] = rec[t * REC_WORDS + 3];
+        int lastp = -1;
+        for (int c = 0; c < P; ++c) lastp = max(lastp, (int)(uint32_t)rec[c * REC_WORDS + 4]);
+        __syncthreads();
+        for (int i = t; i < n; i += CT) {
+          const uint64_t e = ent[i];
+          const float z = key2f((uint32_t)(e >> 32));
+          if (z >= tau) {
+            const int pos = (int)(uint32_t)e;
+            const uint64_t w = mass_of(z, m);
+            atomicAdd(reinterpret_cast<unsigned long long*>(&s.cm[chunk_of(a, R, DT::VEC, pos)]), (unsigned long long)w);
+            if (w > 0) lastp = max(lastp, pos);
+          }
+        }
+        last = blk_max_i(lastp, s);  // its barriers also publish cm
+      }
+    }
+    if (overfull) {
+      // the crossing bucket did not fit the staging: its sub-buckets (GDB steps of the bucket, each
+      // chunk's masses merged) give the sub-bucket where the cumulative crosses; one pass over the row
+      // stages that sub-bucket's values (a comparison per value, masses only inside bucket bb)
+      bool all = true;
+      for (int c = 0; c < P; ++c) all = all && rec[c * REC_WORDS + 2] != 0;
+      if (all) {
+        constexpr int BPT = GDB / CT;
+        const int i0 = t * BPT;
+        uint64_t hv[BPT];
+        uint64_t sum = 0;
+#pragma unroll
+        for (int q = 0; q < BPT; ++q) {
+          uint64_t v = 0;
+          for (int c = 0; c < P; ++c) v += a.stg[(row * P + c) * (int64_t)SSTRIDE + SCAP + i0 + q];
+          hv[q] = v;
+          sum += v;
+        }
+        uint64_t tot;
+        const uint64_t excl = blk_excl_scan_u64(sum, s, &tot);
+        const double target = (double)d.p * (double)total;
+        int mine = 0x7fffffff;
+        if ((double)before + (double)excl < target && (double)before + (double)(excl + sum) >= target) {
+          uint64_t cum = excl;
+          int q = 0;
+          while (q < BPT - 1 && (double)before + (double)(cum + hv[q]) < target) cum += hv[q++];
+          mine = i0 + q;
+          s.bc_q[1] = cum;
+        }
+        const int sbb = blk_min_i(mine, s);
+        const uint64_t before2 = before + s.bc_q[1];
+        __syncthreads();
+        if (sbb != 0x7fffffff) {
+          // per chunk: the mass of bucket bb's sub-buckets below sbb (kept whatever the cut)
+          if (t < P) {
+            uint64_t v = rec[t * REC_WORDS + 3];
+            const uint64_t* sh = a.stg + (row * P + t) * (int64_t)SSTRIDE + SCAP;
+            for (int i = 0; i < sbb; ++i) v += sh[i];
+            s.cm[t] = v;
+          }
+          int lastp = -1;
+          for (int c = 0; c < P; ++c) lastp = max(lastp, (int)(uint32_t)rec[c * REC_WORDS + 4]);
+          if (t == 0) s.n_list = 0;
+          __syncthreads();
+          uint64_t* ent = r_gstage;
+          for (int c = 0; c < P; ++c) {
+            for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
+              if (z > -INFINITY && z >= lo && gp_dbucket(z, m) == bb) {
+                const int sb = gp_dsub(z, m, bb);
+                if (sb < sbb) {
+                  if (mass_of(z, m) > 0) lastp = max(lastp, pos);
+                } else if (sb == sbb) {
+                  const int i = atomicAdd(&s.n_list, 1);
+                  if (i < GKCAP2) ent[i] = ((uint64_t)f2key(z) << 32) | (uint32_t)pos;
+                }
+              }
+            });
+          }
+          __syncthreads();
+          const int n2 = s.n_list;
+          __syncthreads();
+          if (n2 <= GKCAP2) {
+            const uint32_t kk = gp_topp_key(StagedPairs{ent, n2}, s, s.c.gen, lo, m, target, (double)before2);
+            if (kk) {
+              tau = fmaxf(lo, key2f(kk));
+              for (int i = t; i < n2; i += CT) {
+                const uint64_t e = ent[i];
+                const float z = key2f((uint32_t)(e >> 32));
+                if (z >= tau) {
+                  const int pos = (int)(uint32_t)e;
+                  const uint64_t w = mass_of(z, m);
+                  atomicAdd(reinterpret_cast<unsigned long long*>(&s.cm[chunk_of(a, R, DT::VEC, pos)]),
+                            (unsigned long long)w);
+                  if (w > 0) lastp = max(lastp, pos);
+                }
+              }
+              last = blk_max_i(lastp, s);  // its barriers also publish cm
+              fast = true;
+            }
+          }
+        }
+      }
+    }
+  }
+  float zid = -INFINITY;
+  int id;
+  if (fast) {
+    id = gp_draw<DT, SEG>(a, R, s, tau, m, d.u, &zid, true, last);
+  } else {
+    // the crossing bucket did not fit the staging: the single-workgroup nucleus selection
+    bool fused = gp_topp_fused<DT, SEG>(a, R, s, lo, m, (double)d.p, tau, last);
+    if (!fused) {
+      const uint32_t kk = gp_topp<DT, SEG>(a, R, s, lo, m, (double)d.p);
+      tau = kk ? fmaxf(lo, key2f(kk)) : lo;
+    }
+    id = gp_draw<DT, SEG>(a, R, s, tau, m, d.u, &zid, fused, last);
+  }
+  // leave the workspace as it was found
+  __syncthreads();
+  if (d.topp) {
+    uint64_t* lbase = a.lists + (row * P) * (int64_t)LCAPC;
+    for (int i = t; i < P * LCAPC; i += CT) lbase[i] = 0;
+    for (int c = 0; c < P; ++c) {
+      const uint64_t w2 = rec[c * REC_WORDS + 2];
+      const int nc = w2 ? min((int)(w2 - 1), SCAP) : 0;
+      uint64_t* sb = a.stg + (row * P + c) * (int64_t)SSTRIDE;
+      for (int i = t; i < nc; i += CT) sb[i] = 0;
+      if (w2) for (int i = t; i < GDB; i += CT) sb[SCAP + i] = 0;
+    }
+  }
+  __syncthreads();
+  uint64_t* rw = a.rec + (row * P) * (int64_t)REC_WORDS;
+  for (int i = t; i < P * REC_WORDS; i += CT) rw[i] = 0;
+  if (t < RS_WORDS) a.rstate[row * RS_WORDS + t] = 0;
+  if (t == 0) {
+    a.out_ids[row] = id;
+    a.out_logprobs[row] = id >= 0 ? (float)((double)zid - (double)m - d.L) : -INFINITY;
     if (a.next_tokens) {
       const int32_t dst = a.backfill_dest[row];
       if (dst >= 0 && (int64_t)dst < a.next_len) a.next_tokens[dst] = id;
@@ -2059,13 +2465,15 @@ SGeo geometry(int64_t B, int64_t V, albireo_dtype_t dtype) {
 }
 
 struct WsParts {
-  int64_t rec, lists, total;
+  int64_t rec, lists, rstate, stg, total;
 };
 WsParts ws_parts(int64_t B, int P) {
   WsParts w;
   w.rec = 0;
   w.lists = align256(w.rec + B * P * (int64_t)REC_WORDS * 8);
-  w.total = align256(w.lists + B * P * (int64_t)LCAPC * 8);
+  w.rstate = align256(w.lists + B * P * (int64_t)LCAPC * 8);
+  w.stg = align256(w.rstate + B * (int64_t)RS_WORDS * 8);
+  w.total = align256(w.stg + B * P * (int64_t)SSTRIDE * 8);
   return w;
 }
 
@@ -2145,17 +2553,36 @@ albireo_status_t launch(const Request& q) {
   const WsParts w = ws_parts(q.B, g.P);
   a.rec = reinterpret_cast<uint64_t*>(q.ws + w.rec);
   a.lists = reinterpret_cast<uint64_t*>(q.ws + w.lists);
+  a.rstate = reinterpret_cast<uint64_t*>(q.ws + w.rstate);
+  a.stg = reinterpret_cast<uint64_t*>(q.ws + w.stg);
   void* args[] = {&a};
-  const void *fc, *fr;
-  if (q.dtype == ALBIREO_BF16) {
-    fc = q.shards ? reinterpret_cast<const void*>(&k_stream<BF16T, true>) : reinterpret_cast<const void*>(&k_stream<BF16T, false>);
-    fr = q.shards ? reinterpret_cast<const void*>(&k_resolve<BF16T, true>) : reinterpret_cast<const void*>(&k_resolve<BF16T, false>);
-  } else {
-    fc = q.shards ? reinterpret_cast<const void*>(&k_stream<F32T, true>) : reinterpret_cast<const void*>(&k_stream<F32T, false>);
-    fr = q.shards ? reinterpret_cast<const void*>(&k_resolve<F32T, true>) : reinterpret_cast<const void*>(&k_resolve<F32T, false>);
+  const void *fc, *fr, *ga, *gb, *gc;
+#define ALBIREO_STREAM_KERNELS(DT)                                                                  \
+  if (q.shards) {                                                                                   \
+    fc = reinterpret_cast<const void*>(&k_stream<DT, true>);                                        \
+    fr = reinterpret_cast<const void*>(&k_resolve<DT, true>);                                       \
+    ga = reinterpret_cast<const void*>(&k_gen_a<DT, true>);                                         \
+    gb = reinterpret_cast<const void*>(&k_gen_b<DT, true>);                                         \
+    gc = reinterpret_cast<const void*>(&k_gen_c<DT, true>);                                         \
+  } else {                                                                                          \
+    fc = reinterpret_cast<const void*>(&k_stream<DT, false>);                                       \
+    fr = reinterpret_cast<const void*>(&k_resolve<DT, false>);                                      \
+    ga = reinterpret_cast<const void*>(&k_gen_a<DT, false>);                                        \
+    gb = reinterpret_cast<const void*>(&k_gen_b<DT, false>);                                        \
+    gc = reinterpret_cast<const void*>(&k_gen_c<DT, false>);                                        \
   }
+  if (q.dtype == ALBIREO_BF16) {
+    ALBIREO_STREAM_KERNELS(BF16T)
+  } else {
+    ALBIREO_STREAM_KERNELS(F32T)
+  }
+#undef ALBIREO_STREAM_KERNELS
+  // chunk pass, row resolution, then the deferred rows' chunk-parallel general path
   hipError_t e = hipLaunchKernel(fc, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
   if (e == hipSuccess) e = hipLaunchKernel(fr, dim3((unsigned)q.B), dim3(CT), args, 0, q.stream);
+  if (e == hipSuccess) e = hipLaunchKernel(ga, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
+  if (e == hipSuccess) e = hipLaunchKernel(gb, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
+  if (e == hipSuccess) e = hipLaunchKernel(gc, dim3((unsigned)q.B), dim3(CT), args, 0, q.stream);
   return e == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
 }
 
