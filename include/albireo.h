@@ -209,7 +209,7 @@ albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64
  * buffer, so the call allocates nothing (no hipMalloc, no allocating library routine).
  *   Arguments and outputs as albireo_sample, without workspace / workspace_bytes.
  *   Limit: a shape whose albireo_sample workspace exceeds ALBIREO_NOALLOC_SCRATCH_BYTES (96 MiB: about
- *   10.1 KB per row chunk, so B * P up to about 9700 row chunks, P = ceil(floor(V / 8) / 4864) for bf16
+ *   12.1 KB per row chunk, so B * P up to about 8100 row chunks, P = ceil(floor(V / 8) / 4864) for bf16
  *   and ceil(floor(V / 4) / 4864) for fp32) returns ALBIREO_E_SCRATCH before anything is enqueued.
  *   Every GPU the library runs on holds one such array until the process ends, shared by all calls on
  *   that GPU: two calls that overlap in time on one GPU (different streams, or threads) race on it and

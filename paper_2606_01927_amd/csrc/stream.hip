@@ -69,7 +69,7 @@ constexpr int REC_WORDS = 8;               // 64-bit words per chunk record (5 u
 constexpr int RS_WORDS = 8;
 constexpr uint64_t RS_DEFER = 1;  // word 0: the row is deferred
 constexpr uint64_t RS_TOPP = 2;   // word 0: its kept set is a nucleus (else all values >= lo)
-constexpr int SCAP = 256;         // crossing-bucket values staged per chunk
+constexpr int SCAP = 512;         // crossing-bucket values staged per chunk
 constexpr int SSTRIDE = SCAP + GEN_WORDS;  // per chunk: the staged values, then the crossing bucket's
                                            // mass per sub-bucket
 
@@ -1759,15 +1759,28 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
   SRow R;
   row_setup<DT, SEG>(a, row, 0, R);
   const int P = R.P;
-  // the output history to LDS, grouped by chunk, for the overlay rebuilds of this row's passes
   if (t == 0) s.hst_on = 0;
-  const int64_t nh = R.h_hi - R.h_lo;
-  if (R.pen_on && nh > 0 && nh <= HSTAGE) {
-    for (int64_t i = t; i < nh; i += CT) r_hstage[i] = a.prm.hist_ids[R.h_lo + i];
-    if (t == 0) s.hst_on = 1;
-  }
+  // before a pass over the whole row: the output history to LDS, grouped by chunk, for the overlay
+  // rebuilds (the draw's walk over one chunk reads its ids from memory)
+  auto history_to_lds = [&]() __attribute__((always_inline)) {
+    const int64_t nh = R.h_hi - R.h_lo;
+    if (R.pen_on && nh > 0 && nh <= HSTAGE) {
+      constexpr int Q = HSTAGE / CT;
+      int32_t v[Q];
+      static_for<Q>([&](auto I) {  // every load in flight before any is stored
+        constexpr int q = decltype(I)::value;
+        v[q] = a.prm.hist_ids[R.h_lo + min((int64_t)(t + q * CT), nh - 1)];
+      });
+      static_for<Q>([&](auto I) {
+        constexpr int q = decltype(I)::value;
+        if (t + q * CT < nh) r_hstage[t + q * CT] = v[q];
+      });
+      if (t == 0) s.hst_on = 1;
+    }
+    __syncthreads();
+    stage_history<DT>(a, R, s);
+  };
   __syncthreads();
-  stage_history<DT>(a, R, s);
   const uint64_t* rec = a.rec + (row * P) * (int64_t)REC_WORDS;
   const float m = d.m, lo = d.lo;
   float tau = lo;
@@ -1784,7 +1797,8 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
     int bb;
     uint64_t before, total;
     fast = merge_hists(a, R, s, (double)d.p, bb, before, total);
-    bool overfull = false;  // the crossing bucket's values did not fit the staging
+    bool overfull = false;     // the crossing bucket's values did not fit the staging
+    bool staged_all = false;   // but every chunk's share of them is staged
     int n = 0;
     if (fast) {
       if (t == 0) {
@@ -1799,9 +1813,11 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
           off += s.cnt[c];
         }
         s.bc_i[0] = ok && off <= GKCAP2 ? off : -1;
+        s.bc_i[1] = ok ? 1 : 0;  // every chunk staged its whole crossing bucket
       }
       __syncthreads();
       n = s.bc_i[0];
+      staged_all = s.bc_i[1] != 0;
       __syncthreads();
       fast = n >= 0;
       overfull = !fast;
@@ -1869,29 +1885,44 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
         __syncthreads();
         if (sbb != 0x7fffffff) {
           // per chunk: the mass of bucket bb's sub-buckets below sbb (kept whatever the cut)
-          if (t < P) {
-            uint64_t v = rec[t * REC_WORDS + 3];
-            const uint64_t* sh = a.stg + (row * P + t) * (int64_t)SSTRIDE + SCAP;
-            for (int i = 0; i < sbb; ++i) v += sh[i];
-            s.cm[t] = v;
+          if (t < P) s.cm[t] = rec[t * REC_WORDS + 3];
+          __syncthreads();
+          for (int f = t; f < P * sbb; f += CT) {
+            const int c = f / sbb, i = f - c * sbb;
+            const uint64_t v = a.stg[(row * P + c) * (int64_t)SSTRIDE + SCAP + i];
+            if (v) atomicAdd(reinterpret_cast<unsigned long long*>(&s.cm[c]), (unsigned long long)v);
           }
           int lastp = -1;
           for (int c = 0; c < P; ++c) lastp = max(lastp, (int)(uint32_t)rec[c * REC_WORDS + 4]);
           if (t == 0) s.n_list = 0;
           __syncthreads();
           uint64_t* ent = r_gstage;
-          for (int c = 0; c < P; ++c) {
-            for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
-              if (z > -INFINITY && z >= lo && gp_dbucket(z, m) == bb) {
-                const int sb = gp_dsub(z, m, bb);
-                if (sb < sbb) {
-                  if (mass_of(z, m) > 0) lastp = max(lastp, pos);
-                } else if (sb == sbb) {
-                  const int i = atomicAdd(&s.n_list, 1);
-                  if (i < GKCAP2) ent[i] = ((uint64_t)f2key(z) << 32) | (uint32_t)pos;
-                }
+          auto take = [&](float z, int pos) __attribute__((always_inline)) {
+            const int sb = gp_dsub(z, m, bb);
+            if (sb < sbb) {
+              if (mass_of(z, m) > 0) lastp = max(lastp, pos);
+            } else if (sb == sbb) {
+              const int i = atomicAdd(&s.n_list, 1);
+              if (i < GKCAP2) ent[i] = ((uint64_t)f2key(z) << 32) | (uint32_t)pos;
+            }
+          };
+          if (staged_all) {
+            // the bucket's values are in the chunks' staging: no pass over the row
+            for (int c = 0; c < P; ++c) {
+              const uint64_t* src = a.stg + (row * P + c) * (int64_t)SSTRIDE;
+              for (int i = t; i < s.cnt[c]; i += CT) {
+                const uint64_t e = src[i];
+                take(key2f((uint32_t)(e >> 32)), (int)(uint32_t)e);
               }
-            });
+            }
+          } else {
+            // one pass over the row: a comparison per value, masses only inside bucket bb
+            history_to_lds();
+            for (int c = 0; c < P; ++c) {
+              for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
+                if (z > -INFINITY && z >= lo && gp_dbucket(z, m) == bb) take(z, pos);
+              });
+            }
           }
           __syncthreads();
           const int n2 = s.n_list;
@@ -1924,7 +1955,8 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
   if (fast) {
     id = gp_draw<DT, SEG>(a, R, s, tau, m, d.u, &zid, true, last);
   } else {
-    // the crossing bucket did not fit the staging: the single-workgroup nucleus selection
+    // the crossing sub-bucket did not fit the staging: the single-workgroup nucleus selection
+    history_to_lds();
     bool fused = gp_topp_fused<DT, SEG>(a, R, s, lo, m, (double)d.p, tau, last);
     if (!fused) {
       const uint32_t kk = gp_topp<DT, SEG>(a, R, s, lo, m, (double)d.p);
