@@ -355,3 +355,42 @@ def test_apply_penalties_bit_exact(lib, oracle_mod):
         torch.cuda.synchronize()
         ref = oracle_mod.sample(w, penalised=True)["penalised"]
         assert np.array_equal(np_(out).view(np.uint32), ref.view(np.uint32))
+
+
+def test_workspace_left_zero_after_deferred_rows(lib, oracle_mod):
+    """The workspace contract on the streaming route with rows that the chunk-parallel general path
+    resolves: after calls whose rows are deferred (nucleus rows whose crossing bucket fits the
+    staging, rows where it does not, plain rows, rows with penalties and top-n), every byte of the
+    caller's workspace is zero again, and a second call through the same workspace gives the same
+    outputs."""
+    import torch
+
+    from workloads.device import to_device
+
+    rng = np.random.default_rng(41)
+    V = 200003  # bf16: 6 chunks per row
+    base = rng.normal(0, 2, size=V).astype(np.float32)
+    tied = base.copy(); tied[rng.random(V) < 0.4] = 1.25
+    rows = [base, base * 0.5, tied, np.round(base * 8) / 8, base]
+    P_ = np.array([0.9, 0.6, 0.95, 0.8, 1.0], np.float32)  # the last row: no filter at all
+    w = _rowset(rows, dtype="bf16", temperature=np.array([1.0, 1.3, 0.9, 1.0, 0.8], np.float32),
+                top_k=np.zeros(len(rows), np.int32), top_p=P_)
+    hr = np.random.default_rng(42)
+    lens = hr.integers(100, 900, size=w.B)
+    w.hist_offsets = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    w.hist_ids = hr.integers(0, V, size=int(lens.sum())).astype(np.int32)
+    w.repetition_penalty = np.full(w.B, 1.2, np.float32)
+    w.n_top = 3
+    assert lib.sample_route(w.B, V, torch.bfloat16) == lib.ROUTE_STREAM
+    logits, u, p = to_device(w)
+    ws = lib.Workspace("cuda")
+    out = lib.sample(logits, u, p, n_top=3, V=V, workspace=ws)
+    torch.cuda.synchronize()
+    first = [np_(x) for x in out]
+    assert int(torch.count_nonzero(ws.buf)) == 0
+    second = [np_(x) for x in lib.sample(logits, u, p, n_top=3, V=V, workspace=ws)]
+    torch.cuda.synchronize()
+    assert int(torch.count_nonzero(ws.buf)) == 0
+    for x, y in zip(first, second):
+        assert np.array_equal(x, y)
+    compare_sample(oracle_mod.sample(w), out, n_top=3)
