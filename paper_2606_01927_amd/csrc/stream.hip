@@ -1,9 +1,11 @@
-// stream.hip -- the streaming kernel of the per-sequence sampling step (sec. 6.1, Eq. opt_sample: every
+// stream.hip -- the streaming kernels of the per-sequence sampling step (sec. 6.1, Eq. opt_sample: every
 // worker runs the unchanged per-row sampling computation on its rows; the computation is the one of
 // the workload of sec. 8.1: penalties, temperature, top-k, top-p, min-p, greedy, and the draw).
 //
 // A row of the [B, V] logits is cut into P chunks of at most CSLOTS 16-byte slots (38912 bf16 or 19456
-// fp32 logits).  Two launches on the caller's stream sample a batch.
+// fp32 logits).  Five launches on the caller's stream sample a batch: the chunk kernel, the resolution
+// kernel and, for the rows whose kept set has no small bound, three chunk-parallel general-path launches
+// (which return at once for every other row).
 //
 // The chunk kernel runs one 256-thread workgroup per chunk (four resident per CU).  A chunk workgroup
 //   * issues every 16-byte load of its chunk up front with the non-temporal hint (each logit is read
@@ -25,7 +27,10 @@
 // min-p, the nucleus and the inverse-CDF draw in ascending token id on the (small) kept set.  Rows whose
 // kept set has no small bound (top-p alone, no filter, lists over capacity) take the general path:
 // distance histograms, the crossing bucket and the draw over re-reads of the row's logits with the
-// penalty overlay rebuilt per chunk, so nothing of size [B, V] is ever written.  No workgroup ever
+// penalty overlay rebuilt per chunk, so nothing of size [B, V] is ever written.  Such rows without a
+// top-k are deferred to the three general-path launches, which spread the re-reads over the row's
+// chunks (k_gen_a, k_gen_b) and finish each row in one workgroup (k_gen_c); rows with a top-k that
+// needs the whole-row count selection are resolved by the resolution kernel itself.  No workgroup ever
 // waits for another.
 //
 // Everything that combines values across threads, waves or chunks does so in a fixed order or in
