@@ -394,3 +394,37 @@ def test_workspace_left_zero_after_deferred_rows(lib, oracle_mod):
     for x, y in zip(first, second):
         assert np.array_equal(x, y)
     compare_sample(oracle_mod.sample(w), out, n_top=3)
+
+
+def test_deferred_rows_edge_cases(lib, oracle_mod):
+    """Edge cases of the chunk-parallel general path on streamed rows (no top-k): p <= 0 and p -> 0
+    (the top group only), a nucleus cut inside a group of equal values spread over chunks, min-p
+    together with a nucleus, masked entries, a row whose finite values are all in one chunk, no filter
+    at all, and a greedy row beside them."""
+    import torch
+
+    rng = np.random.default_rng(51)
+    V = 200003  # fp32: 11 chunks per row
+    base = rng.normal(0, 1.5, size=V).astype(np.float32)
+    rows, T, Pp, MP = [], [], [], []
+
+    def add(x, t=1.0, p=1.0, mp=0.0):
+        rows.append(np.asarray(x, np.float32)); T.append(t); Pp.append(p); MP.append(mp)
+
+    x = base.copy(); x[[10, 90000, 180000]] = 7.0
+    add(x, p=-1.0)                                  # p <= 0: the tied top group only
+    add(x, p=1e-7)                                  # p -> 0: the same
+    g = base.copy(); g[rng.choice(V, 3000, replace=False)] = 4.0
+    add(g, p=0.5)                                   # the cut falls inside 3000 equal values
+    add(base, p=0.9, mp=0.05)                       # min-p and a nucleus
+    h = base.copy(); h[rng.random(V) < 0.7] = -np.inf
+    add(h, p=0.8)                                   # masked entries
+    one = np.full(V, -np.inf, np.float32); one[100:5000] = base[100:5000]
+    add(one, p=0.7)                                 # every finite value in the first chunk
+    add(base, t=1.3)                                # no filter
+    add(base, t=0.0)                                # greedy
+    w = _rowset(rows, temperature=np.array(T, np.float32), top_k=np.zeros(len(rows), np.int32),
+                top_p=np.array(Pp, np.float32), min_p=np.array(MP, np.float32))
+    assert lib.sample_route(w.B, V, torch.float32) == lib.ROUTE_STREAM
+    out = _run(lib, w)
+    compare_sample(oracle_mod.sample(w), out)
