@@ -619,8 +619,11 @@ __device__ __forceinline__ int overlay_rank(const SSm& s, int b) {
 // branch) and then with its new value, so every f must ignore -inf.  Every thread of the workgroup must
 // call it (it synchronises).
 // ----------------------------------------------------------------------------------------------
-template <class DT, bool SEG, class F>
-__device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s, int c, F&& f) {
+// hreg: the caller's register copy of the row's first HPT * CT history ids (this thread's share), read
+// by the overlay build instead of memory.
+template <class DT, bool SEG, int HPT, class F>
+__device__ __forceinline__ void for_chunk_h(const SArgs& a, const SRow& R, SSm& s, int c,
+                                            const int32_t (&hreg)[HPT > 0 ? HPT : 1], F&& f) {
   constexpr int VEC = DT::VEC;
   const int t = threadIdx.x;
   int64_t s0, s1;
@@ -635,8 +638,7 @@ __device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s,
   bool x_all = true;  // every marked position is tracked: the element loop masks them all
   if (R.pen_on) {
     uint32_t fl = 0;
-    const int32_t none[1] = {0};
-    n_x = build_overlay<0>(a, R, s, c, s0, s1, VEC, none, &fl);
+    n_x = build_overlay<HPT>(a, R, s, c, s0, s1, VEC, hreg, &fl);
     x_all = !(fl & FLAG_LIMIT);
   }
   const float r = R.r;
@@ -702,6 +704,23 @@ __device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s,
   }
   if (hpos >= 0) f(value(hx, hpos), hpos);
   __syncthreads();  // the overlay is rebuilt for the next chunk
+}
+template <class DT, bool SEG, class F>
+__device__ __forceinline__ void for_chunk(const SArgs& a, const SRow& R, SSm& s, int c, F&& f) {
+  const int32_t none[1] = {0};
+  for_chunk_h<DT, SEG, 0>(a, R, s, c, none, f);
+}
+// The first HPT * CT ids of the row's output history into registers (this thread's share, all loads in
+// flight together; a dummy address when there is nothing to read), for for_chunk_h.
+template <int HPT>
+__device__ __forceinline__ void history_regs(const SArgs& a, const SRow& R, int32_t (&hreg)[HPT]) {
+  const int t = threadIdx.x;
+  const int nh = R.pen_on ? (int)min(R.h_hi - R.h_lo, (int64_t)HPT * CT) : 0;
+  const int32_t* hrow = nh > 0 ? a.prm.hist_ids + R.h_lo : reinterpret_cast<const int32_t*>(a.rec);
+  static_for<HPT>([&](auto Q) {
+    constexpr int q = decltype(Q)::value;
+    hreg[q] = hrow[min(t + q * CT, max(nh - 1, 0))];
+  });
 }
 
 // ----------------------------------------------------------------------------------------------
@@ -1671,6 +1690,8 @@ __global__ __launch_bounds__(CT) void k_gen_a(SArgs a) {
   if (!d.on) return;
   SRow R;
   row_setup<DT, SEG>(a, row, c, R);
+  int32_t hreg[16];
+  history_regs<16>(a, R, hreg);
   if (t == 0) s.hst_on = 0;
   uint64_t* h64 = s.c.gen;
   for (int b = t; b < GDB; b += CT) h64[b] = 0;
@@ -1679,7 +1700,7 @@ __global__ __launch_bounds__(CT) void k_gen_a(SArgs a) {
   int last = -1;
   const float m = d.m, lo = d.lo;
   const bool topp = d.topp;
-  for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
+  for_chunk_h<DT, SEG, 16>(a, R, s, c, hreg, [&](float z, int pos) __attribute__((always_inline)) {
     if (z > -INFINITY && z >= lo) {
       const uint64_t w = mass_of(z, m);
       if (w) {
@@ -1713,6 +1734,8 @@ __global__ __launch_bounds__(CT) void k_gen_b(SArgs a) {
   if (!d.on || !d.topp) return;
   SRow R;
   row_setup<DT, SEG>(a, row, c, R);
+  int32_t hreg[16];
+  history_regs<16>(a, R, hreg);
   if (t == 0) {
     s.hst_on = 0;
     s.n_list = 0;
@@ -1727,7 +1750,7 @@ __global__ __launch_bounds__(CT) void k_gen_b(SArgs a) {
   uint64_t* sub = s.c.list;  // the crossing bucket's mass per sub-bucket
   for (int i = t; i < GDB; i += CT) sub[i] = 0;
   __syncthreads();
-  for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
+  for_chunk_h<DT, SEG, 16>(a, R, s, c, hreg, [&](float z, int pos) __attribute__((always_inline)) {
     if (z > -INFINITY && z >= lo) {
       const int b = gp_dbucket(z, m);
       if (b < bb) {
