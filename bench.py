@@ -357,7 +357,7 @@ def main():
     # the kernels the library routes this shape to (the same host decision the call takes)
     route = alb.sample_route(B, V, logits0.dtype, p)
     kernel = {alb.ROUTE_ONE_WORKGROUP: "k_sample (one launch per step)",
-              alb.ROUTE_STREAM: "k_stream, k_resolve, k_gen_a/b/c (five launches per step; the time is all)",
+              alb.ROUTE_STREAM: "k_stream, k_resolve, k_gen_a/b/s/c (six launches per step; the time is all)",
               alb.ROUTE_COOPERATIVE: "k_sample_multi (one cooperative launch per step)"}[route]
 
     res = {

@@ -3,9 +3,9 @@
 // the workload of sec. 8.1: penalties, temperature, top-k, top-p, min-p, greedy, and the draw).
 //
 // A row of the [B, V] logits is cut into P chunks of at most CSLOTS 16-byte slots (38912 bf16 or 19456
-// fp32 logits).  Five launches on the caller's stream sample a batch: the chunk kernel, the resolution
-// kernel and, for the rows whose kept set has no small bound, three chunk-parallel general-path launches
-// (which return at once for every other row).
+// fp32 logits).  Six launches on the caller's stream sample a batch: the chunk kernel, the resolution
+// kernel and, for the rows whose kept set has no small bound, four general-path launches (which return
+// at once for every other row).
 //
 // The chunk kernel runs one 256-thread workgroup per chunk (four resident per CU).  A chunk workgroup
 //   * issues every 16-byte load of its chunk up front with the non-temporal hint (each logit is read
@@ -28,8 +28,8 @@
 // kept set has no small bound (top-p alone, no filter, lists over capacity) take the general path:
 // distance histograms, the crossing bucket and the draw over re-reads of the row's logits with the
 // penalty overlay rebuilt per chunk, so nothing of size [B, V] is ever written.  Such rows without a
-// top-k are deferred to the three general-path launches, which spread the re-reads over the row's
-// chunks (k_gen_a, k_gen_b) and finish each row in one workgroup (k_gen_c); rows with a top-k that
+// top-k are deferred to the general-path launches, which spread the re-reads over the row's chunks
+// (k_gen_a, k_gen_b, k_gen_s) and finish each row in one workgroup (k_gen_c); rows with a top-k that
 // needs the whole-row count selection are resolved by the resolution kernel itself.  No workgroup ever
 // waits for another.
 //
@@ -1678,6 +1678,61 @@ __device__ __forceinline__ bool merge_hists(const SArgs& a, const SRow& R, SSm& 
   return bb != 0x7fffffff;
 }
 
+// The crossing bucket's sub-bucket where the cumulative, continued from `before`, reaches p times the
+// total (as the single-workgroup second round finds it), from the chunks' sub-bucket masses; the mass of
+// the sub-buckets above it in *cum.  Returns 0x7fffffff when it is never reached.
+__device__ __forceinline__ int merge_subs(const SArgs& a, const SRow& R, SSm& s, double target,
+                                          uint64_t before, uint64_t* cum_out) {
+  constexpr int BPT = GDB / CT;
+  const int i0 = (int)threadIdx.x * BPT;
+  uint64_t hv[BPT];
+  uint64_t sum = 0;
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    uint64_t v = 0;
+    for (int c = 0; c < R.P; ++c) v += a.stg[(R.row * R.P + c) * (int64_t)SSTRIDE + SCAP + i0 + q];
+    hv[q] = v;
+    sum += v;
+  }
+  uint64_t tot;
+  const uint64_t excl = blk_excl_scan_u64(sum, s, &tot);
+  int mine = 0x7fffffff;
+  if ((double)before + (double)excl < target && (double)before + (double)(excl + sum) >= target) {
+    uint64_t cum = excl;
+    int q = 0;
+    while (q < BPT - 1 && (double)before + (double)(cum + hv[q]) < target) cum += hv[q++];
+    mine = i0 + q;
+    s.bc_q[1] = cum;
+  }
+  const int sbb = blk_min_i(mine, s);
+  *cum_out = s.bc_q[1];
+  __syncthreads();
+  return sbb;
+}
+
+// Whether every chunk of the row published its crossing-bucket staging (k_gen_b), and whether each
+// holds its whole share (at most SCAP values) with at most GKCAP2 in all.  Uniform over the workgroup.
+struct StageCounts {
+  bool all_written, all_fit;
+  int total;
+};
+__device__ __forceinline__ StageCounts stage_counts(const SArgs& a, const SRow& R) {
+  StageCounts r{true, true, 0};
+  const uint64_t* rec = a.rec + (R.row * R.P) * (int64_t)REC_WORDS;
+  for (int c = 0; c < R.P; ++c) {
+    const uint64_t w2 = rec[c * REC_WORDS + 2];
+    if (!w2) {
+      r.all_written = false;
+      r.all_fit = false;
+      continue;
+    }
+    const int nc = (int)(w2 - 1);
+    if (nc > SCAP) r.all_fit = false;
+    r.total += min(nc, SCAP);
+  }
+  return r;
+}
+
 template <class DT, bool SEG>
 __global__ __launch_bounds__(CT) void k_gen_a(SArgs a) {
   __shared__ SSm s;
@@ -1774,6 +1829,57 @@ __global__ __launch_bounds__(CT) void k_gen_b(SArgs a) {
     a.rec[L * REC_WORDS + 2] = (uint64_t)(uint32_t)s.n_list + 1;  // + 1: written
     a.rec[L * REC_WORDS + 3] = acc;
     a.rec[L * REC_WORDS + 4] = (uint64_t)(uint32_t)last;
+  }
+}
+
+// Rows whose crossing bucket put more than SCAP values into some chunk: every chunk merges the chunks'
+// sub-bucket masses to the crossing sub-bucket and stages that sub-bucket's values in place of the
+// bucket's (records words 5 and 6: their count + 1 and the last position kept with positive mass
+// among the sub-buckets above it).
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT) void k_gen_s(SArgs a) {
+  __shared__ SSm s;
+  const int t = threadIdx.x;
+  int64_t L = blockIdx.x;
+  if (a.xcd_map) L = (L & 7) * (a.grid >> 3) + (L >> 3);
+  const int64_t row = L / a.P;
+  const int c = (int)(L - row * a.P);
+  const Deferred d = deferred_of(a, row);
+  if (!d.on || !d.topp) return;
+  SRow R;
+  row_setup<DT, SEG>(a, row, c, R);
+  const StageCounts sc = stage_counts(a, R);
+  if (!sc.all_written || sc.all_fit) return;  // k_gen_c finishes these rows without it
+  int32_t hreg[16];
+  history_regs<16>(a, R, hreg);
+  if (t == 0) {
+    s.hst_on = 0;
+    s.n_list = 0;
+  }
+  int bb;
+  uint64_t before, total;
+  if (!merge_hists(a, R, s, (double)d.p, bb, before, total)) return;
+  uint64_t cum;
+  const int sbb = merge_subs(a, R, s, (double)d.p * (double)total, before, &cum);
+  if (sbb == 0x7fffffff) return;
+  const float m = d.m, lo = d.lo;
+  uint64_t* stg = a.stg + L * (int64_t)SSTRIDE;
+  int lastp = -1;
+  for_chunk_h<DT, SEG, 16>(a, R, s, c, hreg, [&](float z, int pos) __attribute__((always_inline)) {
+    if (z > -INFINITY && z >= lo && gp_dbucket(z, m) == bb) {
+      const int sb = gp_dsub(z, m, bb);
+      if (sb < sbb) {
+        if (mass_of(z, m) > 0) lastp = max(lastp, pos);
+      } else if (sb == sbb) {
+        const int i = atomicAdd(&s.n_list, 1);
+        if (i < SCAP) stg[i] = ((uint64_t)f2key(z) << 32) | (uint32_t)pos;
+      }
+    }
+  });
+  lastp = blk_max_i(lastp, s);  // its barriers also publish n_list
+  if (t == 0) {
+    a.rec[L * REC_WORDS + 5] = (uint64_t)(uint32_t)s.n_list + 1;
+    a.rec[L * REC_WORDS + 6] = (uint64_t)(uint32_t)lastp;
   }
 }
 
@@ -1944,12 +2050,38 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
               }
             }
           } else {
-            // one pass over the row: a comparison per value, masses only inside bucket bb
-            history_to_lds();
+            bool sub_staged = true;  // k_gen_s staged the sub-bucket's values in every chunk
+            int n_sub = 0;
             for (int c = 0; c < P; ++c) {
-              for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
-                if (z > -INFINITY && z >= lo && gp_dbucket(z, m) == bb) take(z, pos);
-              });
+              const uint64_t w5 = rec[c * REC_WORDS + 5];
+              const int nc = w5 ? (int)(w5 - 1) : -1;
+              if (nc < 0 || nc > SCAP) sub_staged = false;
+              else n_sub += nc;
+            }
+            if (sub_staged && n_sub <= GKCAP2) {
+              for (int c = 0; c < P; ++c) lastp = max(lastp, (int)(uint32_t)rec[c * REC_WORDS + 6]);
+              if (t == 0) {
+                int off = 0;
+                for (int c = 0; c < P; ++c) {
+                  s.cut[c] = off;
+                  off += (int)(rec[c * REC_WORDS + 5] - 1);
+                }
+                s.n_list = off;
+              }
+              __syncthreads();
+              for (int c = 0; c < P; ++c) {
+                const uint64_t* src = a.stg + (row * P + c) * (int64_t)SSTRIDE;
+                const int nc = (int)(rec[c * REC_WORDS + 5] - 1);
+                for (int i = t; i < nc; i += CT) ent[s.cut[c] + i] = src[i];
+              }
+            } else {
+              // one pass over the row: a comparison per value, masses only inside bucket bb
+              history_to_lds();
+              for (int c = 0; c < P; ++c) {
+                for_chunk<DT, SEG>(a, R, s, c, [&](float z, int pos) __attribute__((always_inline)) {
+                  if (z > -INFINITY && z >= lo && gp_dbucket(z, m) == bb) take(z, pos);
+                });
+              }
             }
           }
           __syncthreads();
@@ -1999,7 +2131,8 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
     for (int i = t; i < P * LCAPC; i += CT) lbase[i] = 0;
     for (int c = 0; c < P; ++c) {
       const uint64_t w2 = rec[c * REC_WORDS + 2];
-      const int nc = w2 ? min((int)(w2 - 1), SCAP) : 0;
+      const uint64_t w5 = rec[c * REC_WORDS + 5];
+      const int nc = max(w2 ? min((int)(w2 - 1), SCAP) : 0, w5 ? min((int)(w5 - 1), SCAP) : 0);
       uint64_t* sb = a.stg + (row * P + c) * (int64_t)SSTRIDE;
       for (int i = t; i < nc; i += CT) sb[i] = 0;
       if (w2) for (int i = t; i < GDB; i += CT) sb[SCAP + i] = 0;
@@ -2616,19 +2749,21 @@ albireo_status_t launch(const Request& q) {
   a.rstate = reinterpret_cast<uint64_t*>(q.ws + w.rstate);
   a.stg = reinterpret_cast<uint64_t*>(q.ws + w.stg);
   void* args[] = {&a};
-  const void *fc, *fr, *ga, *gb, *gc;
+  const void *fc, *fr, *ga, *gb, *gs, *gc;
 #define ALBIREO_STREAM_KERNELS(DT)                                                                  \
   if (q.shards) {                                                                                   \
     fc = reinterpret_cast<const void*>(&k_stream<DT, true>);                                        \
     fr = reinterpret_cast<const void*>(&k_resolve<DT, true>);                                       \
     ga = reinterpret_cast<const void*>(&k_gen_a<DT, true>);                                         \
     gb = reinterpret_cast<const void*>(&k_gen_b<DT, true>);                                         \
+    gs = reinterpret_cast<const void*>(&k_gen_s<DT, true>);                                         \
     gc = reinterpret_cast<const void*>(&k_gen_c<DT, true>);                                         \
   } else {                                                                                          \
     fc = reinterpret_cast<const void*>(&k_stream<DT, false>);                                       \
     fr = reinterpret_cast<const void*>(&k_resolve<DT, false>);                                      \
     ga = reinterpret_cast<const void*>(&k_gen_a<DT, false>);                                        \
     gb = reinterpret_cast<const void*>(&k_gen_b<DT, false>);                                        \
+    gs = reinterpret_cast<const void*>(&k_gen_s<DT, false>);                                        \
     gc = reinterpret_cast<const void*>(&k_gen_c<DT, false>);                                        \
   }
   if (q.dtype == ALBIREO_BF16) {
@@ -2642,6 +2777,7 @@ albireo_status_t launch(const Request& q) {
   if (e == hipSuccess) e = hipLaunchKernel(fr, dim3((unsigned)q.B), dim3(CT), args, 0, q.stream);
   if (e == hipSuccess) e = hipLaunchKernel(ga, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
   if (e == hipSuccess) e = hipLaunchKernel(gb, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
+  if (e == hipSuccess) e = hipLaunchKernel(gs, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
   if (e == hipSuccess) e = hipLaunchKernel(gc, dim3((unsigned)q.B), dim3(CT), args, 0, q.stream);
   return e == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
 }
