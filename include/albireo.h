@@ -156,7 +156,7 @@ albireo_status_t albireo_penalty_state_append(const albireo_penalty_state_t* sta
 typedef enum {
   ALBIREO_ROUTE_NONE = 0,          /* no kernel of this build takes the shape (ALBIREO_E_UNSUPPORTED) */
   ALBIREO_ROUTE_ONE_WORKGROUP = 1, /* one launch, one workgroup per row, the row held in registers    */
-  ALBIREO_ROUTE_STREAM = 2,        /* two launches: a workgroup per row chunk, then one per row       */
+  ALBIREO_ROUTE_STREAM = 2,        /* a workgroup per row chunk, then one per row (six launches)     */
   ALBIREO_ROUTE_COOPERATIVE = 3    /* one cooperative launch of chunk workgroups (B x chunks >= 2^31) */
 } albireo_route_t;
 
