@@ -1613,11 +1613,15 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
 //     m) and, for a nucleus, its mass per distance bucket, into the chunk's list slot;
 //   k_gen_b (one workgroup per chunk, nucleus rows): every chunk of the row merges the histograms to the
 //     bucket where the cumulative reaches p times the total; the chunk sums its mass above that bucket
-//     and stages the bucket's values;
-//   k_gen_c (one workgroup per row): the cut inside the staged bucket, the per-chunk kept masses and
-//     the draw over the crossing chunk; it writes the row's id and logprob and zeroes what the row used.
-// Every sum is an integer sum of the same masses the single-workgroup general path takes, so the result
-// is the same; a row whose crossing bucket does not fit the staging takes that path in k_gen_c.
+//     and stages the bucket's values (up to SCAP) and the bucket's mass per sub-bucket;
+//   k_gen_s (one workgroup per chunk, rows where a chunk had more than SCAP of the bucket's values):
+//     every chunk merges the sub-bucket masses to the crossing sub-bucket and stages its values instead;
+//   k_gen_c (one workgroup per row): the cut inside the staged bucket or sub-bucket, the per-chunk kept
+//     masses and the draw over the crossing chunk; it writes the row's id and logprob and zeroes what
+//     the row used.
+// Every sum is an integer sum of the same masses the single-workgroup general path takes and the staged
+// sets are the same, so the result is the same; a row whose staging does not fit takes that path (or a
+// pass over the row for its crossing sub-bucket) in k_gen_c.
 // ----------------------------------------------------------------------------------------------
 struct Deferred {
   bool on, topp;
