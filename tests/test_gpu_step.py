@@ -51,7 +51,7 @@ def _seq_ids(B, salt):
     return np.random.default_rng(1000 + salt).integers(0, 2**40, size=B, dtype=np.int64)
 
 
-CASES = [(1, 4, 32000), (2, 64, 30011), (3, 32, 152064), (4, 8, 152064), (5, 16, 60013)]
+CASES = [(1, 4, 32000), (2, 64, 30011), (3, 32, 152064), (4, 8, 152064), (5, 16, 60013), (5, 16, 256000)]
 
 
 @pytest.mark.parametrize("cfg,B,V", CASES, ids=["c%d_B%d_V%d" % c for c in CASES])
@@ -120,13 +120,15 @@ def test_backfill_bit_exact(B, n_next, lib, oracle_mod):
     assert np.array_equal(np_(got), oracle_mod.backfill(ids, dest, nxt))
 
 
-def test_sample_step_backfill(lib, oracle_mod):
+@pytest.mark.parametrize("V", [30011, 200003], ids=["one_workgroup", "streamed"])
+def test_sample_step_backfill(V, lib, oracle_mod):
     """The fused backfill writes what the standalone scatter of the same call's ids writes; an empty
-    row sends -1; unnamed slots keep their contents."""
+    row sends -1; unnamed slots keep their contents.  The streamed width also sends the ids of the
+    rows the chunk-parallel general path resolves (the mix's top-p rows without top-k)."""
     import torch
     from workloads.device import to_device
 
-    w = workloads.generate(2, B=64, V=30011, variant=4)
+    w = workloads.generate(2, B=64, V=V, variant=4)
     w.logits = np.array(w.logits, copy=True)
     w.logits[5, :] = 0xFF80  # bf16 -inf: an empty row
     logits, _, p = to_device(w)
