@@ -126,6 +126,7 @@ struct SArgs {
   uint64_t* lists;   // [B * P * LCAPC] candidate keys
   uint64_t* rstate;  // [B * RS_WORDS] deferred rows' state
   uint64_t* stg;     // [B * P * SSTRIDE] deferred rows' staged crossing-bucket values and sub-buckets
+  int32_t* dq;       // [2 + B] deferred rows: their count, k_gen_c's arrivals, the row indices
 };
 
 struct SRow {
@@ -1592,6 +1593,7 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
     if (defer) {
       uint64_t* rs = a.rstate + row * RS_WORDS;
       for (int i = 0; i < 4; ++i) rs[i] = defer_w[i];
+      a.dq[2 + atomicAdd(&a.dq[0], 1)] = (int32_t)row;
     } else {
       float lp = -INFINITY;
       if (!empty) lp = (float)((double)zid - (double)m - L);
@@ -1609,16 +1611,19 @@ __device__ __forceinline__ void resolve_row(const SArgs& a, const SRow& R, SSm& 
 // Deferred rows: the general path of a row with no top-k, spread over its chunks.  The resolution
 // kernel leaves such a row's maximum m, the lower cut lo (min-p, or m for p <= 0), its uniform, p and
 // log-normaliser in the row's state.  Then
-//   k_gen_a (one workgroup per chunk): the chunk's kept mass (values >= lo, fixed-point masses against
+//   k_gen_a (per chunk): the chunk's kept mass (values >= lo, fixed-point masses against
 //     m) and, for a nucleus, its mass per distance bucket, into the chunk's list slot;
-//   k_gen_b (one workgroup per chunk, nucleus rows): every chunk of the row merges the histograms to the
+//   k_gen_b (per chunk, nucleus rows): every chunk of the row merges the histograms to the
 //     bucket where the cumulative reaches p times the total; the chunk sums its mass above that bucket
 //     and stages the bucket's values (up to SCAP) and the bucket's mass per sub-bucket;
-//   k_gen_s (one workgroup per chunk, rows where a chunk had more than SCAP of the bucket's values):
+//   k_gen_s (per chunk, rows where a chunk had more than SCAP of the bucket's values):
 //     every chunk merges the sub-bucket masses to the crossing sub-bucket and stages its values instead;
-//   k_gen_c (one workgroup per row): the cut inside the staged bucket or sub-bucket, the per-chunk kept
+//   k_gen_c (per row): the cut inside the staged bucket or sub-bucket, the per-chunk kept
 //     masses and the draw over the crossing chunk; it writes the row's id and logprob and zeroes what
 //     the row used.
+// The resolution kernel appends each deferred row to a list in the workspace; these launches walk that
+// list, one workgroup per (row, chunk) or per row at a time, so a call without deferred rows costs four
+// small grids that find the list empty.
 // Every sum is an integer sum of the same masses the single-workgroup general path takes and the staged
 // sets are the same, so the result is the same; a row whose staging does not fit takes that path (or a
 // pass over the row for its crossing sub-bucket) in k_gen_c.
@@ -1738,13 +1743,9 @@ __device__ __forceinline__ StageCounts stage_counts(const SArgs& a, const SRow& 
 }
 
 template <class DT, bool SEG>
-__global__ __launch_bounds__(CT) void k_gen_a(SArgs a) {
-  __shared__ SSm s;
+__device__ __forceinline__ void gen_a_item(const SArgs& a, SSm& s, int64_t row, int c) {
   const int t = threadIdx.x;
-  int64_t L = blockIdx.x;
-  if (a.xcd_map) L = (L & 7) * (a.grid >> 3) + (L >> 3);
-  const int64_t row = L / a.P;
-  const int c = (int)(L - row * a.P);
+  const int64_t L = row * a.P + c;
   const Deferred d = deferred_of(a, row);
   if (!d.on) return;
   SRow R;
@@ -1782,13 +1783,9 @@ __global__ __launch_bounds__(CT) void k_gen_a(SArgs a) {
 }
 
 template <class DT, bool SEG>
-__global__ __launch_bounds__(CT) void k_gen_b(SArgs a) {
-  __shared__ SSm s;
+__device__ __forceinline__ void gen_b_item(const SArgs& a, SSm& s, int64_t row, int c) {
   const int t = threadIdx.x;
-  int64_t L = blockIdx.x;
-  if (a.xcd_map) L = (L & 7) * (a.grid >> 3) + (L >> 3);
-  const int64_t row = L / a.P;
-  const int c = (int)(L - row * a.P);
+  const int64_t L = row * a.P + c;
   const Deferred d = deferred_of(a, row);
   if (!d.on || !d.topp) return;
   SRow R;
@@ -1841,13 +1838,9 @@ __global__ __launch_bounds__(CT) void k_gen_b(SArgs a) {
 // bucket's (records words 5 and 6: their count + 1 and the last position kept with positive mass
 // among the sub-buckets above it).
 template <class DT, bool SEG>
-__global__ __launch_bounds__(CT) void k_gen_s(SArgs a) {
-  __shared__ SSm s;
+__device__ __forceinline__ void gen_s_item(const SArgs& a, SSm& s, int64_t row, int c) {
   const int t = threadIdx.x;
-  int64_t L = blockIdx.x;
-  if (a.xcd_map) L = (L & 7) * (a.grid >> 3) + (L >> 3);
-  const int64_t row = L / a.P;
-  const int c = (int)(L - row * a.P);
+  const int64_t L = row * a.P + c;
   const Deferred d = deferred_of(a, row);
   if (!d.on || !d.topp) return;
   SRow R;
@@ -1888,10 +1881,8 @@ __global__ __launch_bounds__(CT) void k_gen_s(SArgs a) {
 }
 
 template <class DT, bool SEG>
-__global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
-  __shared__ SSm s;
+__device__ __forceinline__ void gen_c_item(const SArgs& a, SSm& s, int64_t row) {
   const int t = threadIdx.x;
-  const int64_t row = blockIdx.x;
   const Deferred d = deferred_of(a, row);
   if (!d.on) return;
   SRow R;
@@ -2152,6 +2143,58 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
     if (a.next_tokens) {
       const int32_t dst = a.backfill_dest[row];
       if (dst >= 0 && (int64_t)dst < a.next_len) a.next_tokens[dst] = id;
+    }
+  }
+}
+
+// The deferred-row launches take the resolution kernel's list of deferred rows (dq[0] rows, their
+// indices from dq[2]): a grid of at most GEN_GRID workgroups walks the (row, chunk) items, so that a
+// call with no deferred row costs one small grid per launch.  The last workgroup of k_gen_c to finish
+// (counted in dq[1]) zeroes the list once every workgroup has read it.
+constexpr int GEN_GRID = 2048;
+
+template <class DT, bool SEG, int K>
+__device__ __forceinline__ void gen_chunks(const SArgs& a, SSm& s) {
+  const int64_t n = (int64_t)a.dq[0] * a.P;
+  for (int64_t item = blockIdx.x; item < n; item += gridDim.x) {
+    const int64_t row = a.dq[2 + item / a.P];
+    const int c = (int)(item % a.P);
+    if (K == 0) gen_a_item<DT, SEG>(a, s, row, c);
+    else if (K == 1) gen_b_item<DT, SEG>(a, s, row, c);
+    else gen_s_item<DT, SEG>(a, s, row, c);
+    __syncthreads();  // the next item reuses the LDS
+  }
+}
+
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT) void k_gen_a(SArgs a) {
+  __shared__ SSm s;
+  gen_chunks<DT, SEG, 0>(a, s);
+}
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT) void k_gen_b(SArgs a) {
+  __shared__ SSm s;
+  gen_chunks<DT, SEG, 1>(a, s);
+}
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT) void k_gen_s(SArgs a) {
+  __shared__ SSm s;
+  gen_chunks<DT, SEG, 2>(a, s);
+}
+
+template <class DT, bool SEG>
+__global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
+  __shared__ SSm s;
+  const int n = a.dq[0];
+  for (int i = blockIdx.x; i < n; i += gridDim.x) {
+    gen_c_item<DT, SEG>(a, s, a.dq[2 + i]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    if (atomicAdd(reinterpret_cast<unsigned int*>(&a.dq[1]), 1u) == gridDim.x - 1) {
+      for (int i = 0; i < n; ++i) a.dq[2 + i] = 0;
+      a.dq[0] = 0;
+      a.dq[1] = 0;
     }
   }
 }
@@ -2662,7 +2705,7 @@ SGeo geometry(int64_t B, int64_t V, albireo_dtype_t dtype) {
 }
 
 struct WsParts {
-  int64_t rec, lists, rstate, stg, total;
+  int64_t rec, lists, rstate, stg, dq, total;
 };
 WsParts ws_parts(int64_t B, int P) {
   WsParts w;
@@ -2670,7 +2713,8 @@ WsParts ws_parts(int64_t B, int P) {
   w.lists = align256(w.rec + B * P * (int64_t)REC_WORDS * 8);
   w.rstate = align256(w.lists + B * P * (int64_t)LCAPC * 8);
   w.stg = align256(w.rstate + B * (int64_t)RS_WORDS * 8);
-  w.total = align256(w.stg + B * P * (int64_t)SSTRIDE * 8);
+  w.dq = align256(w.stg + B * P * (int64_t)SSTRIDE * 8);
+  w.total = align256(w.dq + (2 + B) * 4);
   return w;
 }
 
@@ -2752,6 +2796,7 @@ albireo_status_t launch(const Request& q) {
   a.lists = reinterpret_cast<uint64_t*>(q.ws + w.lists);
   a.rstate = reinterpret_cast<uint64_t*>(q.ws + w.rstate);
   a.stg = reinterpret_cast<uint64_t*>(q.ws + w.stg);
+  a.dq = reinterpret_cast<int32_t*>(q.ws + w.dq);
   void* args[] = {&a};
   const void *fc, *fr, *ga, *gb, *gs, *gc;
 #define ALBIREO_STREAM_KERNELS(DT)                                                                  \
@@ -2779,10 +2824,11 @@ albireo_status_t launch(const Request& q) {
   // chunk pass, row resolution, then the deferred rows' chunk-parallel general path
   hipError_t e = hipLaunchKernel(fc, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
   if (e == hipSuccess) e = hipLaunchKernel(fr, dim3((unsigned)q.B), dim3(CT), args, 0, q.stream);
-  if (e == hipSuccess) e = hipLaunchKernel(ga, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
-  if (e == hipSuccess) e = hipLaunchKernel(gb, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
-  if (e == hipSuccess) e = hipLaunchKernel(gs, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
-  if (e == hipSuccess) e = hipLaunchKernel(gc, dim3((unsigned)q.B), dim3(CT), args, 0, q.stream);
+  const unsigned gg = (unsigned)min(a.grid, (int64_t)GEN_GRID), gr = (unsigned)min(q.B, (int64_t)GEN_GRID);
+  if (e == hipSuccess) e = hipLaunchKernel(ga, dim3(gg), dim3(CT), args, 0, q.stream);
+  if (e == hipSuccess) e = hipLaunchKernel(gb, dim3(gg), dim3(CT), args, 0, q.stream);
+  if (e == hipSuccess) e = hipLaunchKernel(gs, dim3(gg), dim3(CT), args, 0, q.stream);
+  if (e == hipSuccess) e = hipLaunchKernel(gc, dim3(gr), dim3(CT), args, 0, q.stream);
   return e == hipSuccess ? ALBIREO_OK : ALBIREO_E_LAUNCH;
 }
 
