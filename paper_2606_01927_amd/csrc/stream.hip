@@ -2148,10 +2148,12 @@ __device__ __forceinline__ void gen_c_item(const SArgs& a, SSm& s, int64_t row) 
 }
 
 // The deferred-row launches take the resolution kernel's list of deferred rows (dq[0] rows, their
-// indices from dq[2]): a grid of at most GEN_GRID workgroups walks the (row, chunk) items, so that a
-// call with no deferred row costs one small grid per launch.  The last workgroup of k_gen_c to finish
-// (counted in dq[1]) zeroes the list once every workgroup has read it.
-constexpr int GEN_GRID = 2048;
+// indices from dq[2]): at most GEN_GRID workgroups walk the (row, chunk) items and at most GEN_ROWS the
+// rows, so that a call with no deferred row costs one small grid per launch (the two sizes measured
+// best on rows of 152064 and 256000 logits).  The last workgroup of k_gen_c to finish (counted in
+// dq[1]) zeroes the list once every workgroup has read it.
+constexpr int GEN_GRID = 1024;
+constexpr int GEN_ROWS = 512;
 
 template <class DT, bool SEG, int K>
 __device__ __forceinline__ void gen_chunks(const SArgs& a, SSm& s) {
@@ -2824,7 +2826,7 @@ albireo_status_t launch(const Request& q) {
   // chunk pass, row resolution, then the deferred rows' chunk-parallel general path
   hipError_t e = hipLaunchKernel(fc, dim3((unsigned)a.grid), dim3(CT), args, 0, q.stream);
   if (e == hipSuccess) e = hipLaunchKernel(fr, dim3((unsigned)q.B), dim3(CT), args, 0, q.stream);
-  const unsigned gg = (unsigned)min(a.grid, (int64_t)GEN_GRID), gr = (unsigned)min(q.B, (int64_t)GEN_GRID);
+  const unsigned gg = (unsigned)min(a.grid, (int64_t)GEN_GRID), gr = (unsigned)min(q.B, (int64_t)GEN_ROWS);
   if (e == hipSuccess) e = hipLaunchKernel(ga, dim3(gg), dim3(CT), args, 0, q.stream);
   if (e == hipSuccess) e = hipLaunchKernel(gb, dim3(gg), dim3(CT), args, 0, q.stream);
   if (e == hipSuccess) e = hipLaunchKernel(gs, dim3(gg), dim3(CT), args, 0, q.stream);
