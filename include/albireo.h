@@ -177,7 +177,8 @@ albireo_route_t albireo_sample_route(int64_t B, int64_t V, albireo_dtype_t dtype
  * Bytes of device workspace needed by any entry point for this shape on the current device.
  * The workspace must be 256-byte aligned and zero-filled before its first use; every call leaves it
  * zero-filled again on return (stream order).  One workspace per stream: two calls that run
- * concurrently must not share one.
+ * concurrently must not share one.  A call that returns ALBIREO_E_LAUNCH may have enqueued part of its
+ * launches: zero-fill the workspace again before its next use (the Python binding does so for its own).
  */
 size_t albireo_workspace_size(int64_t B, int64_t V, albireo_dtype_t dtype, int32_t n_top);
 
@@ -213,7 +214,9 @@ albireo_status_t albireo_sample(const void* logits, albireo_dtype_t dtype, int64
  *   and ceil(floor(V / 4) / 4864) for fp32) returns ALBIREO_E_SCRATCH before anything is enqueued.
  *   Every GPU the library runs on holds one such array until the process ends, shared by all calls on
  *   that GPU: two calls that overlap in time on one GPU (different streams, or threads) race on it and
- *   must be serialised by the caller.  Nothing in it needs to be zero between calls.
+ *   must be serialised by the caller.  Nothing in it needs to be zero between calls: every call leaves
+ *   it zero-filled, and after a call that returns ALBIREO_E_LAUNCH (the runtime refused a launch
+ *   part-way) the next call on that GPU first zero-fills the whole array with one more launch.
  */
 #define ALBIREO_NOALLOC_SCRATCH_BYTES (96u << 20)
 albireo_status_t albireo_sample_noalloc(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V,

@@ -250,6 +250,24 @@ class Workspace:
         off = (-base) % 256
         return base + off, self.buf.numel() - off
 
+    def refill(self, stream=None) -> None:
+        """Zero the buffer again on the stream: a call that returned ALBIREO_E_LAUNCH may have run part
+        of its launches and left it non-zero."""
+        if self.buf is not None:
+            s = torch.cuda.current_stream(self.device) if stream is None else stream
+            with torch.cuda.stream(s):
+                self.buf.zero_()
+
+
+def _fail(st, name, ws=None, stream=None):
+    """Raise the error of a sampling call, zeroing its Workspace first after a refused launch."""
+    if st == E_LAUNCH and isinstance(ws, Workspace):
+        try:
+            ws.refill(stream)
+        except RuntimeError:
+            pass  # the device refused the fill as well; the launch error is the one to report
+    raise AlbireoError(st, name)
+
 
 _default_ws = {}
 
@@ -301,7 +319,7 @@ def sample(logits: torch.Tensor, uniforms: torch.Tensor, params: Optional[Sampli
                              tids.data_ptr() if n_top else None, tlps.data_ptr() if n_top else None,
                              flags.data_ptr(), wptr, wbytes, _stream(stream))
     if st != OK:
-        raise AlbireoError(st, "albireo_sample")
+        _fail(st, "albireo_sample", ws, stream)
     return ids, lps, tids, tlps, flags
 
 
@@ -344,10 +362,15 @@ class PreparedSample:
                      tids.data_ptr() if n_top else None, tlps.data_ptr() if n_top else None, flags.data_ptr(),
                      self.wptr, self.wbytes, _stream(stream))
         self.fn = _lib.albireo_sample
+        self.stream = stream
 
     def __call__(self, logits_ptr: int) -> None:
         st = self.fn(logits_ptr, self.dt, self.B, self.V, self.ld, *self.tail)
         if st != OK:
+            if st == E_LAUNCH and self.keep[3] is not None:  # zero this call's buffer again (the Workspace may hold a newer one)
+                buf, dev = self.keep[3], self.keep[3].device
+                with torch.cuda.stream(torch.cuda.current_stream(dev) if self.stream is None else self.stream):
+                    buf.zero_()
             raise AlbireoError(st, "albireo_sample")
 
 
@@ -394,7 +417,7 @@ def sample_step(logits: torch.Tensor, seed: int, step: int, seq_ids: Optional[to
                                   tids.data_ptr() if n_top else None, tlps.data_ptr() if n_top else None,
                                   flags.data_ptr(), wptr, wbytes, _stream(stream))
     if st != OK:
-        raise AlbireoError(st, "albireo_sample_step")
+        _fail(st, "albireo_sample_step", ws, stream)
     return ids, lps, tids, tlps, flags
 
 
@@ -451,7 +474,7 @@ def sample_sharded(recv: torch.Tensor, V: Optional[int] = None, uniforms: Option
                                      tlps.data_ptr() if n_top else None, flags.data_ptr(), wptr, wbytes,
                                      _stream(stream))
     if st != OK:
-        raise AlbireoError(st, "albireo_sample_sharded")
+        _fail(st, "albireo_sample_sharded", ws, stream)
     return ids, lps, tids, tlps, flags
 
 
@@ -523,7 +546,7 @@ def topk_topp(logits: torch.Tensor, params: Optional[SamplingParams] = None, V: 
                                 pr.data_ptr() if pr is not None else None, thr.data_ptr(), kept.data_ptr(),
                                 lnorm.data_ptr(), flags.data_ptr(), wptr, wbytes, _stream(stream))
     if st != OK:
-        raise AlbireoError(st, "albireo_topk_topp")
+        _fail(st, "albireo_topk_topp", ws, stream)
     return pr, thr, kept, lnorm, flags
 
 

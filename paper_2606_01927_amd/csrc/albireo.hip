@@ -2597,6 +2597,13 @@ __global__ __launch_bounds__(256) void k_backfill(const int32_t* ids, const int3
   }
 }
 
+// Zero n sixteen-byte words (grid-stride): restores the no-alloc scratch after a call whose launches
+// the runtime refused part-way.
+__global__ __launch_bounds__(256) void k_zero16(uint4* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    p[i] = make_uint4(0, 0, 0, 0);
+}
+
 // The prompt history (repetition only) and the per-sequence penalty state, beside the output history.
 struct PenExtra {
   const int64_t* prompt_offsets;
@@ -3021,10 +3028,11 @@ static __device__ __align__(256) unsigned char scratch[ALBIREO_NOALLOC_SCRATCH_B
 namespace {
 constexpr int SCRATCH_DEVICES = 64;
 std::mutex g_scratch_mu;
-void* g_scratch_dev[SCRATCH_DEVICES];  // per device: the address of its copy of `scratch`
+void* g_scratch_dev[SCRATCH_DEVICES];   // per device: the address of its copy of `scratch`
+bool g_scratch_dirty[SCRATCH_DEVICES];  // per device: a call returned ALBIREO_E_LAUNCH since the last fill
 
-// The current device's scratch address (looked up on the first call on that device).
-albireo_status_t scratch_for_current_device(void** out) {
+// The current device's scratch address (looked up on the first call on that device) and index.
+albireo_status_t scratch_for_current_device(void** out, int* dev_out) {
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SCRATCH_DEVICES) return ALBIREO_E_LAUNCH;
   std::lock_guard<std::mutex> lock(g_scratch_mu);
@@ -3034,6 +3042,7 @@ albireo_status_t scratch_for_current_device(void** out) {
     g_scratch_dev[dev] = p;
   }
   *out = g_scratch_dev[dev];
+  *dev_out = dev;
   return ALBIREO_OK;
 }
 }  // namespace
@@ -3080,10 +3089,27 @@ albireo_status_t albireo_sample_noalloc(const void* logits, albireo_dtype_t dtyp
       albireo_workspace_size(B, V, dtype, n_top) > (size_t)ALBIREO_NOALLOC_SCRATCH_BYTES)
     return ALBIREO_E_SCRATCH;
   void* ws = nullptr;
-  const albireo_status_t st = scratch_for_current_device(&ws);
+  int dev = -1;
+  albireo_status_t st = scratch_for_current_device(&ws, &dev);
   if (st != ALBIREO_OK) return st;
-  return sample_impl(logits, dtype, B, V, ld, nullptr, params, uniforms, nullptr, out_ids, out_logprobs, n_top,
-                     out_top_ids, out_top_logprobs, out_flags, ws, (size_t)ALBIREO_NOALLOC_SCRATCH_BYTES, stream);
+  {
+    // a call whose launches the runtime refused part-way may have left the array non-zero: zero all of
+    // it (stream order) before it serves again
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_dirty[dev]) {
+      const int64_t n = (int64_t)ALBIREO_NOALLOC_SCRATCH_BYTES / 16;
+      hipLaunchKernelGGL(k_zero16, dim3(2048), dim3(256), 0, stream, static_cast<uint4*>(ws), n);
+      if (hipGetLastError() != hipSuccess) return ALBIREO_E_LAUNCH;
+      g_scratch_dirty[dev] = false;
+    }
+  }
+  st = sample_impl(logits, dtype, B, V, ld, nullptr, params, uniforms, nullptr, out_ids, out_logprobs, n_top,
+                   out_top_ids, out_top_logprobs, out_flags, ws, (size_t)ALBIREO_NOALLOC_SCRATCH_BYTES, stream);
+  if (st == ALBIREO_E_LAUNCH) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    g_scratch_dirty[dev] = true;
+  }
+  return st;
 }
 
 albireo_status_t albireo_sample_step(const void* logits, albireo_dtype_t dtype, int64_t B, int64_t V, int64_t ld,

@@ -68,3 +68,20 @@ def test_invalid_arguments_route_nowhere():
     assert sample_route(-1, 32000, F32) == ROUTE_NONE
     assert sample_route(8, (1 << 31) - 16, BF16) == ROUTE_NONE
     assert _lib.albireo_sample_route(8, 32000, 7, None, 0) == ROUTE_NONE
+
+
+def test_refused_launch_refills_the_workspace(monkeypatch):
+    """After ALBIREO_E_LAUNCH the binding zero-fills its Workspace before raising; other errors leave it."""
+    import paper_2606_01927_amd as alb
+
+    ws = alb.Workspace("cpu")
+    calls = []
+    monkeypatch.setattr(ws, "refill", lambda stream=None: calls.append(stream))
+    with pytest.raises(alb.AlbireoError):
+        alb._fail(alb.E_INVALID, "albireo_sample", ws)
+    assert calls == []
+    with pytest.raises(alb.AlbireoError):
+        alb._fail(alb.E_LAUNCH, "albireo_sample", ws, "s")
+    assert calls == ["s"]
+    with pytest.raises(alb.AlbireoError):
+        alb._fail(alb.E_LAUNCH, "albireo_sample", None)  # a caller's raw pointer: nothing to refill
