@@ -2150,8 +2150,10 @@ __device__ __forceinline__ void gen_c_item(const SArgs& a, SSm& s, int64_t row) 
 // The deferred-row launches take the resolution kernel's list of deferred rows (dq[0] rows, their
 // indices from dq[2]): at most GEN_GRID workgroups walk the (row, chunk) items and at most GEN_ROWS the
 // rows, so that a call with no deferred row costs one small grid per launch (the two sizes measured
-// best on rows of 152064 and 256000 logits).  The last workgroup of k_gen_c to finish (counted in
-// dq[1]) zeroes the list once every workgroup has read it.
+// best on rows of 152064 and 256000 logits).  The workgroups of k_gen_c that take a row count their
+// arrivals in dq[1], and the last of them zeroes the list once all of them have read it; the others
+// do nothing whether they read dq[0] before or after it is zeroed, so a call without deferred rows
+// makes no atomic on the counter (one contended counter cost every workgroup a few microseconds).
 constexpr int GEN_GRID = 1024;
 constexpr int GEN_ROWS = 512;
 
@@ -2192,8 +2194,9 @@ __global__ __launch_bounds__(CT, 1) void k_gen_c(SArgs a) {
     gen_c_item<DT, SEG>(a, s, a.dq[2 + i]);
     __syncthreads();
   }
-  if (threadIdx.x == 0) {
-    if (atomicAdd(reinterpret_cast<unsigned int*>(&a.dq[1]), 1u) == gridDim.x - 1) {
+  const unsigned working = (unsigned)min(n, (int)gridDim.x);
+  if (threadIdx.x == 0 && blockIdx.x < working) {
+    if (atomicAdd(reinterpret_cast<unsigned int*>(&a.dq[1]), 1u) == working - 1) {
       for (int i = 0; i < n; ++i) a.dq[2 + i] = 0;
       a.dq[0] = 0;
       a.dq[1] = 0;
